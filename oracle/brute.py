@@ -1,0 +1,99 @@
+"""Pure-Python brute-force twin of the oracle, for tiny inputs.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/ternary.py``).  No numpy: plain
+loops over Python lists, ``math.fsum`` for exact sums, ``fractions.Fraction``
+for exact comparisons and ``struct`` for float32 rounding.  It re-derives each
+step of the quantizer of Sec. 3.1 in a different formulation from the
+vectorized oracle, so agreement between the two pins both:
+
+* the scale is the exactly rounded mean absolute value of the group, rounded
+  once more to float32;
+* the code is zero exactly when the float32 quotient |w| / (s + eps) rounds to
+  at most one half.  Round-to-nearest-even of a real quotient v gives a float32
+  <= 1/2 iff v <= 1/2 + 2**-25 (the midpoint between 1/2 and the next float32,
+  1/2 + 2**-24, rounds to the even 1/2).  Half-to-even rounding then sends
+  1/2 to 0 and everything in (1/2, 1] to 1, so the code is
+  sign(w) * [|w| > (s + eps) * (1/2 + 2**-25)], evaluated exactly with
+  rationals.  A zero divisor (all-zero group at eps = 0) gives +-inf -> +-1
+  for non-zero w and 0 for w = 0.
+"""
+
+from __future__ import annotations
+
+import math
+import struct
+from fractions import Fraction
+
+_HALF_PLUS = Fraction(1, 2) + Fraction(1, 2 ** 25)
+
+
+def f32(x: float) -> float:
+    """Round a Python float to the nearest float32 (ties to even)."""
+    return struct.unpack("<f", struct.pack("<f", x))[0]
+
+
+def scales(W, g):
+    """Per-row, per-group float32 scales: fl32(fsum|w| / g)."""
+    out = []
+    for row in W:
+        K = len(row)
+        assert K % g == 0
+        out.append([f32(math.fsum(abs(f32(w)) for w in row[j:j + g]) / g)
+                    for j in range(0, K, g)])
+    return out
+
+
+def codes(W, s32, g, eps):
+    """Codes in {-1, 0, 1} by the exact threshold formulation above."""
+    eps32 = f32(eps)
+    out = []
+    for row, srow in zip(W, s32):
+        qrow = []
+        for k, w in enumerate(row):
+            w = f32(w)
+            d = f32(srow[k // g] + eps32)
+            if w == 0.0:
+                qrow.append(0)
+            elif d == 0.0:
+                qrow.append(1 if w > 0 else -1)
+            elif Fraction(abs(w)) > Fraction(d) * _HALF_PLUS:
+                qrow.append(1 if w > 0 else -1)
+            else:
+                qrow.append(0)
+        out.append(qrow)
+    return out
+
+
+def pack_row(qrow):
+    """One row of codes -> list of bytes, element by element from the format:
+    element e of word w sits at bit 2*(e//2) + 16*(e%2), two's complement."""
+    K = len(qrow)
+    assert K % 16 == 0
+    out = []
+    for w0 in range(0, K, 16):
+        word = 0
+        for e in range(16):
+            two_bit = {0: 0, 1: 1, -1: 3}[qrow[w0 + e]]
+            word |= two_bit << (2 * (e // 2) + 16 * (e % 2))
+        out.extend(word.to_bytes(4, "little"))
+    return out
+
+
+def gemm(X, q, s, g):
+    """Y[m][n] = sum_k X[m][k] * s[n][k//g] * q[n][k], exact-rounded fsum."""
+    return [[math.fsum(X[m][k] * s[n][k // g] * q[n][k] for k in range(len(X[m])))
+             for n in range(len(q))] for m in range(len(X))]
+
+
+def gemm_dx(dY, q, s, g):
+    """dX[m][k] = sum_n dY[m][n] * s[n][k//g] * q[n][k]."""
+    N, K = len(q), len(q[0])
+    return [[math.fsum(dY[m][n] * s[n][k // g] * q[n][k] for n in range(N))
+             for k in range(K)] for m in range(len(dY))]
+
+
+def gemm_dw(dY, X):
+    """dW[n][k] = sum_m dY[m][n] * X[m][k]."""
+    M, N, K = len(dY), len(dY[0]), len(X[0])
+    return [[math.fsum(dY[m][n] * X[m][k] for m in range(M)) for k in range(K)]
+            for n in range(N)]
