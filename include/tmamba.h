@@ -1,0 +1,163 @@
+/*
+ * tmamba.h — C ABI of the grouped-absmean ternary (W1.58A16) linear layer
+ * for AMD MI355X (gfx950).
+ *
+ * The operation (paper: "Ternary Mamba: Grouped Quantization-Aware Training
+ * of W1.58A16 State Space Models", Sec. 3.1, TernaryLinear Module):
+ *   - the latent weight W [N, K] (out x in) is split into groups of g
+ *     consecutive input-dimension elements of one output row;
+ *   - group scale s[n, j] = mean_i |W[n, j*g + i]|, recomputed on every call
+ *     (not a learned parameter);
+ *   - code q[n, k] = round(clip(W[n, k] / (s + eps), -1, 1)) in {-1, 0, +1},
+ *     round-half-to-even;
+ *   - dequantized weight What[n, k] = s[n, k/g] * q[n, k];
+ *   - forward Y = X . What^T; the straight-through estimator passes the
+ *     gradient through the quantizer unchanged, so dX = dY . What and
+ *     dW = dY^T . X.
+ * Deployment storage is 2-bit codes plus per-group scales (Sec. 8).
+ *
+ * Conventions for every call
+ *   - Every array pointer is DEVICE memory, allocated and owned by the caller.
+ *     The library allocates and frees nothing, keeps no mutable global state
+ *     and is safe to call from several host threads.
+ *   - Arrays are dense, row-major, with the shapes given per call.  bfloat16
+ *     data is passed as uint16_t bit patterns.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL is the default
+ *     stream) and the call returns without synchronizing.  Device faults, if
+ *     any, surface at the caller's next synchronization.
+ *   - All arguments are checked on the host before anything is enqueued.
+ *     On any error nothing is enqueued and a status code is returned: no
+ *     exceptions cross the ABI, nothing aborts, nothing is printed.
+ *   - Outputs must not overlap inputs or each other (TM_EINVAL).
+ *   - Group sizes: g in {32, 64, 128, 256, 512}; K % g == 0 and K % 64 == 0.
+ *
+ * Packed code format (one row = K/4 bytes = K/16 little-endian uint32 words;
+ * word w holds elements k = 16*w + e, e = 0..15):
+ *   element e = 2*i   at bits [2*i,      2*i + 2)
+ *   element e = 2*i+1 at bits [16 + 2*i, 16 + 2*i + 2)
+ *   2-bit value = two's complement of the code: 00 -> 0, 01 -> +1, 11 -> -1.
+ *   10 is never written; the kernels read it as 0.
+ */
+#ifndef TMAMBA_H
+#define TMAMBA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TM_OK = 0,
+  TM_EINVAL = 1,   /* null required pointer, overlapping arrays, bad eps/flag */
+  TM_ESHAPE = 2,   /* a size < 1, K % g, K % 64, g not allowed, B/count range */
+  TM_EALIGN = 3,   /* a pointer below its required alignment */
+  TM_EHIP = 4,     /* the HIP runtime rejected a launch */
+  TM_ENOTIMPL = 5  /* reserved */
+} tm_status;
+
+typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
+
+#define TM_ABI_VERSION 1
+
+/* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
+int tm_abi_version(void);
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* tm_status_str(tm_status s);
+
+/*
+ * tm_ternarize_pack — Sec. 3.1 (group scale, ternary code) and Sec. 8 (packed
+ * 2-bit storage), plus the zero-code count behind the zero ratio of Sec. 3.1
+ * and Table 1.  One pass over W.
+ *
+ *   W           float32 [N, K]            in   (16-byte aligned, finite)
+ *   N, K, g     K % g == 0, K % 64 == 0
+ *   eps         float32, finite, >= 0; added to the scale before the
+ *               division only (eps = 0 is the paper's formula)
+ *   codes       uint8 [N, K/4]            out  (16-byte aligned)
+ *   scales      float32 [N, K/g]          out  (4-byte aligned): the group
+ *               mean, accumulated in float64 and rounded once to float32
+ *   scales_f16  uint16 [N, K/g] or NULL   out  float16 bits, RNE of `scales`
+ *   zero_count  uint64 [1] or NULL        out  number of zero codes; set on
+ *               the stream (zeroed, then accumulated)
+ * The code decision is the float32 one: q = 0 exactly when the float32
+ * quotient |W| / fl32(s + eps) rounds to at most 1/2.
+ */
+tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g,
+                            float eps, uint8_t* codes, float* scales,
+                            uint16_t* scales_f16, uint64_t* zero_count,
+                            tm_stream stream);
+
+/*
+ * tm_tgemm_fwd — Sec. 3.1 forward: Y = X . What^T with What = q * s.
+ *
+ *   X       bf16 [M, K]      in   (16-byte aligned)
+ *   codes   uint8 [N, K/4]   in   packed codes (16-byte aligned)
+ *   scales  float32 [N, K/g] in   (4-byte aligned)
+ *   Y       float32 [M, N]   out  (16-byte aligned)
+ * Products are exact (bf16 times {-1,0,1}) and accumulated in float32 on the
+ * matrix cores; the group scale is applied in float32 per group.  Groups
+ * whose scale is 0 contribute 0 whatever their codes.  Precondition (met by
+ * any weights that are not extreme): within a row n, the largest nonzero
+ * scale divided by the smallest, times sum_k |X[m, k]|, stays below 1e38.
+ */
+tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
+                       const float* scales, int64_t M, int64_t N, int64_t K,
+                       int32_t g, float* Y, tm_stream stream);
+
+/*
+ * tm_tgemm_bwd_dx — Sec. 3.1 straight-through backward w.r.t. the input:
+ * dX = dY . What (contraction over N).
+ *
+ *   dY      bf16 [M, N]      in   (16-byte aligned; N % 8 == 0)
+ *   codes   uint8 [N, K/4]   in   the codes of the forward call
+ *   scales  float32 [N, K/g] in   the scales of the forward call
+ *   dX      float32 [M, K]   out  (16-byte aligned)
+ * The scale varies along the contraction, so each dequantized weight is
+ * split into two bfloat16 terms (hi + lo) whose sum carries 16 bits of the
+ * float32 scale; both terms run on the matrix cores.
+ */
+tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes,
+                          const float* scales, int64_t M, int64_t N, int64_t K,
+                          int32_t g, float* dX, tm_stream stream);
+
+/*
+ * tm_tgemm_bwd_dw_ste — Sec. 3.1 straight-through backward w.r.t. the latent
+ * weight (identity estimator: no clip mask, no gradient through the scale):
+ * dW = dY^T . X (contraction over the M tokens).
+ *
+ *   dY          bf16 [M, N]    in   (16-byte aligned; N % 8 == 0)
+ *   X           bf16 [M, K]    in   (16-byte aligned)
+ *   dW          float32 [N, K] out  (16-byte aligned)
+ *   accumulate  0: dW = dY^T X;  1: dW += dY^T X
+ * The token dimension is split across workgroups and reduced with float32
+ * atomic adds, so the last bits of dW depend on the summation order.
+ */
+tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
+                              int64_t M, int64_t N, int64_t K, float* dW,
+                              int32_t accumulate, tm_stream stream);
+
+/*
+ * tm_tgemv — decode-time product with packed weights (Sec. 8: batch-1
+ * decoding is bound by weight traffic), strided-batched over `count`
+ * same-shape matrices (e.g. the 48 in_proj layers):
+ *   y[c, b, n] = sum_k x[c, b, k] * q_c[n, k] * s16_c[n, k/g]
+ *
+ *   x           bf16 [count, B, K]       in   (16-byte aligned)
+ *   codes       uint8 [count, N, K/4]    in   (16-byte aligned)
+ *   scales_f16  uint16 [count, N, K/g]   in   float16 bits (2-byte aligned)
+ *   count       1 .. 65535;  B  1 .. 16
+ *   y           float32 [count, B, N]    out  (16-byte aligned)
+ * Products are exact and accumulated in float32; the float16 scale is applied
+ * in float32 per group.
+ */
+tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
+                   const uint16_t* scales_f16, int32_t count, int32_t B,
+                   int64_t N, int64_t K, int32_t g, float* y, tm_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TMAMBA_H */

@@ -1,0 +1,172 @@
+// C ABI of the ternary linear library: argument checks, then one launcher.
+// Every check runs on the host before any HIP call, so a rejected call
+// enqueues nothing (and can be exercised on a machine without a GPU).
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/tmamba.h"
+#include "launchers.hpp"
+
+namespace {
+
+struct Span {
+  uintptr_t lo = 0, hi = 0;  // [lo, hi)
+};
+
+bool bytes_of(int64_t a, int64_t b, int64_t elem, int64_t* out) {
+  int64_t t;
+  if (a < 0 || b < 0) return false;
+  if (__builtin_mul_overflow(a, b, &t)) return false;
+  if (__builtin_mul_overflow(t, elem, &t)) return false;
+  if (t > (int64_t(1) << 46)) return false;  // 64 TiB: far beyond any device
+  *out = t;
+  return true;
+}
+
+Span span(const void* p, int64_t bytes) {
+  Span s;
+  s.lo = reinterpret_cast<uintptr_t>(p);
+  s.hi = s.lo + static_cast<uintptr_t>(bytes);
+  return s;
+}
+
+bool overlap(Span a, Span b) {
+  if (a.lo == 0 || b.lo == 0 || a.hi == a.lo || b.hi == b.lo) return false;
+  return a.lo < b.hi && b.lo < a.hi;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool group_ok(int32_t g) { return g == 32 || g == 64 || g == 128 || g == 256 || g == 512; }
+
+tm_status shape_kg(int64_t K, int32_t g) {
+  if (!group_ok(g)) return TM_ESHAPE;
+  if (K < 1 || K % g != 0 || K % 64 != 0) return TM_ESHAPE;
+  return TM_OK;
+}
+
+tm_status hip_status(hipError_t e) { return e == hipSuccess ? TM_OK : TM_EHIP; }
+
+hipStream_t to_hip(tm_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+constexpr int64_t kMaxGridBlocks = (int64_t(1) << 31) - 1;
+
+}  // namespace
+
+extern "C" {
+
+int tm_abi_version(void) { return TM_ABI_VERSION; }
+
+const char* tm_status_str(tm_status s) {
+  switch (s) {
+    case TM_OK: return "TM_OK";
+    case TM_EINVAL: return "TM_EINVAL: null pointer, overlapping arrays or bad scalar argument";
+    case TM_ESHAPE: return "TM_ESHAPE: unsupported sizes (size < 1, K % g, K % 64, g, B or count)";
+    case TM_EALIGN: return "TM_EALIGN: pointer below its required alignment";
+    case TM_EHIP: return "TM_EHIP: the HIP runtime rejected a launch";
+    case TM_ENOTIMPL: return "TM_ENOTIMPL: not implemented";
+  }
+  return "unknown tm_status";
+}
+
+tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g, float eps,
+                            uint8_t* codes, float* scales, uint16_t* scales_f16,
+                            uint64_t* zero_count, tm_stream stream) {
+  if (!W || !codes || !scales) return TM_EINVAL;
+  if (!std::isfinite(eps) || eps < 0.f) return TM_EINVAL;
+  if (N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t wb, cb, sb, hb;
+  if (!bytes_of(N, K, 4, &wb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
+      !bytes_of(N, K / g, 2, &hb))
+    return TM_ESHAPE;
+  if ((N * (K / 16) + 255) / 256 > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) ||
+      !aligned(scales_f16, 2) || !aligned(zero_count, 8))
+    return TM_EALIGN;
+  const Span in = span(W, wb), c = span(codes, cb), s = span(scales, sb),
+             h = span(scales_f16, scales_f16 ? hb : 0), z = span(zero_count, zero_count ? 8 : 0);
+  const Span outs[4] = {c, s, h, z};
+  for (int i = 0; i < 4; ++i) {
+    if (overlap(in, outs[i])) return TM_EINVAL;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return TM_EINVAL;
+  }
+  return hip_status(tmk::launch_ternarize_pack(W, N, K, g, eps, codes, scales, scales_f16,
+                                              zero_count, to_hip(stream)));
+}
+
+tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales, int64_t M,
+                       int64_t N, int64_t K, int32_t g, float* Y, tm_stream stream) {
+  if (!X || !codes || !scales || !Y) return TM_EINVAL;
+  if (M < 1 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t xb, cb, sb, yb;
+  if (!bytes_of(M, K, 2, &xb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
+      !bytes_of(M, N, 4, &yb))
+    return TM_ESHAPE;
+  if (((M + 255) / 256) * ((N + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(Y, 16))
+    return TM_EALIGN;
+  const Span y = span(Y, yb);
+  if (overlap(y, span(X, xb)) || overlap(y, span(codes, cb)) || overlap(y, span(scales, sb)))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, to_hip(stream)));
+}
+
+tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,
+                          int64_t M, int64_t N, int64_t K, int32_t g, float* dX,
+                          tm_stream stream) {
+  if (!dY || !codes || !scales || !dX) return TM_EINVAL;
+  if (M < 1 || N < 1 || N % 8 != 0) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t yb, cb, sb, xb;
+  if (!bytes_of(M, N, 2, &yb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
+      !bytes_of(M, K, 4, &xb))
+    return TM_ESHAPE;
+  if (((M + 255) / 256) * ((K + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(dY, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(dX, 16))
+    return TM_EALIGN;
+  const Span o = span(dX, xb);
+  if (overlap(o, span(dY, yb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales, sb)))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_tgemm_bwd_dx(dY, codes, scales, M, N, K, g, dX, to_hip(stream)));
+}
+
+tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,
+                              int64_t K, float* dW, int32_t accumulate, tm_stream stream) {
+  if (!dY || !X || !dW) return TM_EINVAL;
+  if (accumulate != 0 && accumulate != 1) return TM_EINVAL;
+  if (M < 1 || N < 1 || N % 8 != 0 || K < 1 || K % 64 != 0) return TM_ESHAPE;
+  int64_t yb, xb, wb;
+  if (!bytes_of(M, N, 2, &yb) || !bytes_of(M, K, 2, &xb) || !bytes_of(N, K, 4, &wb))
+    return TM_ESHAPE;
+  if (((N + 255) / 256) * ((K + 255) / 256) * ((M + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(dY, 16) || !aligned(X, 16) || !aligned(dW, 16)) return TM_EALIGN;
+  const Span o = span(dW, wb);
+  if (overlap(o, span(dY, yb)) || overlap(o, span(X, xb))) return TM_EINVAL;
+  return hip_status(tmk::launch_tgemm_bwd_dw(dY, X, M, N, K, dW, accumulate, to_hip(stream)));
+}
+
+tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
+                   int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
+                   tm_stream stream) {
+  if (!x || !codes || !scales_f16 || !y) return TM_EINVAL;
+  if (count < 1 || count > 65535 || B < 1 || B > 16 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t cbm, sbm, xb, cb, sb, yb, ybm;
+  if (!bytes_of(N, K / 4, 1, &cbm) || !bytes_of(N, K / g, 2, &sbm) ||
+      !bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of(count, cbm, 1, &cb) ||
+      !bytes_of(count, sbm, 1, &sb) || !bytes_of((int64_t)B, N, 4, &ybm) ||
+      !bytes_of(count, ybm, 1, &yb))
+    return TM_ESHAPE;
+  if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
+    return TM_EALIGN;
+  const Span o = span(y, yb);
+  if (overlap(o, span(x, xb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales_f16, sb)))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// Shared device helpers for the gfx950 ternary kernels.
+//
+// Code decode: the packed format keeps, in every 32-bit word of 16 codes,
+// element 2i at bits [2i, 2i+2) and element 2i+1 at bits [16+2i, 16+2i+2),
+// each as a 2-bit two's complement (00 -> 0, 01 -> +1, 11 -> -1).  Shifting
+// the word left by 14 - 2i puts the pair's two codes at bits 14-15 and 30-31;
+// masking with 0xC000C000 then leaves, in each 16-bit half, either 0x0000
+// (code 0), 0x4000 (bfloat16 +2.0, code +1) or 0xC000 (bfloat16 -2.0, code -1).
+// So one shift and one AND turn two codes into two exact bfloat16 operands
+// equal to 2*q; the factor 2 is removed in float32 after the contraction.
+// The unused pattern 10 decodes to 0x8000 (-0.0) and contributes nothing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tmk {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+constexpr uint32_t kPairMask = 0xC000C000u;
+
+// Pair i (elements 2i, 2i+1 of the word) as two bfloat16 values 2*q.
+template <int I>
+__device__ __forceinline__ uint32_t decode_pair(uint32_t w) {
+  static_assert(I >= 0 && I < 8, "pair index");
+  return (w << (14 - 2 * I)) & kPairMask;
+}
+
+// Eight codes (half H of a word: elements 8H .. 8H+7) as an MFMA operand of
+// eight bfloat16 values 2*q, in element order.
+template <int H>
+__device__ __forceinline__ bf16x8 decode_half(uint32_t w) {
+  u32x4 v;
+  v.x = decode_pair<4 * H + 0>(w);
+  v.y = decode_pair<4 * H + 1>(w);
+  v.z = decode_pair<4 * H + 2>(w);
+  v.w = decode_pair<4 * H + 3>(w);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Same with the half chosen at run time (h in {0, 1}).
+__device__ __forceinline__ bf16x8 decode_half_rt(uint32_t w, uint32_t h) {
+  const uint32_t ws = w << (8u - 8u * h);  // half h moved to the top byte pair
+  u32x4 v;
+  v.x = (ws << 6) & kPairMask;
+  v.y = (ws << 4) & kPairMask;
+  v.z = (ws << 2) & kPairMask;
+  v.w = ws & kPairMask;
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 16-byte global load / store through plain vector types.
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ void st16(void* p, u32x4 v) {
+  *reinterpret_cast<u32x4*>(p) = v;
+}
+
+// Remap a linear workgroup id so that consecutive ids run on the same XCD.
+// The dispatcher hands workgroup i to XCD i % 8; ids that share an XCD share
+// its L2, so tiles that reuse the same operand rows should be consecutive
+// after the remap.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t bid, uint32_t nblocks) {
+  constexpr uint32_t kXcd = 8;
+  const uint32_t per = nblocks / kXcd;   // full rounds
+  const uint32_t tail = nblocks % kXcd;  // XCDs that get one extra block
+  const uint32_t xcd = bid % kXcd;
+  const uint32_t local = bid / kXcd;
+  // XCD x owns ids [start(x), start(x) + per + (x < tail))
+  const uint32_t start = xcd * per + (xcd < tail ? xcd : tail);
+  return start + local;
+}
+
+}  // namespace tmk

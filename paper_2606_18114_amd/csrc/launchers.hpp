@@ -1,0 +1,23 @@
+// Host-side launchers implemented in the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace tmk {
+
+hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, float eps,
+                                 uint8_t* codes, float* scales, uint16_t* scales_f16,
+                                 uint64_t* zero_count, hipStream_t stream);
+hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
+                            int64_t M, int64_t N, int64_t K, int g, float* Y,
+                            hipStream_t stream);
+hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,
+                               int64_t M, int64_t N, int64_t K, int g, float* dX,
+                               hipStream_t stream);
+hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,
+                               int64_t K, float* dW, int accumulate, hipStream_t stream);
+hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
+                        int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
+
+}  // namespace tmk

@@ -1,0 +1,185 @@
+"""Thin ctypes binding of ``libtmamba.so`` (declared in ``include/tmamba.h``).
+
+Argument marshalling only: every function checks tensor dtypes, devices and
+contiguity, allocates missing outputs with torch (the library itself
+allocates nothing), and passes raw device pointers plus the current HIP
+stream to the C ABI.  All arithmetic runs in the library's HIP kernels.
+There is no fallback: if the library is missing, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtmamba.so")
+_lib = None
+
+TM_STATUS = {0: "TM_OK", 1: "TM_EINVAL", 2: "TM_ESHAPE", 3: "TM_EALIGN", 4: "TM_EHIP",
+             5: "TM_ENOTIMPL"}
+
+# exported symbol -> (restype, argtypes)
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+SIGNATURES = {
+    "tm_abi_version": (ctypes.c_int, []),
+    "tm_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+    "tm_ternarize_pack": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P]),
+    "tm_tgemm_fwd": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_tgemm_bwd_dx": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_tgemm_bwd_dw_ste": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _I32, _P]),
+    "tm_tgemv": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _I64, _I32, _P, _P]),
+}
+
+
+class TernaryError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        msg = lib().tm_status_str(status).decode() if status in TM_STATUS else "unknown"
+        super().__init__(f"{fn} failed: {msg}")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(
+                f"{_LIB_PATH} is missing: build it with `python -m paper_2606_18114_amd.build` "
+                "(or __graft_entry__.build()); there is no fallback implementation")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise TernaryError(fn, status)
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, name: str, dtypes, ndim: int) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU (got {t.device})")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims (got shape {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+_BF16 = (torch.bfloat16, torch.int16, torch.uint16)
+_U8 = (torch.uint8,)
+_F32 = (torch.float32,)
+_F16 = (torch.float16, torch.int16, torch.uint16)
+
+
+def ternarize_pack(W: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
+                   codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
+                   scales_f16: Optional[torch.Tensor] = None,
+                   zero_count: Optional[torch.Tensor] = None, want_f16: bool = True,
+                   want_zero_count: bool = True):
+    """W float32 [N, K] -> (codes uint8 [N, K/4], scales f32 [N, K/g],
+    scales_f16 float16 [N, K/g] or None, zero_count int64 [1] or None)."""
+    _need(W, "W", _F32, 2)
+    N, K = W.shape
+    dev = W.device
+    if codes is None:
+        codes = torch.empty((N, K // 4), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((N, max(K // g, 1)), dtype=torch.float32, device=dev)
+    if scales_f16 is None and want_f16:
+        scales_f16 = torch.empty((N, max(K // g, 1)), dtype=torch.float16, device=dev)
+    if zero_count is None and want_zero_count:
+        zero_count = torch.empty((1,), dtype=torch.int64, device=dev)
+    st = lib().tm_ternarize_pack(_ptr(W), N, K, g, eps, _ptr(codes), _ptr(scales),
+                                 _ptr(scales_f16), _ptr(zero_count), _stream())
+    _check("tm_ternarize_pack", st)
+    return codes, scales, scales_f16, zero_count
+
+
+def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
+              Y: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Y[M, N] = X . (q * s)^T in float32."""
+    _need(X, "X", _BF16, 2)
+    _need(codes, "codes", _U8, 2)
+    _need(scales, "scales", _F32, 2)
+    M, K = X.shape
+    N = codes.shape[0]
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    st = lib().tm_tgemm_fwd(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y), _stream())
+    _check("tm_tgemm_fwd", st)
+    return Y
+
+
+def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
+                 dX: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """dX[M, K] = dY . (q * s) in float32."""
+    _need(dY, "dY", _BF16, 2)
+    _need(codes, "codes", _U8, 2)
+    _need(scales, "scales", _F32, 2)
+    M, N = dY.shape
+    K = codes.shape[1] * 4
+    if dX is None:
+        dX = torch.empty((M, K), dtype=torch.float32, device=dY.device)
+    st = lib().tm_tgemm_bwd_dx(_ptr(dY), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(dX),
+                               _stream())
+    _check("tm_tgemm_bwd_dx", st)
+    return dX
+
+
+def tgemm_bwd_dw_ste(dY: torch.Tensor, X: torch.Tensor, dW: Optional[torch.Tensor] = None,
+                     accumulate: bool = False) -> torch.Tensor:
+    """dW[N, K] (+)= dY^T . X in float32 (identity straight-through estimator)."""
+    _need(dY, "dY", _BF16, 2)
+    _need(X, "X", _BF16, 2)
+    M, N = dY.shape
+    K = X.shape[1]
+    if dW is None:
+        if accumulate:
+            raise ValueError("accumulate=True needs an existing dW")
+        dW = torch.empty((N, K), dtype=torch.float32, device=dY.device)
+    st = lib().tm_tgemm_bwd_dw_ste(_ptr(dY), _ptr(X), M, N, K, _ptr(dW), int(accumulate),
+                                   _stream())
+    _check("tm_tgemm_bwd_dw_ste", st)
+    return dW
+
+
+def tgemv(x: torch.Tensor, codes: torch.Tensor, scales_f16: torch.Tensor, g: int = 128,
+          y: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """x bf16 [count, B, K], codes uint8 [count, N, K/4], scales_f16 [count, N, K/g]
+    -> y float32 [count, B, N]."""
+    _need(x, "x", _BF16, 3)
+    _need(codes, "codes", _U8, 3)
+    _need(scales_f16, "scales_f16", _F16, 3)
+    count, B, K = x.shape
+    N = codes.shape[1]
+    if y is None:
+        y = torch.empty((count, B, N), dtype=torch.float32, device=x.device)
+    st = lib().tm_tgemv(_ptr(x), _ptr(codes), _ptr(scales_f16), count, B, N, K, g, _ptr(y),
+                        _stream())
+    _check("tm_tgemv", st)
+    return y

@@ -1,0 +1,163 @@
+"""The C ABI on the host: the library loads, exports every declared symbol,
+and rejects bad arguments with the documented status codes before any HIP
+call.  No test here passes arguments that would reach a kernel launch."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_18114_amd import ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tmamba.h")
+
+OK, EINVAL, ESHAPE, EALIGN = 0, 1, 2, 3
+P = 0x7F0000000000  # a 4 KiB-aligned fake device address, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(ops.lib_path()):
+        from paper_2606_18114_amd import build
+        build.build(verbose=False)
+    return ops.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:tm_status|int|const char\*)\s+(tm_[a-z0-9_]+)\(",
+                                 text, re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) == 7
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in ops.SIGNATURES, n
+    assert L.tm_abi_version() == 1
+
+
+def test_status_strings(L):
+    for code, name in ops.TM_STATUS.items():
+        assert L.tm_status_str(code).decode().startswith(name)
+    assert L.tm_status_str(99).decode() == "unknown tm_status"
+
+
+def tp(L, W=P, N=8, K=128, g=128, eps=1e-5, codes=P + 2 ** 20, scales=P + 2 ** 21,
+       s16=0, zc=0):
+    return L.tm_ternarize_pack(W, N, K, g, eps, codes, scales, s16, zc, None)
+
+
+def test_ternarize_pack_validation(L):
+    assert tp(L, W=0) == EINVAL
+    assert tp(L, codes=0) == EINVAL
+    assert tp(L, scales=0) == EINVAL
+    assert tp(L, eps=-1.0) == EINVAL
+    assert tp(L, eps=float("nan")) == EINVAL
+    assert tp(L, eps=float("inf")) == EINVAL
+    assert tp(L, N=0) == ESHAPE
+    assert tp(L, K=0) == ESHAPE
+    assert tp(L, g=100) == ESHAPE
+    assert tp(L, g=16) == ESHAPE
+    assert tp(L, K=96, g=32) == ESHAPE          # K % 64
+    assert tp(L, K=192, g=128) == ESHAPE        # K % g
+    assert tp(L, N=2 ** 40, K=2 ** 20) == ESHAPE  # size overflow
+    assert tp(L, W=P + 4) == EALIGN
+    assert tp(L, codes=P + 2 ** 20 + 8) == EALIGN
+    assert tp(L, scales=P + 2 ** 21 + 2) == EALIGN
+    assert tp(L, s16=P + 2 ** 22 + 1) == EALIGN
+    assert tp(L, zc=P + 2 ** 23 + 4) == EALIGN
+    # outputs overlapping the input or each other
+    assert tp(L, codes=P + 64) == EINVAL
+    assert tp(L, scales=P + 2 ** 20 + 16) == EINVAL
+    assert tp(L, s16=P + 2 ** 21) == EINVAL
+    assert tp(L, zc=P + 2 ** 20) == EINVAL
+
+
+def fwd(L, X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):
+    return L.tm_tgemm_fwd(X, codes, scales, M, N, K, g, Y, None)
+
+
+def test_tgemm_fwd_validation(L):
+    for kw in ("X", "codes", "scales", "Y"):
+        assert fwd(L, **{kw: 0}) == EINVAL, kw
+    assert fwd(L, M=0) == ESHAPE
+    assert fwd(L, N=-1) == ESHAPE
+    assert fwd(L, K=544) == ESHAPE
+    assert fwd(L, g=48) == ESHAPE
+    assert fwd(L, K=256, g=512) == ESHAPE
+    assert fwd(L, X=P + 2) == EALIGN
+    assert fwd(L, codes=P + 2 ** 24 + 4) == EALIGN
+    assert fwd(L, scales=P + 2 ** 25 + 2) == EALIGN
+    assert fwd(L, Y=P + 2 ** 26 + 4) == EALIGN
+    assert fwd(L, Y=P + 4096) == EINVAL                 # Y overlaps X
+    assert fwd(L, Y=P + 2 ** 24 - 4096) == EINVAL       # Y overlaps codes
+
+
+def dx(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,
+       dX=P + 2 ** 26):
+    return L.tm_tgemm_bwd_dx(dY, codes, scales, M, N, K, g, dX, None)
+
+
+def test_tgemm_bwd_dx_validation(L):
+    for kw in ("dY", "codes", "scales", "dX"):
+        assert dx(L, **{kw: 0}) == EINVAL, kw
+    assert dx(L, N=250) == ESHAPE                        # dY rows not 16-byte multiples
+    assert dx(L, M=0) == ESHAPE
+    assert dx(L, K=100) == ESHAPE
+    assert dx(L, dY=P + 8) == EALIGN
+    assert dx(L, dX=P + 2 ** 26 + 8) == EALIGN
+    assert dx(L, dX=P) == EINVAL
+
+
+def dw(L, dY=P, X=P + 2 ** 24, M=16, N=256, K=512, dW=P + 2 ** 26, acc=0):
+    return L.tm_tgemm_bwd_dw_ste(dY, X, M, N, K, dW, acc, None)
+
+
+def test_tgemm_bwd_dw_validation(L):
+    for kw in ("dY", "X", "dW"):
+        assert dw(L, **{kw: 0}) == EINVAL, kw
+    assert dw(L, acc=2) == EINVAL
+    assert dw(L, M=0) == ESHAPE
+    assert dw(L, N=12) == ESHAPE
+    assert dw(L, K=96) == ESHAPE
+    assert dw(L, X=P + 2 ** 24 + 2) == EALIGN
+    assert dw(L, dW=P + 2 ** 24) == EINVAL
+
+
+def gv(L, x=P, codes=P + 2 ** 24, s16=P + 2 ** 25, count=2, B=1, N=256, K=512, g=128,
+       y=P + 2 ** 26):
+    return L.tm_tgemv(x, codes, s16, count, B, N, K, g, y, None)
+
+
+def test_tgemv_validation(L):
+    for kw in ("x", "codes", "s16", "y"):
+        assert gv(L, **{kw: 0}) == EINVAL, kw
+    assert gv(L, count=0) == ESHAPE
+    assert gv(L, count=65536) == ESHAPE
+    assert gv(L, B=0) == ESHAPE
+    assert gv(L, B=17) == ESHAPE
+    assert gv(L, K=544, g=32) == ESHAPE
+    assert gv(L, s16=P + 2 ** 25 + 1) == EALIGN
+    assert gv(L, y=P + 2 ** 26 + 4) == EALIGN
+    assert gv(L, y=P + 2 ** 24 + 256) == EINVAL          # y overlaps the codes
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(ops, "_lib", None)
+    monkeypatch.setattr(ops, "_LIB_PATH", str(tmp_path / "libtmamba.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        ops.lib()
+
+
+def test_product_path_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2606_18114_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle", text, re.M), f
+                assert "oracle/" not in text, f

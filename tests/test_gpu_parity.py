@@ -1,0 +1,337 @@
+"""GPU parity: every entry point of libtmamba.so against the CPU oracle.
+
+Bars:
+* codes bit-exact except on elements the oracle flags as within 1e-6
+  (relative) of the +-0.5 rounding boundary; those are counted and reported;
+* zero count equal to the number of zeros in the GPU's own codes, and within
+  the number of boundary elements of the oracle's count;
+* scales within 1e-6 relative (in practice bit-exact), float16 scales within
+  one float16 ulp of the oracle's rounding;
+* GEMM / GEMV outputs within 2e-3 relative Frobenius error of the float64
+  reference computed from the GPU's own codes and scales.  The design bound is
+  tighter (products are exact, accumulation is float32, dX carries 16 bits of
+  the scale), so the tests also hold each output to 1e-4.
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import ternary as O  # noqa: E402
+from paper_2606_18114_amd import synth  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+REL_BAR = 2e-3      # the contract
+REL_DESIGN = 1e-4   # what the exact-product kernels are held to
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_18114_amd import ops
+    ops.lib()  # raises if the library is missing: no fallback
+    return ops
+
+
+def _ops():
+    from paper_2606_18114_amd import ops
+    return ops
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits, np.uint16).view(np.int16)).cuda().view(
+        torch.bfloat16)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def host_codes(codes_t, K):
+    return O.unpack(host(codes_t), K)
+
+
+def check_ternarize(W, g, eps, label):
+    ops = _ops()
+    print(f"[ternarize] {label} N={W.shape[0]} K={W.shape[1]} g={g} eps={eps}", flush=True)
+    c, s, s16, z = ops.ternarize_pack(dev_f32(W), g, eps)
+    N, K = W.shape
+    q_gpu = host_codes(c, K)
+    s_gpu = host(s)
+    s16_gpu = host(s16)
+    z_gpu = int(host(z)[0])
+    s64 = O.group_scales_f64(W, g)
+    s32 = s64.astype(np.float32)
+    # scales: 1e-6 relative (and zero exactly where the oracle is zero)
+    assert np.all((s_gpu == 0) == (s32 == 0))
+    rel = np.abs(s_gpu.astype(np.float64) - s64) / np.maximum(s64, 1e-300)
+    assert rel.max() <= 1e-6, rel.max()
+    # codes: decided in float32 from the GPU's float32 scale
+    q_ref = O.ternary_codes(W, s_gpu, g, eps)
+    band = O.boundary_mask(W, s64, g, eps)
+    diff = q_gpu != q_ref
+    assert not np.any(diff & ~band), f"{int((diff & ~band).sum())} codes differ off the boundary"
+    # zero count: exact on the GPU's own codes, and close to the oracle's
+    assert z_gpu == O.zero_count(q_gpu)
+    _, _, q_orc, z_orc = O.ternarize(W, g, eps)
+    assert abs(z_gpu - z_orc) <= int(band.sum())
+    # float16 scales: RNE of the float32 scale
+    ref16 = O.scales_f16(s_gpu)
+    assert np.array_equal(s16_gpu.view(np.uint16), ref16.view(np.uint16))
+    print(f"  boundary elements {int(band.sum())}, code mismatches there {int(diff.sum())}, "
+          f"scale max rel err {rel.max():.2e}, zero ratio {z_gpu / W.size:.4f}", flush=True)
+    return c, s, s16, q_gpu, s_gpu
+
+
+# --------------------------------------------------------------------------
+# ternarize_pack
+# --------------------------------------------------------------------------
+
+def test_ternarize_single_linear():
+    W, _ = synth.single_linear_inputs(synth.C1)
+    check_ternarize(W, 128, 1e-5, "single linear 256x512")
+
+
+@pytest.mark.parametrize("g", synth.C5_GROUPS)
+def test_ternarize_group_sizes_ragged_rows(g):
+    W = synth.weights(np.random.default_rng(g), 301, 1024, outliers=True)
+    check_ternarize(W, g, 1e-5, "301x1024 outliers")
+
+
+def test_ternarize_in_proj_full():
+    W = synth.layer_weight(synth.C3, synth.SEED_W)
+    check_ternarize(W, 128, 1e-5, "in_proj 8512x2048 outliers")
+
+
+def test_ternarize_edge_cases():
+    g = 32
+    W = np.zeros((6, 128), np.float32)
+    W[1, :g] = 0.03                                       # constant group
+    W[2, 5] = -0.7                                        # single nonzero
+    W[3, :] = np.float32(2.0 ** -140)                     # subnormal weights
+    W[4, :] = -0.0                                        # negative zeros
+    W[5, :4] = [1.5, -0.5, 0.25, -1.75]                   # exact ties at eps=0
+    W[5, 4:g] = 0.0
+    for eps in (0.0, 1e-5):
+        c, s, s16, q, sg = check_ternarize(W, g, eps, f"edge cases eps={eps}")
+        assert not q[0].any() and sg[0].tolist() == [0, 0, 0, 0]
+        assert np.all(q[1, :g] == 1) and q[2, 5] == -1 and np.count_nonzero(q[2]) == 1
+        assert not q[4].any()
+    # at eps = 0 the tie W = -0.5 (s = 1) must round to 0, W = 1.5 to +1
+    _, _, _, q, _ = check_ternarize(W, g, 0.0, "ties")
+    assert q[5, :4].tolist() == [1, 0, 0, -1]
+
+
+def test_ternarize_deterministic():
+    ops = _ops()
+    W = dev_f32(synth.weights(np.random.default_rng(5), 1000, 2048, outliers=True))
+    a = [host(t) for t in ops.ternarize_pack(W, 128, 1e-5)]
+    b = [host(t) for t in ops.ternarize_pack(W, 128, 1e-5)]
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+# --------------------------------------------------------------------------
+# forward GEMM
+# --------------------------------------------------------------------------
+
+def gemm_case(M, N, K, g, seed, outliers=True, label=""):
+    ops = _ops()
+    print(f"[fwd] {label} M={M} N={N} K={K} g={g} seed={seed}", flush=True)
+    rng = np.random.default_rng(seed)
+    W = synth.weights(rng, N, K, outliers)
+    X = synth.activations(rng, M, K)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5, want_f16=False, want_zero_count=False)
+    Y = ops.tgemm_fwd(dev_bf16(X), c, s, g)
+    q, sg = host_codes(c, K), host(s)
+    return X, q, sg, host(Y)
+
+
+@pytest.mark.parametrize("g", synth.C5_GROUPS)
+def test_fwd_ragged_tiles(g):
+    # M and N not multiples of the 256 x 256 tile, several K chunks
+    X, q, s, Y = gemm_case(300, 520, 1024, g, seed=g, label="ragged")
+    ref = O.gemm_fwd(X, q, s, g)
+    err = O.rel_fro_error(Y, ref)
+    print(f"  rel fro err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN <= REL_BAR
+
+
+def test_fwd_single_linear():
+    ops = _ops()
+    W, X = synth.single_linear_inputs(synth.C1)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), 128, 1e-5)
+    Y = host(ops.tgemm_fwd(dev_bf16(X), c, s, 128))
+    q, sg = host_codes(c, 512), host(s)
+    err = O.rel_fro_error(Y, O.gemm_fwd(X, q, sg, 128))
+    # end to end against the oracle's own codes as well
+    _, s32, q_o, _ = O.ternarize(W, 128, 1e-5)
+    err2 = O.rel_fro_error(Y, O.gemm_fwd(X, q_o, s32, 128))
+    print(f"[fwd] single linear rel err {err:.3e} (oracle codes {err2:.3e})", flush=True)
+    assert err <= REL_DESIGN and err2 <= REL_BAR
+
+
+def test_fwd_out_proj_full():
+    ops = _ops()
+    cfg = synth.C2
+    W = synth.layer_weight(cfg, synth.SEED_W)
+    X = synth.layer_acts(cfg.M, cfg.K, synth.SEED_X)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), 128, 1e-5)
+    Y = host(ops.tgemm_fwd(dev_bf16(X), c, s, 128))
+    err = O.rel_fro_error(Y, O.gemm_fwd(X, host_codes(c, cfg.K), host(s), 128))
+    print(f"[fwd] out_proj 4096x4096->2048 rel err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
+def test_fwd_in_proj_full_sampled_rows():
+    ops = _ops()
+    cfg = synth.C3
+    W = synth.layer_weight(cfg, synth.SEED_W)
+    X = synth.layer_acts(cfg.M, cfg.K, synth.SEED_X)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), 128, 1e-5)
+    Y = ops.tgemm_fwd(dev_bf16(X), c, s, 128)
+    rows = np.sort(np.random.default_rng(9).choice(cfg.M, 256, replace=False))
+    Ys = host(Y[torch.from_numpy(rows).cuda()])
+    err = O.rel_fro_error(Ys, O.gemm_fwd(X[rows], host_codes(c, cfg.K), host(s), 128))
+    print(f"[fwd] in_proj 16384x2048->8512, 256 sampled rows, rel err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
+def test_fwd_exact_cases():
+    """Selections and small integers are exact: one-hot tokens pick columns of
+    What, integer tokens with power-of-two scales give exact integer sums."""
+    ops = _ops()
+    N, K, g = 96, 256, 64
+    rng = np.random.default_rng(3)
+    q = rng.integers(-1, 2, (N, K)).astype(np.int8)
+    sc = (2.0 ** rng.integers(-3, 3, (N, K // g))).astype(np.float32)
+    sc[5, 1] = 0.0                                     # a zero-scale group
+    c = torch.from_numpy(O.pack(q)).cuda()
+    s = dev_f32(sc)
+    eye = np.zeros((K, K), np.float32)
+    eye[np.arange(K), np.arange(K)] = 1
+    Y = host(ops.tgemm_fwd(dev_bf16(synth.f32_to_bf16_bits(eye)), c, s, g))
+    np.testing.assert_array_equal(Y, O.dequantize(q, sc, g).T)
+    Xi = rng.integers(-8, 9, (40, K)).astype(np.float32)
+    Y = host(ops.tgemm_fwd(dev_bf16(synth.f32_to_bf16_bits(Xi)), c, s, g))
+    np.testing.assert_array_equal(Y, O.gemm_fwd(Xi, q, sc, g))
+
+
+# --------------------------------------------------------------------------
+# backward
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("g", [32, 128, 512])
+def test_bwd_dx_ragged(g):
+    ops = _ops()
+    M, N, K = 300, 520, 1024
+    print(f"[dx] ragged M={M} N={N} K={K} g={g}", flush=True)
+    rng = np.random.default_rng(40 + g)
+    W = synth.weights(rng, N, K, True)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5)
+    dX = host(ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g))
+    err = O.rel_fro_error(dX, O.gemm_bwd_dx(dY, host_codes(c, K), host(s), g))
+    print(f"  rel fro err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
+def test_bwd_dx_in_proj_sampled_rows():
+    ops = _ops()
+    cfg = synth.C3
+    W = synth.layer_weight(cfg, synth.SEED_W)
+    dY = synth.layer_acts(cfg.M, cfg.N, synth.SEED_DY, std=synth.DY_STD)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), 128, 1e-5)
+    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, 128)
+    rows = np.sort(np.random.default_rng(10).choice(cfg.M, 256, replace=False))
+    got = host(dX[torch.from_numpy(rows).cuda()])
+    err = O.rel_fro_error(got, O.gemm_bwd_dx(dY[rows], host_codes(c, cfg.K), host(s), 128))
+    print(f"[dx] in_proj dY 16384x8512, 256 sampled rows, rel err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
+def test_bwd_dw_ragged_and_accumulate():
+    ops = _ops()
+    M, N, K = 700, 264, 320
+    print(f"[dw] ragged M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(77)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    X = synth.activations(rng, M, K)
+    dW = ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X))
+    ref = O.gemm_bwd_dw(dY, X)
+    err = O.rel_fro_error(host(dW), ref)
+    ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X), dW=dW, accumulate=True)
+    err2 = O.rel_fro_error(host(dW), 2 * ref)
+    print(f"  rel fro err {err:.3e}, accumulated {err2:.3e}", flush=True)
+    assert err <= REL_DESIGN and err2 <= REL_DESIGN
+
+
+def test_bwd_dw_one_hot_tokens():
+    """One-hot token rows make dW rows copies of dY columns (exact)."""
+    ops = _ops()
+    M, N, K = 64, 128, 64
+    eye = np.zeros((M, K), np.float32)
+    eye[np.arange(M), np.arange(M) % K] = 1
+    dY = synth.activations(np.random.default_rng(8), M, N)
+    dW = host(ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(synth.f32_to_bf16_bits(eye))))
+    np.testing.assert_array_equal(dW, synth.bf16_bits_to_f32(dY).T)
+
+
+def test_bwd_dw_in_proj_sampled_rows():
+    ops = _ops()
+    cfg = synth.C3
+    X = synth.layer_acts(cfg.M, cfg.K, synth.SEED_X)
+    dY = synth.layer_acts(cfg.M, cfg.N, synth.SEED_DY, std=synth.DY_STD)
+    dW = ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X))
+    rows = np.sort(np.random.default_rng(11).choice(cfg.N, 128, replace=False))
+    got = host(dW[torch.from_numpy(rows).cuda()])
+    err = O.rel_fro_error(got, O.gemm_bwd_dw(dY[:, rows], X))
+    print(f"[dw] in_proj 16384 tokens, 128 sampled rows of dW, rel err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
+# --------------------------------------------------------------------------
+# decode GEMV
+# --------------------------------------------------------------------------
+
+def gemv_case(count, B, N, K, g, seed, outliers):
+    ops = _ops()
+    print(f"[gemv] count={count} B={B} N={N} K={K} g={g}", flush=True)
+    rng = np.random.default_rng(seed)
+    codes, s16s, qs, s16h = [], [], [], []
+    for _ in range(count):
+        W = synth.weights(rng, N, K, outliers)
+        c, s, s16, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5)
+        codes.append(c)
+        s16s.append(s16)
+        qs.append(host_codes(c, K))
+        s16h.append(host(s16))
+    x = synth.activations(rng, count * B, K).reshape(count, B, K)
+    y = host(ops.tgemv(dev_bf16(x), torch.stack(codes), torch.stack(s16s), g))
+    errs = [O.rel_fro_error(y[i], O.gemv(x[i], qs[i], s16h[i], g)) for i in range(count)]
+    print(f"  max rel fro err {max(errs):.3e}", flush=True)
+    assert max(errs) <= REL_DESIGN
+
+
+@pytest.mark.parametrize("g", synth.C5_GROUPS)
+@pytest.mark.parametrize("B", [1, 4])
+def test_gemv_ragged(g, B):
+    gemv_case(3, B, 200, 1536, g, seed=g + B, outliers=True)
+
+
+def test_gemv_batch16_small_k():
+    gemv_case(2, 16, 70, 512, 128, seed=1, outliers=False)
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_gemv_decode_shapes(B):
+    gemv_case(2, B, synth.IN_PROJ_N, synth.D_MODEL, 128, seed=1000 + B, outliers=True)
+    gemv_case(2, B, synth.D_MODEL, synth.D_INNER, 128, seed=2000 + B, outliers=False)
