@@ -251,34 +251,55 @@ def main():
 
     # ---------------- CPU oracle baseline (bounded sample) ----------------
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(W_h, X_h, g, eps)
+        out["cpu_baseline"] = cpu_baseline(W_h, X_h, dY_h, g, eps, dec)
 
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(W_h, X_h, g, eps):
+def cpu_baseline(W_h, X_h, dY_h, g, eps, dec):
     """The oracle as it stands, timed on the host on a bounded sample of the
-    same in_proj workload: ternarize the full 8512 x 2048 weight, then the
-    float64 forward GEMM for 2048 of the 16384 token rows."""
+    same workload: the whole in_proj QAT step at full size (ternarize, float64
+    forward, dX and dW GEMMs) and the batch-1 decode GEMV of 4 in_proj and 4
+    out_proj layers.  `value` is the oracle's forward-GEMM TFLOP/s."""
     from oracle import ternary as O
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
-    rows = 2048
+    N, K = W_h.shape
+    M = X_h.shape[0]
+    t = {}
     t0 = time.perf_counter()
     _, s32, q, _ = O.ternarize(W_h, g, eps)
-    t1 = time.perf_counter()
-    O.gemm_fwd(X_h[:rows], q, s32, g)
-    t2 = time.perf_counter()
-    N, K = W_h.shape
-    tflops = 2.0 * rows * N * K / (t2 - t1) / 1e12
-    return {"value": round(tflops, 4), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"float64 forward GEMM on {rows} of 16384 in_proj token rows "
-                      f"({2.0 * rows * N * K / 1e9:.1f} GFLOP, {t2 - t1:.2f}s); "
-                      f"ternarize of the 8512x2048 weight took {t1 - t0:.2f}s "
-                      f"({N * K * 4 / (t1 - t0) / 1e9:.3f} GB/s)"}
+    t["ternarize"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.gemm_fwd(X_h, q, s32, g)
+    t["fwd"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.gemm_bwd_dx(dY_h, q, s32, g)
+    t["dx"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.gemm_bwd_dw(dY_h, X_h)
+    t["dw"] = time.perf_counter() - t0
+    gemv_bytes, t0 = 0.0, time.perf_counter()
+    for kind in ("in", "out"):
+        d = dec[kind]
+        c = d["cfg"]
+        for layer in range(4):
+            ql = O.unpack(d["codes"][layer].cpu().numpy(), c.K)
+            xl = d["x"][layer].cpu().view(dtype=__import__("torch").int16).numpy().view(np.uint16)
+            O.gemv(xl, ql, d["s16"][layer].cpu().numpy(), c.g)
+            gemv_bytes += c.N * c.K / 4 + 2 * c.N * c.K / c.g
+    t["gemv8"] = time.perf_counter() - t0
+    fl = 2.0 * M * N * K
+    return {"value": round(fl / t["fwd"] / 1e12, 4), "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"full in_proj QAT step on the host: ternarize {t['ternarize']:.2f}s "
+                       f"({N * K * 4 / t['ternarize'] / 1e9:.2f} GB/s), float64 fwd {t['fwd']:.2f}s, "
+                       f"dX {t['dx']:.2f}s, dW {t['dw']:.2f}s ({fl / 1e9:.0f} GFLOP each); "
+                       f"decode GEMV of 8 of the 96 layers {t['gemv8']:.2f}s "
+                       f"({gemv_bytes / t['gemv8'] / 1e9:.3f} GB/s of packed weights)")}
 
 
 if __name__ == "__main__":

@@ -118,8 +118,8 @@ def test_ternarize_edge_cases():
     W[2, 5] = -0.7                                        # single nonzero
     W[3, :] = np.float32(2.0 ** -140)                     # subnormal weights
     W[4, :] = -0.0                                        # negative zeros
-    W[5, :4] = [1.5, -0.5, 0.25, -1.75]                   # exact ties at eps=0
-    W[5, 4:g] = 0.0
+    W[5, :4] = [1.5, -0.5, 0.25, -1.75]                   # exact ties at eps=0:
+    W[5, 4:g] = np.where(np.arange(4, g) % 2, 1.0, -1.0)  # sum |w| = 32, s = 1
     for eps in (0.0, 1e-5):
         c, s, s16, q, sg = check_ternarize(W, g, eps, f"edge cases eps={eps}")
         assert not q[0].any() and sg[0].tolist() == [0, 0, 0, 0]
