@@ -1,11 +1,13 @@
 // Grouped-absmean ternarizer (paper Sec. 3.1) with 2-bit packing (Sec. 8)
 // and the zero-code count (Sec. 3.1, Table 1), in one pass over W.
 //
-// One thread owns 16 consecutive weights of a row, i.e. one packed word.
-// The g/16 threads of a group are adjacent lanes of one wave, so the group's
-// sum of |w| is a float64 butterfly over those lanes.  With the sum in
-// float64 the mean rounds once to float32, which is what the float64 oracle
-// produces as well.
+// A wave reads 1024 consecutive weights per iteration as four fully
+// coalesced 1 KiB loads; each lane holds 4 weights of a load, so a group of g
+// weights sits on g/4 adjacent lanes (two loads for g = 512) and its sum of
+// |w| is a float64 butterfly over those lanes.  With the sum in float64 the
+// mean rounds once to float32, which is what the float64 oracle produces.
+// Four adjacent lanes OR their codes into one packed 32-bit word.  The grid
+// is persistent and each workgroup adds its zero count to the output once.
 //
 // Code decision, identical to the float32 expression
 //   q = round_half_even(clip(fl32(w / fl32(s + eps)), -1, 1)):
@@ -21,78 +23,100 @@ namespace tmk {
 
 __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 
-template <int G>
-__global__ __launch_bounds__(256) void ternarize_pack_kernel(
-    const float* __restrict__ W, int64_t n_words, float eps,
-    uint32_t* __restrict__ codes, float* __restrict__ scales,
-    uint16_t* __restrict__ scales_f16, unsigned long long* __restrict__ zero_count) {
-  constexpr int kLanesPerGroup = G / 16;
-  const int64_t word = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const bool live = word < n_words;
+constexpr int kTernUnit = 1024;  // weights per wave iteration (4 loads x 64 lanes x 4)
+constexpr int kTernWaves = 16;   // waves per workgroup
 
-  float w[16];
-  if (live) {
-    const float* src = W + word * 16;
+template <int G>
+__global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
+    const float* __restrict__ W, int64_t total, float eps, uint32_t* __restrict__ codes,
+    float* __restrict__ scales, uint16_t* __restrict__ scales_f16,
+    unsigned long long* __restrict__ zero_count) {
+  constexpr int L = G / 4 < 64 ? G / 4 : 64;  // lanes holding one group within a load
+  __shared__ uint32_t wave_zeros[kTernWaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t nunits = (total + kTernUnit - 1) / kTernUnit;
+  uint32_t zeros = 0;
+
+  for (int64_t u = (int64_t)blockIdx.x * kTernWaves + wave; u < nunits;
+       u += (int64_t)gridDim.x * kTernWaves) {
+    const int64_t base = u * kTernUnit;
+    // load i covers weights [base + 256 i, base + 256 i + 256); lane l holds 4 of them
+    float w[4][4];
+    bool ok[4];
+    double ps[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
+      const int64_t off = base + 256 * i + 4 * lane;
+      ok[i] = off < total;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (ok[i]) v = ld16(W + off);
       // __uint_as_float, not __builtin_bit_cast: this compiler reads every
       // element of a vector as its first one when bit-casting v.y, v.z, v.w
-      const u32x4 v = ld16(src + 4 * i);
-      w[4 * i + 0] = __uint_as_float(v.x);
-      w[4 * i + 1] = __uint_as_float(v.y);
-      w[4 * i + 2] = __uint_as_float(v.z);
-      w[4 * i + 3] = __uint_as_float(v.w);
+      w[i][0] = __uint_as_float(v.x);
+      w[i][1] = __uint_as_float(v.y);
+      w[i][2] = __uint_as_float(v.z);
+      w[i][3] = __uint_as_float(v.w);
+      ps[i] = ((double)fabsf(w[i][0]) + (double)fabsf(w[i][1])) +
+              ((double)fabsf(w[i][2]) + (double)fabsf(w[i][3]));
     }
-  } else {
+    // group sums: butterfly over the L lanes of each group (float64, exact)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) w[i] = 0.0f;
-  }
-
-  double sum = 0.0;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-  for (int i = 0; i < 16; ++i) sum += (double)fabsf(w[i]);
-#pragma unroll
-  for (int off = 1; off < kLanesPerGroup; off <<= 1) sum += __shfl_xor(sum, off, 64);
-
-  const float s = (float)(sum / (double)G);
-  const float d = s + eps;
-  const double thr = (double)d * (0.5 + 0x1p-25);
-
-  uint32_t packed = 0;
-  int zeros = 0;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const uint32_t bits = __float_as_uint(w[e]);
-    const bool nz = (double)fabsf(w[e]) > thr;
-    const uint32_t code = nz ? ((bits >> 31) ? 3u : 1u) : 0u;
-    packed |= code << (2 * (e / 2) + 16 * (e % 2));
-    zeros += nz ? 0 : 1;
-  }
-
-  if (live) {
-    codes[word] = packed;
-    if ((word % kLanesPerGroup) == 0) {
-      const int64_t grp = word / kLanesPerGroup;
-      scales[grp] = s;
-      if (scales_f16) scales_f16[grp] = __builtin_bit_cast(uint16_t, (_Float16)s);
+      for (int o = 1; o < L; o <<= 1) ps[i] += __shfl_xor(ps[i], o, 64);
+    if constexpr (G == 512) {  // a group spans two loads
+      ps[0] += ps[1];
+      ps[1] = ps[0];
+      ps[2] += ps[3];
+      ps[3] = ps[2];
     }
-  } else {
-    zeros = 0;
+
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float sc = (float)(ps[i] / (double)G);
+      const float d = sc + eps;
+      const double thr = (double)d * (0.5 + 0x1p-25);
+      uint32_t part = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = 4 * (lane & 3) + j;  // element within its 16-weight word
+        const bool nz = (double)fabsf(w[i][j]) > thr;
+        const uint32_t code = nz ? ((__float_as_uint(w[i][j]) >> 31) ? 3u : 1u) : 0u;
+        part |= code << (2 * (e / 2) + 16 * (e % 2));
+        zeros += (nz || !ok[i]) ? 0u : 1u;
+      }
+      part |= __shfl_xor(part, 1, 64);
+      part |= __shfl_xor(part, 2, 64);
+      const int64_t off = base + 256 * i + 4 * lane;
+      if (ok[i] && (lane & 3) == 0) codes[off / 16] = part;
+      if (ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) {
+        const int64_t grp = off / G;
+        scales[grp] = sc;
+        if (scales_f16) scales_f16[grp] = __builtin_bit_cast(uint16_t, (_Float16)sc);
+      }
+    }
   }
 
   if (zero_count) {
-    // wave-wide sum, one 64-bit atomic per wave
-    int z = zeros;
+    uint32_t z = zeros;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) z += __shfl_xor(z, off, 64);
-    if ((threadIdx.x & 63) == 0 && z) atomicAdd(zero_count, (unsigned long long)z);
+    for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, 64);
+    if (lane == 0) wave_zeros[wave] = z;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long t = 0;
+#pragma unroll
+      for (int i = 0; i < kTernWaves; ++i) t += wave_zeros[i];
+      if (t) atomicAdd(zero_count, t);
+    }
   }
 }
 
 hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, float eps,
                                  uint8_t* codes, float* scales, uint16_t* scales_f16,
                                  uint64_t* zero_count, hipStream_t stream) {
-  const int64_t n_words = N * (K / 16);
+  const int64_t total = N * K;
   auto* zc = reinterpret_cast<unsigned long long*>(zero_count);
   if (zc) {
     // a fill kernel rather than a memset node, so the call can be captured
@@ -100,14 +124,17 @@ hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, fl
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const dim3 grid((unsigned)((n_words + 255) / 256)), block(256);
+  // a persistent grid: at most 512 workgroups, each adding its zero count once
+  int64_t blocks = (total / kTernUnit + kTernWaves) / kTernWaves;
+  if (blocks > 512) blocks = 512;
+  const dim3 grid((unsigned)blocks), block(64 * kTernWaves);
   auto* cw = reinterpret_cast<uint32_t*>(codes);
   switch (g) {
-    case 32:  hipLaunchKernelGGL(ternarize_pack_kernel<32>, grid, block, 0, stream, W, n_words, eps, cw, scales, scales_f16, zc); break;
-    case 64:  hipLaunchKernelGGL(ternarize_pack_kernel<64>, grid, block, 0, stream, W, n_words, eps, cw, scales, scales_f16, zc); break;
-    case 128: hipLaunchKernelGGL(ternarize_pack_kernel<128>, grid, block, 0, stream, W, n_words, eps, cw, scales, scales_f16, zc); break;
-    case 256: hipLaunchKernelGGL(ternarize_pack_kernel<256>, grid, block, 0, stream, W, n_words, eps, cw, scales, scales_f16, zc); break;
-    case 512: hipLaunchKernelGGL(ternarize_pack_kernel<512>, grid, block, 0, stream, W, n_words, eps, cw, scales, scales_f16, zc); break;
+    case 32:  hipLaunchKernelGGL(ternarize_pack_kernel<32>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
+    case 64:  hipLaunchKernelGGL(ternarize_pack_kernel<64>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
+    case 128: hipLaunchKernelGGL(ternarize_pack_kernel<128>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
+    case 256: hipLaunchKernelGGL(ternarize_pack_kernel<256>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
+    case 512: hipLaunchKernelGGL(ternarize_pack_kernel<512>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -81,6 +81,25 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   float cref[2] = {0.f, 0.f};
   uint32_t msk[2] = {0u, 0u};
 
+  // Group scales run one stage ahead: the scales used by the boundaries of
+  // stage kc are loaded at the start of stage kc - 1, before that stage's
+  // operand prefetch, so waiting for them never waits for the prefetch.  A
+  // 64-column stage holds at most two group starts (g = 32).  Every load in
+  // the loop is unconditional (the last stage reloads itself) so the
+  // compiler can count outstanding loads exactly.
+  constexpr int kStarts = G == 32 ? 2 : 1;
+  float snext[kStarts][2], scur[kStarts][2];
+  auto load_scales = [&](int kc_) {
+#pragma unroll
+    for (int q = 0; q < kStarts; ++q) {
+      int64_t j = ((int64_t)kc_ * kFwdBK + 32 * q) / G;
+      j = j < ng ? j : ng - 1;
+#pragma unroll
+      for (int b = 0; b < 2; ++b) snext[q][b] = srow[b][j];
+    }
+  };
+  load_scales(0);
+
   // prologue: stage chunk 0
   u32x4 xv[4], cv[2], cvn[2];
 #pragma unroll
@@ -93,9 +112,14 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
 
   for (int kc = 0; kc < nchunks; ++kc) {
     const int buf = kc & 1;
-    const bool more = kc + 1 < nchunks;
-    if (more) {
-      const int64_t ko = (int64_t)(kc + 1) * kFwdBK;
+    const int kn = kc + 1 < nchunks ? kc + 1 : kc;
+#pragma unroll
+    for (int q = 0; q < kStarts; ++q)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) scur[q][b] = snext[q][b];
+    load_scales(kn);
+    {
+      const int64_t ko = (int64_t)kn * kFwdBK;
 #pragma unroll
       for (int i = 0; i < 4; ++i) xv[i] = ld16(xsrc[i] + ko);
 #pragma unroll
@@ -107,13 +131,13 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       const int64_t kcol = (int64_t)kc * kFwdBK + 16 * t;
       const bool boundary = (t == 0 && (kcol % G) == 0) || (G == 32 && t == 2);
       if (boundary) {
-        const int64_t j = kcol / G;
+        const int q = (G == 32 && t == 2) ? kStarts - 1 : 0;
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
-          const float s = srow[b][j];
-          msk[b] = s != 0.f ? 0xFFFFFFFFu : 0u;
-          const float r = (s != 0.f && cref[b] != 0.f) ? cref[b] / s : 1.f;
-          cref[b] = s != 0.f ? s : cref[b];
+          const float sv = scur[q][b];
+          msk[b] = sv != 0.f ? 0xFFFFFFFFu : 0u;
+          const float r = (sv != 0.f && cref[b] != 0.f) ? cref[b] / sv : 1.f;
+          cref[b] = sv != 0.f ? sv : cref[b];
 #pragma unroll
           for (int a = 0; a < 4; ++a) acc[a][b] *= r;
         }
@@ -133,12 +157,10 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       }
     }
 
-    if (more) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st16(&xs[buf ^ 1][xrow[i]][xcol[i]], xv[i]);
+    for (int i = 0; i < 4; ++i) st16(&xs[buf ^ 1][xrow[i]][xcol[i]], xv[i]);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) cv[b] = cvn[b];
-    }
+    for (int b = 0; b < 2; ++b) cv[b] = cvn[b];
     __syncthreads();
   }
 

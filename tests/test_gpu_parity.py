@@ -331,6 +331,12 @@ def test_gemv_batch16_small_k():
     gemv_case(2, 16, 70, 512, 128, seed=1, outliers=False)
 
 
+@pytest.mark.parametrize("g", [32, 128])
+def test_gemv_batch16_long_k(g):
+    # B * K exceeds the LDS staging budget: x is staged in several K parts
+    gemv_case(2, 16, 300, 4096, g, seed=3, outliers=True)
+
+
 @pytest.mark.parametrize("B", [1, 4])
 def test_gemv_decode_shapes(B):
     gemv_case(2, B, synth.IN_PROJ_N, synth.D_MODEL, 128, seed=1000 + B, outliers=True)
