@@ -50,6 +50,31 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_SOURCES = {"tgemm_fwd": "tgemm_fwd.hip", "tgemv_in_proj": "tgemv.hip",
+                  "tgemv_out_proj": "tgemv.hip"}
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE counters (scaled by a plain-copy calibration), or None when
+    there are none or the kernel source has changed since they were taken."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)["kernels"][kernel]
+    except (OSError, KeyError, ValueError):
+        return None
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_18114_amd", "csrc")
+    for name in (KERNEL_SOURCES[kernel], "common.hpp"):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("source_sha256"):
+        return None
+    return int(rec["read_bytes"]) + int(rec["write_bytes"])
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -179,6 +204,8 @@ def main():
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
 
     fwd = kernels["tgemm_fwd"]
+    t_in, t_out = measured_traffic("tgemv_in_proj"), measured_traffic("tgemv_out_proj")
+    dec_traffic = None if t_in is None or t_out is None else t_in + t_out
     out = {
         "metric": "ternary GEMM TFLOP/s (in_proj, 16k tokens) + batch-1 tgemv GB/s, % of roofline",
         "value": fwd["achieved"],
@@ -203,11 +230,12 @@ def main():
         "tgemv_frac_hbm": round(dec_gbps / PEAK_HBM_GBPS, 4),
         "tgemv_us_per_token": round(dec_ms * 1e3, 2),
         "roofline": {"bound": "mfma", "achieved": fwd["achieved"], "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": fwd["frac"], "traffic": None,
+                     "unit": "TFLOP/s", "frac": fwd["frac"],
+                     "traffic": measured_traffic("tgemm_fwd"),
                      "kernel": "tgemm_fwd (in_proj)", "algorithmic_per_launch": fl},
         "roofline_tgemv": {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS,
                            "unit": "GB/s", "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
-                           "traffic": None, "algorithmic_per_token": dec_bytes},
+                           "traffic": dec_traffic, "algorithmic_per_token": dec_bytes},
         "kernels": kernels,
         "zero_ratio": None,
     }
