@@ -96,6 +96,7 @@ tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g,
  *   codes   uint8 [N, K/4]   in   packed codes (16-byte aligned)
  *   scales  float32 [N, K/g] in   (4-byte aligned)
  *   Y       float32 [M, N]   out  (16-byte aligned)
+ *   K <= 2^22 and N <= 2^26 (TM_ESHAPE otherwise).
  * Products are exact (bf16 times {-1,0,1}) and accumulated in float32 on the
  * matrix cores; the group scale is applied in float32 per group.  Groups
  * whose scale is 0 contribute 0 whatever their codes.  Precondition (met by

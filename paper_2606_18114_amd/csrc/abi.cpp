@@ -106,6 +106,7 @@ tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* sca
       !bytes_of(M, N, 4, &yb))
     return TM_ESHAPE;
   if (((M + 255) / 256) * ((N + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (K > (int64_t(1) << 22) || N > (int64_t(1) << 26)) return TM_ESHAPE;  // 32-bit tile offsets
   if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(Y, 16))
     return TM_EALIGN;
   const Span y = span(Y, yb);

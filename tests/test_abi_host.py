@@ -89,6 +89,8 @@ def test_tgemm_fwd_validation(L):
     assert fwd(L, K=544) == ESHAPE
     assert fwd(L, g=48) == ESHAPE
     assert fwd(L, K=256, g=512) == ESHAPE
+    assert fwd(L, M=1, K=2 ** 22 + 128, N=8) == ESHAPE  # beyond the 32-bit tile offsets
+    assert fwd(L, M=1, N=2 ** 26 + 8) == ESHAPE
     assert fwd(L, X=P + 2) == EALIGN
     assert fwd(L, codes=P + 2 ** 24 + 4) == EALIGN
     assert fwd(L, scales=P + 2 ** 25 + 2) == EALIGN

@@ -165,6 +165,18 @@ def test_fwd_ragged_tiles(g):
     assert err <= REL_DESIGN <= REL_BAR
 
 
+@pytest.mark.parametrize("M,N,K,g", [(4100, 4100, 576, 32), (4100, 4100, 576, 64),
+                                     (700, 900, 64, 64), (257, 8, 128, 128)])
+def test_fwd_many_tiles_and_short_k(M, N, K, g):
+    # more tiles than compute units (workgroups take several tiles), an odd
+    # number of 64-column stages per tile, a single stage per tile, and a
+    # one-row-past-the-tile M with a narrow N
+    X, q, s, Y = gemm_case(M, N, K, g, seed=K + g, label="tiles")
+    err = O.rel_fro_error(Y, O.gemm_fwd(X, q, s, g))
+    print(f"  rel fro err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
 def test_fwd_single_linear():
     ops = _ops()
     W, X = synth.single_linear_inputs(synth.C1)
