@@ -6,19 +6,22 @@
 // round go to the same XCD, so its workgroups share the rows of X through
 // that XCD's L2.
 //
-// K advances 64 columns per stage through a 4-deep LDS ring filled by
-// direct-to-LDS loads (global_load_lds): no register staging, one barrier per
-// stage, loads issued three stages ahead.  The stage stream runs straight
-// across tile boundaries, so the next tile's first stages load while the
-// current tile finishes and writes Y.
-//   * X stage: 256 rows x 128 bytes; the eight 16-byte pieces of row r are
-//     stored XOR-permuted by fwd_swz(r), which makes the 32-row MFMA operand reads
-//     bank-conflict free.
-//   * code stage: 256 weight rows x 16 bytes (64 codes), plus the float32
-//     scales of the (at most two) groups that start in the stage, 256 x 2.
-//     Every lane decodes
-//     the codes of its own weight row into the MFMA B operand, one shift and
-//     one AND per two codes, giving the exact bfloat16 values 2*q.
+// Operands reach LDS by direct-to-LDS loads (global_load_lds), with no
+// register staging and one barrier per 64-column stage.  The stage stream
+// runs straight across tile boundaries, so the next tile's first stages load
+// while the current tile finishes and writes Y.
+//   * X: a 3-deep ring of 256 x 64 stages, loaded two stages ahead.  The
+//     eight 16-byte pieces of row r are stored XOR-permuted by fwd_xswz(r),
+//     which keeps the 32-row MFMA operand reads free of bank conflicts.
+//   * codes and group scales: a weight row holds only 16 bytes of codes per
+//     stage, so loading them per stage would cost one memory request per
+//     16 bytes.  When K is a multiple of 256 they are loaded in code stages of
+//     four X stages (64 bytes of codes per row, the scales of every group
+//     starting in those 256 columns) into a 2-deep ring, one code stage
+//     ahead; otherwise per stage into a 3-deep ring, two stages ahead.
+//   * Every lane decodes the codes of its own weight row into the MFMA B
+//     operand, one shift and one AND per two codes, giving the exact bfloat16
+//     values 2*q.
 //   * The group scale is applied in float32, not folded into the bfloat16
 //     operand (folding would cost about 2e-3 relative error).  Instead of a
 //     second set of partial accumulators, each accumulator is kept in units
@@ -31,29 +34,44 @@
 // Synchronisation: the direct-to-LDS loads are issued from inline assembly,
 // so the compiler neither tracks them nor inserts waits of its own for them
 // (its LDS-DMA tracking would otherwise wait for every load in flight before
-// each LDS read).  Each wave issues exactly seven such loads per stage, and
-// no other vector-memory loads.  At the end of stage j a wave waits until at
-// most the fourteen loads of stages j+2 and j+3 are outstanding (vector-memory
-// operations retire in order), i.e. its part of stage j+1 has landed, and
-// until its LDS reads are done; the barrier then publishes stage j+1 to all
-// waves and frees the slot of stage j for stage j+4.  Y stores issued in
-// between only make that wait stricter.
+// each LDS read).  Each wave issues a fixed number of them per stage and no
+// other vector-memory loads.  At the end of every stage a wave waits until
+// only the loads issued after the ones the next stage needs are in flight
+// (vector-memory operations retire in order) and its LDS reads are done; the
+// barrier then publishes the next stage to all waves and frees the slots read
+// in this one.  Y stores issued in between only make that wait stricter.
 #include <type_traits>
 
 #include "common.hpp"
 
 namespace tmk {
 
-constexpr int kFwdBM = 256, kFwdBN = 256, kFwdBK = 64, kFwdRing = 4;
+constexpr int kFwdBM = 256, kFwdBN = 256, kFwdBK = 64;
+constexpr int kFwdXRing = 3;
 constexpr int kFwdXStage = kFwdBM * kFwdBK * 2;  // 32 KiB of X per stage
-constexpr int kFwdCStage = kFwdBN * kFwdBK / 4;  // 4 KiB of codes per stage
-constexpr int kFwdSStage = kFwdBN * 2 * 4;       // 2 KiB of scales per stage
-constexpr int kFwdCBase = kFwdRing * kFwdXStage;
-constexpr int kFwdSBase = kFwdCBase + kFwdRing * kFwdCStage;
-constexpr int kFwdLds = kFwdSBase + kFwdRing * kFwdSStage;  // 152 KiB
+
+// SS: X stages per code stage (4 when K % 256 == 0, else 1)
+template <int G, int SS>
+struct FwdCfg {
+  static constexpr int kNs = SS == 1 ? 2 : (256 / G > 2 ? 256 / G : 2);  // scales per row
+  static constexpr int kCRing = SS == 1 ? 3 : 2;
+  static constexpr int kCStage = kFwdBN * 16 * SS;  // code bytes per code stage
+  static constexpr int kSStage = kFwdBN * kNs * 4;  // scale bytes per code stage
+  static constexpr int kCBase = kFwdXRing * kFwdXStage;
+  static constexpr int kSBase = kCBase + kCRing * kCStage;
+  static constexpr int kLds = kSBase + kCRing * kSStage;
+  static constexpr int kScaleDma = SS == 1 ? 1 : kNs / 2;  // per wave per code stage
+  static constexpr int kNc = 2 + kScaleDma;                // code + scale loads per wave
+  static constexpr int kUnroll = SS > G / kFwdBK ? SS : G / kFwdBK;  // stages per loop trip
+  static_assert(kLds <= 160 * 1024, "LDS budget");
+};
 
 // 16-byte piece permutation of X row r inside its stage
-__device__ __forceinline__ int fwd_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int fwd_xswz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// 16-byte chunk permutation of code row r inside a 4-stage code stage
+__device__ __forceinline__ int fwd_cswz(int r) {
+  return (((r >> 1) ^ (r >> 3)) & 1) | (((r >> 2) & 1) << 1);
+}
 
 // Direct-to-LDS loads: lane i of the wave reads 16 (4) bytes at base + voff
 // and writes them to LDS byte address lds_base + 16 i (4 i).  base and
@@ -73,19 +91,30 @@ __device__ __forceinline__ void dma_x4(const void* base, uint32_t voff, uint32_t
 }
 #pragma clang diagnostic pop
 
-// end of a stage: this wave's loads of the next stage have landed (at most
-// the 14 loads of the two stages after it are in flight) and its LDS reads
-// are complete; then all waves meet
+// End of a stage: at most kVm of this wave's loads still in flight, its LDS
+// reads complete, then all waves meet.
+template <int kVm>
 __device__ __forceinline__ void fwd_stage_barrier() {
-  asm volatile("s_waitcnt vmcnt(14) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);  // keep each stage's work inside its stage
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(kVm) : "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int G>
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+template <int G, int SS>
 __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ codes,
     const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
     float* __restrict__ Y, uint32_t tiles_n, uint32_t ntiles) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kFwdLds];
+  using C = FwdCfg<G, SS>;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLds];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -99,64 +128,121 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   const uint32_t nblk = gridDim.x;
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
 
-  // ---- the seven direct-to-LDS loads of one stage ----
-  // Cursor: the stage (ait, ast) whose loads are issued next, its tile's
-  // uniform base pointers and this lane's byte offsets inside the tile (rows
-  // past M or N are clamped to the last one).  Rounds past the last tile
-  // reload the last tile; those loads are never consumed, they only keep the
-  // count per stage fixed.
-  int ait = 0, ast = 0;
-  const uint8_t *xt = nullptr, *ct = nullptr, *stl = nullptr;
-  uint32_t xoff[4], coff[2], soff;
-  auto set_tile = [&](int it) {
+  // Rows of the tile of round `it` (rounds past the last tile reload the
+  // last tile; those loads are never consumed, they only keep the count of
+  // loads per stage fixed).  Rows past M or N are clamped to the last one.
+  auto tile_of = [&](int it, int64_t& m0, int64_t& n0) {
     uint32_t tile = (uint32_t)it * nblk + bid;
     tile = tile < ntiles ? tile : ntiles - 1;
-    const int64_t m0 = (int64_t)(tile / tiles_n) * kFwdBM;
-    const int64_t n0 = (int64_t)(tile % tiles_n) * kFwdBN;
+    m0 = (int64_t)(tile / tiles_n) * kFwdBM;
+    n0 = (int64_t)(tile % tiles_n) * kFwdBN;
+  };
+
+  // ---- X loader: stage (xit, xst), 4 loads of 1 KiB per wave ----
+  int xit = 0, xst = 0, xslot = 0;
+  const uint8_t* xt = nullptr;
+  uint32_t xoff[4];
+  auto set_xtile = [&](int it) {
+    int64_t m0, n0;
+    tile_of(it, m0, n0);
     const int mlast = (int)(M - 1 - m0 < 255 ? M - 1 - m0 : 255);
-    const int nlast = (int)(N - 1 - n0 < 255 ? N - 1 - n0 : 255);
     xt = reinterpret_cast<const uint8_t*>(X + m0 * K);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {  // load I = rows 8I .. 8I+7
+      const int r = 8 * (wave * 4 + i) + (lane >> 3);
+      const int lp = (lane & 7) ^ fwd_xswz(r);  // logical piece this lane fetches
+      xoff[i] = (uint32_t)(r < mlast ? r : mlast) * (uint32_t)K * 2u + 16u * lp;
+    }
+  };
+  // kMayWrap: this call may issue the last stage of a tile (known at
+  // compile time from the stage's position in the unrolled loop)
+  auto dma_x = [&](auto may_wrap) {
+    const uint8_t* base = xt + (int64_t)xst * kFwdBK * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      dma_x16(base, xoff[i], lds0 + xslot * kFwdXStage + 1024 * (wave * 4 + i));
+    xslot = xslot == kFwdXRing - 1 ? 0 : xslot + 1;
+    ++xst;
+    if constexpr (decltype(may_wrap)::value) {
+      if (xst == nst) {
+        xst = 0;
+        set_xtile(++xit);
+      }
+    }
+  };
+
+  // ---- code/scale loader: code stage starting at X stage (cit, cst) ----
+  int cit = 0, cst = 0, cslot = 0;
+  const uint8_t *ct = nullptr, *stl = nullptr;
+  uint32_t coff[2], soff[C::kScaleDma];
+  auto set_ctile = [&](int it) {
+    int64_t m0, n0;
+    tile_of(it, m0, n0);
+    const int nlast = (int)(N - 1 - n0 < 255 ? N - 1 - n0 : 255);
     ct = codes + n0 * kb;
     stl = reinterpret_cast<const uint8_t*>(scales + n0 * ng);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {  // X load I = rows 8I .. 8I+7
-      const int r = 8 * (wave * 4 + i) + (lane >> 3);
-      const int lp = (lane & 7) ^ fwd_swz(r);  // logical piece this lane fetches
-      xoff[i] = (uint32_t)(r < mlast ? r : mlast) * (uint32_t)K * 2u + 16u * lp;
+    for (int j = 0; j < 2; ++j) {
+      const int J = wave * 2 + j;
+      if constexpr (SS == 4) {  // load J = rows 16J .. 16J+15, 64 bytes each
+        const int r = 16 * J + (lane >> 2);
+        const int c = (lane & 3) ^ fwd_cswz(r);  // 16-byte chunk this lane fetches
+        coff[j] = (uint32_t)(r < nlast ? r : nlast) * (uint32_t)kb + 16u * c;
+      } else {  // load J = rows 16J .. 16J+15, 16 bytes each
+        const int r = 16 * J + (lane >> 2);
+        coff[j] = (uint32_t)(r < nlast ? r : nlast) * (uint32_t)kb + 4u * (lane & 3);
+      }
     }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {  // code load J = weight rows 16J .. 16J+15
-      const int r = 16 * (wave * 2 + j) + (lane >> 2);
-      coff[j] = (uint32_t)(r < nlast ? r : nlast) * (uint32_t)kb + 4u * (lane & 3);
-    }
-    {  // scales: rows 32w .. 32w+31, groups at columns k0 and k0 + 32
-      const int r = 32 * wave + (lane >> 1);
-      soff = ((uint32_t)(r < nlast ? r : nlast) * (uint32_t)ng + (G == 32 ? (lane & 1) : 0)) * 4u;
-    }
-  };
-  auto dma = [&](int slot) {
-    const int64_t k0 = (int64_t)ast * kFwdBK;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      dma_x16(xt + 2 * k0, xoff[i], lds0 + slot * kFwdXStage + 1024 * (wave * 4 + i));
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      dma_x4(ct + k0 / 4, coff[j], lds0 + kFwdCBase + slot * kFwdCStage + 256 * (wave * 2 + j));
-    dma_x4(stl + 4 * (k0 / G), soff, lds0 + kFwdSBase + slot * kFwdSStage + 256 * wave);
-    if (++ast == nst) {
-      ast = 0;
-      set_tile(++ait);
+    for (int l = 0; l < C::kScaleDma; ++l) {  // kNs scales per row, kNs lanes per row
+      const int L = wave * C::kScaleDma + l;
+      const int r = (64 / C::kNs) * L + lane / C::kNs;
+      const int q = lane % C::kNs;  // group within the code stage
+      const bool real = SS == 4 ? G <= 128 : G == 32;  // otherwise a repeat of group 0
+      soff[l] = ((uint32_t)(r < nlast ? r : nlast) * (uint32_t)ng + (real ? q : 0)) * 4u;
     }
   };
-  set_tile(0);
-
-  // prologue: stages 0, 1, 2 in flight
+  auto dma_c = [&](auto may_wrap) {
+    const int64_t k0 = (int64_t)cst * kFwdBK;
 #pragma unroll
-  for (int p = 0; p < 3; ++p) dma(p);
-  fwd_stage_barrier();
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t dst = lds0 + C::kCBase + cslot * C::kCStage;
+      if constexpr (SS == 4)
+        dma_x16(ct + k0 / 4, coff[j], dst + 1024 * (wave * 2 + j));
+      else
+        dma_x4(ct + k0 / 4, coff[j], dst + 256 * (wave * 2 + j));
+    }
+#pragma unroll
+    for (int l = 0; l < C::kScaleDma; ++l)
+      dma_x4(stl + 4 * (k0 / G), soff[l],
+             lds0 + C::kSBase + cslot * C::kSStage + 256 * (wave * C::kScaleDma + l));
+    cslot = cslot == C::kCRing - 1 ? 0 : cslot + 1;
+    cst += SS;
+    if constexpr (decltype(may_wrap)::value) {
+      if (cst == nst) {
+        cst = 0;
+        set_ctile(++cit);
+      }
+    }
+  };
 
-  const int xsw = fwd_swz(l32);  // == fwd_swz(m) for every X row m this lane reads
-  int s = 0;                     // stage counter, ring slot s % 4
+  // prologue: X stages 0 and 1, code stage 0 (and 1 when SS == 1); the
+  // waits below count the loads issued after the ones the next stage needs
+  const std::true_type wraps;
+  set_xtile(0);
+  set_ctile(0);
+  dma_x(wraps);
+  dma_c(wraps);
+  dma_x(wraps);
+  if constexpr (SS == 1) {
+    dma_c(wraps);
+    fwd_stage_barrier<4 + C::kNc>();
+  } else {
+    fwd_stage_barrier<4>();
+  }
+
+  const int xsw = fwd_xswz(l32);  // == fwd_xswz(m) for every X row m this lane reads
+  int xs = 0, cs = 0;             // ring slots of the stage being computed
 
   for (int it = 0;; ++it) {
     const uint32_t tile = (uint32_t)it * nblk + bid;
@@ -174,22 +260,37 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     float cref[2] = {0.f, 0.f};
     uint32_t msk[2] = {0u, 0u};
 
-    // One stage; kGroupStart tells (at compile time) whether a group starts
-    // at its first column.
-    auto stage = [&](auto group_start_tag, int slot) {
-      constexpr bool kGroupStart = decltype(group_start_tag)::value;
-      const uint8_t* xb = lds + slot * kFwdXStage;
+    // One stage: P = its index inside the code stage, kStart = a group
+    // starts at its first column.
+    auto stage = [&](auto p_tag, auto start_tag) {
+      constexpr int P = decltype(p_tag)::value;
+      constexpr bool kStart = decltype(start_tag)::value;
+      const uint8_t* xb = lds + xs * kFwdXStage;
+      const uint8_t* cb = lds + C::kCBase + cs * C::kCStage;
+      const uint8_t* sb = lds + C::kSBase + cs * C::kSStage;
       u32x4 cw[2];
-      float sc[2][2];  // [b][q]: scales of the groups at columns k0, k0 + 32
+      float sc[2][2];  // [b][q]: scales of the groups starting at step 0, step 2
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const int nr = wn * 64 + b * 32 + l32;
-        cw[b] = *reinterpret_cast<const u32x4*>(lds + kFwdCBase + slot * kFwdCStage + 16 * nr);
-        if (kGroupStart) {
-          const u32x2 v =
-              *reinterpret_cast<const u32x2*>(lds + kFwdSBase + slot * kFwdSStage + 8 * nr);
-          sc[b][0] = __uint_as_float(v.x);
-          sc[b][1] = __uint_as_float(v.y);
+        if constexpr (SS == 4) {
+          // chunk P of row nr sits at P ^ fwd_cswz(nr) (== fwd_cswz(l32));
+          // the opaque copy keeps the compiler from holding one address per P
+          uint32_t sw = 16u * fwd_cswz(l32);
+          asm volatile("" : "+v"(sw));
+          cw[b] = *reinterpret_cast<const u32x4*>(cb + 64 * nr + ((16u * P) ^ sw));
+        } else
+          cw[b] = *reinterpret_cast<const u32x4*>(cb + 16 * nr);
+        if constexpr (kStart) {
+          if constexpr (G == 32) {  // groups 2P, 2P + 1 of the code stage
+            const u32x2 v = *reinterpret_cast<const u32x2*>(sb + 4 * C::kNs * nr + 8 * P);
+            sc[b][0] = __uint_as_float(v.x);
+            sc[b][1] = __uint_as_float(v.y);
+          } else {  // the group starting at this stage
+            constexpr int q = SS == 4 && G <= 128 ? P * kFwdBK / G : 0;
+            sc[b][0] = *reinterpret_cast<const float*>(sb + 4 * C::kNs * nr + 4 * q);
+            sc[b][1] = sc[b][0];
+          }
         }
       }
       auto read_a = [&](int t, bf16x8* ao) {
@@ -204,8 +305,7 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       read_a(0, acur);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        constexpr int kGS = G < 64 ? G : 64;  // columns between possible starts
-        const bool start = kGroupStart && (16 * t) % kGS == 0;
+        const bool start = kStart && (G == 32 ? (t % 2) == 0 : t == 0);
         float r[2] = {1.f, 1.f};
         if (start) {
 #pragma unroll
@@ -213,8 +313,8 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
             const float sv = sc[b][t / 2];
             const bool nz = sv != 0.f;
             msk[b] = nz ? 0xFFFFFFFFu : 0u;
-            const float q = cref[b] * __builtin_amdgcn_rcpf(nz ? sv : 1.f);
-            r[b] = (nz && cref[b] != 0.f) ? q : 1.f;
+            const float ratio = cref[b] * __builtin_amdgcn_rcpf(nz ? sv : 1.f);
+            r[b] = (nz && cref[b] != 0.f) ? ratio : 1.f;
             cref[b] = nz ? sv : cref[b];
           }
         }
@@ -238,19 +338,31 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       }
     };
 
-    // a group spans kPer stages (K % g == 0, so nst is a multiple of kPer);
-    // only the first stage of each group rescales
-    constexpr int kPer = G > kFwdBK ? G / kFwdBK : 1;
-    for (int st = 0; st < nst; st += kPer) {
-#pragma unroll
-      for (int p = 0; p < kPer; ++p, ++s) {
-        dma((s + 3) & (kFwdRing - 1));
-        if (p == 0)
-          stage(std::true_type{}, s & (kFwdRing - 1));
+    // kUnroll stages per trip: a whole number of code stages and of groups
+    for (int st = 0; st < nst; st += C::kUnroll) {
+      static_for<0, C::kUnroll>([&](auto i_tag) {
+        constexpr int i = decltype(i_tag)::value;
+        constexpr int P = i % SS;
+        constexpr bool kStart = G <= kFwdBK || (i * kFwdBK) % G == 0;
+        // nst is a multiple of kUnroll, so only these positions move a
+        // cursor past the end of a tile: the X cursor (stage st + i + 2
+        // issued, st + i + 3 next) and the code cursor (code stage starting
+        // at st + i + 4 issued, st + i + 8 next; with SS == 1 like X)
+        constexpr int kCAhead = SS == 1 ? 3 : 2 * SS;
+        dma_x(std::integral_constant<bool, (i + 3) % C::kUnroll == 0>{});
+        if constexpr (P == 0)
+          dma_c(std::integral_constant<bool, (i + kCAhead) % C::kUnroll == 0>{});
+        stage(std::integral_constant<int, P>{}, std::integral_constant<bool, kStart>{});
+        if constexpr (SS == 1 || P < 2)
+          fwd_stage_barrier<4 + C::kNc>();
         else
-          stage(std::false_type{}, s & (kFwdRing - 1));
-        fwd_stage_barrier();
-      }
+          fwd_stage_barrier<4>();
+        xs = xs == kFwdXRing - 1 ? 0 : xs + 1;
+        if constexpr (SS == 1)
+          cs = xs;
+        else if constexpr (P == SS - 1)
+          cs ^= 1;
+      });
     }
 
     // epilogue: lane holds column l32 of each block, rows 8*(i/4) + 4*h + i%4
@@ -295,14 +407,25 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
   const int64_t blocks = ntiles < cus ? ntiles : cus;
   const dim3 grid((unsigned)blocks), block(512);
   const uint32_t t_n = (uint32_t)tn, nt = (uint32_t)ntiles;
+  const bool wide = K % 256 == 0;  // code stages of four X stages
+#define TM_FWD(GG)                                                                             \
+  case GG:                                                                                     \
+    if (wide)                                                                                  \
+      hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 4>), grid, block, 0, stream, X, codes, scales, M, \
+                         N, K, Y, t_n, nt);                                                    \
+    else                                                                                       \
+      hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 1>), grid, block, 0, stream, X, codes, scales, M, \
+                         N, K, Y, t_n, nt);                                                    \
+    break;
   switch (g) {
-    case 32:  hipLaunchKernelGGL(tgemm_fwd_kernel<32>, grid, block, 0, stream, X, codes, scales, M, N, K, Y, t_n, nt); break;
-    case 64:  hipLaunchKernelGGL(tgemm_fwd_kernel<64>, grid, block, 0, stream, X, codes, scales, M, N, K, Y, t_n, nt); break;
-    case 128: hipLaunchKernelGGL(tgemm_fwd_kernel<128>, grid, block, 0, stream, X, codes, scales, M, N, K, Y, t_n, nt); break;
-    case 256: hipLaunchKernelGGL(tgemm_fwd_kernel<256>, grid, block, 0, stream, X, codes, scales, M, N, K, Y, t_n, nt); break;
-    case 512: hipLaunchKernelGGL(tgemm_fwd_kernel<512>, grid, block, 0, stream, X, codes, scales, M, N, K, Y, t_n, nt); break;
+    TM_FWD(32)
+    TM_FWD(64)
+    TM_FWD(128)
+    TM_FWD(256)
+    TM_FWD(512)
     default: return hipErrorInvalidValue;
   }
+#undef TM_FWD
   return hipGetLastError();
 }
 

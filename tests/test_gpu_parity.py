@@ -166,9 +166,13 @@ def test_fwd_ragged_tiles(g):
 
 
 @pytest.mark.parametrize("M,N,K,g", [(4100, 4100, 576, 32), (4100, 4100, 576, 64),
-                                     (700, 900, 64, 64), (257, 8, 128, 128)])
+                                     (700, 900, 64, 64), (257, 8, 128, 128),
+                                     (4100, 4100, 512, 32), (4100, 4100, 512, 64),
+                                     (4100, 4100, 512, 128), (4100, 4100, 512, 256),
+                                     (4100, 4100, 1024, 512)])
 def test_fwd_many_tiles_and_short_k(M, N, K, g):
-    # more tiles than compute units (workgroups take several tiles), an odd
+    # more tiles than compute units (workgroups take several tiles) with K a
+    # multiple of 256 (codes loaded four stages at a time) or not, an odd
     # number of 64-column stages per tile, a single stage per tile, and a
     # one-row-past-the-tile M with a narrow N
     X, q, s, Y = gemm_case(M, N, K, g, seed=K + g, label="tiles")
