@@ -148,7 +148,7 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
  *   x           bf16 [count, B, K]       in   (16-byte aligned)
  *   codes       uint8 [count, N, K/4]    in   (16-byte aligned)
  *   scales_f16  uint16 [count, N, K/g]   in   float16 bits (2-byte aligned)
- *   count       1 .. 65535;  B  1 .. 16
+ *   count       1 .. 65535;  B  1 .. 16;  N * K / 4 <= 2^31 (bytes per matrix)
  *   y           float32 [count, B, N]    out  (16-byte aligned)
  * Products are exact and accumulated in float32; the float16 scale is applied
  * in float32 per group.

@@ -162,6 +162,7 @@ tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scal
       !bytes_of(count, ybm, 1, &yb))
     return TM_ESHAPE;
   if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
+  if (cbm > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside one matrix
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
     return TM_EALIGN;
   const Span o = span(y, yb);

@@ -143,6 +143,7 @@ def test_tgemv_validation(L):
     assert gv(L, B=0) == ESHAPE
     assert gv(L, B=17) == ESHAPE
     assert gv(L, K=544, g=32) == ESHAPE
+    assert gv(L, count=1, B=1, N=2 ** 20, K=2 ** 13 + 128) == ESHAPE  # > 2^31 code bytes per matrix
     assert gv(L, s16=P + 2 ** 25 + 1) == EALIGN
     assert gv(L, y=P + 2 ** 26 + 4) == EALIGN
     assert gv(L, y=P + 2 ** 24 + 256) == EINVAL          # y overlaps the codes

@@ -343,6 +343,14 @@ def test_gemv_ragged(g, B):
     gemv_case(3, B, 200, 1536, g, seed=g + B, outliers=True)
 
 
+@pytest.mark.parametrize("B,K,g", [(1, 576, 32), (1, 576, 64), (1, 640, 128), (4, 768, 256),
+                                   (16, 1600, 64)])
+def test_gemv_ragged_k(B, K, g):
+    # K not a multiple of the 512-column load slot (the last slot is partial),
+    # and for B = 16 also several x parts whose last one is partial
+    gemv_case(2, B, 150, K, g, seed=K + g, outliers=True)
+
+
 def test_gemv_batch16_small_k():
     gemv_case(2, 16, 70, 512, 128, seed=1, outliers=False)
 
