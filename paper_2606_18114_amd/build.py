@@ -56,11 +56,21 @@ COMMON_FLAGS = [
 ]
 
 
+# per-source additions
+EXTRA_FLAGS = {
+    # matrix-core results in ordinary VGPRs: the GEMV reads every partial sum
+    # back into vector arithmetic, which would otherwise cost one
+    # accumulator-register read per value
+    "tgemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
 def _compile(src: str) -> str:
     os.makedirs(OBJ, exist_ok=True)
     obj = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc(), *lang, *COMMON_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *lang, *COMMON_FLAGS, *EXTRA_FLAGS.get(src, []), "-c",
+           os.path.join(CSRC, src), "-o", obj]
     proc = subprocess.run(cmd, capture_output=True, text=True)
     if proc.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{proc.stderr}")

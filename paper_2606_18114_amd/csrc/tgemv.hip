@@ -40,24 +40,37 @@
 
 namespace tmk {
 
+// Launch shape: waves per workgroup, LDS ring depth (slots per wave) and
+// slot width in columns.
 constexpr int kGemvWaves = 4;
-constexpr int kGemvBlocks = 2;                             // 16-row MFMA blocks per wave
-constexpr int kGemvWaveRows = 16 * kGemvBlocks;            // 32
-constexpr int kGemvRows = kGemvWaveRows * kGemvWaves;      // rows per workgroup
-constexpr int kGemvSlotK = 512;                            // columns per ring slot
-constexpr int kGemvSlotCodes = kGemvWaveRows * kGemvSlotK / 4;  // 4 KiB per slot
-constexpr int kGemvXBytes = 32 * 1024;                     // LDS budget for x
+constexpr int kGemvRing = 2;
+constexpr int kGemvSlotK = 512;
+constexpr int kGemvBlocks = 2;                   // 16-row MFMA blocks per wave
+constexpr int kGemvWaveRows = 16 * kGemvBlocks;  // 32
+constexpr int kGemvXBytes = 32 * 1024;           // LDS budget for x
 
-// scales per row per slot and their direct-to-LDS loads per slot
-template <int G>
+template <int G, int WAVES, int RING, int SK>
 struct GemvCfg {
-  static constexpr int kNs = kGemvSlotK / G > 1 ? kGemvSlotK / G : 1;
+  static constexpr int kUnits = SK / 64;                   // 16-byte units per row piece
+  static constexpr int kCodeLoads = kUnits / 2;            // 1 KiB loads per slot (32 rows)
+  static constexpr int kSlotCodes = kGemvWaveRows * SK / 4;
+  static constexpr int kNs = SK / G > 1 ? SK / G : 1;      // scales per row per slot
   static constexpr int kSLoads = (kGemvWaveRows * kNs + 63) / 64;
-  static constexpr int kSlotScales = 256 * kSLoads;  // LDS bytes (4 per value)
-  static constexpr int kSlotBytes = kGemvSlotCodes + kSlotScales;
-  static constexpr int kWaveBytes = 2 * kSlotBytes;
-  static constexpr int kLoads = 4 + kSLoads;  // direct-to-LDS loads per slot
+  static constexpr int kSlotScales = 256 * kSLoads;        // LDS bytes (4 per value)
+  static constexpr int kSlotBytes = kSlotCodes + kSlotScales;
+  static constexpr int kWaveBytes = RING * kSlotBytes;
+  static constexpr int kLoads = kCodeLoads + kSLoads;      // direct-to-LDS loads per slot
+  static constexpr int kRows = kGemvWaveRows * WAVES;      // rows per workgroup
 };
+
+// 16-byte unit permutation of wave row r inside a slot (units per row: U)
+template <int U>
+__device__ __forceinline__ int gemv_swz(int r) {
+  if constexpr (U == 8)
+    return (r & 7) ^ ((r >> 3) & 1);
+  else
+    return (((r >> 1) ^ (r >> 3)) & 1) | (((r >> 2) & 1) << 1);
+}
 
 // calls f(integral_constant<int, I>) for I in [I0, N), fully unrolled
 template <int I, int N, typename F>
@@ -67,8 +80,6 @@ __device__ __forceinline__ void gemv_static_for(F&& f) {
     gemv_static_for<I + 1, N>(f);
   }
 }
-
-__device__ __forceinline__ int gemv_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
@@ -83,18 +94,20 @@ __device__ __forceinline__ void gemv_dma2(const void* base, uint32_t voff, uint3
 }
 #pragma clang diagnostic pop
 
-template <int G>
-__global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
+template <int G, int WAVES, int RING, int SK, int NV>
+__global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
     const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
     float* __restrict__ y) {
-  using Cfg = GemvCfg<G>;
+  using Cfg = GemvCfg<G, WAVES, RING, SK>;
   constexpr int C = G < 128 ? G : 128;   // chunk width
   constexpr int SPC = C / 32;            // MFMA steps per chunk
-  constexpr int CPS = kGemvSlotK / C;    // chunks per slot
+  constexpr int CPS = SK / C;            // chunks per slot
   constexpr int NB = kGemvBlocks;
+  constexpr int U = Cfg::kUnits;
+  // NV: batch rows a lane's partial sums can hold (1 when B == 1, else 4)
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
-  // [waves][2 slots][codes 4 KiB | scales], then x [B][KP] + zero pad
+  // [waves][RING slots][codes | scales], then x [B][KP] + zero pad
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -103,22 +116,27 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
   const int64_t mat = blockIdx.y;
   const int64_t kb = K / 4;  // code bytes per row
   const int64_t ng = K / G;
-  const int nslot = (int)((K + kGemvSlotK - 1) / kGemvSlotK);
-  const int64_t row0 = (int64_t)blockIdx.x * kGemvRows + wave * kGemvWaveRows;  // wave's rows
-  const uint32_t wlds = (uint32_t)(uintptr_t)smem + wave * Cfg::kWaveBytes;
-  uint16_t* xs = reinterpret_cast<uint16_t*>(smem + kGemvWaves * Cfg::kWaveBytes);
+  const int nslot = (int)((K + SK - 1) / SK);
+  const int64_t row0 = (int64_t)blockIdx.x * Cfg::kRows + wave * kGemvWaveRows;  // wave's rows
+  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+  const uint32_t wlds = lds0 + wave * Cfg::kWaveBytes;
+  const int xoff_b = WAVES * Cfg::kWaveBytes;  // byte offset of x in LDS
+  uint16_t* xs = reinterpret_cast<uint16_t*>(smem + xoff_b);
 
   // ---- load plan of one slot (uniform base + per-lane offsets) ----
-  // codes: load j covers wave rows 8j .. 8j+7, lane -> row 8j + lane/8, unit
-  // lane%8 of the LDS row, which holds logical unit (lane%8) ^ gemv_swz(row)
+  // codes: load j covers wave rows (64/U) j .. +64/U - 1; lane -> row
+  // (64/U) j + lane/U, unit lane%U of the LDS row piece, which holds logical
+  // unit (lane%U) ^ gemv_swz(row)
   const uint8_t* cbase = codes + (mat * N) * kb;
-  uint32_t coff[4];
+  uint32_t coff[Cfg::kCodeLoads];
+  int cunit[Cfg::kCodeLoads];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = 8 * j + (lane >> 3);
+  for (int j = 0; j < Cfg::kCodeLoads; ++j) {
+    const int r = (64 / U) * j + lane / U;
     int64_t n = row0 + r;
     n = n < N ? n : N - 1;
-    coff[j] = (uint32_t)(n * kb) + 16u * ((lane & 7) ^ gemv_swz(r));
+    cunit[j] = (lane % U) ^ gemv_swz<U>(r);
+    coff[j] = (uint32_t)(n * kb) + 16u * cunit[j];
   }
   // scales: load m, lane -> value 64m + lane = (row v / kNs, group v % kNs)
   const uint16_t* sbase = scales_f16 + (mat * N) * ng;
@@ -133,29 +151,45 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
     srow[m] = n * ng;
     sgrp[m] = v % Cfg::kNs;
   }
+  int islot = 0;  // ring buffer of the next slot to issue
   auto issue = [&](int s) {  // loads of slot s (past the end: the last slot again)
     const int sc = s < nslot ? s : nslot - 1;
-    const uint32_t dst = wlds + (s & 1) * Cfg::kSlotBytes;
-    const int64_t kcol = (int64_t)sc * kGemvSlotK;
+    const uint32_t dst = wlds + islot * Cfg::kSlotBytes;
+    islot = islot == RING - 1 ? 0 : islot + 1;
+    const int64_t kcol = (int64_t)sc * SK;
     // a row piece past K (last slot of a ragged K) re-reads its last unit
-    const uint32_t units = (uint32_t)((K - kcol) / 64 < 8 ? (K - kcol) / 64 : 8);
+    const int units = (int)((K - kcol) / 64 < U ? (K - kcol) / 64 : U);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < Cfg::kCodeLoads; ++j) {
       uint32_t off = coff[j];
-      const uint32_t u = (lane & 7) ^ gemv_swz(8 * j + (lane >> 3));
-      if (u >= units) off -= 16u * (u - (units - 1));
+      if (cunit[j] >= units) off -= 16u * (uint32_t)(cunit[j] - (units - 1));
       gemv_dma16(cbase + kcol / 4, off, dst + 1024 * j);
     }
 #pragma unroll
     for (int m = 0; m < Cfg::kSLoads; ++m) {
       int64_t grp = kcol / G + sgrp[m];
       grp = grp < ng ? grp : ng - 1;
-      gemv_dma2(sbase, (uint32_t)((srow[m] + grp) * 2), dst + kGemvSlotCodes + 256 * m);
+      gemv_dma2(sbase, (uint32_t)((srow[m] + grp) * 2), dst + Cfg::kSlotCodes + 256 * m);
     }
   };
-
+  // x part [B][kp0, kp0 + kpl) -> xs[B][KP]: 1 KiB loads spread over the waves
+  // (a load past the part re-reads its last 16 bytes; those columns are
+  // never used), then the zero pad
   const uint16_t* xm = x + mat * (int64_t)B * K;
   const int zpad = B * (int)KP;  // element offset of the zero pad in xs
+  auto stage_x = [&](int64_t kp0, int kpl) {
+    const int per_row = (kpl + 511) / 512;
+    for (int i = wave; i < B * per_row; i += WAVES) {
+      const int b = i / per_row, ch = i % per_row;
+      int e = 512 * ch + 8 * lane;
+      e = e < kpl - 8 ? e : kpl - 8;
+      gemv_dma16(xm + (int64_t)b * K + kp0, (uint32_t)(2 * e),
+                 lds0 + xoff_b + 2 * (b * (int)KP + 512 * ch));
+    }
+    for (int i = threadIdx.x; i < C / 8; i += 64 * WAVES)
+      st16(&xs[zpad + 8 * i], u32x4{0u, 0u, 0u, 0u});
+  };
+
   // lanes whose batch row b = l16 exists read x; the others read the zero pad
   const bool xl = l16 < B;
   const int xbase = xl ? l16 * (int)KP : zpad;
@@ -171,31 +205,32 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
   f32x4 pb[2][NB];
   float spend[NB] = {0.f, 0.f};
 
-  int s = 0;  // next slot to compute; slots s, s + 1 are in flight
+  // prologue: x part 0 and the first RING code slots in flight together
+  stage_x(0, (int)(K < KP ? K : KP));
+  for (int p = 0; p < RING; ++p) issue(p);
+  // own x loads landed (only code loads newer), zero pad written; then a plain
+  // barrier, which unlike __syncthreads does not wait for the code loads
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(RING * Cfg::kLoads) : "memory");
+
+  int s = 0;      // next slot to compute; slots s .. s + RING - 1 are in flight
+  int cslot = 0;  // its ring buffer
   for (int64_t kp0 = 0; kp0 < K; kp0 += KP) {
     const int kpl = (int)(K - kp0 < KP ? K - kp0 : KP);
-    // ---- stage x[:, kp0 : kp0 + kpl] and the zero pad ----
-    __syncthreads();
-    for (int i = threadIdx.x; i < B * kpl / 8; i += 64 * kGemvWaves) {
-      const int b = i / (kpl / 8), c8 = i % (kpl / 8);
-      st16(&xs[b * (int)KP + 8 * c8], ld16(xm + (int64_t)b * K + kp0 + 8 * c8));
+    if (kp0 > 0) {  // next x part: every wave is done with the previous one
+      __syncthreads();
+      stage_x(kp0, kpl);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
     }
-    for (int i = threadIdx.x; i < C / 8; i += 64 * kGemvWaves)
-      st16(&xs[zpad + 8 * i], u32x4{0u, 0u, 0u, 0u});
-    __syncthreads();
-    if (kp0 == 0) {
-      issue(0);
-      issue(1);
-    }
-
     // slots of this part (KP is a multiple of the slot width)
-    const int send = (int)((kp0 + kpl + kGemvSlotK - 1) / kGemvSlotK);
+    const int send = (int)((kp0 + kpl + SK - 1) / SK);
     for (; s < send; ++s) {
-      // slot s landed: only slot s + 1's loads may still be in flight
-      asm volatile("s_waitcnt vmcnt(%0)" :: "n"(Cfg::kLoads) : "memory");
-      const uint8_t* cs = smem + wave * Cfg::kWaveBytes + (s & 1) * Cfg::kSlotBytes;
-      const uint8_t* ss = cs + kGemvSlotCodes;
-      const int64_t kcol = (int64_t)s * kGemvSlotK;
+      // slot s landed: only the RING - 1 slots after it may still be in flight
+      asm volatile("s_waitcnt vmcnt(%0)" :: "n"((RING - 1) * Cfg::kLoads) : "memory");
+      const uint8_t* cs = smem + wave * Cfg::kWaveBytes + cslot * Cfg::kSlotBytes;
+      const uint8_t* ss = cs + Cfg::kSlotCodes;
+      cslot = cslot == RING - 1 ? 0 : cslot + 1;
+      const int64_t kcol = (int64_t)s * SK;
       const int cend = (int)((K - kcol) / C < CPS ? (K - kcol) / C : CPS);
       gemv_static_for<0, CPS>([&](auto c_tag) {
         constexpr int c = decltype(c_tag)::value;
@@ -208,7 +243,7 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
         for (int j = 0; j < NB; ++j) {
           const int r = 16 * j + l16;
           const int byte = C == 128 ? 32 * c + 8 * q : (C == 64 ? 16 * c + 4 * q : 8 * c + 4 * (q >> 1));
-          const uint8_t* p = cs + 128 * r + 16 * ((byte >> 4) ^ gemv_swz(r)) + (byte & 15);
+          const uint8_t* p = cs + (SK / 4) * r + 16 * ((byte >> 4) ^ gemv_swz<U>(r)) + (byte & 15);
           if constexpr (C == 128) {
             const u32x2 v = *reinterpret_cast<const u32x2*>(p);
             cw[j][0] = v.x;
@@ -221,6 +256,20 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
           const uint32_t sraw = *reinterpret_cast<const uint32_t*>(ss + 4 * (r * Cfg::kNs + jj));
           sv[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)sraw);
         }
+        // the chunk's B operands: step t takes word t / 2 (C = 128) or the
+        // only word (C = 64), half t % 2; C = 32 picks its half per lane
+        bf16x8 bops[NB][SPC];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          if constexpr (C == 128) {
+            decode_words(u32x2{cw[j][0], cw[j][1]}, bops[j][0], bops[j][1], bops[j][2], bops[j][3]);
+          } else if constexpr (C == 64) {
+            bops[j][0] = decode_half<0>(cw[j][0]);
+            bops[j][1] = decode_half<1>(cw[j][0]);
+          } else {
+            bops[j][0] = decode_half_rt(cw[j][0], (uint32_t)(q & 1));
+          }
+        }
         const uint32_t kb0 = (uint32_t)(kcol - kp0 + (int64_t)c * C) & kmask;
 #pragma unroll
         for (int t = 0; t < SPC; ++t) {
@@ -229,30 +278,27 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
           const bf16x8 af = as_bf16x8(
               *reinterpret_cast<const u32x4*>(&xs[xbase + kb0 + 16 * word + 8 * half]));
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
-            const uint32_t w = cw[j][C == 128 ? (t >> 1) : 0];
-            bf16x8 bop;
-            if constexpr (C == 32)
-              bop = decode_half_rt(w, (uint32_t)(q & 1));
-            else
-              bop = ((C == 64 ? t : t & 1) != 0) ? decode_half<1>(w) : decode_half<0>(w);
-            pb[buf][j] = mfma16(af, bop, t == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pb[buf][j]);
-          }
+          for (int j = 0; j < NB; ++j)
+            pb[buf][j] = mfma16(af, bops[j][t], t == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pb[buf][j]);
         }
         if (c > 0) {
 #pragma unroll
-          for (int j = 0; j < NB; ++j) acc[j] += spend[j] * pb[buf ^ 1][j];
+          for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int i = 0; i < NV; ++i) acc[j][i] += spend[j] * pb[buf ^ 1][j][i];
         }
 #pragma unroll
         for (int j = 0; j < NB; ++j) spend[j] = sv[j];
         if (c + 1 == cend) {  // the slot's last chunk: nothing to overlap with
 #pragma unroll
-          for (int j = 0; j < NB; ++j) acc[j] += spend[j] * pb[buf][j];
+          for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int i = 0; i < NV; ++i) acc[j][i] += spend[j] * pb[buf][j][i];
         }
       });
-      // this wave's reads of the slot are done: refill it with slot s + 2
+      // this wave's reads of the slot are done: refill its buffer
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      issue(s + 2);
+      issue(s + RING);
     }
   }
   // loads issued past the end must land before the workgroup's LDS is released
@@ -265,25 +311,31 @@ __global__ __launch_bounds__(64 * kGemvWaves) void tgemv_kernel(
     const int64_t n = row0 + 16 * j + l16;
     if (n >= N) continue;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NV; ++i) {
       const int b = 4 * q + i;
       if (b < B) ym[(int64_t)b * N + n] = 0.5f * acc[j][i];
     }
   }
 }
 
-template <int G>
+template <int G, int WAVES = kGemvWaves, int RING = kGemvRing, int SK = kGemvSlotK>
 static void launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                      int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+  using Cfg = GemvCfg<G, WAVES, RING, SK>;
   constexpr int C = G < 128 ? G : 128;
   // x part staged in LDS: B * KP bf16 plus a C-wide zero pad; KP is a
-  // multiple of the slot width so that slots never straddle two parts
-  int64_t KP = ((kGemvXBytes / 2 - C) / B) / kGemvSlotK * kGemvSlotK;
-  if (KP > K) KP = K;
-  const size_t lds = (size_t)kGemvWaves * GemvCfg<G>::kWaveBytes + (size_t)(B * KP + C) * 2;
-  const dim3 grid((unsigned)((N + kGemvRows - 1) / kGemvRows), (unsigned)count);
-  const dim3 block(64 * kGemvWaves);
-  hipLaunchKernelGGL((tgemv_kernel<G>), grid, block, lds, stream, x, codes, s16, B, N, K, KP, y);
+  // multiple of 512 columns (whole slots, whole x loads)
+  int64_t KP = ((kGemvXBytes / 2 - C) / B) / 512 * 512;
+  if (KP > K) KP = (K + 511) / 512 * 512;
+  const size_t lds = (size_t)WAVES * Cfg::kWaveBytes + (size_t)(B * KP + C) * 2;
+  const dim3 grid((unsigned)((N + Cfg::kRows - 1) / Cfg::kRows), (unsigned)count);
+  const dim3 block(64 * WAVES);
+  if (B == 1)
+    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1>), grid, block, lds, stream, x, codes,
+                       s16, B, N, K, KP, y);
+  else
+    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 4>), grid, block, lds, stream, x, codes,
+                       s16, B, N, K, KP, y);
 }
 
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
