@@ -132,6 +132,7 @@ tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes,
  *   X           bf16 [M, K]    in   (16-byte aligned)
  *   dW          float32 [N, K] out  (16-byte aligned)
  *   accumulate  0: dW = dY^T X;  1: dW += dY^T X
+ *   N, K <= 2^26 (TM_ESHAPE otherwise)
  * The token dimension is split across workgroups and reduced with float32
  * atomic adds, so the last bits of dW depend on the summation order.
  */

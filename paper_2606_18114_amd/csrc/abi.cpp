@@ -143,6 +143,7 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X, int64_t M, 
   if (!bytes_of(M, N, 2, &yb) || !bytes_of(M, K, 2, &xb) || !bytes_of(N, K, 4, &wb))
     return TM_ESHAPE;
   if (((N + 255) / 256) * ((K + 255) / 256) * ((M + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (N > (int64_t(1) << 26) || K > (int64_t(1) << 26)) return TM_ESHAPE;  // 32-bit row offsets
   if (!aligned(dY, 16) || !aligned(X, 16) || !aligned(dW, 16)) return TM_EALIGN;
   const Span o = span(dW, wb);
   if (overlap(o, span(dY, yb)) || overlap(o, span(X, xb))) return TM_EINVAL;

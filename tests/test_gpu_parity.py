@@ -290,6 +290,25 @@ def test_bwd_dw_ragged_and_accumulate():
     assert err <= REL_DESIGN and err2 <= REL_DESIGN
 
 
+@pytest.mark.parametrize("M,N,K", [(1000, 4352, 4096), (96, 8512, 4096)])
+def test_bwd_dw_split_tiles(M, N, K):
+    # more output tiles than compute units: whole tiles plus tiles cut along
+    # the tokens and summed with atomics (ragged token tail in the first case,
+    # two whole tiles per workgroup in the second), then accumulated on top
+    ops = _ops()
+    print(f"[dw] split tiles M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + N)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    X = synth.activations(rng, M, K)
+    dW = ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X))
+    ref = O.gemm_bwd_dw(dY, X)
+    err = O.rel_fro_error(host(dW), ref)
+    ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X), dW=dW, accumulate=True)
+    err2 = O.rel_fro_error(host(dW), 2 * ref)
+    print(f"  rel fro err {err:.3e}, accumulated {err2:.3e}", flush=True)
+    assert err <= REL_DESIGN and err2 <= REL_DESIGN
+
+
 def test_bwd_dw_one_hot_tokens():
     """One-hot token rows make dW rows copies of dY columns (exact)."""
     ops = _ops()
