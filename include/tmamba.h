@@ -115,9 +115,13 @@ tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
  *   codes   uint8 [N, K/4]   in   the codes of the forward call
  *   scales  float32 [N, K/g] in   the scales of the forward call
  *   dX      float32 [M, K]   out  (16-byte aligned)
+ *   N <= 2^22 and K <= 2^26 (TM_ESHAPE otherwise)
  * The scale varies along the contraction, so each dequantized weight is
  * split into two bfloat16 terms (hi + lo) whose sum carries 16 bits of the
- * float32 scale; both terms run on the matrix cores.
+ * float32 scale; both terms run on the matrix cores.  When there are more
+ * 256 x 256 output tiles than compute units and their count is not a
+ * multiple of it, some tiles are split along N and reduced with float32
+ * atomic adds, so the last bits of dX then depend on the summation order.
  */
 tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes,
                           const float* scales, int64_t M, int64_t N, int64_t K,

@@ -121,6 +121,7 @@ tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float*
   if (!dY || !codes || !scales || !dX) return TM_EINVAL;
   if (M < 1 || N < 1 || N % 8 != 0) return TM_ESHAPE;
   if (tm_status st = shape_kg(K, g)) return st;
+  if (N > (int64_t(1) << 22) || K > (int64_t(1) << 26)) return TM_ESHAPE;
   int64_t yb, cb, sb, xb;
   if (!bytes_of(M, N, 2, &yb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
       !bytes_of(M, K, 4, &xb))

@@ -17,6 +17,8 @@ hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const f
                                hipStream_t stream);
 hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,
                                int64_t K, float* dW, int accumulate, hipStream_t stream);
+// dst[0 .. n) = 0 (float32), by a plain fill kernel
+hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
 

@@ -31,6 +31,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "launchers.hpp"
 
 namespace tmk {
 
@@ -284,6 +285,13 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dw_kernel(
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream) {
+  const int64_t threads = (n + 3) / 4;
+  hipLaunchKernelGGL(fill_zero_f32, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                     dst, n);
+  return hipGetLastError();
+}
+
 hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,
                                int64_t K, float* dW, int accumulate, hipStream_t stream) {
   const int64_t tn = (N + kDwTN - 1) / kDwTN, tk = (K + kDwTK - 1) / kDwTK;
@@ -304,11 +312,7 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
   const int64_t nst = (M + kDwBM - 1) / kDwBM;
   if (parts > nst) parts = nst;
   if (rem && !accumulate) {  // the cut tiles are summed with atomics
-    const int64_t n = N * K;
-    const int64_t threads = (n + 3) / 4;
-    hipLaunchKernelGGL(fill_zero_f32, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                       stream, dW, n);
-    hipError_t e = hipGetLastError();
+    const hipError_t e = launch_fill_zero_f32(dW, N * K, stream);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(tgemm_bwd_dw_kernel, dim3((unsigned)P), dim3(256), 0, stream, dY, X, M, N,

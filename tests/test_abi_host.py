@@ -110,6 +110,7 @@ def test_tgemm_bwd_dx_validation(L):
     assert dx(L, N=250) == ESHAPE                        # dY rows not 16-byte multiples
     assert dx(L, M=0) == ESHAPE
     assert dx(L, K=100) == ESHAPE
+    assert dx(L, N=2 ** 22 + 8) == ESHAPE                # 32-bit dY row offsets
     assert dx(L, dY=P + 8) == EALIGN
     assert dx(L, dX=P + 2 ** 26 + 8) == EALIGN
     assert dx(L, dX=P) == EINVAL

@@ -274,6 +274,40 @@ def test_bwd_dx_in_proj_sampled_rows():
     assert err <= REL_DESIGN
 
 
+@pytest.mark.parametrize("M,N,K,g", [(4352, 520, 4096, 128), (2000, 1032, 2304, 64),
+                                     (520, 96, 8448, 32), (64, 4104, 512, 512)])
+def test_bwd_dx_split_and_ragged_tiles(M, N, K, g):
+    # 272 output tiles (one whole tile per workgroup plus 16 tiles cut along
+    # the contraction and summed with atomics, ragged N), ragged M and N, a
+    # single K tile row, and a long contraction with a ragged tail
+    ops = _ops()
+    print(f"[dx] tiles M={M} N={N} K={K} g={g}", flush=True)
+    rng = np.random.default_rng(M + N + K)
+    W = synth.weights(rng, N, K, True)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5)
+    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g)
+    rows = np.sort(np.random.default_rng(3).choice(M, min(M, 384), replace=False))
+    got = host(dX[torch.from_numpy(rows).cuda()])
+    err = O.rel_fro_error(got, O.gemm_bwd_dx(dY[rows], host_codes(c, K), host(s), g))
+    print(f"  rel fro err {err:.3e} over {len(rows)} rows", flush=True)
+    assert err <= REL_DESIGN
+
+
+def test_bwd_dx_exact_unit_scales():
+    """Scales that are powers of two make every product and partial sum exact."""
+    ops = _ops()
+    M, N, K, g = 272, 96, 512, 128
+    rng = np.random.default_rng(21)
+    q = rng.integers(-1, 2, size=(N, K)).astype(np.float32)
+    # |W| = 0.5 on every element: s = 0.5 exactly, codes = sign
+    W = np.where(q == 0, 0.5, q * 0.5).astype(np.float32)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 0.0)
+    dYi = synth.f32_to_bf16_bits(rng.integers(-4, 5, size=(M, N)).astype(np.float32))
+    dX = host(ops.tgemm_bwd_dx(dev_bf16(dYi), c, s, g))
+    np.testing.assert_array_equal(dX, O.gemm_bwd_dx(dYi, host_codes(c, K), host(s), g))
+
+
 def test_bwd_dw_ragged_and_accumulate():
     ops = _ops()
     M, N, K = 700, 264, 320
