@@ -15,8 +15,8 @@
 // per wave (4 x 4 MFMA blocks, accumulators in AGPRs), 32 tokens per stage.
 // Stages flow through a 4-deep LDS ring filled by direct-to-LDS loads
 // (global_load_lds) three stages ahead; in every token row the 32-byte units
-// are XOR-permuted by (row % 4), which keeps the four rows of a transpose read
-// in distinct banks.
+// are XOR-permuted (dw_swz) so that transpose reads are free of bank
+// conflicts.
 //
 // Work split (persistent, one workgroup per CU): the T output tiles are
 // dealt round-robin, whole, T / P per workgroup; the T % P remaining tiles
@@ -77,9 +77,15 @@ __device__ __forceinline__ void dw_static_for(F&& f) {
   }
 }
 
+// XOR applied to the 32-byte unit index of token row r: f = (r%4) ^ 2 (r%4)
+// is distinct modulo 4 and in its two upper bits over any four consecutive
+// rows, so the four rows of a transpose read land in distinct 32-byte bank
+// groups, and so do the two column groups (units u, u + 1) read together
+__device__ __forceinline__ int dw_swz(int r) { return (r & 3) ^ ((r & 3) << 1); }
+
 // byte offset of (token row r, column c) inside an operand tile, c % 4 == 0
 __device__ __forceinline__ uint32_t dw_off(int r, int c) {
-  return (uint32_t)(r * 512 + 32 * ((c >> 4) ^ (r & 3)) + 2 * (c & 15));
+  return (uint32_t)(r * 512 + 32 * ((c >> 4) ^ dw_swz(r)) + 2 * (c & 15));
 }
 
 __global__ __launch_bounds__(256) void tgemm_bwd_dw_kernel(
@@ -139,7 +145,7 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dw_kernel(
     for (int i = 0; i < 4; ++i) {
       const int r = 2 * (wave * 4 + i) + r_lo;
       const int p = lane & 31;
-      const int lp = 2 * ((p >> 1) ^ (r & 3)) + (p & 1);
+      const int lp = 2 * ((p >> 1) ^ dw_swz(r)) + (p & 1);
       int64_t cn = n0 + 8 * lp;
       cn = cn < N ? cn : N - 8;  // past N: re-read the last piece (columns unused)
       int64_t ck = k0 + 8 * lp;
