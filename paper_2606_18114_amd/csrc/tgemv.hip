@@ -12,8 +12,8 @@
 // of one matrix and walks the whole K range; a workgroup of 4 waves covers
 // 128 rows and first copies x of its matrix into LDS.
 //
-// Loads: the codes of a wave's 32 rows are staged through a wave-private,
-// 2-deep LDS ring in slots of 512 columns (128 bytes per row), filled by
+// Loads: the codes of a wave's 32 rows are staged through a wave-private LDS
+// ring (kGemvRing slots) of 512 columns (128 bytes per row), filled by
 // direct-to-LDS loads (global_load_lds) that each read 8 whole rows' 128-byte
 // pieces.  The eight 16-byte units of a row piece are stored XOR-permuted by
 // gemv_swz(row), so the MFMA operand reads below are bank-conflict free.  The
@@ -41,9 +41,12 @@
 namespace tmk {
 
 // Launch shape: waves per workgroup, LDS ring depth (slots per wave) and
-// slot width in columns.
+// slot width in columns.  One slot per wave (the next slot's loads are issued
+// once the current one is consumed) measured faster than two or more: the
+// smaller LDS footprint fits more workgroups per CU, and the other waves
+// cover each wave's load latency.
 constexpr int kGemvWaves = 4;
-constexpr int kGemvRing = 2;
+constexpr int kGemvRing = 1;
 constexpr int kGemvSlotK = 512;
 constexpr int kGemvBlocks = 2;                   // 16-row MFMA blocks per wave
 constexpr int kGemvWaveRows = 16 * kGemvBlocks;  // 32
