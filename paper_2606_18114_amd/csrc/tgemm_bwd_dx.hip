@@ -17,11 +17,11 @@
 //   * dY [256 x 32] bf16, the packed codes [32 x 256] and the stage's scales
 //     reach a 4-deep LDS ring by direct-to-LDS loads (global_load_lds) issued
 //     three stages ahead.  The 64-byte dY rows have their four 16-byte units
-//     XOR-permuted by ((row / 2) % 4), so the 16-byte operand reads of eight
-//     consecutive rows hit distinct banks;
+//     XOR-permuted (dx_yoff), so the 16-byte operand reads are free of bank
+//     conflicts on the 64-bank LDS;
 //   * one stage ahead, all threads decode the codes into the two bfloat16
 //     planes q*s_hi and q*s_lo [32 n][256 k] (double-buffered), in natural
-//     order with the 32-byte units of each row XOR-permuted by (row % 4);
+//     order with the 32-byte units of each row XOR-permuted (dx_poff);
 //   * an MFMA B operand (8 consecutive n of one column k) comes from a plane
 //     by two gfx950 transpose reads ds_read_b64_tr_b16: in each group of 16
 //     lanes, lane j passes the address of 4 columns of row j / 4 and lane i
