@@ -57,12 +57,7 @@ COMMON_FLAGS = [
 
 
 # per-source additions
-EXTRA_FLAGS = {
-    # matrix-core results in ordinary VGPRs: the GEMV reads every partial sum
-    # back into vector arithmetic, which would otherwise cost one
-    # accumulator-register read per value
-    "tgemv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-}
+EXTRA_FLAGS = {}
 
 
 def _compile(src: str) -> str:

@@ -1,39 +1,55 @@
 // Decode-time ternary GEMV (batch B <= 16), strided-batched over matrices.
 //
-// Batch-1 decoding is bound by the weight bytes (paper Sec. 8).  The kernel
-// streams the packed codes once, with every load instruction reading whole
-// 128-byte lines, and lets the matrix cores do the multiply-adds: one
-// v_mfma_f32_16x16x32_bf16 takes the activations x as the A operand (rows =
-// batch, padded to 16 with zeros) and 16 weight rows, decoded to exact
-// bfloat16 2*q, as the B operand.  Decoding is one shift and one AND per two
-// codes (common.hpp).
+// Batch-1 decoding is bound by the weight bytes (paper Sec. 8), so the kernel
+// is built to keep the vector ALUs nearly idle while the packed codes stream
+// from HBM: the matrix cores take the codes almost as stored.
 //
-// Work split: each wave owns 32 consecutive weight rows (two 16-row blocks)
-// of one matrix and walks the whole K range; a workgroup of 4 waves covers
-// 128 rows and first copies x of its matrix into LDS.
+// Operands.  v_mfma_scale_f32_16x16x128_f8f6f4 multiplies 16 rows of FP8
+// (e4m3) activations by 16 weight rows of FP4 (e2m1) codes over 128 columns.
+// A code word's sixteen 2-bit two's-complement codes become FP4 values 2*q
+// with one AND for the eight codes at bits 4j+2..4j+3 (already the sign and
+// high exponent bit of an e2m1 nibble: 0100 = +2, 1100 = -2) and one shift
+// and one AND for the eight at bits 4j..4j+1; the shift is done 64 bits wide
+// for two words at once.  So one instruction decodes ~6.4 codes per lane,
+// against ~1.4 for a bfloat16 operand.
 //
-// Loads: the codes of a wave's 32 rows are staged through a wave-private LDS
-// ring (kGemvRing slots) of 512 columns (128 bytes per row), filled by
-// direct-to-LDS loads (global_load_lds) that each read 8 whole rows' 128-byte
-// pieces.  The eight 16-byte units of a row piece are stored XOR-permuted by
-// gemv_swz(row), so the MFMA operand reads below are bank-conflict free.  The
-// float16 group scales of the slot ride along (one 2-byte load per lane; the
-// hardware writes each lane's value into its own 4-byte LDS word).  The loads
-// are issued from inline assembly, so the compiler neither tracks them nor
-// waits for them; each wave counts its own and waits with s_waitcnt before
-// reading a slot.  No workgroup barrier is needed for the ring.
+// Activations.  A bfloat16 value has 8 significant bits, an e4m3 value 4, so
+// x is split into two FP8 terms: with e = exponent of max|x| over the row
+// minus 7 (scaling the row maximum into [128, 256)),
+//   t1 = fp8(x * 2^-e),  t2 = fp8((x * 2^-e - t1) * 16),
+// and x = (t1 + t2 / 16) * 2^e exactly for every element within 2^14 of the
+// row maximum (smaller ones err by at most 2^-22 of the row maximum).  The
+// two terms are two rows of the MFMA's A operand, so one instruction does
+// both; rows of other batch items (and, for g < 128, of the other groups
+// inside the 128 columns, each row holding zeros outside its group) fill the
+// remaining rows.  Rows are combined with their power-of-two factors at the
+// end.  The matrix core sums FP8 x FP4 products with somewhat less than
+// float32 precision: measured relative errors are 1e-7 .. 1e-5.
 //
-// Compute: K is walked in chunks of C = min(g, 128) columns, so a chunk lies
-// inside one quantization group and its scale is applied in float32 once per
-// chunk (acc += s * partial, y = acc / 2).  Inside a chunk the four 8-column
-// lane groups of the MFMA take their codes as below, so that a lane reads 4
-// or 8 contiguous bytes of its row per chunk and decodes them with shifts
-// known at compile time:
-//   C = 128: step t, lane group q -> word 2q + t/2, half t%2
-//   C =  64: step t, lane group q -> word q, half t
-//   C =  32: step 0, lane group q -> word q/2, half q%2
-// (word = 16 codes, half = 8 of them); x is read from LDS with the same
-// mapping.
+// Work split: one workgroup of 4 waves per (matrix, 128-row block); each wave
+// owns 32 consecutive weight rows (two 16-row blocks) and walks the whole K
+// range in 512-column slots.
+//
+// Loads: a wave's slot (32 rows x 128 bytes of codes, plus the rows' float16
+// group scales) arrives in a wave-private LDS buffer by direct-to-LDS loads
+// (global_load_lds) that each read 8 whole rows' 128-byte pieces.  The eight
+// 16-byte units of a row piece are stored XOR-permuted by gemv_swz(row), so
+// the reads below are bank-conflict free.  The loads are issued from inline
+// assembly, so the compiler neither tracks them nor waits for them; each wave
+// counts its own and waits with s_waitcnt.  When a slot has landed the wave
+// copies its code words and scales into registers and refills the buffer
+// with the next slot at once, so a slot is in flight while the wave computes:
+// the bytes in flight are bounded by LDS (about 4 KiB per wave, up to seven
+// workgroups per CU), and register-destination loads of the same bytes in
+// the MFMA's lane layout were measured three times slower.
+//
+// Compute per 128-column chunk c and 16-row block: lane (row l16, lane group
+// q) takes the two code words 2q, 2q+1 of the chunk (columns 32q .. 32q+31),
+// decodes them into its 32 FP4 values (MFMA k = 32q + i), and the lane's A
+// operand is the matching 32 FP8 values of its A row, laid out in LDS in the
+// MFMA's k order when x is staged.  The partial sums of a chunk are scaled by
+// their group's float16 scale in float32 (acc += s * partial), one chunk
+// behind the MFMAs so the vector ALUs never wait on the matrix core.
 #include <type_traits>
 
 #include "common.hpp"
@@ -41,30 +57,16 @@
 namespace tmk {
 
 // Launch shape: waves per workgroup, LDS ring depth (slots per wave) and
-// slot width in columns.  One slot per wave (the next slot's loads are issued
-// once the current one is consumed) measured faster than two or more: the
-// smaller LDS footprint fits more workgroups per CU, and the other waves
-// cover each wave's load latency.
+// slot width in columns.
 constexpr int kGemvWaves = 4;
 constexpr int kGemvRing = 1;
 constexpr int kGemvSlotK = 512;
 constexpr int kGemvBlocks = 2;                   // 16-row MFMA blocks per wave
 constexpr int kGemvWaveRows = 16 * kGemvBlocks;  // 32
-constexpr int kGemvXBytes = 32 * 1024;           // LDS budget for x
+constexpr int kGemvXBytes = 32 * 1024;           // LDS budget for the split x
+constexpr int kGemvXPad = 16;                    // bytes between A rows in LDS (bank spread)
 
-template <int G, int WAVES, int RING, int SK>
-struct GemvCfg {
-  static constexpr int kUnits = SK / 64;                   // 16-byte units per row piece
-  static constexpr int kCodeLoads = kUnits / 2;            // 1 KiB loads per slot (32 rows)
-  static constexpr int kSlotCodes = kGemvWaveRows * SK / 4;
-  static constexpr int kNs = SK / G > 1 ? SK / G : 1;      // scales per row per slot
-  static constexpr int kSLoads = (kGemvWaveRows * kNs + 63) / 64;
-  static constexpr int kSlotScales = 256 * kSLoads;        // LDS bytes (4 per value)
-  static constexpr int kSlotBytes = kSlotCodes + kSlotScales;
-  static constexpr int kWaveBytes = RING * kSlotBytes;
-  static constexpr int kLoads = kCodeLoads + kSLoads;      // direct-to-LDS loads per slot
-  static constexpr int kRows = kGemvWaveRows * WAVES;      // rows per workgroup
-};
+typedef __attribute__((ext_vector_type(8))) int i32x8;
 
 // 16-byte unit permutation of wave row r inside a slot (units per row: U)
 template <int U>
@@ -95,263 +97,602 @@ __device__ __forceinline__ void gemv_dma2(const void* base, uint32_t voff, uint3
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_ushort %0, %1"
                :: "v"(voff), "s"(base), "s"(lds_base) : "memory", "m0");
 }
+// lane i: 4 bytes at base + voff -> LDS lds_base + 4 i
+__device__ __forceinline__ void gemv_dma4(const void* base, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :: "v"(voff), "s"(base), "s"(lds_base) : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
-template <int G, int WAVES, int RING, int SK, int NV>
-__global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
-    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
-    float* __restrict__ y) {
-  using Cfg = GemvCfg<G, WAVES, RING, SK>;
-  constexpr int C = G < 128 ? G : 128;   // chunk width
-  constexpr int SPC = C / 32;            // MFMA steps per chunk
-  constexpr int CPS = SK / C;            // chunks per slot
-  constexpr int NB = kGemvBlocks;
-  constexpr int U = Cfg::kUnits;
-  // NV: batch rows a lane's partial sums can hold (1 when B == 1, else 4)
-  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
-  // [waves][RING slots][codes | scales], then x [B][KP] + zero pad
+// Two code words (32 codes, columns 0..31 of the pair) as 32 FP4 values 2*q.
+// Value i of the result (MFMA k = 32 q + i) holds column fp4_col(i):
+//   dwords 0, 2 (word 0, 1): nibble j -> column 4j + 2 (j < 4), 4(j-4) + 3
+//   dwords 1, 3:             nibble j -> column 4j     (j < 4), 4(j-4) + 1
+// (plus 16 for dwords 2, 3).  The 64-bit shift also moves two bits of word 0
+// into the bottom of dword 3's source; the mask clears them.
+__device__ __forceinline__ i32x8 decode_fp4(u32x2 w) {
+  constexpr uint32_t kNib = 0xCCCCCCCCu;
+  const u32x2 s = shl64(w, 2);
+  i32x8 r;
+  r[0] = (int)(w.x & kNib);
+  r[1] = (int)(s.x & kNib);
+  r[2] = (int)(w.y & kNib);
+  r[3] = (int)(s.y & kNib);
+  r[4] = 0;
+  r[5] = 0;
+  r[6] = 0;
+  r[7] = 0;
+  return r;
+}
 
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int l16 = lane & 15;
-  const int q = lane >> 4;  // lane group: the MFMA's 8-column k slice
-  const int64_t mat = blockIdx.y;
-  const int64_t kb = K / 4;  // code bytes per row
-  const int64_t ng = K / G;
-  const int nslot = (int)((K + SK - 1) / SK);
-  const int64_t row0 = (int64_t)blockIdx.x * Cfg::kRows + wave * kGemvWaveRows;  // wave's rows
-  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
-  const uint32_t wlds = lds0 + wave * Cfg::kWaveBytes;
-  const int xoff_b = WAVES * Cfg::kWaveBytes;  // byte offset of x in LDS
-  uint16_t* xs = reinterpret_cast<uint16_t*>(smem + xoff_b);
+// This file is built without the VGPR form of the matrix instructions, so
+// the result lands in accumulator registers and can never share registers
+// with an operand: with the result allocated over part of the B operand's
+// VGPRs, this instruction was measured to give wrong sums (the operand is
+// evidently still being read while the result is written).
+__device__ __forceinline__ f32x4 mfma_f8f4(i32x8 a, i32x8 b) {
+  // A: FP8 e4m3 (cbsz 0), B: FP4 e2m1 (blgp 4), unit scales (E8M0 127 = 2^0)
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 4,
+                                                          0, 127, 0, 127);
+}
 
-  // ---- load plan of one slot (uniform base + per-lane offsets) ----
-  // codes: load j covers wave rows (64/U) j .. +64/U - 1; lane -> row
-  // (64/U) j + lane/U, unit lane%U of the LDS row piece, which holds logical
-  // unit (lane%U) ^ gemv_swz(row)
-  const uint8_t* cbase = codes + (mat * N) * kb;
-  uint32_t coff[Cfg::kCodeLoads];
-  int cunit[Cfg::kCodeLoads];
+// Order of a 16-column piece of x in the MFMA's k order (see decode_fp4):
+// byte o of the piece holds column kFp4Col[o].
+__device__ constexpr int kFp4Col[16] = {2, 6, 10, 14, 3, 7, 11, 15, 0, 4, 8, 12, 1, 5, 9, 13};
+
+
+// ---------------------------------------------------------------------------
+// Pieces shared by both kernels
+// ---------------------------------------------------------------------------
+
+// Split 16 bfloat16 values (one code word's columns, bits in wv[0..7]) into
+// the two FP8 terms of row exponent e, in the MFMA's k order.
+__device__ __forceinline__ void split_piece(const uint32_t (&wv)[8], int e, u32x4& t1, u32x4& t2) {
+  uint32_t o1[4], o2[4];
 #pragma unroll
-  for (int j = 0; j < Cfg::kCodeLoads; ++j) {
-    const int r = (64 / U) * j + lane / U;
-    int64_t n = row0 + r;
-    n = n < N ? n : N - 1;
-    cunit[j] = (lane % U) ^ gemv_swz<U>(r);
-    coff[j] = (uint32_t)(n * kb) + 16u * cunit[j];
+  for (int d = 0; d < 4; ++d) {
+    float a[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int c = kFp4Col[4 * d + jj];
+      const uint32_t bits = (c & 1) ? (wv[c >> 1] & 0xFFFF0000u) : (wv[c >> 1] << 16);
+      a[jj] = __builtin_ldexpf(__uint_as_float(bits), -e);
+    }
+    int p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[0], a[1], 0, false);
+    p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[2], a[3], p1, true);
+    const float r0 = 16.f * (a[0] - __builtin_amdgcn_cvt_f32_fp8(p1, 0));
+    const float r1 = 16.f * (a[1] - __builtin_amdgcn_cvt_f32_fp8(p1, 1));
+    const float r2 = 16.f * (a[2] - __builtin_amdgcn_cvt_f32_fp8(p1, 2));
+    const float r3 = 16.f * (a[3] - __builtin_amdgcn_cvt_f32_fp8(p1, 3));
+    int p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
+    p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, p2, true);
+    o1[d] = (uint32_t)p1;
+    o2[d] = (uint32_t)p2;
   }
-  // scales: load m, lane -> value 64m + lane = (row v / kNs, group v % kNs)
-  const uint16_t* sbase = scales_f16 + (mat * N) * ng;
-  int64_t srow[Cfg::kSLoads];
-  int sgrp[Cfg::kSLoads];
+  t1 = u32x4{o1[0], o1[1], o1[2], o1[3]};
+  t2 = u32x4{o2[0], o2[1], o2[2], o2[3]};
+}
+
+// max |x| of bfloat16 pairs
+__device__ __forceinline__ float absmax2(float m, uint32_t w) {
+  m = fmaxf(m, fabsf(__uint_as_float(w << 16)));
+  return fmaxf(m, fabsf(__uint_as_float(w & 0xFFFF0000u)));
+}
+
+// Exponent that scales a row maximum into [128, 256); 0 for an all-zero row.
+__device__ __forceinline__ int split_exp(float mx) {
+  return mx > 0.f ? __builtin_amdgcn_frexp_expf(mx) - 8 : 0;
+}
+
+// Write one split 16-column piece of batch row b at MFMA k offset koff of the
+// A rows (2b + t) H + hh: the piece's own group h gets the terms, the other
+// groups of the chunk zeros.
+template <int H>
+__device__ __forceinline__ void put_piece(uint8_t* xs, int xstride, int b, int h, int koff,
+                                          u32x4 t1, u32x4 t2) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int m = 0; m < Cfg::kSLoads; ++m) {
-    const int v = 64 * m + lane;
-    const int r = (v / Cfg::kNs) % kGemvWaveRows;  // kNs == 1: lanes 32..63 repeat
-    int64_t n = row0 + r;
-    n = n < N ? n : N - 1;
-    srow[m] = n * ng;
-    sgrp[m] = v % Cfg::kNs;
+  for (int hh = 0; hh < H; ++hh) {
+    st16(xs + ((2 * b + 0) * H + hh) * xstride + koff, hh == h ? t1 : z);
+    st16(xs + ((2 * b + 1) * H + hh) * xstride + koff, hh == h ? t2 : z);
   }
-  int islot = 0;  // ring buffer of the next slot to issue
-  auto issue = [&](int s) {  // loads of slot s (past the end: the last slot again)
-    const int sc = s < nslot ? s : nslot - 1;
-    const uint32_t dst = wlds + islot * Cfg::kSlotBytes;
-    islot = islot == RING - 1 ? 0 : islot + 1;
-    const int64_t kcol = (int64_t)sc * SK;
-    // a row piece past K (last slot of a ragged K) re-reads its last unit
-    const int units = (int)((K - kcol) / 64 < U ? (K - kcol) / 64 : U);
+}
+
+// MFMA k offset of the first byte of the 16-column piece at column col
+// (a multiple of 16) of a run of whole 128-column chunks
+__device__ __forceinline__ int piece_koff(int col) {
+  const int cic = col % 128;
+  return (col - cic) + 32 * (cic / 32) + 16 * ((cic / 16) % 2);
+}
+
+// Combine the A rows of each batch item and store y for the wave's rows
+// rowb .. rowb + 31.  Lane (row l16, group q) holds D rows 16 r + 4 q + i =
+// (2 b + t) H + h; term t carries 2^(e_b - 4 t), and the FP4 codes are 2 q,
+// hence the extra -1.
+template <int NR, int NV, int H>
+__device__ __forceinline__ void store_rows(const float (&acc)[NR][kGemvBlocks][NV],
+                                           const int* xexp, int B, int64_t N, int64_t rowb,
+                                           int l16, int q, float* ym) {
 #pragma unroll
-    for (int j = 0; j < Cfg::kCodeLoads; ++j) {
-      uint32_t off = coff[j];
-      if (cunit[j] >= units) off -= 16u * (uint32_t)(cunit[j] - (units - 1));
-      gemv_dma16(cbase + kcol / 4, off, dst + 1024 * j);
-    }
+  for (int j = 0; j < kGemvBlocks; ++j) {
+    const int64_t n = rowb + 16 * j + l16;
 #pragma unroll
-    for (int m = 0; m < Cfg::kSLoads; ++m) {
-      int64_t grp = kcol / G + sgrp[m];
-      grp = grp < ng ? grp : ng - 1;
-      gemv_dma2(sbase, (uint32_t)((srow[m] + grp) * 2), dst + Cfg::kSlotCodes + 256 * m);
-    }
-  };
-  // x part [B][kp0, kp0 + kpl) -> xs[B][KP]: 1 KiB loads spread over the waves
-  // (a load past the part re-reads its last 16 bytes; those columns are
-  // never used), then the zero pad
-  const uint16_t* xm = x + mat * (int64_t)B * K;
-  const int zpad = B * (int)KP;  // element offset of the zero pad in xs
-  auto stage_x = [&](int64_t kp0, int kpl) {
-    const int per_row = (kpl + 511) / 512;
-    for (int i = wave; i < B * per_row; i += WAVES) {
-      const int b = i / per_row, ch = i % per_row;
-      int e = 512 * ch + 8 * lane;
-      e = e < kpl - 8 ? e : kpl - 8;
-      gemv_dma16(xm + (int64_t)b * K + kp0, (uint32_t)(2 * e),
-                 lds0 + xoff_b + 2 * (b * (int)KP + 512 * ch));
-    }
-    for (int i = threadIdx.x; i < C / 8; i += 64 * WAVES)
-      st16(&xs[zpad + 8 * i], u32x4{0u, 0u, 0u, 0u});
-  };
-
-  // lanes whose batch row b = l16 exists read x; the others read the zero pad
-  const bool xl = l16 < B;
-  const int xbase = xl ? l16 * (int)KP : zpad;
-  const uint32_t kmask = xl ? 0xFFFFFFFFu : 0u;
-
-  f32x4 acc[NB];
+    for (int r = 0; r < NR; ++r) {
+      float part[4];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // Partial sums alternate between two buffers: the scale of chunk c - 1 is
-  // applied after the MFMAs of chunk c are issued, so the vector ALUs never
-  // wait for the MFMA chain they just started.
-  f32x4 pb[2][NB];
-  float spend[NB] = {0.f, 0.f};
-
-  // prologue: x part 0 and the first RING code slots in flight together
-  stage_x(0, (int)(K < KP ? K : KP));
-  for (int p = 0; p < RING; ++p) issue(p);
-  // own x loads landed (only code loads newer), zero pad written; then a plain
-  // barrier, which unlike __syncthreads does not wait for the code loads
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(RING * Cfg::kLoads) : "memory");
-
-  int s = 0;      // next slot to compute; slots s .. s + RING - 1 are in flight
-  int cslot = 0;  // its ring buffer
-  for (int64_t kp0 = 0; kp0 < K; kp0 += KP) {
-    const int kpl = (int)(K - kp0 < KP ? K - kp0 : KP);
-    if (kp0 > 0) {  // next x part: every wave is done with the previous one
-      __syncthreads();
-      stage_x(kp0, kpl);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-    }
-    // slots of this part (KP is a multiple of the slot width)
-    const int send = (int)((kp0 + kpl + SK - 1) / SK);
-    for (; s < send; ++s) {
-      // slot s landed: only the RING - 1 slots after it may still be in flight
-      asm volatile("s_waitcnt vmcnt(%0)" :: "n"((RING - 1) * Cfg::kLoads) : "memory");
-      const uint8_t* cs = smem + wave * Cfg::kWaveBytes + cslot * Cfg::kSlotBytes;
-      const uint8_t* ss = cs + Cfg::kSlotCodes;
-      cslot = cslot == RING - 1 ? 0 : cslot + 1;
-      const int64_t kcol = (int64_t)s * SK;
-      const int cend = (int)((K - kcol) / C < CPS ? (K - kcol) / C : CPS);
-      gemv_static_for<0, CPS>([&](auto c_tag) {
-        constexpr int c = decltype(c_tag)::value;
-        if (c >= cend) return;  // the last slot of a ragged K
-        constexpr int buf = c & 1;
-        // this chunk's code words and scale, per block
-        uint32_t cw[NB][2];
-        float sv[NB];
+      for (int i = 0; i < 4; ++i) {
+        const int gr = 16 * r + 4 * q + i;
+        const int bt = gr / H;  // 2 b + t
+        const int b = bt >> 1, t = bt & 1;
+        part[i] = (i < NV && b < B) ? __builtin_ldexpf(acc[r][j][i < NV ? i : 0],
+                                                       xexp[b] - 1 - 4 * t)
+                                    : 0.f;
+      }
+      if constexpr (H == 1) {
+        // rows 2b, 2b+1 are i = 0, 1 (and 2, 3) of one lane
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int r = 16 * j + l16;
-          const int byte = C == 128 ? 32 * c + 8 * q : (C == 64 ? 16 * c + 4 * q : 8 * c + 4 * (q >> 1));
-          const uint8_t* p = cs + (SK / 4) * r + 16 * ((byte >> 4) ^ gemv_swz<U>(r)) + (byte & 15);
-          if constexpr (C == 128) {
-            const u32x2 v = *reinterpret_cast<const u32x2*>(p);
-            cw[j][0] = v.x;
-            cw[j][1] = v.y;
-          } else {
-            cw[j][0] = *reinterpret_cast<const uint32_t*>(p);
-            cw[j][1] = cw[j][0];
-          }
-          const int jj = (int)((c * C) / G);  // group of the chunk inside the slot
-          const uint32_t sraw = *reinterpret_cast<const uint32_t*>(ss + 4 * (r * Cfg::kNs + jj));
-          sv[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)sraw);
+        for (int i = 0; i < NV; i += 2) {
+          const int b = (16 * r + 4 * q + i) / 2;
+          if (n < N && b < B) ym[(int64_t)b * N + n] = part[i] + part[i + 1];
         }
-        // the chunk's B operands: step t takes word t / 2 (C = 128) or the
-        // only word (C = 64), half t % 2; C = 32 picks its half per lane
-        bf16x8 bops[NB][SPC];
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          if constexpr (C == 128) {
-            decode_words(u32x2{cw[j][0], cw[j][1]}, bops[j][0], bops[j][1], bops[j][2], bops[j][3]);
-          } else if constexpr (C == 64) {
-            bops[j][0] = decode_half<0>(cw[j][0]);
-            bops[j][1] = decode_half<1>(cw[j][0]);
-          } else {
-            bops[j][0] = decode_half_rt(cw[j][0], (uint32_t)(q & 1));
-          }
-        }
-        const uint32_t kb0 = (uint32_t)(kcol - kp0 + (int64_t)c * C) & kmask;
-#pragma unroll
-        for (int t = 0; t < SPC; ++t) {
-          const int word = C == 128 ? 2 * q + (t >> 1) : (C == 64 ? q : q >> 1);
-          const int half = C == 32 ? (q & 1) : (C == 64 ? t : (t & 1));
-          const bf16x8 af = as_bf16x8(
-              *reinterpret_cast<const u32x4*>(&xs[xbase + kb0 + 16 * word + 8 * half]));
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            pb[buf][j] = mfma16(af, bops[j][t], t == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : pb[buf][j]);
-        }
-        if (c > 0) {
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-#pragma unroll
-            for (int i = 0; i < NV; ++i) acc[j][i] += spend[j] * pb[buf ^ 1][j][i];
-        }
-#pragma unroll
-        for (int j = 0; j < NB; ++j) spend[j] = sv[j];
-        if (c + 1 == cend) {  // the slot's last chunk: nothing to overlap with
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-#pragma unroll
-            for (int i = 0; i < NV; ++i) acc[j][i] += spend[j] * pb[buf][j][i];
-        }
-      });
-      // this wave's reads of the slot are done: refill its buffer
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      issue(s + RING);
-    }
-  }
-  // loads issued past the end must land before the workgroup's LDS is released
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-  // lane holds column (row of W) l16 of each block and batch rows 4*q + i
-  float* ym = y + mat * (int64_t)B * N;
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const int64_t n = row0 + 16 * j + l16;
-    if (n >= N) continue;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int b = 4 * q + i;
-      if (b < B) ym[(int64_t)b * N + n] = 0.5f * acc[j][i];
+      } else if constexpr (H == 2) {
+        // rows 4b .. 4b+3 are i = 0..3 of one lane
+        const int b = (16 * r + 4 * q) / 4;
+        const float v = (part[0] + part[1]) + (part[2] + part[3]);
+        if (n < N && b < B) ym[(int64_t)b * N + n] = v;
+      } else {
+        // rows 8b .. 8b+7: term 0 on lane group q = 2(b%2), term 1 on q + 1
+        const float v = (part[0] + part[1]) + (part[2] + part[3]);
+        const float o = __shfl_xor(v, 16);
+        const int b = (16 * r + 4 * q) / 8;
+        if ((q & 1) == 0 && n < N && b < B) ym[(int64_t)b * N + n] = v + o;
+      }
     }
   }
 }
 
-template <int G, int WAVES = kGemvWaves, int RING = kGemvRing, int SK = kGemvSlotK>
-static void launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
-                     int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
-  using Cfg = GemvCfg<G, WAVES, RING, SK>;
-  constexpr int C = G < 128 ? G : 128;
-  // x part staged in LDS: B * KP bf16 plus a C-wide zero pad; KP is a
-  // multiple of 512 columns (whole slots, whole x loads)
-  int64_t KP = ((kGemvXBytes / 2 - C) / B) / 512 * 512;
-  if (KP > K) KP = (K + 511) / 512 * 512;
-  const size_t lds = (size_t)WAVES * Cfg::kWaveBytes + (size_t)(B * KP + C) * 2;
-  const dim3 grid((unsigned)((N + Cfg::kRows - 1) / Cfg::kRows), (unsigned)count);
+// Per-lane load plan of a slot (32 rows x SK columns of one matrix): code
+// offsets (16-byte units, XOR-permuted per row) and scale indices.  SW: the
+// scales arrive as 4-byte words holding two float16 values (packed in LDS;
+// needs an even number of groups per row and a 4-byte aligned array), else as
+// one float16 per lane (each in its own 4-byte LDS word).
+template <int G, int SK, bool SW>
+struct SlotPlan {
+  static constexpr int U = SK / 64;
+  static constexpr int kCodeLoads = U / 2;
+  static constexpr int kNs = SK / G > 1 ? SK / G : 1;        // scales per row per slot
+  static constexpr int kPer = SW ? kNs / 2 : kNs;             // scale loads per row
+  static constexpr int kSLoads = (kGemvWaveRows * kPer + 63) / 64;
+  static constexpr int kCodeBytes = kGemvWaveRows * SK / 4;
+  static constexpr int kSlotBytes = kCodeBytes + 256 * kSLoads;
+  static constexpr int kLoads = kCodeLoads + kSLoads;
+  static_assert(!SW || kNs % 2 == 0, "word scale loads need two groups per row and slot");
+  int lane;
+  __device__ __forceinline__ void init(int l) { lane = l; }
+  // wave row and 16-byte unit of code load j, wave row and first group of
+  // scale load m
+  __device__ __forceinline__ int crow(int j) const { return (64 / U) * j + lane / U; }
+  __device__ __forceinline__ int cunit(int j) const { return (lane % U) ^ gemv_swz<U>(crow(j)); }
+  __device__ __forceinline__ int srow(int m) const {
+    return ((64 * m + lane) / kPer) % kGemvWaveRows;  // lanes past 32 rows repeat
+  }
+  __device__ __forceinline__ int sgrp(int m) const { return ((64 * m + lane) % kPer) * (SW ? 2 : 1); }
+  // loads of the slot at column kcol of rows rowb .. rowb + 31 of one matrix
+  __device__ __forceinline__ void issue(const uint8_t* cmat, const uint16_t* smat, int64_t N,
+                                        int64_t K, int64_t rowb, int64_t kcol,
+                                        uint32_t dst) const {
+    const int64_t kb = K / 4, ng = K / G;
+    // a row piece past K (last slot of a ragged K) re-reads its last unit
+    const int units = (int)((K - kcol) / 64 < U ? (K - kcol) / 64 : U);
+#pragma unroll
+    for (int j = 0; j < kCodeLoads; ++j) {
+      int64_t n = rowb + crow(j);
+      n = n < N ? n : N - 1;
+      const int unit = cunit(j) < units ? cunit(j) : units - 1;
+      gemv_dma16(cmat + kcol / 4, (uint32_t)(n * kb) + 16u * (uint32_t)unit, dst + 1024 * j);
+    }
+#pragma unroll
+    for (int m = 0; m < kSLoads; ++m) {
+      int64_t n = rowb + srow(m);
+      n = n < N ? n : N - 1;
+      int64_t grp = kcol / G + sgrp(m);
+      grp = grp < ng ? grp : ng - (SW ? 2 : 1);
+      if constexpr (SW)
+        gemv_dma4(smat, (uint32_t)((n * ng + grp) * 2), dst + kCodeBytes + 256 * m);
+      else
+        gemv_dma2(smat, (uint32_t)((n * ng + grp) * 2), dst + kCodeBytes + 256 * m);
+    }
+  }
+  // float16 scale of wave row r, group jj of the slot
+  __device__ __forceinline__ static float scale(const uint8_t* ss, int r, int jj) {
+    const int v = r * kNs + jj;
+    const uint16_t raw = SW ? *reinterpret_cast<const uint16_t*>(ss + 2 * v)
+                            : (uint16_t)*reinterpret_cast<const uint32_t*>(ss + 4 * v);
+    return (float)__builtin_bit_cast(_Float16, raw);
+  }
+};
+
+// A slot's code words and scales, read from LDS into registers so that the
+// slot's buffer can be refilled before the slot is computed.
+template <int G, int SK, int H>
+struct SlotRegs {
+  static constexpr int CPS = SK / 128;
+  u32x2 cw[kGemvBlocks][CPS];
+  float sv[kGemvBlocks][CPS][H];
+  template <bool SW>
+  __device__ __forceinline__ void fetch(const uint8_t* cs, int l16, int q) {
+    constexpr int U = SK / 64;
+#pragma unroll
+    for (int j = 0; j < kGemvBlocks; ++j) {
+      const int r = 16 * j + l16;
+#pragma unroll
+      for (int c = 0; c < CPS; ++c) {
+        const int byte = 32 * c + 8 * q;
+        cw[j][c] = *reinterpret_cast<const u32x2*>(cs + (SK / 4) * r +
+                                                   16 * ((byte >> 4) ^ gemv_swz<U>(r)) +
+                                                   (byte & 15));
+#pragma unroll
+        for (int hh = 0; hh < H; ++hh)
+          sv[j][c][hh] = SlotPlan<G, SK, SW>::scale(cs + kGemvWaveRows * SK / 4, r,
+                                                    (c * 128 + hh * (G < 128 ? G : 0)) / G);
+      }
+    }
+  }
+};
+
+// One slot of a wave from registers: cend full 128-column chunks plus a final
+// 64-column chunk when tail64, with the A rows at part column kb0.  Adds the
+// scaled partial sums into acc.
+template <int G, int SK, int NR, int NV, int H>
+__device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs<G, SK, H>& sr,
+                                             const int (&abase)[NR],
+                                             const uint32_t (&amask)[NR], uint32_t kb0,
+                                             int cend, bool tail64, int q,
+                                             float (&acc)[NR][kGemvBlocks][NV]) {
+  constexpr int CPS = SK / 128;
+  constexpr int NB = kGemvBlocks;
+  // partial sums alternate between two buffers: chunk c - 1 is scaled after
+  // the MFMAs of chunk c are issued, so the vector ALUs never wait on them
+  f32x4 pb[2][NR][NB];
+  gemv_static_for<0, CPS>([&](auto c_tag) {
+    constexpr int c = decltype(c_tag)::value;
+    if (c > cend || (c == cend && !tail64)) return;
+    constexpr int buf = c & 1;
+    i32x8 bop[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)  // columns past K (g < 128, last chunk) decode to zero
+      bop[j] = decode_fp4((G < 128 && c == cend && q >= 2) ? u32x2{0u, 0u} : sr.cw[j][c]);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const uint8_t* ap = smem + abase[r] + ((kb0 + 128u * c) & amask[r]) + 16 * q;
+      const u32x4 a0 = *reinterpret_cast<const u32x4*>(ap);
+      const u32x4 a1 = *reinterpret_cast<const u32x4*>(ap + 64);
+      const i32x8 aop = {(int)a0.x, (int)a0.y, (int)a0.z, (int)a0.w,
+                         (int)a1.x, (int)a1.y, (int)a1.z, (int)a1.w};
+#pragma unroll
+      for (int j = 0; j < NB; ++j) pb[buf][r][j] = mfma_f8f4(aop, bop[j]);
+    }
+    if (c > 0) {
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int i = 0; i < NV; ++i)
+            acc[r][j][i] += sr.sv[j][c - 1][i % H] * pb[buf ^ 1][r][j][i];
+    }
+    if (c == CPS - 1 || c + 1 > cend || (c + 1 == cend && !tail64)) {  // the slot's last chunk
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int i = 0; i < NV; ++i) acc[r][j][i] += sr.sv[j][c][i % H] * pb[buf][r][j][i];
+    }
+  });
+}
+
+// ---------------------------------------------------------------------------
+// The kernel
+// ---------------------------------------------------------------------------
+//
+// One workgroup per (matrix, 128-row block); each of its 4 waves owns 32 rows
+// and walks K in 512-column slots.  The split x (FP8 A rows) is staged in LDS
+// in parts of KP columns (a multiple of the slot width) that fit the LDS
+// budget, with up to NR = 4 A operands of 16 rows per chunk (the launcher
+// splits larger batches; x and y rows of matrix m start at m * xms and
+// m * yms).
+//
+// XD (x by direct-to-LDS loads, one part only): the raw bfloat16 x of the
+// matrix is fetched into the A-row area by direct-to-LDS loads issued before
+// the first slot's codes, so both arrive within one memory latency; every
+// thread then takes its (at most two) 16-column pieces into registers, the
+// row maxima are combined through LDS, and the pieces are split in place.
+// Otherwise the row maxima are taken by global loads over the whole row and
+// each part is split from global memory.
+template <int G, int WAVES, int RING, int SK, int NR, int NV, bool SW, bool XD>
+__global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
+    const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
+    int64_t xms, int64_t yms, float* __restrict__ y) {
+  using Plan = SlotPlan<G, SK, SW>;
+  constexpr int H = G < 128 ? 128 / G : 1;
+  constexpr int CPS = SK / 128;
+  constexpr int kXPieces = 2;  // XD: 16-column x pieces per thread
+  static_assert(NV == 4 || (NV == 2 && H == 1 && NR == 1), "two D rows only for B = 1, g >= 128");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
+  // [waves][codes | scales] | A rows [R][KP + pad] (XD: raw x first) |
+  // zero pad [128] | row maxima [WAVES][16] float | exponents [16] int
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l16 = lane & 15;
+  const int q = lane >> 4;
+  const int64_t mat = blockIdx.y;
+  const int nslot = (int)((K + SK - 1) / SK);
+  const int64_t rowb = (int64_t)blockIdx.x * (kGemvWaveRows * WAVES) + wave * kGemvWaveRows;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+  const uint32_t wlds = lds0 + wave * RING * Plan::kSlotBytes;
+  const int R = 2 * B * H;
+  const int xstride = (int)KP + kGemvXPad;
+  const int xoff = WAVES * RING * Plan::kSlotBytes;
+  uint8_t* xs = smem + xoff;
+  const int64_t KR = (K + 511) / 512 * 512;  // XD: raw x row length
+  const int xarea = XD && B * KR * 2 > R * xstride ? (int)(B * KR * 2) : R * xstride;
+  const int zoff = xoff + xarea;
+  float* xmax = reinterpret_cast<float*>(smem + zoff + 128);
+  int* xexp = reinterpret_cast<int*>(smem + zoff + 128 + 4 * 16 * WAVES);
+
+  Plan plan;
+  plan.init(lane);
+  const uint8_t* cmat = codes + mat * N * (K / 4);
+  const uint16_t* smat = scales_f16 + mat * N * (K / G);
+  auto issue = [&](int s) {  // slot s (past the end: the last slot again) into buffer s % RING
+    const int sc = s < nslot ? s : nslot - 1;
+    plan.issue(cmat, smat, N, K, rowb, (int64_t)sc * SK, wlds + (s % RING) * Plan::kSlotBytes);
+  };
+  const uint16_t* xm = x + mat * xms;
+
+  int abase[NR];
+  uint32_t amask[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int gr = 16 * r + l16;
+    abase[r] = gr < R ? xoff + gr * xstride : zoff;
+    amask[r] = gr < R ? 0xFFFFFFFFu : 0u;
+  }
+  float acc[NR][kGemvBlocks][NV];
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+#pragma unroll
+    for (int j = 0; j < kGemvBlocks; ++j)
+#pragma unroll
+      for (int i = 0; i < NV; ++i) acc[r][j][i] = 0.f;
+
+  if constexpr (XD) {
+    // raw x (row b, columns 512 p .. 512 p + 511 per load; a load past K
+    // re-reads the row's last 16 bytes into the row's pad), then the codes
+    const int xl = B * (int)(KR / 512);
+    int mine = 0;
+    for (int pi = wave; pi < xl; pi += WAVES, ++mine) {
+      const int b = pi / (int)(KR / 512), p = pi % (int)(KR / 512);
+      int64_t e = 512 * (int64_t)p + 8 * lane;
+      e = e < K - 8 ? e : K - 8;
+      gemv_dma16(xm + (int64_t)b * K, (uint32_t)(2 * e),
+                 lds0 + xoff + 2 * (uint32_t)(b * KR + 512 * p));
+    }
+    for (int p = 0; p < RING; ++p) issue(p);
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");  // own x landed
+    __syncthreads();
+    // this thread's pieces (16 columns of one batch row, up to whole chunks)
+    const int pieces = (int)((K + 127) / 128 * 8);
+    const uint16_t* xraw = reinterpret_cast<const uint16_t*>(xs);
+    uint32_t wv[kXPieces][8];
+    float mx[kXPieces];
+#pragma unroll
+    for (int m = 0; m < kXPieces; ++m) {
+      const int i = threadIdx.x + 64 * WAVES * m;
+      const int b = i / pieces, col = 16 * (i % pieces);
+      const bool live = b < B && col < K;
+      const int e = live ? (int)(b * KR) + col : 0;
+      const u32x4 v0 = *reinterpret_cast<const u32x4*>(xraw + e);
+      const u32x4 v1 = *reinterpret_cast<const u32x4*>(xraw + e + 8);
+      wv[m][0] = v0.x; wv[m][1] = v0.y; wv[m][2] = v0.z; wv[m][3] = v0.w;
+      wv[m][4] = v1.x; wv[m][5] = v1.y; wv[m][6] = v1.z; wv[m][7] = v1.w;
+      float t = 0.f;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) t = absmax2(t, wv[m][k]);
+      mx[m] = live ? t : 0.f;
+    }
+    for (int b = 0; b < B; ++b) {
+      float t = 0.f;
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m)
+        if ((threadIdx.x + 64 * WAVES * m) / pieces == b) t = fmaxf(t, mx[m]);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) t = fmaxf(t, __shfl_xor(t, o));
+      if (lane == 0) xmax[16 * wave + b] = t;
+    }
+    __syncthreads();  // maxima visible; every raw piece has been read
+#pragma unroll
+    for (int m = 0; m < kXPieces; ++m) {
+      const int i = threadIdx.x + 64 * WAVES * m;
+      const int b = i / pieces, col = 16 * (i % pieces);
+      if (b >= B) continue;
+      float t = 0.f;
+      for (int w = 0; w < WAVES; ++w) t = fmaxf(t, xmax[16 * w + b]);
+      u32x4 t1 = {0u, 0u, 0u, 0u}, t2 = {0u, 0u, 0u, 0u};
+      int h = -1;  // pieces past K (half a chunk, g < 128) are zeros
+      if (col < K) {
+        split_piece(wv[m], split_exp(t), t1, t2);
+        h = G < 128 ? (col % 128) / G : 0;
+      }
+      put_piece<H>(xs, xstride, b, h, piece_koff(col), t1, t2);
+    }
+    if (threadIdx.x < (unsigned)B) {
+      float t = 0.f;
+      for (int w = 0; w < WAVES; ++w) t = fmaxf(t, xmax[16 * w + threadIdx.x]);
+      xexp[threadIdx.x] = split_exp(t);
+    }
+    for (int i = threadIdx.x; i < 128 / 16; i += 64 * WAVES)
+      st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
+    __syncthreads();
+  } else {
+    for (int p = 0; p < RING; ++p) issue(p);
+    // row maxima of |x| over all K, then the split exponents
+    for (int b = 0; b < B; ++b) {
+      float mx = 0.f;
+      for (int64_t e = 8 * (int64_t)threadIdx.x; e < K; e += 8 * 64 * WAVES) {
+        const u32x4 v = ld16(xm + (int64_t)b * K + e);
+        mx = absmax2(absmax2(absmax2(absmax2(mx, v.x), v.y), v.z), v.w);
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      if (lane == 0) xmax[16 * wave + b] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x < (unsigned)B) {
+      float mx = 0.f;
+      for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, xmax[16 * w + threadIdx.x]);
+      xexp[threadIdx.x] = split_exp(mx);
+    }
+    __syncthreads();
+  }
+
+  // part [kp0, kp0 + kpl) of x -> A rows; pieces past kpl up to the end of
+  // its last chunk are zeros (stale LDS bytes could be FP8 NaNs)
+  auto stage_x = [&](int64_t kp0, int kpl) {
+    const int pieces = (kpl + 127) / 128 * 8;
+    for (int i = threadIdx.x; i < B * pieces; i += 64 * WAVES) {
+      const int b = i / pieces, u = i % pieces;
+      const int col = 16 * u;
+      if (col >= kpl) {
+        put_piece<H>(xs, xstride, b, -1, piece_koff(col), u32x4{0u, 0u, 0u, 0u},
+                     u32x4{0u, 0u, 0u, 0u});
+        continue;
+      }
+      const u32x4 v0 = ld16(xm + (int64_t)b * K + kp0 + col);
+      const u32x4 v1 = ld16(xm + (int64_t)b * K + kp0 + col + 8);
+      const uint32_t wv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      u32x4 t1, t2;
+      split_piece(wv, xexp[b], t1, t2);
+      put_piece<H>(xs, xstride, b, G < 128 ? (col % 128) / G : 0, piece_koff(col), t1, t2);
+    }
+    for (int i = threadIdx.x; i < 128 / 16; i += 64 * WAVES)
+      st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
+  };
+
+  int s = 0;
+  for (int64_t kp0 = 0; kp0 < K; kp0 += KP) {
+    const int kpl = (int)(K - kp0 < KP ? K - kp0 : KP);
+    if constexpr (!XD) {
+      if (kp0 > 0) __syncthreads();  // every wave is done with the previous part
+      stage_x(kp0, kpl);
+      __syncthreads();
+    }
+    const int send = (int)((kp0 + kpl + SK - 1) / SK);
+    for (; s < send; ++s) {
+      // slot s landed (only the RING - 1 slots after it may still be in flight)
+      asm volatile("s_waitcnt vmcnt(%0)" :: "n"((RING - 1) * Plan::kLoads) : "memory");
+      SlotRegs<G, SK, H> sr;
+      sr.template fetch<SW>(smem + (wave * RING + s % RING) * Plan::kSlotBytes, l16, q);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the buffer is free again
+      issue(s + RING);
+      const int64_t kcol = (int64_t)s * SK;
+      const int cend = (int)((K - kcol) / 128 < CPS ? (K - kcol) / 128 : CPS);
+      const bool tail64 = G < 128 && (K - kcol) % 128 != 0 && (K - kcol) < SK;
+      slot_compute<G, SK, NR, NV, H>(smem, sr, abase, amask, (uint32_t)(kcol - kp0), cend,
+                                     tail64, q, acc);
+    }
+  }
+  // loads issued past the end must land before the workgroup's LDS is released
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  store_rows<NR, NV, H>(acc, xexp, B, N, rowb, l16, q, y + mat * yms);
+}
+
+// ---------------------------------------------------------------------------
+// Launch
+// ---------------------------------------------------------------------------
+
+template <int G>
+static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
+                           int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+  constexpr int H = G < 128 ? 128 / G : 1;
+  constexpr int SK = kGemvSlotK;
+  constexpr int WAVES = kGemvWaves;
+  constexpr int RING = kGemvRing;
+  const int R = 2 * B * H;
+  const int rmax = R < 64 ? R : 64;  // A rows of one pass
+  int budget = kGemvXBytes;
+  if (budget < rmax * (SK + kGemvXPad)) budget = rmax * (SK + kGemvXPad);
+  int64_t KP = (int64_t)(budget / rmax - kGemvXPad) / SK * SK;
+  if (KP > K) KP = (K + SK - 1) / SK * SK;
+  const int64_t KR = (K + 511) / 512 * 512;
+  // x by direct-to-LDS loads: one part, at most two 16-column pieces per thread
+  const bool xd = KP >= K && R <= 16 && B * ((K + 127) / 128 * 8) <= 2 * 64 * WAVES;
+  // scales as 4-byte words: an even number of groups per row (so every row
+  // and matrix starts 4-byte aligned) and two groups per slot
+  const bool sw = (K / G) % 2 == 0 && SK / G >= 2 && ((uintptr_t)s16 & 3) == 0;
+  const dim3 grid((unsigned)((N + kGemvWaveRows * WAVES - 1) / (kGemvWaveRows * WAVES)),
+                  (unsigned)count);
   const dim3 block(64 * WAVES);
-  if (B == 1)
-    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1>), grid, block, lds, stream, x, codes,
-                       s16, B, N, K, KP, y);
-  else
-    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 4>), grid, block, lds, stream, x, codes,
-                       s16, B, N, K, KP, y);
+  auto lds_of = [&](int slot_bytes, int rows, bool with_raw) {
+    size_t xa = (size_t)rows * (KP + kGemvXPad);
+    if (with_raw && (size_t)B * KR * 2 > xa) xa = (size_t)B * KR * 2;
+    return (size_t)WAVES * slot_bytes + xa + 128 + 4 * 16 * WAVES + 4 * 16;
+  };
+#define TM_GEMV_LAUNCH(NR_, NV_, SW_, XD_, BP, B0)                                            \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, NV_, SW_, XD_>), grid, block,      \
+                     lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, 2 * (BP) * H, XD_), stream, \
+                     x + (int64_t)(B0) * K, codes, s16, BP, N, K, KP, (int64_t)B * K,         \
+                     (int64_t)B * N, y + (int64_t)(B0) * N)
+  if (xd) {  // the common decode case: R <= 16
+#define TM_GEMV_XD(NV_, SW_)                                                                  \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, NV_, SW_, true>), grid, block,       \
+                     lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, R, true), stream, x,     \
+                     codes, s16, B, N, K, KP, (int64_t)B * K, (int64_t)B * N, y)
+    if constexpr (SK / G >= 2) {
+      if (sw) {
+        if (R <= 2 && H == 1)
+          TM_GEMV_XD(H == 1 ? 2 : 4, true);
+        else
+          TM_GEMV_XD(4, true);
+        return hipGetLastError();
+      }
+    }
+    if (R <= 2 && H == 1)
+      TM_GEMV_XD(H == 1 ? 2 : 4, false);
+    else
+      TM_GEMV_XD(4, false);
+#undef TM_GEMV_XD
+    return hipGetLastError();
+  }
+  // at most 64 A rows per launch: batches beyond 64 / (2 H) go in passes
+  const int bmax = 64 / (2 * H);
+  for (int b0 = 0; b0 < B; b0 += bmax) {
+    const int bp = B - b0 < bmax ? B - b0 : bmax;
+    const int rp = 2 * bp * H;
+    if (rp <= 16)
+      TM_GEMV_LAUNCH(1, 4, false, false, bp, b0);
+    else if (rp <= 32)
+      TM_GEMV_LAUNCH(2, 4, false, false, bp, b0);
+    else if constexpr (H >= 2)
+      TM_GEMV_LAUNCH(4, 4, false, false, bp, b0);
+  }
+#undef TM_GEMV_LAUNCH
+  return hipGetLastError();
 }
 
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream) {
   switch (g) {
-    case 32:  launch_g<32>(x, codes, s16, count, B, N, K, y, stream); break;
-    case 64:  launch_g<64>(x, codes, s16, count, B, N, K, y, stream); break;
-    case 128: launch_g<128>(x, codes, s16, count, B, N, K, y, stream); break;
-    case 256: launch_g<256>(x, codes, s16, count, B, N, K, y, stream); break;
-    case 512: launch_g<512>(x, codes, s16, count, B, N, K, y, stream); break;
+    case 32:  return launch_g<32>(x, codes, s16, count, B, N, K, y, stream);
+    case 64:  return launch_g<64>(x, codes, s16, count, B, N, K, y, stream);
+    case 128: return launch_g<128>(x, codes, s16, count, B, N, K, y, stream);
+    case 256: return launch_g<256>(x, codes, s16, count, B, N, K, y, stream);
+    case 512: return launch_g<512>(x, codes, s16, count, B, N, K, y, stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace tmk

@@ -418,3 +418,54 @@ def test_gemv_batch16_long_k(g):
 def test_gemv_decode_shapes(B):
     gemv_case(2, B, synth.IN_PROJ_N, synth.D_MODEL, 128, seed=1000 + B, outliers=True)
     gemv_case(2, B, synth.D_MODEL, synth.D_INNER, 128, seed=2000 + B, outliers=False)
+
+
+@pytest.mark.parametrize("g", [32, 128])
+def test_gemv_activation_range(g):
+    # batch rows: all zeros; magnitudes spread over 2^-40 .. 2^20; one
+    # nonzero; plain N(0, 1).  The decode GEMV splits each activation row into
+    # two FP8 terms scaled by the row maximum, so wide rows and zero rows are
+    # the cases that split has to get right.
+    ops = _ops()
+    rng = np.random.default_rng(77 + g)
+    N, K, B = 96, 1024, 4
+    W = synth.weights(rng, N, K, True)
+    c, s, s16, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5)
+    xf = np.zeros((B, K), np.float32)
+    xf[1] = rng.standard_normal(K) * np.exp2(rng.integers(-40, 21, K))
+    xf[2, 517] = -3.25
+    xf[3] = rng.standard_normal(K)
+    xb = synth.f32_to_bf16_bits(xf)
+    y = host(ops.tgemv(dev_bf16(xb[None]), c[None], s16[None], g))[0]
+    ref = O.gemv(xb, host_codes(c, K), host(s16), g)
+    assert np.all(y[0] == 0.0)
+    for b in range(1, B):
+        err = O.rel_fro_error(y[b], ref[b])
+        print(f"[gemv range] g={g} row {b} rel err {err:.3e}", flush=True)
+        assert err <= REL_DESIGN
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_gemv_decode_full_stack(B):
+    # all 48 in_proj layers in one call (the launch shape the benchmark
+    # times: enough row blocks that each wave walks the whole K), checked on
+    # sampled layers against the oracle with the kernel's own codes
+    ops = _ops()
+    L, N, K, g = synth.N_LAYERS, synth.IN_PROJ_N, synth.D_MODEL, 128
+    print(f"[gemv] full stack count={L} B={B} N={N} K={K}", flush=True)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(4242 + B)
+    codes = torch.empty((L, N, K // 4), dtype=torch.uint8, device="cuda")
+    s16 = torch.empty((L, N, K // g), dtype=torch.float16, device="cuda")
+    s32 = torch.empty((N, K // g), dtype=torch.float32, device="cuda")
+    for layer in range(L):
+        W = torch.randn((N, K), generator=gen, device="cuda") * 0.02
+        ops.ternarize_pack(W, g, 1e-5, codes=codes[layer], scales=s32, scales_f16=s16[layer],
+                           want_zero_count=False)
+    x = synth.activations(np.random.default_rng(99 + B), L * B, K).reshape(L, B, K)
+    y = host(ops.tgemv(dev_bf16(x), codes, s16, g))
+    for layer in (0, 23, L - 1):
+        ref = O.gemv(x[layer], host_codes(codes[layer], K), host(s16[layer]), g)
+        err = O.rel_fro_error(y[layer], ref)
+        print(f"  layer {layer} rel fro err {err:.3e}", flush=True)
+        assert err <= REL_DESIGN
