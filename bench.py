@@ -9,10 +9,14 @@ All inputs are resident in HBM before the timed region.  Per-kernel times
 come from HIP events recorded on the stream the kernels run on.
 
 The headline `value` is the in_proj forward ternary GEMM in TFLOP/s
-(2*M*N*K algorithmic flops over the kernel's mean duration); the batch-1
-decode GEMV bandwidth and every other kernel are reported beside it.
+(2*M*N*K algorithmic flops over the kernel's mean duration); every other
+kernel is reported beside it.  The decode GEMV is also timed the way a server
+runs it, tokens back to back (batch 1 and 4), after the step loop; that
+figure is `roofline_tgemv` (inside the step the GEMV follows the training
+kernels' output writes, whose write-back from the caches competes with it).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+    python bench.py --sweep-g     # group-size workload: one JSON line per g
 """
 
 from __future__ import annotations
@@ -43,6 +47,8 @@ def parse():
     ap.add_argument("--decode-batch", type=int, default=1)
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--sweep-g", action="store_true",
+                    help="group-size workload (in_proj W, X 2048 x 2048, g = 32 .. 512)")
     return ap.parse_args()
 
 
@@ -85,6 +91,8 @@ def main():
     import torch
     from paper_2606_18114_amd import ops, synth
 
+    if args.sweep_g:
+        return sweep_g(args)
     if not os.path.exists(ops.lib_path()):
         from paper_2606_18114_amd import build
         build.build()
@@ -131,8 +139,11 @@ def main():
                                scales_f16=arena_s[layer], want_zero_count=False)
         xs = np.stack([synth.layer_acts(B, k, synth.decode_seed(f"{kind}_x", layer))
                        for layer in range(L)])
+        x4 = np.stack([synth.layer_acts(4, k, synth.decode_seed(f"{kind}_x", layer))
+                       for layer in range(L)])
         dec[kind] = dict(cfg=dcfg, codes=arena_c, s16=arena_s, x=bf16(xs),
-                         y=torch.empty((L, B, n), dtype=torch.float32, device=dev))
+                         y=torch.empty((L, B, n), dtype=torch.float32, device=dev),
+                         x4=bf16(x4), y4=torch.empty((L, 4, n), dtype=torch.float32, device=dev))
     torch.cuda.synchronize()
     log(f"decode arenas ready in {time.time() - t0:.1f}s")
 
@@ -162,6 +173,7 @@ def main():
     torch.cuda.synchronize()
     events = [mk() for _ in range(args.steps)]
     torch.cuda.synchronize()
+    torch.cuda._sleep(2_000_000)  # the GPU spins while the host queues the first launches
     t_start = time.perf_counter()
     for i in range(args.steps):
         step(events[i])
@@ -172,12 +184,33 @@ def main():
     per = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in events]))
            for i, n in enumerate(names)}
 
+    # ---------------- decode as a server runs it: tokens back to back ----------------
+    def serving(batch, tokens):
+        xk, yk = ("x", "y") if batch == B else ("x4", "y4")
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(tokens)]
+        for _ in range(3):
+            for kind in ("in", "out"):
+                d = dec[kind]
+                ops.tgemv(d[xk], d["codes"], d["s16"], d["cfg"].g, y=d[yk])
+        torch.cuda.synchronize()
+        torch.cuda._sleep(2_000_000)
+        for t in range(tokens):
+            for i, kind in enumerate(("in", "out")):
+                d = dec[kind]
+                ev[t][i].record()
+                ops.tgemv(d[xk], d["codes"], d["s16"], d["cfg"].g, y=d[yk])
+            ev[t][2].record()
+        torch.cuda.synchronize()
+        return (float(np.mean([e[0].elapsed_time(e[1]) for e in ev])),
+                float(np.mean([e[1].elapsed_time(e[2]) for e in ev])))
+    serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
+
     # ---------------- algorithmic work per launch ----------------
     fl = 2.0 * M * N * K
     dcfg_in, dcfg_out = synth.DECODE_IN, synth.DECODE_OUT
 
-    def gemv_bytes(c):
-        return L * (c.N * c.K / 4 + 2 * c.N * c.K / c.g + 2 * B * c.K + 4 * B * c.N)
+    def gemv_bytes(c, batch=B):
+        return L * (c.N * c.K / 4 + 2 * c.N * c.K / c.g + 2 * batch * c.K + 4 * batch * c.N)
 
     work = {
         "ternarize_pack": ("hbm", N * K * (4 + 0.25 + 4 / g + 2 / g)),
@@ -199,9 +232,21 @@ def main():
             ach = amount / sec / 1e9
             kernels[n] = dict(ms=round(per[n], 4), bound="hbm", achieved=round(ach, 1),
                               unit="GB/s", frac=round(ach / PEAK_HBM_GBPS, 4))
+    # in the step (after the training kernels) ...
     dec_ms = per["tgemv_in_proj"] + per["tgemv_out_proj"]
     dec_bytes = gemv_bytes(dcfg_in) + gemv_bytes(dcfg_out)
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
+    # ... and tokens back to back
+    decode_serving = {}
+    for b, (t_in_ms, t_out_ms) in serve.items():
+        nb = gemv_bytes(dcfg_in, b) + gemv_bytes(dcfg_out, b)
+        gbps = nb / ((t_in_ms + t_out_ms) * 1e-3) / 1e9
+        decode_serving[f"B{b}"] = {
+            "us_per_token": round((t_in_ms + t_out_ms) * 1e3, 2),
+            "in_proj_us": round(t_in_ms * 1e3, 2), "out_proj_us": round(t_out_ms * 1e3, 2),
+            "GBps": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM_GBPS, 4),
+            "bytes_per_token": nb}
+    srv = decode_serving[f"B{B}"]
 
     fwd = kernels["tgemm_fwd"]
     t_in, t_out = measured_traffic("tgemv_in_proj"), measured_traffic("tgemv_out_proj")
@@ -226,16 +271,20 @@ def main():
                         "(in_proj 8512x2048 + out_proj 2048x4096, 2-bit codes + fp16 scales)",
             "M": M, "N": N, "K": K, "g": g, "eps": eps, "decode_layers": L, "decode_batch": B,
         },
-        "tgemv_GBps": round(dec_gbps, 1),
-        "tgemv_frac_hbm": round(dec_gbps / PEAK_HBM_GBPS, 4),
-        "tgemv_us_per_token": round(dec_ms * 1e3, 2),
+        "tgemv_GBps": srv["GBps"],
+        "tgemv_frac_hbm": srv["frac_hbm"],
+        "tgemv_us_per_token": srv["us_per_token"],
+        "tgemv_in_step": {"GBps": round(dec_gbps, 1), "frac_hbm": round(dec_gbps / PEAK_HBM_GBPS, 4),
+                          "us_per_token": round(dec_ms * 1e3, 2)},
+        "decode_serving": decode_serving,
         "roofline": {"bound": "mfma", "achieved": fwd["achieved"], "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": fwd["frac"],
                      "traffic": measured_traffic("tgemm_fwd"),
                      "kernel": "tgemm_fwd (in_proj)", "algorithmic_per_launch": fl},
-        "roofline_tgemv": {"bound": "hbm", "achieved": round(dec_gbps, 1), "peak": PEAK_HBM_GBPS,
-                           "unit": "GB/s", "frac": round(dec_gbps / PEAK_HBM_GBPS, 4),
-                           "traffic": dec_traffic, "algorithmic_per_token": dec_bytes},
+        "roofline_tgemv": {"bound": "hbm", "achieved": srv["GBps"], "peak": PEAK_HBM_GBPS,
+                           "unit": "GB/s", "frac": srv["frac_hbm"],
+                           "traffic": dec_traffic, "algorithmic_per_token": dec_bytes,
+                           "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to back"},
         "kernels": kernels,
         "zero_ratio": None,
     }
@@ -285,10 +334,13 @@ def main():
 
 
 def cpu_baseline(W_h, X_h, dY_h, g, eps, dec):
-    """The oracle as it stands, timed on the host on a bounded sample of the
-    same workload: the whole in_proj QAT step at full size (ternarize, float64
-    forward, dX and dW GEMMs) and the batch-1 decode GEMV of 4 in_proj and 4
-    out_proj layers.  `value` is the oracle's forward-GEMM TFLOP/s."""
+    """The oracle as it stands, timed on the host over one whole step of the
+    same workload: the in_proj QAT step at full size (ternarize, float64
+    forward, dX and dW GEMMs) and one batch-1 decode token over all 96 packed
+    matrices (unpack + float64 GEMV per matrix; the packed arenas are copied
+    to the host before timing).  `value` is the oracle's forward-GEMM TFLOP/s,
+    the unit of the headline."""
+    import torch
     from oracle import ternary as O
     try:
         from threadpoolctl import threadpool_info
@@ -297,6 +349,9 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec):
         threads = os.cpu_count() or 1
     N, K = W_h.shape
     M = X_h.shape[0]
+    host = {kind: (dec[kind]["cfg"], dec[kind]["codes"].cpu().numpy(), dec[kind]["s16"].cpu().numpy(),
+                   dec[kind]["x"].cpu().view(torch.int16).numpy().view(np.uint16))
+            for kind in ("in", "out")}
     t = {}
     t0 = time.perf_counter()
     _, s32, q, _ = O.ternarize(W_h, g, eps)
@@ -310,24 +365,83 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec):
     t0 = time.perf_counter()
     O.gemm_bwd_dw(dY_h, X_h)
     t["dw"] = time.perf_counter() - t0
-    gemv_bytes, t0 = 0.0, time.perf_counter()
+    gemv_bytes, nmat, t0 = 0.0, 0, time.perf_counter()
     for kind in ("in", "out"):
-        d = dec[kind]
-        c = d["cfg"]
-        for layer in range(4):
-            ql = O.unpack(d["codes"][layer].cpu().numpy(), c.K)
-            xl = d["x"][layer].cpu().view(dtype=__import__("torch").int16).numpy().view(np.uint16)
-            O.gemv(xl, ql, d["s16"][layer].cpu().numpy(), c.g)
+        c, codes, s16, x = host[kind]
+        for layer in range(codes.shape[0]):
+            O.gemv(x[layer], O.unpack(codes[layer], c.K), s16[layer], c.g)
             gemv_bytes += c.N * c.K / 4 + 2 * c.N * c.K / c.g
-    t["gemv8"] = time.perf_counter() - t0
+            nmat += 1
+    t["gemv"] = time.perf_counter() - t0
     fl = 2.0 * M * N * K
+    total = sum(t.values())
     return {"value": round(fl / t["fwd"] / 1e12, 4), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
-            "sample": (f"full in_proj QAT step on the host: ternarize {t['ternarize']:.2f}s "
-                       f"({N * K * 4 / t['ternarize'] / 1e9:.2f} GB/s), float64 fwd {t['fwd']:.2f}s, "
-                       f"dX {t['dx']:.2f}s, dW {t['dw']:.2f}s ({fl / 1e9:.0f} GFLOP each); "
-                       f"decode GEMV of 8 of the 96 layers {t['gemv8']:.2f}s "
-                       f"({gemv_bytes / t['gemv8'] / 1e9:.3f} GB/s of packed weights)")}
+            "sample": (f"one whole step on the host ({total:.1f}s): in_proj QAT step, ternarize "
+                       f"{t['ternarize']:.2f}s ({N * K * 4 / t['ternarize'] / 1e9:.2f} GB/s of W), "
+                       f"float64 fwd {t['fwd']:.2f}s, dX {t['dx']:.2f}s, dW {t['dw']:.2f}s "
+                       f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
+                       f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
+
+
+def sweep_g(args):
+    """Group-size workload: the in_proj weights (8512 x 2048, with outliers)
+    ternarized and applied to 2048 x 2048 bf16 activations for g = 32 .. 512.
+    One JSON line per g: zero ratio and NRMSE of the quantizer, ternarize
+    GB/s, forward TFLOP/s, and the sampled forward error against the oracle."""
+    import torch
+    from oracle import ternary as O
+    from paper_2606_18114_amd import ops, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    N, K, M = synth.IN_PROJ_N, synth.D_MODEL, 2048
+    W_h = synth.layer_weight(synth.C3, synth.SEED_W)
+    X_h = synth.layer_acts(M, K, synth.SEED_X)
+    W = torch.from_numpy(W_h).to(dev)
+    X = torch.from_numpy(X_h.view(np.int16)).to(dev).view(torch.bfloat16)
+    Y = torch.empty((M, N), dtype=torch.float32, device=dev)
+    rows = np.sort(np.random.default_rng(7).choice(M, 64, replace=False))
+    reps = max(args.steps, 5)
+    for g in synth.C5_GROUPS:
+        codes = torch.empty((N, K // 4), dtype=torch.uint8, device=dev)
+        scales = torch.empty((N, K // g), dtype=torch.float32, device=dev)
+        zc = torch.empty((1,), dtype=torch.int64, device=dev)
+        for _ in range(3):
+            ops.ternarize_pack(W, g, 1e-5, codes=codes, scales=scales, zero_count=zc)
+            ops.tgemm_fwd(X, codes, scales, g, Y=Y)
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+        torch.cuda._sleep(2_000_000)
+        for e in ev:
+            e[0].record()
+            ops.ternarize_pack(W, g, 1e-5, codes=codes, scales=scales, zero_count=zc)
+            e[1].record()
+            ops.tgemm_fwd(X, codes, scales, g, Y=Y)
+            e[2].record()
+        torch.cuda.synchronize()
+        t_tern = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        t_fwd = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+        q = O.unpack(codes.cpu().numpy(), K)
+        s = scales.cpu().numpy()
+        s64, _, q_ref, z_ref = O.ternarize(W_h, g, 1e-5)
+        band = O.boundary_mask(W_h, s64, g, 1e-5)
+        z = int(zc.item())
+        tern_bytes = N * K * (4 + 0.25 + 4 / g)
+        fl = 2.0 * M * N * K
+        err = O.rel_fro_error(Y[torch.from_numpy(rows).to(dev)].cpu().numpy(),
+                              O.gemm_fwd(X_h[rows], q, s, g))
+        print(json.dumps({
+            "workload": f"group sweep: in_proj W {N}x{K} (1% Laplace outliers), X bf16 {M}x{K}",
+            "g": g, "zero_ratio": round(z / (N * K), 5), "zero_ratio_oracle": round(z_ref / (N * K), 5),
+            "boundary_elements": int(band.sum()),
+            "codes_differing_off_boundary": int(np.sum((q != q_ref) & ~band)),
+            "nrmse": round(O.nrmse(W_h, q, s, g), 5),
+            "ternarize_ms": round(t_tern, 4), "ternarize_GBps": round(tern_bytes / t_tern / 1e6, 1),
+            "fwd_ms": round(t_fwd, 4), "fwd_TFLOPs": round(fl / t_fwd / 1e9, 1),
+            "fwd_frac_mfma": round(fl / t_fwd / 1e9 / PEAK_BF16_TFLOPS, 4),
+            "fwd_rel_fro_sampled": float(f"{err:.3e}")}), flush=True)
 
 
 if __name__ == "__main__":
