@@ -217,6 +217,9 @@ def main():
                 e0.elapsed_time(e1) / tokens)
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
 
+    # ---------------- QAT block: both projections through autograd ----------------
+    qat_block = qat_block_step(args, dev, X, synth)
+
     # ---------------- algorithmic work per launch ----------------
     fl = 2.0 * M * N * K
     dcfg_in, dcfg_out = synth.DECODE_IN, synth.DECODE_OUT
@@ -299,6 +302,7 @@ def main():
                            "traffic": dec_traffic, "algorithmic_per_token": dec_bytes,
                            "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to back"},
         "kernels": kernels,
+        "qat_block": qat_block,
         "zero_ratio": None,
     }
     out["zero_ratio"] = round(int(zc.item()) / (N * K), 5)
@@ -344,6 +348,50 @@ def main():
         out["cpu_baseline"] = cpu_baseline(W_h, X_h, dY_h, g, eps, dec)
 
     print(json.dumps(out), flush=True)
+
+
+def qat_block_step(args, dev, X_in, synth):
+    """One QAT step of a Mamba-2 1.3B block's two ternary projections through
+    the autograd layer (forward, straight-through backward, 16384 tokens):
+    in_proj 2048 -> 8512 on the block input, out_proj 4096 -> 2048 on a
+    synthetic SSM output.  The upstream gradients are given; the time covers
+    the library calls plus the layer's gradient casts to bfloat16."""
+    import torch
+    from paper_2606_18114_amd.qat import TernaryLinear, flops_per_step
+
+    torch.manual_seed(7)
+    M = X_in.shape[0]
+    lin = TernaryLinear(synth.D_MODEL, synth.IN_PROJ_N, device=dev)
+    lout = TernaryLinear(synth.D_INNER, synth.D_MODEL, device=dev)
+    z = torch.randn((M, synth.D_INNER), device=dev).to(torch.bfloat16).requires_grad_(True)
+    x = X_in.detach().requires_grad_(True)  # gradients flow on to the layers below
+    g_in = torch.randn((M, synth.IN_PROJ_N), device=dev) * synth.DY_STD
+    g_out = torch.randn((M, synth.D_MODEL), device=dev) * synth.DY_STD
+
+    def step():
+        lin.weight.grad = lout.weight.grad = x.grad = z.grad = None
+        y1 = lin(x)
+        y2 = lout(z)
+        torch.autograd.backward([y1, y2], [g_in, g_out])
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    reps = max(args.steps // 2, 5)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(2_000_000)
+    e0.record()
+    for _ in range(reps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    fl = flops_per_step(M, lin) + flops_per_step(M, lout)
+    return {"ms_per_step": round(ms, 4), "TFLOPs": round(fl / (ms * 1e-3) / 1e12, 1),
+            "frac_mfma": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "tokens": M, "zero_ratio_in_proj": round(lin.zero_ratio(), 5),
+            "what": "TernaryLinear in_proj 2048->8512 + out_proj 4096->2048, forward + "
+                    "straight-through backward (dX and dW), 16384 tokens, g=128"}
 
 
 def cpu_baseline(W_h, X_h, dY_h, g, eps, dec):

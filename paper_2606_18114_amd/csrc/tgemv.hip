@@ -597,7 +597,9 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       SlotRegs<G, SK, H> sr;
       sr.template fetch<SW>(smem + (wave * RING + s % RING) * Plan::kSlotBytes, l16, q);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the buffer is free again
-      issue(s + RING);
+      // (one slot in flight: nothing to issue past the end; deeper rings keep
+      // their wait counts exact by reloading the last slot)
+      if (RING > 1 || s + RING < nslot) issue(s + RING);
       const int64_t kcol = (int64_t)s * SK;
       const int cend = (int)((K - kcol) / 128 < CPS ? (K - kcol) / 128 : CPS);
       const bool tail64 = G < 128 && (K - kcol) % 128 != 0 && (K - kcol) < SK;
