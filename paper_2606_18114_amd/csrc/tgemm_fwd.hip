@@ -127,6 +127,8 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   const uint32_t bid = xcd_remap(blockIdx.x, gridDim.x);
   const uint32_t nblk = gridDim.x;
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  // in-tile row offsets of the output fit 32 bits (131 rows of N floats)
+  const bool small_pitch = N < (int64_t(1) << 22);
 
   // Rows of the tile of round `it` (rounds past the last tile reload the
   // last tile; those loads are never consumed, they only keep the count of
@@ -365,21 +367,58 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       });
     }
 
-    // epilogue: lane holds column l32 of each block, rows 8*(i/4) + 4*h + i%4
+    // epilogue: lane holds column l32 of each block, rows 8*(i/4) + 4*h + i%4.
+    // Row offsets inside the tile are compile-time multiples of the row
+    // pitch, so a store costs one address add; tiles wholly inside M skip
+    // the row test (rows past M only occur in the last row of tiles).
+    {
+      const int64_t mrow = m0 + wm * 128;
+      uint8_t* ytile = reinterpret_cast<uint8_t*>(Y + mrow * N + n0);
+      const bool full_m = mrow + 128 <= M;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int64_t n = n0 + wn * 64 + b * 32 + l32;
-      if (n >= N) continue;
-      const float f = 0.5f * cref[b];
-      const uint32_t voff = (uint32_t)((4 * h * N + n - n0) * 4);
+      for (int b = 0; b < 2; ++b) {
+        const int nl = wn * 64 + b * 32 + l32;  // column in the tile
+        if (n0 + nl >= N) continue;
+        const float f = 0.5f * cref[b];
+        uint8_t* ylane = ytile + ((int64_t)(4 * h) * N + nl) * 4;
+        if (small_pitch && full_m) {
+          // a 32-bit lane offset from the uniform tile base, stepped row by
+          // row (rows a*32 + 8*i4 + i1); the empty asm keeps the compiler
+          // from precomputing all 64 offsets (which it would spill)
+          uint32_t pv = (uint32_t)N * 4u;
+          asm volatile("" : "+v"(pv));
+          const uint32_t pv4 = 4u * pv;
+          uint32_t o = (uint32_t)((4 * h) * N + nl) * 4u;
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
+          for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int64_t mu = m0 + wm * 128 + a * 32 + 8 * (i / 4) + (i % 4);  // uniform part
-          if (mu + 4 * h < M)
-            *reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Y + mu * N + n0) + voff) =
-                f * acc[a][b][i];
+            for (int i4 = 0; i4 < 4; ++i4) {
+#pragma unroll
+              for (int i1 = 0; i1 < 4; ++i1) {
+                *reinterpret_cast<float*>(ytile + o) = f * acc[a][b][4 * i4 + i1];
+                o += pv;
+              }
+              o += pv4;  // rows 8 i4 + 4 .. 8 i4 + 7 belong to the other k half
+            }
+        } else {
+          // rows past M (last row of tiles), or a pitch beyond 32-bit offsets
+          int64_t pv = N * 4;
+          asm volatile("" : "+v"(pv));
+          uint8_t* yp = ylane;
+          int64_t row = mrow + 4 * h;
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+#pragma unroll
+              for (int i1 = 0; i1 < 4; ++i1) {
+                if (row < M) *reinterpret_cast<float*>(yp) = f * acc[a][b][4 * i4 + i1];
+                yp += pv;
+                ++row;
+              }
+              yp += 4 * pv;
+              row += 4;
+            }
         }
       }
     }
