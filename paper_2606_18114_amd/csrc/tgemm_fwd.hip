@@ -395,7 +395,8 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
             for (int i4 = 0; i4 < 4; ++i4) {
 #pragma unroll
               for (int i1 = 0; i1 < 4; ++i1) {
-                *reinterpret_cast<float*>(ytile + o) = f * acc[a][b][4 * i4 + i1];
+                __builtin_nontemporal_store(f * acc[a][b][4 * i4 + i1],
+                                            reinterpret_cast<float*>(ytile + o));
                 o += pv;
               }
               o += pv4;  // rows 8 i4 + 4 .. 8 i4 + 7 belong to the other k half
