@@ -97,3 +97,20 @@ def gemm_dw(dY, X):
     M, N, K = len(dY), len(dY[0]), len(X[0])
     return [[math.fsum(dY[m][n] * X[m][k] for m in range(M)) for k in range(K)]
             for n in range(N)]
+
+
+def codes_thresh(W, s32, g, eps, row_mult):
+    """Codes with a per-row threshold multiplier m: the divisor is
+    fl32(fl32(m * s) + eps), decided by the same exact comparison as `codes`."""
+    tau = [[f32(f32(m) * s) for s in srow] for srow, m in zip(s32, row_mult)]
+    return codes(W, tau, g, eps)
+
+
+def group_code_dot(q, d, g):
+    """sum of q * d over each group, exactly (Fractions), returned as floats."""
+    out = []
+    for qrow, drow in zip(q, d):
+        out.append([float(sum(Fraction(int(qq)) * Fraction(dd)
+                              for qq, dd in zip(qrow[j:j + g], drow[j:j + g])))
+                    for j in range(0, len(qrow), g)])
+    return out
