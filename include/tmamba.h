@@ -58,7 +58,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 1
+#define TM_ABI_VERSION 2
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -161,6 +161,61 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
                    const uint16_t* scales_f16, int32_t count, int32_t B,
                    int64_t N, int64_t K, int32_t g, float* y, tm_stream stream);
+
+/*
+ * Scale-parameterization variants (paper appendix, Decoupled Quantization
+ * Ablations; Sec. 4, Zero-Ratio Collapse).
+ *
+ * tm_ternarize_pack_thresh — tm_ternarize_pack with a per-row rounding
+ * threshold: row n's codes divide by fl32(fl32(row_mult[n] * s) + eps)
+ * instead of fl32(s + eps).  The stored scales are still the group absmean
+ * s, which keeps scaling the codes.  This is the appendix's asymmetric gate
+ * thresholds: 0.8 x absmean on in_proj rows 0-4095, 1 elsewhere.
+ *   row_mult   float32 [N] or NULL (NULL: every multiplier 1, the same as
+ *              tm_ternarize_pack); 4-byte aligned, device memory.  Each
+ *              value must be finite and > 0; other values give unspecified
+ *              codes (they are not checked: the array is on the device).
+ *   every other argument as for tm_ternarize_pack.
+ */
+tm_status tm_ternarize_pack_thresh(const float* W, int64_t N, int64_t K, int32_t g,
+                                   float eps, const float* row_mult, uint8_t* codes,
+                                   float* scales, uint16_t* scales_f16,
+                                   uint64_t* zero_count, tm_stream stream);
+
+/*
+ * tm_ternarize_codes — the codes of a2/a3 against caller-given per-group
+ * thresholds instead of the absmean:
+ *   q[n, k] = RoundClip(W[n, k] / fl32(tau[n, k/g] + eps), -1, 1),
+ * packed and counted as by tm_ternarize_pack.  This is the forward of the
+ * learnable-scale layer of Sec. 4 (tau = the learned s_g, which also scales
+ * the codes) and of a fixed threshold tau_g chosen by the caller.
+ *   W     float32 [N, K]    in   (16-byte aligned)
+ *   tau   float32 [N, K/g]  in   (4-byte aligned); each value finite and
+ *         > 0, else the codes are unspecified (device data is not checked)
+ *   codes uint8 [N, K/4]    out  (16-byte aligned)
+ *   zero_count uint64 [1]   out, or NULL (8-byte aligned); zeroed on-stream
+ *   No scales are written.  Status codes and ownership as tm_ternarize_pack.
+ */
+tm_status tm_ternarize_codes(const float* W, int64_t N, int64_t K, int32_t g, float eps,
+                             const float* tau, uint8_t* codes, uint64_t* zero_count,
+                             tm_stream stream);
+
+/*
+ * tm_group_code_dot — gradient of a per-group magnitude that multiplies the
+ * codes:
+ *   out[n, j] = sum_{i < g} q[n, j*g + i] * dW[n, j*g + i].
+ * With What = alpha_g * q (decoupled quantization: the absmean only decides
+ * the codes) this is d alpha_g.  For a learnable scale (Sec. 4) it is the
+ * gradient through the magnitude; the hard forward rounding passes nothing
+ * back through the threshold.  dW is the gradient with respect to the
+ * dequantized weights, i.e. the output of tm_tgemm_bwd_dw_ste.
+ *   codes  uint8 [N, K/4]   in   (16-byte aligned), packed as above
+ *   dW     float32 [N, K]   in   (16-byte aligned)
+ *   out    float32 [N, K/g] out  (4-byte aligned); sums taken in float64,
+ *          rounded once
+ */
+tm_status tm_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, int64_t K,
+                            int32_t g, float* out, tm_stream stream);
 
 #ifdef __cplusplus
 }

@@ -29,6 +29,7 @@ SOURCES = [
     "tgemm_bwd_dx.hip",
     "tgemm_bwd_dw.hip",
     "tgemv.hip",
+    "group_code_dot.hip",
 ]
 
 ARCH = "gfx950"

@@ -72,6 +72,14 @@ const char* tm_status_str(tm_status s) {
 tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g, float eps,
                             uint8_t* codes, float* scales, uint16_t* scales_f16,
                             uint64_t* zero_count, tm_stream stream) {
+  return tm_ternarize_pack_thresh(W, N, K, g, eps, nullptr, codes, scales, scales_f16,
+                                  zero_count, stream);
+}
+
+tm_status tm_ternarize_pack_thresh(const float* W, int64_t N, int64_t K, int32_t g, float eps,
+                                   const float* row_mult, uint8_t* codes, float* scales,
+                                   uint16_t* scales_f16, uint64_t* zero_count,
+                                   tm_stream stream) {
   if (!W || !codes || !scales) return TM_EINVAL;
   if (!std::isfinite(eps) || eps < 0.f) return TM_EINVAL;
   if (N < 1) return TM_ESHAPE;
@@ -82,18 +90,55 @@ tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g, flo
     return TM_ESHAPE;
   if ((N * (K / 16) + 255) / 256 > kMaxGridBlocks) return TM_ESHAPE;
   if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) ||
-      !aligned(scales_f16, 2) || !aligned(zero_count, 8))
+      !aligned(scales_f16, 2) || !aligned(zero_count, 8) || !aligned(row_mult, 4))
     return TM_EALIGN;
   const Span in = span(W, wb), c = span(codes, cb), s = span(scales, sb),
-             h = span(scales_f16, scales_f16 ? hb : 0), z = span(zero_count, zero_count ? 8 : 0);
+             h = span(scales_f16, scales_f16 ? hb : 0), z = span(zero_count, zero_count ? 8 : 0),
+             m = span(row_mult, row_mult ? N * 4 : 0);
   const Span outs[4] = {c, s, h, z};
   for (int i = 0; i < 4; ++i) {
-    if (overlap(in, outs[i])) return TM_EINVAL;
+    if (overlap(in, outs[i]) || overlap(m, outs[i])) return TM_EINVAL;
     for (int j = i + 1; j < 4; ++j)
       if (overlap(outs[i], outs[j])) return TM_EINVAL;
   }
-  return hip_status(tmk::launch_ternarize_pack(W, N, K, g, eps, codes, scales, scales_f16,
-                                              zero_count, to_hip(stream)));
+  return hip_status(tmk::launch_ternarize_pack(W, N, K, g, eps, row_mult, nullptr, codes,
+                                              scales, scales_f16, zero_count, to_hip(stream)));
+}
+
+tm_status tm_ternarize_codes(const float* W, int64_t N, int64_t K, int32_t g, float eps,
+                             const float* tau, uint8_t* codes, uint64_t* zero_count,
+                             tm_stream stream) {
+  if (!W || !tau || !codes) return TM_EINVAL;
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t wb, cb, tb;
+  if (!bytes_of(N, K, 4, &wb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &tb))
+    return TM_ESHAPE;
+  if ((N * (K / 16) + 255) / 256 > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(W, 16) || !aligned(tau, 4) || !aligned(codes, 16) || !aligned(zero_count, 8))
+    return TM_EALIGN;
+  const Span c = span(codes, cb), z = span(zero_count, zero_count ? 8 : 0);
+  const Span ins[2] = {span(W, wb), span(tau, tb)};
+  for (const Span& in : ins)
+    if (overlap(in, c) || overlap(in, z)) return TM_EINVAL;
+  if (overlap(c, z)) return TM_EINVAL;
+  return hip_status(tmk::launch_ternarize_pack(W, N, K, g, eps, nullptr, tau, codes, nullptr,
+                                              nullptr, zero_count, to_hip(stream)));
+}
+
+tm_status tm_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, int64_t K,
+                            int32_t g, float* out, tm_stream stream) {
+  if (!codes || !dW || !out) return TM_EINVAL;
+  if (N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t cb, wb, ob;
+  if (!bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K, 4, &wb) || !bytes_of(N, K / g, 4, &ob))
+    return TM_ESHAPE;
+  if (!aligned(codes, 16) || !aligned(dW, 16) || !aligned(out, 4)) return TM_EALIGN;
+  const Span o = span(out, ob);
+  if (overlap(o, span(codes, cb)) || overlap(o, span(dW, wb))) return TM_EINVAL;
+  return hip_status(tmk::launch_group_code_dot(codes, dW, N, K, g, out, to_hip(stream)));
 }
 
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales, int64_t M,

@@ -7,8 +7,13 @@
 namespace tmk {
 
 hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, float eps,
-                                 uint8_t* codes, float* scales, uint16_t* scales_f16,
-                                 uint64_t* zero_count, hipStream_t stream);
+                                 const float* row_mult, const float* tau_in, uint8_t* codes,
+                                 float* scales,
+                                 uint16_t* scales_f16, uint64_t* zero_count,
+                                 hipStream_t stream);
+// out[n, j] = sum over group j of row n of q * dW (float64 sums, float32 out)
+hipError_t launch_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, int64_t K,
+                                 int g, float* out, hipStream_t stream);
 hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int g, float* Y,
                             hipStream_t stream);

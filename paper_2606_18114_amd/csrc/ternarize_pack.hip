@@ -26,9 +26,16 @@ __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 constexpr int kTernUnit = 1024;  // weights per wave iteration (4 loads x 64 lanes x 4)
 constexpr int kTernWaves = 16;   // waves per workgroup
 
+// row_mult (optional, [N]): the code of row n divides by fl32(row_mult[n] * s)
+// + eps instead of s + eps (the appendix's asymmetric gate thresholds); the
+// stored scale is the absmean either way.
+// tau_in (optional, [N, K/g]): the caller's per-group thresholds replace the
+// absmean (a learned scale, Sec. 4); no scales are written then.
 template <int G>
 __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
-    const float* __restrict__ W, int64_t total, float eps, uint32_t* __restrict__ codes,
+    const float* __restrict__ W, int64_t total, int64_t K, float eps,
+    const float* __restrict__ row_mult, const float* __restrict__ tau_in,
+    uint32_t* __restrict__ codes,
     float* __restrict__ scales, uint16_t* __restrict__ scales_f16,
     unsigned long long* __restrict__ zero_count) {
   constexpr int L = G / 4 < 64 ? G / 4 : 64;  // lanes holding one group within a load
@@ -74,8 +81,15 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
 
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float sc = (float)(ps[i] / (double)G);
-      const float d = sc + eps;
+      float sc = (float)(ps[i] / (double)G);
+      if (tau_in) sc = tau_in[(ok[i] ? base + 256 * i + 4 * lane : 0) / G];  // uniform branch
+      float tau = sc;
+      if (row_mult) {  // (uniform branch) the threshold of this element's row
+        const int64_t off = base + 256 * i + 4 * lane;
+        const int64_t row = (ok[i] ? off : 0) / K;
+        tau = __fmul_rn(row_mult[row], sc);  // rounded on its own: no fused m * s + eps
+      }
+      const float d = __fadd_rn(tau, eps);
       const double thr = (double)d * (0.5 + 0x1p-25);
       uint32_t part = 0;
 #pragma unroll
@@ -90,7 +104,7 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
       part |= __shfl_xor(part, 2, 64);
       const int64_t off = base + 256 * i + 4 * lane;
       if (ok[i] && (lane & 3) == 0) codes[off / 16] = part;
-      if (ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) {
+      if (!tau_in && ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) {
         const int64_t grp = off / G;
         scales[grp] = sc;
         if (scales_f16) scales_f16[grp] = __builtin_bit_cast(uint16_t, (_Float16)sc);
@@ -114,8 +128,10 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
 }
 
 hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, float eps,
-                                 uint8_t* codes, float* scales, uint16_t* scales_f16,
-                                 uint64_t* zero_count, hipStream_t stream) {
+                                 const float* row_mult, const float* tau_in, uint8_t* codes,
+                                 float* scales,
+                                 uint16_t* scales_f16, uint64_t* zero_count,
+                                 hipStream_t stream) {
   const int64_t total = N * K;
   auto* zc = reinterpret_cast<unsigned long long*>(zero_count);
   if (zc) {
@@ -130,11 +146,11 @@ hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, fl
   const dim3 grid((unsigned)blocks), block(64 * kTernWaves);
   auto* cw = reinterpret_cast<uint32_t*>(codes);
   switch (g) {
-    case 32:  hipLaunchKernelGGL(ternarize_pack_kernel<32>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
-    case 64:  hipLaunchKernelGGL(ternarize_pack_kernel<64>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
-    case 128: hipLaunchKernelGGL(ternarize_pack_kernel<128>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
-    case 256: hipLaunchKernelGGL(ternarize_pack_kernel<256>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
-    case 512: hipLaunchKernelGGL(ternarize_pack_kernel<512>, grid, block, 0, stream, W, total, eps, cw, scales, scales_f16, zc); break;
+    case 32:  hipLaunchKernelGGL(ternarize_pack_kernel<32>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
+    case 64:  hipLaunchKernelGGL(ternarize_pack_kernel<64>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
+    case 128: hipLaunchKernelGGL(ternarize_pack_kernel<128>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
+    case 256: hipLaunchKernelGGL(ternarize_pack_kernel<256>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
+    case 512: hipLaunchKernelGGL(ternarize_pack_kernel<512>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -33,6 +33,10 @@ SIGNATURES = {
     "tm_tgemm_bwd_dx": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
     "tm_tgemm_bwd_dw_ste": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _I32, _P]),
     "tm_tgemv": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _I64, _I32, _P, _P]),
+    "tm_ternarize_pack_thresh": (ctypes.c_int,
+                                 [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P, _P]),
+    "tm_group_code_dot": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P]),
+    "tm_ternarize_codes": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P]),
 }
 
 
@@ -100,11 +104,18 @@ def ternarize_pack(W: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
                    codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
                    scales_f16: Optional[torch.Tensor] = None,
                    zero_count: Optional[torch.Tensor] = None, want_f16: bool = True,
-                   want_zero_count: bool = True):
+                   want_zero_count: bool = True, row_mult: Optional[torch.Tensor] = None):
     """W float32 [N, K] -> (codes uint8 [N, K/4], scales f32 [N, K/g],
-    scales_f16 float16 [N, K/g] or None, zero_count int64 [1] or None)."""
+    scales_f16 float16 [N, K/g] or None, zero_count int64 [1] or None).
+
+    row_mult (float32 [N], optional) multiplies each row's rounding threshold
+    (``tm_ternarize_pack_thresh``); the stored scales stay the absmean."""
     _need(W, "W", _F32, 2)
     N, K = W.shape
+    if row_mult is not None:
+        _need(row_mult, "row_mult", _F32, 1)
+        if row_mult.shape[0] != N:
+            raise ValueError(f"row_mult has {row_mult.shape[0]} entries, W has {N} rows")
     dev = W.device
     if codes is None:
         codes = torch.empty((N, K // 4), dtype=torch.uint8, device=dev)
@@ -114,10 +125,52 @@ def ternarize_pack(W: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
         scales_f16 = torch.empty((N, max(K // g, 1)), dtype=torch.float16, device=dev)
     if zero_count is None and want_zero_count:
         zero_count = torch.empty((1,), dtype=torch.int64, device=dev)
-    st = lib().tm_ternarize_pack(_ptr(W), N, K, g, eps, _ptr(codes), _ptr(scales),
-                                 _ptr(scales_f16), _ptr(zero_count), _stream())
-    _check("tm_ternarize_pack", st)
+    if row_mult is None:
+        st = lib().tm_ternarize_pack(_ptr(W), N, K, g, eps, _ptr(codes), _ptr(scales),
+                                     _ptr(scales_f16), _ptr(zero_count), _stream())
+        _check("tm_ternarize_pack", st)
+    else:
+        st = lib().tm_ternarize_pack_thresh(_ptr(W), N, K, g, eps, _ptr(row_mult), _ptr(codes),
+                                            _ptr(scales), _ptr(scales_f16), _ptr(zero_count),
+                                            _stream())
+        _check("tm_ternarize_pack_thresh", st)
     return codes, scales, scales_f16, zero_count
+
+
+def ternarize_codes(W: torch.Tensor, tau: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
+                    codes: Optional[torch.Tensor] = None,
+                    zero_count: Optional[torch.Tensor] = None, want_zero_count: bool = True):
+    """Codes of W against the given per-group thresholds tau float32 [N, K/g]
+    -> (codes uint8 [N, K/4], zero_count int64 [1] or None)."""
+    _need(W, "W", _F32, 2)
+    _need(tau, "tau", _F32, 2)
+    N, K = W.shape
+    if tau.shape != (N, K // g):
+        raise ValueError(f"tau has shape {tuple(tau.shape)}, expected {(N, K // g)}")
+    if codes is None:
+        codes = torch.empty((N, K // 4), dtype=torch.uint8, device=W.device)
+    if zero_count is None and want_zero_count:
+        zero_count = torch.empty((1,), dtype=torch.int64, device=W.device)
+    st = lib().tm_ternarize_codes(_ptr(W), N, K, g, eps, _ptr(tau), _ptr(codes),
+                                  _ptr(zero_count), _stream())
+    _check("tm_ternarize_codes", st)
+    return codes, zero_count
+
+
+def group_code_dot(codes: torch.Tensor, dW: torch.Tensor, g: int = 128,
+                   out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """out[n, j] = sum over group j of row n of q * dW (float32 [N, K/g]): the
+    gradient of a per-group magnitude that multiplies the codes."""
+    _need(codes, "codes", _U8, 2)
+    _need(dW, "dW", _F32, 2)
+    N, K = dW.shape
+    if codes.shape != (N, K // 4):
+        raise ValueError(f"codes has shape {tuple(codes.shape)}, expected {(N, K // 4)}")
+    if out is None:
+        out = torch.empty((N, max(K // g, 1)), dtype=torch.float32, device=dW.device)
+    st = lib().tm_group_code_dot(_ptr(codes), _ptr(dW), N, K, g, _ptr(out), _stream())
+    _check("tm_group_code_dot", st)
+    return out
 
 
 def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,

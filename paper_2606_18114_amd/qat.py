@@ -13,6 +13,14 @@ the quantizer unchanged, so ``dX = dY . (q s)`` (``tm_tgemm_bwd_dx``) and
 ``dW = dY^T . X`` (``tm_tgemm_bwd_dw_ste``).  The incoming gradient is taken
 in bfloat16, the precision the backward kernels read.
 
+The scale variants the paper tests against this layer are options of the
+same module: a learned magnitude next to the absmean threshold (decoupled),
+a learned scale that is threshold and magnitude at once (learnable, whose
+zero ratio collapses in Sec. 4), and per-row threshold multipliers (the
+appendix's 0.8 x absmean on the gate rows).  Their extra calls are
+``tm_ternarize_pack_thresh``, ``tm_ternarize_codes`` and, in the backward,
+``tm_group_code_dot`` for the gradient of the learned scale.
+
 Every product runs in the library's kernels; this module only wires them
 into autograd (a dtype cast of the gradient and reshapes are the only torch
 operations on the data).  ``pack_for_decode`` returns the deployment format
@@ -28,12 +36,26 @@ import torch
 from . import ops
 
 
+SCALE_MODES = ("absmean", "decoupled", "learnable")
+
+
 class TernaryLinearFn(torch.autograd.Function):
-    """y = x . (q s)^T with q, s recomputed from `weight`; straight-through backward."""
+    """y = x . (q m)^T with straight-through backward.
+
+    mode "absmean": q and the magnitude m = s are recomputed from `weight`
+    (Sec. 3.1); `scale` is None.  mode "decoupled": q from the recomputed
+    absmean threshold, m = `scale` (a learned alpha_g, appendix Decoupled
+    Quantization Ablations).  mode "learnable": `scale` is the learned s_g of
+    Sec. 4, used as the rounding threshold and as the magnitude.  `row_mult`
+    (float32 [out] or None) multiplies each row's absmean threshold.
+    The gradient of a learned magnitude is sum_group q * dWhat; the hard
+    forward rounding passes nothing back through the threshold.
+    """
 
     @staticmethod
-    def forward(ctx, x: torch.Tensor, weight: torch.Tensor, g: int, eps: float,
-                zero_count: Optional[torch.Tensor]) -> torch.Tensor:
+    def forward(ctx, x: torch.Tensor, weight: torch.Tensor, scale: Optional[torch.Tensor],
+                g: int, eps: float, zero_count: Optional[torch.Tensor], mode: str,
+                row_mult: Optional[torch.Tensor]) -> torch.Tensor:
         N, K = weight.shape
         if x.shape[-1] != K:
             raise ValueError(f"x has {x.shape[-1]} features, the layer takes {K}")
@@ -42,62 +64,119 @@ class TernaryLinearFn(torch.autograd.Function):
         if x2.dtype != torch.bfloat16:
             raise TypeError(f"x must be bfloat16 (got {x2.dtype}): the layer is W1.58A16")
         x2 = x2.contiguous()
-        codes, scales, _, _ = ops.ternarize_pack(weight.detach().contiguous(), g, eps,
-                                                 zero_count=zero_count, want_f16=False,
-                                                 want_zero_count=zero_count is not None)
-        y = ops.tgemm_fwd(x2, codes, scales, g)
-        ctx.save_for_backward(x2, codes, scales)
+        w = weight.detach().contiguous()
+        want_zc = zero_count is not None
+        if mode == "learnable":
+            mag = scale.detach().contiguous()
+            codes, _ = ops.ternarize_codes(w, mag, g, eps, zero_count=zero_count,
+                                           want_zero_count=want_zc)
+        else:
+            codes, absmean, _, _ = ops.ternarize_pack(w, g, eps, zero_count=zero_count,
+                                                      want_f16=False, want_zero_count=want_zc,
+                                                      row_mult=row_mult)
+            mag = absmean if mode == "absmean" else scale.detach().contiguous()
+        y = ops.tgemm_fwd(x2, codes, mag, g)
+        ctx.save_for_backward(x2, codes, mag)
         ctx.g = g
         ctx.lead = lead
         ctx.x_dtype = x.dtype
+        ctx.learned = mode != "absmean"
         return y.reshape(*lead, N)
 
     @staticmethod
     def backward(ctx, gy: torch.Tensor):
-        x2, codes, scales = ctx.saved_tensors
+        x2, codes, mag = ctx.saved_tensors
         N = codes.shape[0]
         dy = gy.reshape(-1, N)
         if dy.dtype != torch.bfloat16:
             dy = dy.to(torch.bfloat16)
         dy = dy.contiguous()
-        dx = dw = None
+        dx = dw = dscale = None
         if ctx.needs_input_grad[0]:
-            dx = ops.tgemm_bwd_dx(dy, codes, scales, ctx.g)
+            dx = ops.tgemm_bwd_dx(dy, codes, mag, ctx.g)
             dx = dx.to(ctx.x_dtype).reshape(*ctx.lead, x2.shape[1])
-        if ctx.needs_input_grad[1]:
-            dw = ops.tgemm_bwd_dw_ste(dy, x2)
-        return dx, dw, None, None, None
+        want_scale = ctx.learned and ctx.needs_input_grad[2]
+        if ctx.needs_input_grad[1] or want_scale:
+            dw_hat = ops.tgemm_bwd_dw_ste(dy, x2)   # gradient w.r.t. the dequantized weights
+            if want_scale:
+                dscale = ops.group_code_dot(codes, dw_hat, ctx.g)
+            if ctx.needs_input_grad[1]:
+                dw = dw_hat
+        return dx, dw, dscale, None, None, None, None, None
 
 
 class TernaryLinear(torch.nn.Module):
     """Grouped-absmean ternary linear layer (no bias; the Mamba-2 projections
     have none).  weight: float32 [out_features, in_features]; groups of `g`
-    consecutive input features of one output row share a scale."""
+    consecutive input features of one output row share a scale.
+
+    scale_mode "absmean" (the paper's layer): the scale is recomputed from
+    the weights on every call and is not a parameter.  "decoupled": codes
+    from the recomputed absmean, magnitude the parameter `scale`.
+    "learnable": the parameter `scale` is both threshold and magnitude.  The
+    parameter starts at the absmean of the weights (``reset_scale``, run on
+    the first call if not done before).  threshold_mult (float32 [out]) scales
+    each row's absmean threshold (e.g. 0.8 on the gate rows of in_proj).
+    """
 
     def __init__(self, in_features: int, out_features: int, g: int = 128, eps: float = 1e-5,
-                 device: Optional[torch.device] = None, track_zero_ratio: bool = True):
+                 device: Optional[torch.device] = None, track_zero_ratio: bool = True,
+                 scale_mode: str = "absmean", threshold_mult: Optional[torch.Tensor] = None):
         super().__init__()
         if in_features % g or in_features % 64:
             raise ValueError(f"in_features={in_features} must be a multiple of g={g} and of 64")
+        if scale_mode not in SCALE_MODES:
+            raise ValueError(f"scale_mode must be one of {SCALE_MODES}")
+        if threshold_mult is not None:
+            if scale_mode == "learnable":
+                raise ValueError("a learnable scale is its own threshold: no threshold_mult")
+            if threshold_mult.shape != (out_features,):
+                raise ValueError(f"threshold_mult must have shape ({out_features},)")
         self.in_features, self.out_features, self.g, self.eps = in_features, out_features, g, eps
+        self.scale_mode = scale_mode
         self.weight = torch.nn.Parameter(
             torch.empty((out_features, in_features), dtype=torch.float32, device=device))
         torch.nn.init.normal_(self.weight, 0.0, 0.02)
+        if scale_mode == "absmean":
+            self.scale = None
+        else:
+            self.scale = torch.nn.Parameter(
+                torch.zeros((out_features, in_features // g), dtype=torch.float32, device=device))
+        self._scale_ready = scale_mode == "absmean"
+        self.register_buffer(
+            "threshold_mult",
+            None if threshold_mult is None
+            else threshold_mult.detach().to(device=device, dtype=torch.float32).contiguous())
         self._zc = (torch.zeros((1,), dtype=torch.int64, device=device)
                     if track_zero_ratio else None)
 
     @classmethod
-    def from_weight(cls, weight: torch.Tensor, g: int = 128, eps: float = 1e-5) -> "TernaryLinear":
+    def from_weight(cls, weight: torch.Tensor, g: int = 128, eps: float = 1e-5,
+                    **kw) -> "TernaryLinear":
         """Wrap existing (e.g. pretrained) float weights [out, in]."""
-        m = cls(weight.shape[1], weight.shape[0], g, eps, device=weight.device)
+        m = cls(weight.shape[1], weight.shape[0], g, eps, device=weight.device, **kw)
         with torch.no_grad():
             m.weight.copy_(weight.float())
+        if m.scale is not None and weight.is_cuda:
+            m.reset_scale()
         return m
+
+    @torch.no_grad()
+    def reset_scale(self) -> None:
+        """Set the learned scale to the absmean of the current weights."""
+        if self.scale is None:
+            raise RuntimeError("the absmean layer has no scale parameter")
+        ops.ternarize_pack(self.weight.detach().contiguous(), self.g, self.eps,
+                           scales=self.scale.data, want_f16=False, want_zero_count=False)
+        self._scale_ready = True
 
     def forward(self, x: torch.Tensor) -> torch.Tensor:
         if self._zc is not None and self._zc.device != self.weight.device:
             self._zc = self._zc.to(self.weight.device)
-        return TernaryLinearFn.apply(x, self.weight, self.g, self.eps, self._zc)
+        if not self._scale_ready:
+            self.reset_scale()
+        return TernaryLinearFn.apply(x, self.weight, self.scale, self.g, self.eps, self._zc,
+                                     self.scale_mode, self.threshold_mult)
 
     def zero_ratio(self) -> float:
         """Fraction of zero codes in the last forward call (Sec. 3.1 tracks it
@@ -110,13 +189,23 @@ class TernaryLinear(torch.nn.Module):
     def pack_for_decode(self) -> Tuple[torch.Tensor, torch.Tensor]:
         """(codes uint8 [out, in/4], scales float16 [out, in/g]) of the current
         weights: the storage format of the decode GEMV."""
-        codes, _, s16, _ = ops.ternarize_pack(self.weight.detach().contiguous(), self.g,
-                                              self.eps, want_zero_count=False)
-        return codes, s16
+        w = self.weight.detach().contiguous()
+        if self.scale_mode == "absmean":
+            codes, _, s16, _ = ops.ternarize_pack(w, self.g, self.eps, want_zero_count=False,
+                                                  row_mult=self.threshold_mult)
+            return codes, s16
+        if self.scale_mode == "learnable":
+            codes, _ = ops.ternarize_codes(w, self.scale.detach().contiguous(), self.g, self.eps,
+                                           want_zero_count=False)
+        else:
+            codes, _, _, _ = ops.ternarize_pack(w, self.g, self.eps, want_f16=False,
+                                                want_zero_count=False,
+                                                row_mult=self.threshold_mult)
+        return codes, self.scale.detach().to(torch.float16)
 
     def extra_repr(self) -> str:
         return (f"in_features={self.in_features}, out_features={self.out_features}, "
-                f"g={self.g}, eps={self.eps}")
+                f"g={self.g}, eps={self.eps}, scale_mode={self.scale_mode}")
 
 
 def flops_per_step(tokens: int, layer: TernaryLinear) -> float:
@@ -125,4 +214,4 @@ def flops_per_step(tokens: int, layer: TernaryLinear) -> float:
     return 3.0 * 2.0 * tokens * layer.in_features * layer.out_features
 
 
-__all__ = ["TernaryLinear", "TernaryLinearFn", "flops_per_step"]
+__all__ = ["SCALE_MODES", "TernaryLinear", "TernaryLinearFn", "flops_per_step"]

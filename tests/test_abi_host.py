@@ -33,11 +33,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 7
+    assert len(names) == 10
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 1
+    assert L.tm_abi_version() == 2
 
 
 def test_status_strings(L):
@@ -75,6 +75,64 @@ def test_ternarize_pack_validation(L):
     assert tp(L, scales=P + 2 ** 20 + 16) == EINVAL
     assert tp(L, s16=P + 2 ** 21) == EINVAL
     assert tp(L, zc=P + 2 ** 20) == EINVAL
+
+
+def tpt(L, W=P, N=8, K=128, g=128, eps=1e-5, mult=P + 2 ** 23, codes=P + 2 ** 20,
+        scales=P + 2 ** 21, s16=0, zc=0):
+    return L.tm_ternarize_pack_thresh(W, N, K, g, eps, mult, codes, scales, s16, zc, None)
+
+
+def test_ternarize_pack_thresh_validation(L):
+    # the standard checks apply unchanged
+    assert tpt(L, W=0) == EINVAL
+    assert tpt(L, eps=float("nan")) == EINVAL
+    assert tpt(L, g=100) == ESHAPE
+    assert tpt(L, K=192, g=128) == ESHAPE
+    assert tpt(L, W=P + 4) == EALIGN
+    assert tpt(L, codes=P + 64) == EINVAL
+    # the multiplier array: 4-byte aligned, not overlapping an output
+    assert tpt(L, mult=P + 2 ** 23 + 2) == EALIGN
+    assert tpt(L, mult=P + 2 ** 21) == EINVAL            # overlaps the scales
+    assert tpt(L, mult=P + 2 ** 20 + 4) == EINVAL        # overlaps the codes
+
+
+def tc(L, W=P, N=8, K=128, g=128, eps=1e-5, tau=P + 2 ** 23, codes=P + 2 ** 20, zc=0):
+    return L.tm_ternarize_codes(W, N, K, g, eps, tau, codes, zc, None)
+
+
+def test_ternarize_codes_validation(L):
+    for kw in ("W", "tau", "codes"):
+        assert tc(L, **{kw: 0}) == EINVAL, kw
+    assert tc(L, eps=-1.0) == EINVAL
+    assert tc(L, N=0) == ESHAPE
+    assert tc(L, K=192, g=128) == ESHAPE
+    assert tc(L, g=48) == ESHAPE
+    assert tc(L, W=P + 8) == EALIGN
+    assert tc(L, tau=P + 2 ** 23 + 2) == EALIGN
+    assert tc(L, codes=P + 2 ** 20 + 4) == EALIGN
+    assert tc(L, zc=P + 2 ** 22 + 4) == EALIGN
+    assert tc(L, codes=P + 512) == EINVAL               # overlaps W
+    assert tc(L, codes=P + 2 ** 23) == EINVAL           # overlaps tau
+    assert tc(L, zc=P + 2 ** 20 + 8) == EINVAL          # overlaps the codes
+
+
+def gcd(L, codes=P, dW=P + 2 ** 24, N=8, K=512, g=128, out=P + 2 ** 26):
+    return L.tm_group_code_dot(codes, dW, N, K, g, out, None)
+
+
+def test_group_code_dot_validation(L):
+    for kw in ("codes", "dW", "out"):
+        assert gcd(L, **{kw: 0}) == EINVAL, kw
+    assert gcd(L, N=0) == ESHAPE
+    assert gcd(L, K=96, g=32) == ESHAPE
+    assert gcd(L, K=256, g=512) == ESHAPE
+    assert gcd(L, g=16) == ESHAPE
+    assert gcd(L, N=2 ** 40, K=2 ** 20) == ESHAPE
+    assert gcd(L, codes=P + 8) == EALIGN
+    assert gcd(L, dW=P + 2 ** 24 + 4) == EALIGN
+    assert gcd(L, out=P + 2 ** 26 + 2) == EALIGN
+    assert gcd(L, out=P + 256) == EINVAL                 # overlaps the codes
+    assert gcd(L, out=P + 2 ** 24 + 1024) == EINVAL      # overlaps dW
 
 
 def fwd(L, X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):
