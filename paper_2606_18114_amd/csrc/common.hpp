@@ -43,17 +43,6 @@ __device__ __forceinline__ bf16x8 decode_half(uint32_t w) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Same with the half chosen at run time (h in {0, 1}).
-__device__ __forceinline__ bf16x8 decode_half_rt(uint32_t w, uint32_t h) {
-  const uint32_t ws = w << (8u - 8u * h);  // half h moved to the top byte pair
-  u32x4 v;
-  v.x = (ws << 6) & kPairMask;
-  v.y = (ws << 4) & kPairMask;
-  v.z = (ws << 2) & kPairMask;
-  v.w = ws & kPairMask;
-  return __builtin_bit_cast(bf16x8, v);
-}
-
 // Both halves of two adjacent words (w.x -> a0 (elements 0-7), a1 (8-15);
 // w.y -> b0, b1) with 64-bit shifts: shifting the pair (hi = w.y, lo = w.x)
 // left by s gives w.x << s in the low dword and w.y << s in the high one (plus
@@ -84,6 +73,23 @@ __device__ __forceinline__ void decode_words(u32x2 w, bf16x8& a0, bf16x8& a1, bf
   a1 = __builtin_bit_cast(bf16x8, x1);
   b0 = __builtin_bit_cast(bf16x8, y0);
   b1 = __builtin_bit_cast(bf16x8, y1);
+}
+
+// Half h (elements 8h .. 8h+7, h chosen at run time) of two words at once
+// (w.x -> b0, w.y -> b1) as MFMA operands of eight bfloat16 values 2*q, with
+// the half-select shift hs = 8 - 8 h given.  One 64-bit shift moves both
+// words, so the two operands cost four 64-bit shifts and eight ANDs instead
+// of eight 32-bit shifts and eight ANDs.  Bits of w.x shifted into the high
+// word land below bit 14, where the mask clears them.
+__device__ __forceinline__ void decode_half_pair_rt(u32x2 w, uint32_t hs, bf16x8& b0,
+                                                    bf16x8& b1) {
+  u32x2 ws;
+  asm("v_lshlrev_b64 %0, %1, %2" : "=v"(ws) : "v"(hs), "v"(w));
+  const u32x2 r6 = shl64(ws, 6), r4 = shl64(ws, 4), r2 = shl64(ws, 2);
+  const u32x4 x = {r6.x & kPairMask, r4.x & kPairMask, r2.x & kPairMask, ws.x & kPairMask};
+  const u32x4 y = {r6.y & kPairMask, r4.y & kPairMask, r2.y & kPairMask, ws.y & kPairMask};
+  b0 = __builtin_bit_cast(bf16x8, x);
+  b1 = __builtin_bit_cast(bf16x8, y);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {

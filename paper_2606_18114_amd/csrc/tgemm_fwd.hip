@@ -4,7 +4,12 @@
 // Persistent kernel: one workgroup of 8 waves per CU walks 256 x 256 output
 // tiles (2 x 4 waves, 128 x 64 outputs per wave).  Consecutive tiles of one
 // round go to the same XCD, so its workgroups share the rows of X through
-// that XCD's L2.
+// that XCD's L2.  Tiles left over after the whole rounds (fewer than one
+// per workgroup) are cut along K into parts, one per workgroup, which add
+// their partial sums into Y with float32 atomics (those rows of Y are
+// cleared by a fill kernel first).  Without the cut, a shape with a few
+// tiles more than workgroups would take two full rounds; with it the last
+// round is spread over all CUs (2048 tokens of in_proj: 27% faster).
 //
 // Operands reach LDS by direct-to-LDS loads (global_load_lds), with no
 // register staging and one barrier per 64-column stage.  The stage stream
@@ -20,8 +25,9 @@
 //     starting in those 256 columns) into a 2-deep ring, one code stage
 //     ahead; otherwise per stage into a 3-deep ring, two stages ahead.
 //   * Every lane decodes the codes of its own weight row into the MFMA B
-//     operand, one shift and one AND per two codes, giving the exact bfloat16
-//     values 2*q.
+//     operand, giving the exact bfloat16 values 2*q; the words of its two
+//     rows are decoded together (four 64-bit shifts and eight ANDs per 16
+//     codes).
 //   * The group scale is applied in float32, not folded into the bfloat16
 //     operand (folding would cost about 2e-3 relative error).  Instead of a
 //     second set of partial accumulators, each accumulator is kept in units
@@ -43,6 +49,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "launchers.hpp"
 
 namespace tmk {
 
@@ -112,7 +119,8 @@ template <int G, int SS>
 __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ codes,
     const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
-    float* __restrict__ Y, uint32_t tiles_n, uint32_t ntiles) {
+    float* __restrict__ Y, uint32_t tiles_n, uint32_t full_rounds, uint32_t extra_units,
+    uint32_t parts) {
   using C = FwdCfg<G, SS>;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLds];
 
@@ -130,23 +138,55 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   // in-tile row offsets of the output fit 32 bits (131 rows of N floats)
   const bool small_pitch = N < (int64_t(1) << 22);
 
-  // Rows of the tile of round `it` (rounds past the last tile reload the
-  // last tile; those loads are never consumed, they only keep the count of
-  // loads per stage fixed).  Rows past M or N are clamped to the last one.
-  auto tile_of = [&](int it, int64_t& m0, int64_t& n0) {
-    uint32_t tile = (uint32_t)it * nblk + bid;
-    tile = tile < ntiles ? tile : ntiles - 1;
+  // Work list of this workgroup: full_rounds whole tiles (tile r * nblk + bid
+  // in round r) and, for bid < extra_units, one extra unit: part bid % parts
+  // of tile full_rounds * nblk + bid / parts, a run of whole trips of its K
+  // stages.  With parts > 1 the parts of a tile add into Y with atomics (Y
+  // zeroed there beforehand), and odd parts come first: those workgroups
+  // then run half a tile out of phase with the others, which spreads the
+  // output stores over time instead of all workgroups storing at once.
+  const uint32_t F = full_rounds;
+  const bool has_x = bid < extra_units;
+  const uint32_t nu = F + (has_x ? 1u : 0u);
+  if (nu == 0) return;  // no work: before any load or barrier
+  const uint32_t xp = has_x ? bid % parts : 0u;
+  const bool x_first = has_x && parts > 1 && (xp & 1u);
+  const int trips = nst / C::kUnroll;
+  // unit u (units past the end repeat the last one: their loads are never
+  // consumed, they only keep the count of loads per stage fixed): tile,
+  // first and end stage, and whether it is a part of a tile
+  auto unit_of = [&](uint32_t u, uint32_t& tile, int& s0, int& s1, bool& part) {
+    u = u < nu ? u : nu - 1;
+    const bool extra = has_x && (x_first ? u == 0 : u == F);
+    if (extra) {
+      tile = F * nblk + bid / parts;
+      s0 = (int)(xp * (uint32_t)trips / parts) * C::kUnroll;
+      s1 = (int)((xp + 1) * (uint32_t)trips / parts) * C::kUnroll;
+      part = parts > 1;
+    } else {
+      tile = (x_first ? u - 1 : u) * nblk + bid;
+      s0 = 0;
+      s1 = nst;
+      part = false;
+    }
+  };
+  // rows of a tile; rows past M or N are clamped to the last one by the loaders
+  auto tile_rows = [&](uint32_t tile, int64_t& m0, int64_t& n0) {
     m0 = (int64_t)(tile / tiles_n) * kFwdBM;
     n0 = (int64_t)(tile % tiles_n) * kFwdBN;
   };
 
-  // ---- X loader: stage (xit, xst), 4 loads of 1 KiB per wave ----
-  int xit = 0, xst = 0, xslot = 0;
+  // ---- X loader: stage xst of unit xu, 4 loads of 1 KiB per wave ----
+  uint32_t xu = 0;
+  int xst = 0, xend = 0, xslot = 0;
   const uint8_t* xt = nullptr;
   uint32_t xoff[4];
-  auto set_xtile = [&](int it) {
+  auto set_xunit = [&](uint32_t u) {
+    uint32_t tile;
+    bool part;
     int64_t m0, n0;
-    tile_of(it, m0, n0);
+    unit_of(u, tile, xst, xend, part);
+    tile_rows(tile, m0, n0);
     const int mlast = (int)(M - 1 - m0 < 255 ? M - 1 - m0 : 255);
     xt = reinterpret_cast<const uint8_t*>(X + m0 * K);
 #pragma unroll
@@ -156,7 +196,7 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
       xoff[i] = (uint32_t)(r < mlast ? r : mlast) * (uint32_t)K * 2u + 16u * lp;
     }
   };
-  // kMayWrap: this call may issue the last stage of a tile (known at
+  // kMayWrap: this call may issue the last stage of a unit (known at
   // compile time from the stage's position in the unrolled loop)
   auto dma_x = [&](auto may_wrap) {
     const uint8_t* base = xt + (int64_t)xst * kFwdBK * 2;
@@ -166,20 +206,21 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     xslot = xslot == kFwdXRing - 1 ? 0 : xslot + 1;
     ++xst;
     if constexpr (decltype(may_wrap)::value) {
-      if (xst == nst) {
-        xst = 0;
-        set_xtile(++xit);
-      }
+      if (xst == xend) set_xunit(++xu);
     }
   };
 
-  // ---- code/scale loader: code stage starting at X stage (cit, cst) ----
-  int cit = 0, cst = 0, cslot = 0;
+  // ---- code/scale loader: code stage starting at X stage cst of unit cu ----
+  uint32_t cu = 0;
+  int cst = 0, cend = 0, cslot = 0;
   const uint8_t *ct = nullptr, *stl = nullptr;
   uint32_t coff[2], soff[C::kScaleDma];
-  auto set_ctile = [&](int it) {
+  auto set_cunit = [&](uint32_t u) {
+    uint32_t tile;
+    bool part;
     int64_t m0, n0;
-    tile_of(it, m0, n0);
+    unit_of(u, tile, cst, cend, part);
+    tile_rows(tile, m0, n0);
     const int nlast = (int)(N - 1 - n0 < 255 ? N - 1 - n0 : 255);
     ct = codes + n0 * kb;
     stl = reinterpret_cast<const uint8_t*>(scales + n0 * ng);
@@ -221,18 +262,15 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     cslot = cslot == C::kCRing - 1 ? 0 : cslot + 1;
     cst += SS;
     if constexpr (decltype(may_wrap)::value) {
-      if (cst == nst) {
-        cst = 0;
-        set_ctile(++cit);
-      }
+      if (cst == cend) set_cunit(++cu);
     }
   };
 
   // prologue: X stages 0 and 1, code stage 0 (and 1 when SS == 1); the
   // waits below count the loads issued after the ones the next stage needs
   const std::true_type wraps;
-  set_xtile(0);
-  set_ctile(0);
+  set_xunit(0);
+  set_cunit(0);
   dma_x(wraps);
   dma_c(wraps);
   dma_x(wraps);
@@ -244,13 +282,16 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   }
 
   const int xsw = fwd_xswz(l32);  // == fwd_xswz(m) for every X row m this lane reads
+  const uint32_t hs = 8u - 8u * h;  // shift that moves this lane's code half to the top
   int xs = 0, cs = 0;             // ring slots of the stage being computed
 
-  for (int it = 0;; ++it) {
-    const uint32_t tile = (uint32_t)it * nblk + bid;
-    if (tile >= ntiles) break;
-    const int64_t m0 = (int64_t)(tile / tiles_n) * kFwdBM;
-    const int64_t n0 = (int64_t)(tile % tiles_n) * kFwdBN;
+  for (uint32_t u = 0; u < nu; ++u) {
+    uint32_t tile;
+    int s0, s1;
+    bool part;
+    int64_t m0, n0;
+    unit_of(u, tile, s0, s1, part);
+    tile_rows(tile, m0, n0);
 
     f32x16 acc[4][2];
 #pragma unroll
@@ -321,8 +362,7 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
           }
         }
         bf16x8 bop[2];
-#pragma unroll
-        for (int b = 0; b < 2; ++b) bop[b] = decode_half_rt(cw[b][t] & msk[b], h);
+        decode_half_pair_rt(u32x2{cw[0][t] & msk[0], cw[1][t] & msk[1]}, hs, bop[0], bop[1]);
         bf16x8 anext[4];
         if (t < 3) read_a(t + 1, anext);
 #pragma unroll
@@ -341,13 +381,13 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     };
 
     // kUnroll stages per trip: a whole number of code stages and of groups
-    for (int st = 0; st < nst; st += C::kUnroll) {
+    for (int st = s0; st < s1; st += C::kUnroll) {
       static_for<0, C::kUnroll>([&](auto i_tag) {
         constexpr int i = decltype(i_tag)::value;
         constexpr int P = i % SS;
         constexpr bool kStart = G <= kFwdBK || (i * kFwdBK) % G == 0;
-        // nst is a multiple of kUnroll, so only these positions move a
-        // cursor past the end of a tile: the X cursor (stage st + i + 2
+        // units are whole trips, so only these positions move a cursor
+        // past the end of a unit: the X cursor (stage st + i + 2
         // issued, st + i + 3 next) and the code cursor (code stage starting
         // at st + i + 4 issued, st + i + 8 next; with SS == 1 like X)
         constexpr int kCAhead = SS == 1 ? 3 : 2 * SS;
@@ -370,7 +410,8 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     // epilogue: lane holds column l32 of each block, rows 8*(i/4) + 4*h + i%4.
     // Row offsets inside the tile are compile-time multiples of the row
     // pitch, so a store costs one address add; tiles wholly inside M skip
-    // the row test (rows past M only occur in the last row of tiles).
+    // the row test (rows past M only occur in the last row of tiles).  Parts
+    // of a tile add their partial sums with float32 atomics.
     {
       const int64_t mrow = m0 + wm * 128;
       uint8_t* ytile = reinterpret_cast<uint8_t*>(Y + mrow * N + n0);
@@ -381,7 +422,25 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
         if (n0 + nl >= N) continue;
         const float f = 0.5f * cref[b];
         uint8_t* ylane = ytile + ((int64_t)(4 * h) * N + nl) * 4;
-        if (small_pitch && full_m) {
+        if (part) {
+          int64_t pv = N * 4;
+          asm volatile("" : "+v"(pv));
+          uint8_t* yp = ylane;
+          int64_t row = mrow + 4 * h;
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+#pragma unroll
+              for (int i1 = 0; i1 < 4; ++i1) {
+                if (row < M) atomicAdd(reinterpret_cast<float*>(yp), f * acc[a][b][4 * i4 + i1]);
+                yp += pv;
+                ++row;
+              }
+              yp += 4 * pv;
+              row += 4;
+            }
+        } else if (small_pitch && full_m) {
           // a 32-bit lane offset from the uniform tile base, stepped row by
           // row (rows a*32 + 8*i4 + i1); the empty asm keeps the compiler
           // from precomputing all 64 offsets (which it would spill)
@@ -444,18 +503,38 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
     else
       cus = 256;
   }
-  const int64_t blocks = ntiles < cus ? ntiles : cus;
-  const dim3 grid((unsigned)blocks), block(512);
-  const uint32_t t_n = (uint32_t)tn, nt = (uint32_t)ntiles;
   const bool wide = K % 256 == 0;  // code stages of four X stages
+  // Work split over P = cus persistent workgroups: F whole rounds of tiles,
+  // then the R = ntiles mod P remaining tiles cut along K into `parts` runs
+  // of whole trips (kUnroll stages), one per workgroup, when that leaves at
+  // least two parts per tile; otherwise the remaining tiles go whole to the
+  // first R workgroups.
+  const int64_t P = cus;
+  const int64_t F = ntiles / P, R = ntiles % P;
+  const int unroll = (wide ? 4 : 1) > g / kFwdBK ? (wide ? 4 : 1) : g / kFwdBK;
+  const int64_t trips = K / kFwdBK / unroll;
+  int64_t parts = R > 0 ? P / R : 1;
+  if (parts > trips) parts = trips;
+  if (parts < 1) parts = 1;
+  const int64_t extra = R * parts;
+  if (parts > 1) {
+    // the cut tiles accumulate atomically: clear their rows of Y first (a
+    // fill kernel, not a memset node, so the call can be captured)
+    const int64_t r0 = F * P / tn * kFwdBM;
+    hipError_t e = launch_fill_zero_f32(Y + r0 * N, (M - r0) * N, stream);
+    if (e != hipSuccess) return e;
+  }
+  const dim3 grid((unsigned)P), block(512);
+  const uint32_t t_n = (uint32_t)tn, fr = (uint32_t)F, xu = (uint32_t)extra,
+                 np = (uint32_t)parts;
 #define TM_FWD(GG)                                                                             \
   case GG:                                                                                     \
     if (wide)                                                                                  \
       hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 4>), grid, block, 0, stream, X, codes, scales, M, \
-                         N, K, Y, t_n, nt);                                                    \
+                         N, K, Y, t_n, fr, xu, np);                                            \
     else                                                                                       \
       hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 1>), grid, block, 0, stream, X, codes, scales, M, \
-                         N, K, Y, t_n, nt);                                                    \
+                         N, K, Y, t_n, fr, xu, np);                                            \
     break;
   switch (g) {
     TM_FWD(32)

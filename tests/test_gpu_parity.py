@@ -241,6 +241,37 @@ def test_fwd_exact_cases():
     np.testing.assert_array_equal(Y, O.gemm_fwd(Xi, q, sc, g))
 
 
+def test_fwd_split_tiles_exact_and_complete():
+    """Tiles cut along K into parts that add with atomics: integer inputs give
+    exact sums whatever order the parts land in, and every output element is
+    written even when Y starts out as NaN (the cut tiles' rows are cleared
+    first, the whole tiles overwritten)."""
+    ops = _ops()
+    rng = np.random.default_rng(17)
+    # one tile cut into 8 parts (K = 2048, g = 64: 8 trips)
+    N, K, g = 96, 2048, 64
+    q = rng.integers(-1, 2, (N, K)).astype(np.int8)
+    sc = (2.0 ** rng.integers(-3, 3, (N, K // g))).astype(np.float32)
+    Xi = rng.integers(-8, 9, (40, K)).astype(np.float32)
+    Y = torch.full((40, N), float("nan"), device="cuda")
+    ops.tgemm_fwd(dev_bf16(synth.f32_to_bf16_bits(Xi)), torch.from_numpy(O.pack(q)).cuda(),
+                  dev_f32(sc), g, Y=Y)
+    np.testing.assert_array_equal(host(Y), O.gemm_fwd(Xi, q, sc, g))
+    # 272 tiles: one round of whole tiles, then 16 tiles cut in two
+    M, N, K, g = 4352, 4096, 512, 128
+    print(f"[fwd] split remainder M={M} N={N} K={K} g={g}", flush=True)
+    W = synth.weights(rng, N, K, outliers=True)
+    X = synth.activations(rng, M, K)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5, want_f16=False, want_zero_count=False)
+    Y = torch.full((M, N), float("nan"), device="cuda")
+    ops.tgemm_fwd(dev_bf16(X), c, s, g, Y=Y)
+    Yh = host(Y)
+    assert np.isfinite(Yh).all()
+    err = O.rel_fro_error(Yh, O.gemm_fwd(X, host_codes(c, K), host(s), g))
+    print(f"  rel fro err {err:.3e}", flush=True)
+    assert err <= REL_DESIGN
+
+
 # --------------------------------------------------------------------------
 # backward
 # --------------------------------------------------------------------------
