@@ -49,7 +49,15 @@ def parse():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--sweep-g", action="store_true",
                     help="group-size workload (in_proj W, X 2048 x 2048, g = 32 .. 512)")
-    return ap.parse_args()
+    ap.add_argument("--skip", default="",
+                    help="comma list of optional sections to leave out: qat, variants "
+                         "(keeps a profiler trace to the kernels of interest)")
+    args = ap.parse_args()
+    args.skip = {x for x in args.skip.split(",") if x}
+    bad = args.skip - {"qat", "variants"}
+    if bad:
+        ap.error(f"unknown --skip sections: {sorted(bad)}")
+    return args
 
 
 def log(msg):
@@ -218,10 +226,11 @@ def main():
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
 
     # ---------------- QAT block: both projections through autograd ----------------
-    qat_block = qat_block_step(args, dev, X, synth)
+    qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
 
     # ---------------- scale variants on the in_proj shapes ----------------
-    variants = variants_step(args, ops, W, scales, codes, dW, g, eps)
+    variants = (None if "variants" in args.skip
+                else variants_step(args, ops, W, scales, codes, dW, g, eps))
 
     # ---------------- algorithmic work per launch ----------------
     fl = 2.0 * M * N * K
