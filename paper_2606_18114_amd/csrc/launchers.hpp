@@ -4,7 +4,27 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace tmk {
+
+// Compute units of the current device (the persistent grids are sized by
+// it), cached per device; safe to call from several host threads.
+inline int current_cu_count() {
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cache[kMaxDev];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < kMaxDev) {
+    const int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+  }
+  int v = 0;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+    v = 256;
+  if (dev < kMaxDev) cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
 
 hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, float eps,
                                  const float* row_mult, const float* tau_in, uint8_t* codes,

@@ -302,16 +302,7 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
                                int64_t K, float* dW, int accumulate, hipStream_t stream) {
   const int64_t tn = (N + kDwTN - 1) / kDwTN, tk = (K + kDwTK - 1) / kDwTK;
   const int64_t ntiles = tn * tk;
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        v > 0)
-      cus = v;
-    else
-      cus = 256;
-  }
+  const int cus = current_cu_count();
   const int64_t P = ntiles < cus ? ntiles : cus;
   const int64_t rem = ntiles % P;
   int64_t parts = rem ? P / rem : 1;

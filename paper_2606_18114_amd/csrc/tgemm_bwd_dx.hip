@@ -523,16 +523,7 @@ hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const f
                                hipStream_t stream) {
   const int64_t tm = (M + kDxTM - 1) / kDxTM, tk = (K + kDxTK - 1) / kDxTK;
   const int64_t ntiles = tm * tk;
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        v > 0)
-      cus = v;
-    else
-      cus = 256;
-  }
+  const int cus = current_cu_count();
   const int64_t P = ntiles < cus ? ntiles : cus;
   const int64_t rem = ntiles % P;
   int64_t parts = rem ? P / rem : 1;

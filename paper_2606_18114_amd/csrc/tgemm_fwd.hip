@@ -493,16 +493,7 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
                             hipStream_t stream) {
   const int64_t tm = (M + kFwdBM - 1) / kFwdBM, tn = (N + kFwdBN - 1) / kFwdBN;
   const int64_t ntiles = tm * tn;
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        v > 0)
-      cus = v;
-    else
-      cus = 256;
-  }
+  const int cus = current_cu_count();
   const bool wide = K % 256 == 0;  // code stages of four X stages
   // Work split over P = cus persistent workgroups: F whole rounds of tiles,
   // then the R = ntiles mod P remaining tiles cut along K into `parts` runs
