@@ -92,6 +92,46 @@ __device__ __forceinline__ void decode_half_pair_rt(u32x2 w, uint32_t hs, bf16x8
   b1 = __builtin_bit_cast(bf16x8, y);
 }
 
+// Exchange between lanes for all-reduce butterflies, without the LDS
+// crossbar where a DPP pattern exists: partner of lane i for step O is
+// i ^ 1, i ^ 2 (quad permutes), the mirror lane in its 8 (O = 4) or 16
+// (O = 8) lanes, i ^ 16 (ds_swizzle), i ^ 32.  After the steps below O each
+// lane's partner holds the sum of a disjoint set of the same size, so the
+// mirrors pair up as well as an XOR would, and every lane ends with the same
+// sum (two lanes add the same pair in either order).
+template <int O>
+__device__ __forceinline__ uint32_t lane_xchg(uint32_t v) {
+  if constexpr (O == 1)
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+  else if constexpr (O == 2)
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+  else if constexpr (O == 4)
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+  else if constexpr (O == 8)
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+  else if constexpr (O == 16)
+    return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);
+  else
+    return (uint32_t)__shfl_xor((int)v, O, 64);
+}
+template <int O>
+__device__ __forceinline__ double lane_xchg_f64(double v) {
+  const uint64_t u = (uint64_t)__double_as_longlong(v);
+  const uint64_t lo = lane_xchg<O>((uint32_t)u), hi = lane_xchg<O>((uint32_t)(u >> 32));
+  return __longlong_as_double((long long)((hi << 32) | lo));
+}
+// Sum over aligned groups of L lanes (L a power of two <= 64), in every lane.
+template <int L>
+__device__ __forceinline__ double group_sum_f64(double v) {
+  if constexpr (L >= 2) v += lane_xchg_f64<1>(v);
+  if constexpr (L >= 4) v += lane_xchg_f64<2>(v);
+  if constexpr (L >= 8) v += lane_xchg_f64<4>(v);
+  if constexpr (L >= 16) v += lane_xchg_f64<8>(v);
+  if constexpr (L >= 32) v += lane_xchg_f64<16>(v);
+  if constexpr (L >= 64) v += lane_xchg_f64<32>(v);
+  return v;
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
   return __builtin_bit_cast(bf16x8, v);
 }

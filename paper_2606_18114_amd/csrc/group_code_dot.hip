@@ -54,9 +54,7 @@ __global__ __launch_bounds__(64 * kGcdWaves) void group_code_dot_kernel(
       ps[i] = t;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int o = 1; o < L; o <<= 1) ps[i] += __shfl_xor(ps[i], o, 64);
+    for (int i = 0; i < 4; ++i) ps[i] = group_sum_f64<L>(ps[i]);
     if constexpr (G == 512) {  // a group spans two loads
       ps[0] += ps[1];
       ps[2] += ps[3];

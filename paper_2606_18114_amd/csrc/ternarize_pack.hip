@@ -69,9 +69,7 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
     }
     // group sums: butterfly over the L lanes of each group (float64, exact)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int o = 1; o < L; o <<= 1) ps[i] += __shfl_xor(ps[i], o, 64);
+    for (int i = 0; i < 4; ++i) ps[i] = group_sum_f64<L>(ps[i]);
     if constexpr (G == 512) {  // a group spans two loads
       ps[0] += ps[1];
       ps[1] = ps[0];
@@ -100,8 +98,8 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
         part |= code << (2 * (e / 2) + 16 * (e % 2));
         zeros += (nz || !ok[i]) ? 0u : 1u;
       }
-      part |= __shfl_xor(part, 1, 64);
-      part |= __shfl_xor(part, 2, 64);
+      part |= lane_xchg<1>(part);
+      part |= lane_xchg<2>(part);
       const int64_t off = base + 256 * i + 4 * lane;
       if (ok[i] && (lane & 3) == 0) codes[off / 16] = part;
       if (!tau_in && ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) {
