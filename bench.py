@@ -49,6 +49,12 @@ def parse():
                     help="also run a plain 1 GiB device copy (counter calibration)")
     ap.add_argument("--sweep-g", action="store_true",
                     help="group-size workload (in_proj W, X 2048 x 2048, g = 32 .. 512)")
+    ap.add_argument("--micro", action="store_true",
+                    help="measured roofline denominators instead of the step: an MFMA loop "
+                         "(random and zero operands), a 1 GiB HBM read stream, a 1 GiB device "
+                         "copy, and torch.mm bf16 on the in_proj shape as context")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants "
                          "(keeps a profiler trace to the kernels of interest)")
@@ -101,6 +107,8 @@ def main():
 
     if args.sweep_g:
         return sweep_g(args)
+    if args.micro:
+        return micro(args)
     if not os.path.exists(ops.lib_path()):
         from paper_2606_18114_amd import build
         build.build()
@@ -328,6 +336,15 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
+    # ---------------- measured ceilings (context for the fractions) ----------------
+    if not args.no_ceilings:
+        c = measure_ceilings()
+        out["measured_ceilings"] = dict(c, what=MICRO_WHAT)
+        out["roofline"]["frac_of_measured"] = round(
+            fwd["achieved"] / c["mfma_bf16_loop_random_TFLOPs"], 4)
+        out["roofline_tgemv"]["frac_of_measured"] = round(
+            srv["GBps"] / c["hbm_read_stream_1GiB_GBps"], 4)
+
     # ---------------- CPU oracle baseline (bounded sample) ----------------
     # The oracle's outputs of that step are also the reference for a sampled
     # end-to-end parity check of this run's GPU outputs (the GPU codes may
@@ -511,6 +528,87 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
                        f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
                        f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
     return base, par
+
+
+def micro(args):
+    """`--micro`: the measured ceilings alone, as one JSON line."""
+    print(json.dumps({"micro": measure_ceilings(), "peaks": {"bf16_TFLOPs": PEAK_BF16_TFLOPS,
+                                                             "hbm_GBps": PEAK_HBM_GBPS},
+                      "what": MICRO_WHAT}), flush=True)
+
+
+MICRO_WHAT = ("MFMA loop: 4 waves per SIMD, 4 independent 32x32x16 bf16 chains per wave on "
+              "operands loaded once; read stream: 1 GiB, 16-byte loads, 4 in flight per thread, "
+              "32 waves per CU; medians of 5 runs")
+
+
+def measure_ceilings():
+    """Measured denominators: what this GPU sustains on a plain MFMA loop and a
+    plain read stream (libtm_micro.so), and, for context, a device copy and
+    hipBLASLt (torch.mm) on the in_proj forward shape."""
+    import ctypes
+    import torch
+    from paper_2606_18114_amd import build as B
+
+    if not os.path.exists(B.MICRO_OUT):
+        B.build()
+    lib = ctypes.CDLL(B.MICRO_OUT)
+    lib.tmm_grid_threads.restype = ctypes.c_int
+    lib.tmm_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.tmm_read_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    st = torch.cuda.current_stream().cuda_stream
+    threads = lib.tmm_grid_threads()
+
+    def timed(fn, reps=5, warm=2):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return float(np.median(ts))
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"micro kernel launch failed: {rc}")
+
+    out = torch.empty(threads, dtype=torch.float32, device=dev)
+    iters = 20000
+    fl = 2.0 * 32 * 32 * 16 * 4 * iters * (threads // 2 // 64)  # the loop runs on half the grid
+    res = {}
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    for label, opnd in (("random", torch.randn(1024, generator=gen, device=dev)),
+                        ("zero", torch.zeros(1024, device=dev))):
+        o16 = opnd.to(torch.bfloat16)
+        sec = timed(lambda: check(lib.tmm_mfma_loop(o16.data_ptr(), iters, out.data_ptr(), st)))
+        res[f"mfma_bf16_loop_{label}_TFLOPs"] = round(fl / sec / 1e12, 1)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    buf.random_(0, 256, generator=gen)
+    words = torch.empty(threads, dtype=torch.int32, device=dev)
+    sec = timed(lambda: check(lib.tmm_read_stream(buf.data_ptr(), buf.numel(), words.data_ptr(), st)))
+    res["hbm_read_stream_1GiB_GBps"] = round(buf.numel() / sec / 1e9, 1)
+    dst = torch.empty_like(buf)
+    sec = timed(lambda: dst.copy_(buf))
+    res["device_copy_1GiB_GBps"] = round(2 * buf.numel() / sec / 1e9, 1)
+    del buf, dst
+    M, N, K = 16384, 8512, 2048
+    X = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
+    Wt = (torch.randn((N, K), generator=gen, device=dev) * 0.02).to(torch.bfloat16).t().contiguous()
+    sec = timed(lambda: torch.mm(X, Wt))
+    res["torch_mm_bf16_in_proj_TFLOPs"] = round(2.0 * M * N * K / sec / 1e12, 1)
+    del X, Wt
+    torch.cuda.empty_cache()
+    return res
 
 
 def sweep_g(args):

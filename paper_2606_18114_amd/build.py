@@ -4,7 +4,9 @@
 
 Every translation unit under ``csrc/`` is compiled in parallel to an object
 file under ``_build/`` and the objects are linked into
-``paper_2606_18114_amd/libtmamba.so`` next to the Python binding.
+``paper_2606_18114_amd/libtmamba.so`` next to the Python binding.  The
+roofline probes of ``csrc/micro.hip`` (an MFMA loop and an HBM read stream,
+used by ``bench.py --micro``) go into a separate ``libtm_micro.so``.
 """
 
 from __future__ import annotations
@@ -20,6 +22,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libtmamba.so")
+MICRO_OUT = os.path.join(PKG, "libtm_micro.so")
+MICRO_SOURCES = ["micro.hip"]
 OBJ = os.path.join(ROOT, "_build")
 
 SOURCES = [
@@ -73,19 +77,27 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = True) -> str:
-    """Compile every source and link the shared library; returns its path."""
-    t0 = time.time()
-    with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = OUT + ".tmp"
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     proc = subprocess.run(cmd, capture_output=True, text=True)
     if proc.returncode != 0:
         raise RuntimeError(f"link failed:\n{proc.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = True) -> str:
+    """Compile every source and link the shared libraries; returns the path
+    of libtmamba.so."""
+    t0 = time.time()
+    srcs = SOURCES + MICRO_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=min(len(srcs), os.cpu_count() or 4)) as ex:
+        objs = dict(zip(srcs, ex.map(_compile, srcs)))
+    _link([objs[s] for s in SOURCES], OUT)
+    _link([objs[s] for s in MICRO_SOURCES], MICRO_OUT)
     if verbose:
-        print(f"built {OUT} in {time.time() - t0:.1f}s", file=sys.stderr)
+        print(f"built {OUT} and {os.path.basename(MICRO_OUT)} in {time.time() - t0:.1f}s",
+              file=sys.stderr)
     return OUT
 
 
