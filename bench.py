@@ -99,7 +99,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding is described in DESIGN.md, not built)", file=sys.stderr)
+              "(the path is built for one GPU; sharding across GPUs is not)", file=sys.stderr)
         sys.exit(2)
 
     import torch

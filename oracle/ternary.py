@@ -23,7 +23,7 @@ Space Models", Sec. 3.1 (TernaryLinear Module).
 * Deployment storage: 2-bit codes plus per-group scales (Sec. 8, Table 11).
 * Weight NRMSE: per-layer weight quantization error (Sec. 7, App. A.7).
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * groups run along the input dimension K, contiguous, K % g == 0;
 * a non-negative ``eps`` is added to the scale before the division (eps = 0 is

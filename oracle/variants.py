@@ -20,7 +20,7 @@ The paper's appendix (Decoupled Quantization Ablations) and Sec. 4
   is cut by the hard forward quantization (the straight-through estimator of
   Sec. 3.1 passes gradients to W only), which is the reading taken here.
 
-Readings (listed in the design doc): the multiplied threshold is rounded to
+Readings: the multiplied threshold is rounded to
 float32 once (fl32(m * s)), then eps is added in float32, then the quotient is
 taken in float32 as for the standard code; dWhat is the gradient with respect
 to the dequantized weight, dY^T * X.
