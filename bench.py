@@ -538,8 +538,8 @@ def micro(args):
 
 
 MICRO_WHAT = ("MFMA loop: 4 waves per SIMD, 4 independent 32x32x16 bf16 chains per wave on "
-              "operands loaded once; read stream: 1 GiB, 16-byte loads, 4 in flight per thread, "
-              "32 waves per CU; medians of 5 runs")
+              "operands loaded once; read stream: 1 GiB in contiguous 16 KiB chunks per wave, "
+              "16 waves per CU; medians of 5 runs")
 
 
 def measure_ceilings():
@@ -583,7 +583,7 @@ def measure_ceilings():
 
     out = torch.empty(threads, dtype=torch.float32, device=dev)
     iters = 20000
-    fl = 2.0 * 32 * 32 * 16 * 4 * iters * (threads // 2 // 64)  # the loop runs on half the grid
+    fl = 2.0 * 32 * 32 * 16 * 4 * iters * (threads // 64)
     res = {}
     gen = torch.Generator(device=dev)
     gen.manual_seed(0)

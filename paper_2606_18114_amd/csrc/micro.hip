@@ -7,11 +7,13 @@
 //     `operands` (64 lanes x 16 bfloat16: the lane's A then B values), so the
 //     matrix cores see the caller's data, e.g. random values, which draw more
 //     power than zeros.  flops = 2 * 32 * 32 * 16 * 4 * iters * waves.
-//   tmm_read_stream: a grid of four 512-thread workgroups per CU (the most
-//     waves a CU holds) reads `bytes` from `buf` in 16-byte pieces, four
-//     loads in flight per thread (128 KiB per CU), and folds them into one
-//     word per thread (written to `out`) so the loads cannot be dropped.
-//     `bytes` must be a multiple of 64 * tmm_grid_threads().
+//   tmm_read_stream: a grid of two 512-thread workgroups per CU reads `bytes`
+//     from `buf` in contiguous 16 KiB chunks, one chunk per wave at a time
+//     (sixteen 1 KiB loads in flight per wave, 256 KiB per CU), and folds the
+//     data into one word per thread (written to `out`) so the loads cannot
+//     be dropped.  Of the access patterns tried (grid-stride 16-byte pieces,
+//     4 KiB or 16 KiB per wave, 32 rows x 128 bytes at a 512-byte pitch) the
+//     contiguous chunks were fastest.  `bytes` must be a multiple of 16 KiB.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -49,19 +51,21 @@ __global__ __launch_bounds__(kThreads) void mfma_loop_kernel(const uint16_t* __r
 }
 
 __global__ __launch_bounds__(kThreads) void read_stream_kernel(const mu32x4* __restrict__ buf,
-                                                               int64_t pieces,
+                                                               int64_t chunks,
                                                                uint32_t* __restrict__ out) {
-  const int64_t nthreads = (int64_t)gridDim.x * kThreads;
-  const int64_t tid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / 64);
   uint32_t acc = 0;
-  for (int64_t i = tid; i < pieces; i += 4 * nthreads) {
-    const mu32x4 v0 = buf[i];
-    const mu32x4 v1 = buf[i + nthreads];
-    const mu32x4 v2 = buf[i + 2 * nthreads];
-    const mu32x4 v3 = buf[i + 3 * nthreads];
-    acc ^= (v0.x ^ v1.y) ^ (v2.z ^ v3.w);
+  for (int64_t ch = wave; ch < chunks; ch += nwaves) {  // chunk: 1024 pieces of 16 bytes
+    const mu32x4* p = buf + ch * 1024 + lane;
+    mu32x4 v[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = p[64 * j];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc ^= v[j].x ^ v[j].w;
   }
-  out[tid] = acc;
+  out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
 }
 
 int cu_count() {
@@ -76,12 +80,11 @@ int cu_count() {
 
 extern "C" {
 
-// Threads of the largest grid below (4 workgroups of 512 per CU): the length
-// of `out` in elements.
-int tmm_grid_threads(void) { return 4 * cu_count() * kThreads; }
+// Threads of the grids below (2 workgroups of 512 per CU): the length of
+// `out` in elements.
+int tmm_grid_threads(void) { return 2 * cu_count() * kThreads; }
 
-// operands: 1024 bfloat16 (device); out: tmm_grid_threads() floats (device;
-// the first half is written).
+// operands: 1024 bfloat16 (device); out: tmm_grid_threads() floats (device).
 // Returns 0 or the HIP error code of the launch.
 int tmm_mfma_loop(const uint16_t* operands, int iters, float* out, void* stream) {
   if (!operands || !out || iters < 1) return (int)hipErrorInvalidValue;
@@ -90,15 +93,15 @@ int tmm_mfma_loop(const uint16_t* operands, int iters, float* out, void* stream)
   return (int)hipGetLastError();
 }
 
-// buf: `bytes` of device memory, bytes % (64 * tmm_grid_threads()) == 0;
+// buf: `bytes` of device memory, bytes % 16384 == 0, 16-byte aligned;
 // out: tmm_grid_threads() words (device).
 int tmm_read_stream(const void* buf, int64_t bytes, uint32_t* out, void* stream) {
-  const int64_t threads = tmm_grid_threads();
-  if (!buf || !out || bytes <= 0 || bytes % (64 * threads) != 0 ||
+  if (!buf || !out || bytes <= 0 || bytes % 16384 != 0 ||
       reinterpret_cast<uintptr_t>(buf) % 16 != 0)
     return (int)hipErrorInvalidValue;
-  hipLaunchKernelGGL(read_stream_kernel, dim3(4 * cu_count()), dim3(kThreads), 0,
-                     (hipStream_t)stream, reinterpret_cast<const mu32x4*>(buf), bytes / 16, out);
+  hipLaunchKernelGGL(read_stream_kernel, dim3(2 * cu_count()), dim3(kThreads), 0,
+                     (hipStream_t)stream, reinterpret_cast<const mu32x4*>(buf), bytes / 16384,
+                     out);
   return (int)hipGetLastError();
 }
 
