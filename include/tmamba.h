@@ -19,7 +19,10 @@
  * Conventions for every call
  *   - Every array pointer is DEVICE memory, allocated and owned by the caller.
  *     The library allocates and frees nothing, keeps no mutable global state
- *     and is safe to call from several host threads.
+ *     beyond a per-device cache of the CU count, and is safe to call from
+ *     several host threads.
+ *   - Any clearing a call needs is done by a fill kernel on `stream`, never a
+ *     memset node, so the calls can be captured into a HIP graph.
  *   - Arrays are dense, row-major, with the shapes given per call.  bfloat16
  *     data is passed as uint16_t bit patterns.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the default
@@ -102,6 +105,11 @@ tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g,
  * whose scale is 0 contribute 0 whatever their codes.  Precondition (met by
  * any weights that are not extreme): within a row n, the largest nonzero
  * scale divided by the smallest, times sum_k |X[m, k]|, stays below 1e38.
+ * Tiles of 256 x 256 outputs are spread over one workgroup per CU; when the
+ * tile count is not a multiple of the CU count, the tiles left over are cut
+ * along K and their parts add into Y with float32 atomics (those rows of Y
+ * are cleared first).  Their elements may then differ in the last bits from
+ * one call to the next (two parts add exactly in either order).
  */
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
                        const float* scales, int64_t M, int64_t N, int64_t K,
