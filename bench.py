@@ -235,6 +235,8 @@ def main():
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
+    qat_block_bf16 = (None if "qat" in args.skip
+                      else qat_block_step(args, dev, X, synth, out_dtype=torch.bfloat16))
 
     # ---------------- scale variants on the in_proj shapes ----------------
     variants = (None if "variants" in args.skip
@@ -323,6 +325,7 @@ def main():
                            "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to back"},
         "kernels": kernels,
         "qat_block": qat_block,
+        "qat_block_bf16_out": qat_block_bf16,
         "variants": variants,
         "zero_ratio": None,
     }
@@ -414,23 +417,25 @@ def variants_step(args, ops, W, scales, codes, dW, g, eps):
     return res
 
 
-def qat_block_step(args, dev, X_in, synth):
+def qat_block_step(args, dev, X_in, synth, out_dtype=None):
     """One QAT step of a Mamba-2 1.3B block's two ternary projections through
     the autograd layer (forward, straight-through backward, 16384 tokens):
     in_proj 2048 -> 8512 on the block input, out_proj 4096 -> 2048 on a
-    synthetic SSM output.  The upstream gradients are given; the time covers
-    the library calls plus the layer's gradient casts to bfloat16."""
+    synthetic SSM output.  The upstream gradients are given (in the layers'
+    output dtype); the time covers the library calls plus, with float32
+    outputs, the layer's gradient casts to bfloat16."""
     import torch
     from paper_2606_18114_amd.qat import TernaryLinear, flops_per_step
 
     torch.manual_seed(7)
     M = X_in.shape[0]
-    lin = TernaryLinear(synth.D_MODEL, synth.IN_PROJ_N, device=dev)
-    lout = TernaryLinear(synth.D_INNER, synth.D_MODEL, device=dev)
+    od = out_dtype or torch.float32
+    lin = TernaryLinear(synth.D_MODEL, synth.IN_PROJ_N, device=dev, out_dtype=od)
+    lout = TernaryLinear(synth.D_INNER, synth.D_MODEL, device=dev, out_dtype=od)
     z = torch.randn((M, synth.D_INNER), device=dev).to(torch.bfloat16).requires_grad_(True)
     x = X_in.detach().requires_grad_(True)  # gradients flow on to the layers below
-    g_in = torch.randn((M, synth.IN_PROJ_N), device=dev) * synth.DY_STD
-    g_out = torch.randn((M, synth.D_MODEL), device=dev) * synth.DY_STD
+    g_in = (torch.randn((M, synth.IN_PROJ_N), device=dev) * synth.DY_STD).to(od)
+    g_out = (torch.randn((M, synth.D_MODEL), device=dev) * synth.DY_STD).to(od)
 
     def step():
         lin.weight.grad = lout.weight.grad = x.grad = z.grad = None
@@ -455,7 +460,8 @@ def qat_block_step(args, dev, X_in, synth):
             "frac_mfma": round(fl / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "tokens": M, "zero_ratio_in_proj": round(lin.zero_ratio(), 5),
             "what": "TernaryLinear in_proj 2048->8512 + out_proj 4096->2048, forward + "
-                    "straight-through backward (dX and dW), 16384 tokens, g=128"}
+                    "straight-through backward (dX and dW), 16384 tokens, g=128, "
+                    f"{str(od).replace('torch.', '')} outputs"}
 
 
 def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):

@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 2
+#define TM_ABI_VERSION 3
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -114,6 +114,20 @@ tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g,
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
                        const float* scales, int64_t M, int64_t N, int64_t K,
                        int32_t g, float* Y, tm_stream stream);
+
+/*
+ * tm_tgemm_fwd_bf16 — tm_tgemm_fwd with the output in bfloat16: each float32
+ * result is rounded to nearest even once (relative error <= 2^-9 per
+ * element), as a bfloat16 model stores a linear layer's output; the gradient
+ * arriving for it is then bfloat16 too, so the backward calls read it
+ * without a cast.  Tiles are never cut along K here, so repeated calls give
+ * identical bits.
+ *   Y  bfloat16 bits [M, N]  out  (16-byte aligned)
+ *   every other argument, limit and status as for tm_tgemm_fwd.
+ */
+tm_status tm_tgemm_fwd_bf16(const uint16_t* X, const uint8_t* codes,
+                            const float* scales, int64_t M, int64_t N, int64_t K,
+                            int32_t g, uint16_t* Y, tm_stream stream);
 
 /*
  * tm_tgemm_bwd_dx — Sec. 3.1 straight-through backward w.r.t. the input:

@@ -51,6 +51,28 @@ hipStream_t to_hip(tm_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
 constexpr int64_t kMaxGridBlocks = (int64_t(1) << 31) - 1;
 
+// Y holds es-byte elements: 4 (float32) or 2 (bfloat16 bits)
+tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float* scales,
+                            int64_t M, int64_t N, int64_t K, int32_t g, void* Y, int es,
+                            tm_stream stream) {
+  if (!X || !codes || !scales || !Y) return TM_EINVAL;
+  if (M < 1 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t xb, cb, sb, yb;
+  if (!bytes_of(M, K, 2, &xb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
+      !bytes_of(M, N, es, &yb))
+    return TM_ESHAPE;
+  if (((M + 255) / 256) * ((N + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (K > (int64_t(1) << 22) || N > (int64_t(1) << 26)) return TM_ESHAPE;  // 32-bit tile offsets
+  if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(Y, 16))
+    return TM_EALIGN;
+  const Span y = span(Y, yb);
+  if (overlap(y, span(X, xb)) || overlap(y, span(codes, cb)) || overlap(y, span(scales, sb)))
+    return TM_EINVAL;
+  return hip_status(
+      tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, es == 2, to_hip(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -141,23 +163,16 @@ tm_status tm_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, in
   return hip_status(tmk::launch_group_code_dot(codes, dW, N, K, g, out, to_hip(stream)));
 }
 
+
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales, int64_t M,
                        int64_t N, int64_t K, int32_t g, float* Y, tm_stream stream) {
-  if (!X || !codes || !scales || !Y) return TM_EINVAL;
-  if (M < 1 || N < 1) return TM_ESHAPE;
-  if (tm_status st = shape_kg(K, g)) return st;
-  int64_t xb, cb, sb, yb;
-  if (!bytes_of(M, K, 2, &xb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
-      !bytes_of(M, N, 4, &yb))
-    return TM_ESHAPE;
-  if (((M + 255) / 256) * ((N + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
-  if (K > (int64_t(1) << 22) || N > (int64_t(1) << 26)) return TM_ESHAPE;  // 32-bit tile offsets
-  if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(Y, 16))
-    return TM_EALIGN;
-  const Span y = span(Y, yb);
-  if (overlap(y, span(X, xb)) || overlap(y, span(codes, cb)) || overlap(y, span(scales, sb)))
-    return TM_EINVAL;
-  return hip_status(tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, to_hip(stream)));
+  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 4, stream);
+}
+
+tm_status tm_tgemm_fwd_bf16(const uint16_t* X, const uint8_t* codes, const float* scales,
+                            int64_t M, int64_t N, int64_t K, int32_t g, uint16_t* Y,
+                            tm_stream stream) {
+  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 2, stream);
 }
 
 tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,

@@ -115,11 +115,13 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-template <int G, int SS>
+// BF: Y in bfloat16 (each float32 result rounded to nearest even once),
+// else float32.  The bfloat16 form never cuts tiles (parts == 1).
+template <int G, int SS, bool BF>
 __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ codes,
     const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
-    float* __restrict__ Y, uint32_t tiles_n, uint32_t full_rounds, uint32_t extra_units,
+    void* __restrict__ Yv, uint32_t tiles_n, uint32_t full_rounds, uint32_t extra_units,
     uint32_t parts) {
   using C = FwdCfg<G, SS>;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLds];
@@ -414,15 +416,16 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     // of a tile add their partial sums with float32 atomics.
     {
       const int64_t mrow = m0 + wm * 128;
-      uint8_t* ytile = reinterpret_cast<uint8_t*>(Y + mrow * N + n0);
+      constexpr int ES = BF ? 2 : 4;  // bytes per output element
+      uint8_t* ytile = reinterpret_cast<uint8_t*>(Yv) + (mrow * N + n0) * ES;
       const bool full_m = mrow + 128 <= M;
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
         const int nl = wn * 64 + b * 32 + l32;  // column in the tile
         if (n0 + nl >= N) continue;
         const float f = 0.5f * cref[b];
-        uint8_t* ylane = ytile + ((int64_t)(4 * h) * N + nl) * 4;
-        if (part) {
+        uint8_t* ylane = ytile + ((int64_t)(4 * h) * N + nl) * ES;
+        if (!BF && part) {
           int64_t pv = N * 4;
           asm volatile("" : "+v"(pv));
           uint8_t* yp = ylane;
@@ -444,25 +447,29 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
           // a 32-bit lane offset from the uniform tile base, stepped row by
           // row (rows a*32 + 8*i4 + i1); the empty asm keeps the compiler
           // from precomputing all 64 offsets (which it would spill)
-          uint32_t pv = (uint32_t)N * 4u;
+          uint32_t pv = (uint32_t)N * ES;
           asm volatile("" : "+v"(pv));
           const uint32_t pv4 = 4u * pv;
-          uint32_t o = (uint32_t)((4 * h) * N + nl) * 4u;
+          uint32_t o = (uint32_t)((4 * h) * N + nl) * ES;
 #pragma unroll
           for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int i4 = 0; i4 < 4; ++i4) {
 #pragma unroll
               for (int i1 = 0; i1 < 4; ++i1) {
-                __builtin_nontemporal_store(f * acc[a][b][4 * i4 + i1],
-                                            reinterpret_cast<float*>(ytile + o));
+                if constexpr (BF)
+                  *reinterpret_cast<uint16_t*>(ytile + o) =
+                      __builtin_bit_cast(uint16_t, (__bf16)(f * acc[a][b][4 * i4 + i1]));
+                else
+                  __builtin_nontemporal_store(f * acc[a][b][4 * i4 + i1],
+                                              reinterpret_cast<float*>(ytile + o));
                 o += pv;
               }
               o += pv4;  // rows 8 i4 + 4 .. 8 i4 + 7 belong to the other k half
             }
         } else {
           // rows past M (last row of tiles), or a pitch beyond 32-bit offsets
-          int64_t pv = N * 4;
+          int64_t pv = N * ES;
           asm volatile("" : "+v"(pv));
           uint8_t* yp = ylane;
           int64_t row = mrow + 4 * h;
@@ -472,7 +479,13 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
             for (int i4 = 0; i4 < 4; ++i4) {
 #pragma unroll
               for (int i1 = 0; i1 < 4; ++i1) {
-                if (row < M) *reinterpret_cast<float*>(yp) = f * acc[a][b][4 * i4 + i1];
+                const float v = f * acc[a][b][4 * i4 + i1];
+                if (row < M) {
+                  if constexpr (BF)
+                    *reinterpret_cast<uint16_t*>(yp) = __builtin_bit_cast(uint16_t, (__bf16)v);
+                  else
+                    *reinterpret_cast<float*>(yp) = v;
+                }
                 yp += pv;
                 ++row;
               }
@@ -489,7 +502,7 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
 }
 
 hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
-                            int64_t M, int64_t N, int64_t K, int g, float* Y,
+                            int64_t M, int64_t N, int64_t K, int g, void* Y, bool bf16_out,
                             hipStream_t stream) {
   const int64_t tm = (M + kFwdBM - 1) / kFwdBM, tn = (N + kFwdBN - 1) / kFwdBN;
   const int64_t ntiles = tm * tn;
@@ -506,26 +519,34 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
   const int64_t trips = K / kFwdBK / unroll;
   int64_t parts = R > 0 ? P / R : 1;
   if (parts > trips) parts = trips;
-  if (parts < 1) parts = 1;
+  if (parts < 1 || bf16_out) parts = 1;  // bfloat16 results are not summed in parts
   const int64_t extra = R * parts;
   if (parts > 1) {
     // the cut tiles accumulate atomically: clear their rows of Y first (a
     // fill kernel, not a memset node, so the call can be captured)
     const int64_t r0 = F * P / tn * kFwdBM;
-    hipError_t e = launch_fill_zero_f32(Y + r0 * N, (M - r0) * N, stream);
+    hipError_t e = launch_fill_zero_f32(static_cast<float*>(Y) + r0 * N, (M - r0) * N, stream);
     if (e != hipSuccess) return e;
   }
   const dim3 grid((unsigned)P), block(512);
   const uint32_t t_n = (uint32_t)tn, fr = (uint32_t)F, xu = (uint32_t)extra,
                  np = (uint32_t)parts;
+#define TM_FWD_L(GG, SS_, BF_)                                                                 \
+  hipLaunchKernelGGL((tgemm_fwd_kernel<GG, SS_, BF_>), grid, block, 0, stream, X, codes, scales, \
+                     M, N, K, Y, t_n, fr, xu, np)
 #define TM_FWD(GG)                                                                             \
   case GG:                                                                                     \
-    if (wide)                                                                                  \
-      hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 4>), grid, block, 0, stream, X, codes, scales, M, \
-                         N, K, Y, t_n, fr, xu, np);                                            \
-    else                                                                                       \
-      hipLaunchKernelGGL((tgemm_fwd_kernel<GG, 1>), grid, block, 0, stream, X, codes, scales, M, \
-                         N, K, Y, t_n, fr, xu, np);                                            \
+    if (wide) {                                                                                \
+      if (bf16_out)                                                                            \
+        TM_FWD_L(GG, 4, true);                                                                 \
+      else                                                                                     \
+        TM_FWD_L(GG, 4, false);                                                                \
+    } else {                                                                                   \
+      if (bf16_out)                                                                            \
+        TM_FWD_L(GG, 1, true);                                                                 \
+      else                                                                                     \
+        TM_FWD_L(GG, 1, false);                                                                \
+    }                                                                                          \
     break;
   switch (g) {
     TM_FWD(32)
@@ -536,6 +557,7 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
     default: return hipErrorInvalidValue;
   }
 #undef TM_FWD
+#undef TM_FWD_L
   return hipGetLastError();
 }
 

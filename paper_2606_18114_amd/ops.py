@@ -37,6 +37,7 @@ SIGNATURES = {
                                  [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P, _P]),
     "tm_group_code_dot": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P]),
     "tm_ternarize_codes": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P]),
+    "tm_tgemm_fwd_bf16": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
 }
 
 
@@ -174,17 +175,29 @@ def group_code_dot(codes: torch.Tensor, dW: torch.Tensor, g: int = 128,
 
 
 def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
-              Y: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Y[M, N] = X . (q * s)^T in float32."""
+              Y: Optional[torch.Tensor] = None,
+              out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Y[M, N] = X . (q * s)^T in float32, or rounded once to bfloat16
+    (out_dtype=torch.bfloat16, ``tm_tgemm_fwd_bf16``)."""
     _need(X, "X", _BF16, 2)
     _need(codes, "codes", _U8, 2)
     _need(scales, "scales", _F32, 2)
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError(f"out_dtype must be float32 or bfloat16 (got {out_dtype})")
     M, K = X.shape
     N = codes.shape[0]
     if Y is None:
-        Y = torch.empty((M, N), dtype=torch.float32, device=X.device)
-    st = lib().tm_tgemm_fwd(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y), _stream())
-    _check("tm_tgemm_fwd", st)
+        Y = torch.empty((M, N), dtype=out_dtype, device=X.device)
+    if out_dtype == torch.bfloat16:
+        _need(Y, "Y", _BF16, 2)
+        st = lib().tm_tgemm_fwd_bf16(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
+                                     _stream())
+        _check("tm_tgemm_fwd_bf16", st)
+    else:
+        _need(Y, "Y", _F32, 2)
+        st = lib().tm_tgemm_fwd(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
+                                _stream())
+        _check("tm_tgemm_fwd", st)
     return Y
 
 

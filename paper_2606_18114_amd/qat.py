@@ -55,7 +55,8 @@ class TernaryLinearFn(torch.autograd.Function):
     @staticmethod
     def forward(ctx, x: torch.Tensor, weight: torch.Tensor, scale: Optional[torch.Tensor],
                 g: int, eps: float, zero_count: Optional[torch.Tensor], mode: str,
-                row_mult: Optional[torch.Tensor]) -> torch.Tensor:
+                row_mult: Optional[torch.Tensor],
+                out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
         N, K = weight.shape
         if x.shape[-1] != K:
             raise ValueError(f"x has {x.shape[-1]} features, the layer takes {K}")
@@ -75,7 +76,7 @@ class TernaryLinearFn(torch.autograd.Function):
                                                       want_f16=False, want_zero_count=want_zc,
                                                       row_mult=row_mult)
             mag = absmean if mode == "absmean" else scale.detach().contiguous()
-        y = ops.tgemm_fwd(x2, codes, mag, g)
+        y = ops.tgemm_fwd(x2, codes, mag, g, out_dtype=out_dtype)
         ctx.save_for_backward(x2, codes, mag)
         ctx.g = g
         ctx.lead = lead
@@ -102,7 +103,7 @@ class TernaryLinearFn(torch.autograd.Function):
                 dscale = ops.group_code_dot(codes, dw_hat, ctx.g)
             if ctx.needs_input_grad[1]:
                 dw = dw_hat
-        return dx, dw, dscale, None, None, None, None, None
+        return dx, dw, dscale, None, None, None, None, None, None
 
 
 class TernaryLinear(torch.nn.Module):
@@ -117,12 +118,18 @@ class TernaryLinear(torch.nn.Module):
     parameter starts at the absmean of the weights (``reset_scale``, run on
     the first call if not done before).  threshold_mult (float32 [out]) scales
     each row's absmean threshold (e.g. 0.8 on the gate rows of in_proj).
+    out_dtype: float32 (default) or bfloat16, the output rounded once as a
+    bfloat16 model stores it; the incoming gradient then needs no cast.
     """
 
     def __init__(self, in_features: int, out_features: int, g: int = 128, eps: float = 1e-5,
                  device: Optional[torch.device] = None, track_zero_ratio: bool = True,
-                 scale_mode: str = "absmean", threshold_mult: Optional[torch.Tensor] = None):
+                 scale_mode: str = "absmean", threshold_mult: Optional[torch.Tensor] = None,
+                 out_dtype: torch.dtype = torch.float32):
         super().__init__()
+        if out_dtype not in (torch.float32, torch.bfloat16):
+            raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
+        self.out_dtype = out_dtype
         if in_features % g or in_features % 64:
             raise ValueError(f"in_features={in_features} must be a multiple of g={g} and of 64")
         if scale_mode not in SCALE_MODES:
@@ -176,7 +183,7 @@ class TernaryLinear(torch.nn.Module):
         if not self._scale_ready:
             self.reset_scale()
         return TernaryLinearFn.apply(x, self.weight, self.scale, self.g, self.eps, self._zc,
-                                     self.scale_mode, self.threshold_mult)
+                                     self.scale_mode, self.threshold_mult, self.out_dtype)
 
     def zero_ratio(self) -> float:
         """Fraction of zero codes in the last forward call (Sec. 3.1 tracks it
@@ -205,7 +212,8 @@ class TernaryLinear(torch.nn.Module):
 
     def extra_repr(self) -> str:
         return (f"in_features={self.in_features}, out_features={self.out_features}, "
-                f"g={self.g}, eps={self.eps}, scale_mode={self.scale_mode}")
+                f"g={self.g}, eps={self.eps}, scale_mode={self.scale_mode}, "
+                f"out_dtype={self.out_dtype}")
 
 
 def flops_per_step(tokens: int, layer: TernaryLinear) -> float:

@@ -33,11 +33,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 2
+    assert L.tm_abi_version() == 3
 
 
 def test_status_strings(L):
@@ -155,6 +155,20 @@ def test_tgemm_fwd_validation(L):
     assert fwd(L, Y=P + 2 ** 26 + 4) == EALIGN
     assert fwd(L, Y=P + 4096) == EINVAL                 # Y overlaps X
     assert fwd(L, Y=P + 2 ** 24 - 4096) == EINVAL       # Y overlaps codes
+
+
+def test_tgemm_fwd_bf16_validation(L):
+    def f(X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):
+        return L.tm_tgemm_fwd_bf16(X, codes, scales, M, N, K, g, Y, None)
+    for kw in ("X", "codes", "scales", "Y"):
+        assert f(**{kw: 0}) == EINVAL, kw
+    assert f(M=0) == ESHAPE
+    assert f(K=544) == ESHAPE
+    assert f(g=48) == ESHAPE
+    assert f(Y=P + 2 ** 26 + 2) == EALIGN
+    assert f(Y=P + 4096) == EINVAL                 # Y overlaps X
+    # a bfloat16 Y of 16 x 256 is 8 KiB: one byte more reaches the codes
+    assert f(Y=P + 2 ** 24 - 8192 + 16) == EINVAL
 
 
 def dx(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,

@@ -272,6 +272,38 @@ def test_fwd_split_tiles_exact_and_complete():
     assert err <= REL_DESIGN
 
 
+@pytest.mark.parametrize("M,N,K,g", [(300, 520, 1024, 64), (4100, 600, 512, 128),
+                                     (257, 8, 128, 32), (2048, 2048, 576, 64)])
+def test_fwd_bf16_output(M, N, K, g):
+    """The bfloat16 output is the float32 accumulation rounded once: every
+    element lies within half a bfloat16 step (2^-8 relative) of the float64
+    reference plus the float32 accumulation bound (K * 2^-24 times the sum of
+    the absolute products); within the 2e-3 bar overall; two calls agree bit
+    for bit."""
+    ops = _ops()
+    print(f"[fwd bf16] M={M} N={N} K={K} g={g}", flush=True)
+    rng = np.random.default_rng(M + N)
+    W = synth.weights(rng, N, K, outliers=True)
+    X = synth.activations(rng, M, K)
+    c, s, _, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5, want_f16=False, want_zero_count=False)
+    Xd = dev_bf16(X)
+    Yb = ops.tgemm_fwd(Xd, c, s, g, out_dtype=torch.bfloat16)
+    Yb2 = ops.tgemm_fwd(Xd, c, s, g, out_dtype=torch.bfloat16)
+    bits = host(Yb.view(torch.int16)).view(np.uint16)
+    assert np.array_equal(bits, host(Yb2.view(torch.int16)).view(np.uint16))
+    yb = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    q, sg = host_codes(c, K), host(s)
+    ref = O.gemm_fwd(X, q, sg, g)
+    absx = (np.asarray(X, np.uint16) & np.uint16(0x7FFF)).astype(np.uint16)  # |x| as bf16 bits
+    mag = O.gemm_fwd(absx, np.abs(q).astype(np.int8), sg, g)
+    bound = 2.0 ** -8 * np.abs(ref) * 1.0001 + K * 2.0 ** -24 * mag
+    worst = float(np.max(np.abs(yb - ref) / np.maximum(bound, 1e-300)))
+    err = O.rel_fro_error(yb, ref)
+    print(f"  worst error / bound {worst:.3f}, rel err {err:.2e}", flush=True)
+    assert worst <= 1.0
+    assert err <= REL_BAR
+
+
 # --------------------------------------------------------------------------
 # backward
 # --------------------------------------------------------------------------

@@ -132,3 +132,27 @@ def test_zero_ratio_and_decode_packing():
     torch.cuda.synchronize()
     ref = O.gemv(_bits(x), O.unpack(codes.cpu().numpy(), K), s16.cpu().numpy(), g)
     assert O.rel_fro_error(y.cpu().numpy(), ref) <= REL_DESIGN
+
+
+@pytest.mark.gpu
+def test_bf16_output_layer():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_18114_amd.qat import TernaryLinear
+    rng = np.random.default_rng(77)
+    N, K, g = 256, 512, 128
+    W = synth.weights(rng, N, K, outliers=True)
+    layer = TernaryLinear.from_weight(torch.from_numpy(W).cuda(), g=g, out_dtype=torch.bfloat16)
+    x = _bf16(rng.standard_normal((64, K), dtype=np.float32)).requires_grad_(True)
+    y = layer(x)
+    assert y.dtype == torch.bfloat16
+    r = _bf16(rng.standard_normal((64, N), dtype=np.float32) * 0.01)
+    y.backward(r)
+    torch.cuda.synchronize()
+    q, s = _layer_codes(layer)
+    xb, rb = _bits(x), _bits(r)
+    e_y = O.rel_fro_error(y.detach().float().cpu().numpy(), O.gemm_fwd(xb, q, s, g))
+    e_dx = O.rel_fro_error(x.grad.float().cpu().numpy(), O.gemm_bwd_dx(rb, q, s, g))
+    e_dw = O.rel_fro_error(layer.weight.grad.cpu().numpy(), O.gemm_bwd_dw(rb, xb))
+    print(f"[qat bf16 out] y {e_y:.2e} dX {e_dx:.2e} dW {e_dw:.2e}", flush=True)
+    assert e_y <= REL_BAR and e_dx <= REL_BAR and e_dw <= REL_DESIGN
