@@ -526,8 +526,16 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
     del Y_ref, dX_ref, dW_ref
     fl = 2.0 * M * N * K
     total = sum(t.values())
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f
+                              if ln.startswith("model name")), None)
+    except OSError:
+        pass
     base = {"value": round(fl / t["fwd"] / 1e12, 4), "unit": "TFLOP/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model,
+            "cores_available": len(os.sched_getaffinity(0)),
             "sample": (f"one whole step on the host ({total:.1f}s): in_proj QAT step, ternarize "
                        f"{t['ternarize']:.2f}s ({N * K * 4 / t['ternarize'] / 1e9:.2f} GB/s of W), "
                        f"float64 fwd {t['fwd']:.2f}s, dX {t['dx']:.2f}s, dW {t['dw']:.2f}s "
