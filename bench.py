@@ -551,8 +551,9 @@ def micro(args):
                       "what": MICRO_WHAT}), flush=True)
 
 
-MICRO_WHAT = ("MFMA loop: 4 waves per SIMD, 4 independent 32x32x16 bf16 chains per wave on "
-              "operands loaded once; read stream: 1 GiB in contiguous 16 KiB chunks per wave, "
+MICRO_WHAT = ("MFMA loop: 4 waves per SIMD, independent bf16 MFMA chains per wave (4 of "
+              "32x32x16 or 8 of 16x16x32) on operands loaded once; the ceiling is the faster "
+              "shape; read stream: 1 GiB in contiguous 16 KiB chunks per wave, "
               "16 waves per CU; medians of 5 runs")
 
 
@@ -568,7 +569,8 @@ def measure_ceilings():
         B.build()
     lib = ctypes.CDLL(B.MICRO_OUT)
     lib.tmm_grid_threads.restype = ctypes.c_int
-    lib.tmm_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.tmm_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                  ctypes.c_void_p]
     lib.tmm_read_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p]
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -604,8 +606,12 @@ def measure_ceilings():
     for label, opnd in (("random", torch.randn(1024, generator=gen, device=dev)),
                         ("zero", torch.zeros(1024, device=dev))):
         o16 = opnd.to(torch.bfloat16)
-        sec = timed(lambda: check(lib.tmm_mfma_loop(o16.data_ptr(), iters, out.data_ptr(), st)))
-        res[f"mfma_bf16_loop_{label}_TFLOPs"] = round(fl / sec / 1e12, 1)
+        for shape in (32, 16):
+            sec = timed(lambda: check(lib.tmm_mfma_loop(o16.data_ptr(), iters, shape,
+                                                        out.data_ptr(), st)))
+            res[f"mfma_bf16_{shape}x{shape}_loop_{label}_TFLOPs"] = round(fl / sec / 1e12, 1)
+    res["mfma_bf16_loop_random_TFLOPs"] = max(res["mfma_bf16_32x32_loop_random_TFLOPs"],
+                                              res["mfma_bf16_16x16_loop_random_TFLOPs"])
     buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     buf.random_(0, 256, generator=gen)
     words = torch.empty(threads, dtype=torch.int32, device=dev)

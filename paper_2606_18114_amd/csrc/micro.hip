@@ -2,11 +2,12 @@
 // into libtm_micro.so, separate from libtmamba.so).
 //
 //   tmm_mfma_loop: every wave of a full-occupancy grid (two 8-wave
-//     workgroups per CU, so four waves per SIMD) runs `iters` rounds of four
-//     independent v_mfma_f32_32x32x16_bf16 on operands it loaded from
-//     `operands` (64 lanes x 16 bfloat16: the lane's A then B values), so the
-//     matrix cores see the caller's data, e.g. random values, which draw more
-//     power than zeros.  flops = 2 * 32 * 32 * 16 * 4 * iters * waves.
+//     workgroups per CU, so four waves per SIMD) runs `iters` rounds of
+//     independent bf16 MFMAs on operands it loaded from `operands` (64 lanes
+//     x 16 bfloat16: the lane's A then B values), so the matrix cores see the
+//     caller's data, e.g. random values, which draw more power than zeros.
+//     shape 32: four v_mfma_f32_32x32x16_bf16 per round, shape 16: eight
+//     v_mfma_f32_16x16x32_bf16; either way 131072 flops per wave and round.
 //   tmm_read_stream: a grid of two 512-thread workgroups per CU reads `bytes`
 //     from `buf` in contiguous 16 KiB chunks, one chunk per wave at a time
 //     (sixteen 1 KiB loads in flight per wave, 256 KiB per CU), and folds the
@@ -25,28 +26,48 @@ typedef uint32_t mu32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 512;
 
+typedef float mf32x4 __attribute__((ext_vector_type(4)));
+
+template <int SHAPE>
 __global__ __launch_bounds__(kThreads) void mfma_loop_kernel(const uint16_t* __restrict__ operands,
                                                              int iters, float* __restrict__ out) {
   const int lane = threadIdx.x & 63;
-  mbf16x8 a, b;
   const mu32x4 va = *reinterpret_cast<const mu32x4*>(operands + 16 * lane);
   const mu32x4 vb = *reinterpret_cast<const mu32x4*>(operands + 16 * lane + 8);
-  a = __builtin_bit_cast(mbf16x8, va);
-  b = __builtin_bit_cast(mbf16x8, vb);
-  mf32x16 acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) acc[j][i] = 0.f;
-  for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
-  }
+  const mbf16x8 a = __builtin_bit_cast(mbf16x8, va);
+  const mbf16x8 b = __builtin_bit_cast(mbf16x8, vb);
   float s = 0.f;
+  if constexpr (SHAPE == 32) {
+    mf32x16 acc[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s += acc[j][i];
+      for (int i = 0; i < 16; ++i) acc[j][i] = 0.f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s += acc[j][i];
+  } else {
+    mf32x4 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[j][i] = 0.f;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s += acc[j][i];
+  }
   out[blockIdx.x * kThreads + threadIdx.x] = s;
 }
 
@@ -84,12 +105,18 @@ extern "C" {
 // `out` in elements.
 int tmm_grid_threads(void) { return 2 * cu_count() * kThreads; }
 
-// operands: 1024 bfloat16 (device); out: tmm_grid_threads() floats (device).
+// operands: 1024 bfloat16 (device); shape: 32 or 16 (the MFMA);
+// out: tmm_grid_threads() floats (device).
 // Returns 0 or the HIP error code of the launch.
-int tmm_mfma_loop(const uint16_t* operands, int iters, float* out, void* stream) {
-  if (!operands || !out || iters < 1) return (int)hipErrorInvalidValue;
-  hipLaunchKernelGGL(mfma_loop_kernel, dim3(2 * cu_count()), dim3(kThreads), 0,
-                     (hipStream_t)stream, operands, iters, out);
+int tmm_mfma_loop(const uint16_t* operands, int iters, int shape, float* out, void* stream) {
+  if (!operands || !out || iters < 1 || (shape != 32 && shape != 16))
+    return (int)hipErrorInvalidValue;
+  if (shape == 32)
+    hipLaunchKernelGGL(mfma_loop_kernel<32>, dim3(2 * cu_count()), dim3(kThreads), 0,
+                       (hipStream_t)stream, operands, iters, out);
+  else
+    hipLaunchKernelGGL(mfma_loop_kernel<16>, dim3(2 * cu_count()), dim3(kThreads), 0,
+                       (hipStream_t)stream, operands, iters, out);
   return (int)hipGetLastError();
 }
 
