@@ -347,6 +347,8 @@ def main():
             fwd["achieved"] / c["mfma_bf16_loop_random_TFLOPs"], 4)
         out["roofline_tgemv"]["frac_of_measured"] = round(
             srv["GBps"] / c["hbm_read_stream_1GiB_GBps"], 4)
+        out["roofline_tgemv"]["frac_of_measured_decode_pattern"] = round(
+            srv["GBps"] / c["hbm_read_stream_decode_pattern_GBps"], 4)
 
     # ---------------- CPU oracle baseline (bounded sample) ----------------
     # The oracle's outputs of that step are also the reference for a sampled
@@ -554,7 +556,9 @@ def micro(args):
 MICRO_WHAT = ("MFMA loop: 4 waves per SIMD, independent bf16 MFMA chains per wave (4 of "
               "32x32x16 or 8 of 16x16x32) on operands loaded once; the ceiling is the faster "
               "shape; read stream: 1 GiB in contiguous 16 KiB chunks per wave, "
-              "16 waves per CU; medians of 5 runs")
+              "16 waves per CU; medians of 5 runs; decode pattern: the same read stream "
+              "over the decode step's codes and scales (48 in_proj, then 48 out_proj "
+              "matrices, two launches per token), 20 tokens back to back")
 
 
 def measure_ceilings():
@@ -621,6 +625,25 @@ def measure_ceilings():
     sec = timed(lambda: dst.copy_(buf))
     res["device_copy_1GiB_GBps"] = round(2 * buf.numel() / sec / 1e9, 1)
     del buf, dst
+    # the same read stream in the decode step's launch pattern: the packed
+    # codes and half-precision scales of the 48 in_proj and of the 48
+    # out_proj matrices in two buffers, read one after the other as tokens
+    # back to back, one event pair around the run (as the serving timing)
+    from paper_2606_18114_amd import synth
+    sizes = []
+    for c in (synth.DECODE_IN, synth.DECODE_OUT):
+        nb = synth.N_LAYERS * (c.N * c.K // 4 + 2 * c.N * c.K // c.g)
+        sizes.append(nb - nb % 16384)
+    pat = [torch.randint(0, 256, (nb,), dtype=torch.uint8, device=dev, generator=gen)
+           for nb in sizes]
+
+    def token():
+        for b in pat:
+            check(lib.tmm_read_stream(b.data_ptr(), b.numel(), words.data_ptr(), st))
+    tokens = 20
+    sec = timed(lambda: [token() for _ in range(tokens)], reps=3, warm=1)
+    res["hbm_read_stream_decode_pattern_GBps"] = round(sum(sizes) * tokens / sec / 1e9, 1)
+    del pat
     M, N, K = 16384, 8512, 2048
     X = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
     Wt = (torch.randn((N, K), generator=gen, device=dev) * 0.02).to(torch.bfloat16).t().contiguous()
