@@ -5,12 +5,12 @@
 // respect to the dequantized weights (dY^T X, the straight-through dW).
 //
 // HBM bound: one pass over dW (4 bytes per weight) and the packed codes
-// (1/4 byte).  A persistent grid walks 1024-weight units per wave with four
-// coalesced 1 KiB loads of dW; each lane holds 4 consecutive weights of a
-// load and reads the code word holding their codes (the four lanes of a word
-// read it together).  Products are summed in float64 (exact for the 4 terms
-// of a lane, then a butterfly over the g / 4 lanes of a group, two loads for
-// g = 512) and rounded to float32 once.
+// (1/4 byte).  A persistent grid walks 1024-weight units per wave; each lane
+// owns 16 consecutive weights, i.e. one packed code word (all in one group,
+// g >= 32), and reads their dW as four 16-byte loads.  Products are summed
+// in float64 (16 terms per lane, then a butterfly over the g / 16 lanes of a
+// group) and rounded to float32 once; float64 holds these sums exactly
+// unless a group's terms span more than about 2^20 in magnitude.
 #include "common.hpp"
 
 namespace tmk {
@@ -22,48 +22,44 @@ template <int G>
 __global__ __launch_bounds__(64 * kGcdWaves) void group_code_dot_kernel(
     const uint32_t* __restrict__ codes, const float* __restrict__ dW, int64_t total,
     float* __restrict__ out) {
-  constexpr int L = G / 4 < 64 ? G / 4 : 64;  // lanes holding one group within a load
+  constexpr int L = G / 16;  // lanes holding one group
+  static_assert(L >= 2 && L <= 32, "16 weights per lane, groups of 32 .. 512");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t nunits = (total + kGcdUnit - 1) / kGcdUnit;
   for (int64_t u = (int64_t)blockIdx.x * kGcdWaves + wave; u < nunits;
        u += (int64_t)gridDim.x * kGcdWaves) {
+    // wave-uniform unit base, 32-bit lane offset kept opaque so that the
+    // compiler does not hoist the derived addresses out of the loop
     const int64_t base = u * kGcdUnit;
-    double ps[4];
-    bool ok[4];
+    const int64_t rem = total - base;
+    const int lim = rem < kGcdUnit ? (int)rem : kGcdUnit;
+    int lo = 16 * lane;
+    asm volatile("" : "+v"(lo));
+    const bool ok = lo < lim;  // total % 16 == 0: all 16 weights valid or none
+    u32x4 v[4] = {};
+    uint32_t w = 0u;
+    if (ok) {
+      const float* p = dW + base + lo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = ld16(p + 4 * i);
+      w = codes[(base + lo) / 16];
+    }
+    double ps = 0.0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t off = base + 256 * i + 4 * lane;
-      ok[i] = off < total;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      uint32_t w = 0u;
-      if (ok[i]) {
-        v = ld16(dW + off);
-        w = codes[off / 16];
-      }
-      const uint32_t dv[4] = {v.x, v.y, v.z, v.w};
-      double t = 0.0;
+      const uint32_t dv[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = 4 * (lane & 3) + j;  // element within its 16-code word
-        const uint32_t c = (w >> (2 * (e / 2) + 16 * (e % 2))) & 3u;
+      for (int k = 0; k < 4; ++k) {
+        const int j = 4 * i + k;  // element within the word
+        const uint32_t c = (w >> (2 * (j / 2) + 16 * (j % 2))) & 3u;
         // 01 -> +dW, 11 -> -dW, 00 (and the unused 10) -> 0
-        const float f = __uint_as_float(dv[j] ^ ((c >> 1) << 31));
-        t += (c & 1u) ? (double)f : 0.0;
+        const float f = __uint_as_float(dv[k] ^ ((c >> 1) << 31));
+        ps += (c & 1u) ? (double)f : 0.0;
       }
-      ps[i] = t;
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) ps[i] = group_sum_f64<L>(ps[i]);
-    if constexpr (G == 512) {  // a group spans two loads
-      ps[0] += ps[1];
-      ps[2] += ps[3];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t off = base + 256 * i + 4 * lane;
-      if (ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) out[off / G] = (float)ps[i];
-    }
+    ps = group_sum_f64<L>(ps);
+    if (ok && (lane % L) == 0) out[(base + lo) / G] = (float)ps;
   }
 }
 

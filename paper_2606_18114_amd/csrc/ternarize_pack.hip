@@ -1,44 +1,52 @@
 // Grouped-absmean ternarizer (paper Sec. 3.1) with 2-bit packing (Sec. 8)
 // and the zero-code count (Sec. 3.1, Table 1), in one pass over W.
 //
-// A wave reads 1024 consecutive weights per iteration as four fully
-// coalesced 1 KiB loads; each lane holds 4 weights of a load, so a group of g
-// weights sits on g/4 adjacent lanes (two loads for g = 512) and its sum of
-// |w| is a float64 butterfly over those lanes.  With the sum in float64 the
-// mean rounds once to float32, which is what the float64 oracle produces.
-// Four adjacent lanes OR their codes into one packed 32-bit word.  The grid
-// is persistent and each workgroup adds its zero count to the output once.
+// A wave takes 1024 consecutive weights per iteration and each lane owns 16
+// consecutive ones: the 16 codes of one packed 32-bit word, all in one group
+// (g >= 32) and one row (K % 16 == 0).  The lane reads its 64 bytes as four
+// 16-byte loads (together the wave's loads cover 4 KiB), sums |w| in float64,
+// and a butterfly over the g/16 lanes of the group completes the group sum.
+// With the sum in float64 the mean rounds once to float32, which is what the
+// float64 oracle produces.  The lane then decides its 16 codes, stores its
+// word and counts its zeros with one popcount; the grid is persistent and
+// each workgroup adds its zero count to the output once.
 //
 // Code decision, identical to the float32 expression
 //   q = round_half_even(clip(fl32(w / fl32(s + eps)), -1, 1)):
 // the float32 quotient rounds to at most 1/2 exactly when the real quotient
 // is at most 1/2 + 2^-25 (the midpoint between 1/2 and the next float32 is a
 // tie and goes to the even 1/2), and half-to-even rounding sends 1/2 to 0.
-// So q != 0  <=>  |w| > d * (1/2 + 2^-25),  d = fl32(s + eps).  The product
-// of a 24-bit and a 25-bit significand is exact in float64, so the test is a
-// single exact float64 compare per weight and no division is needed.
+// So q != 0  <=>  |w| > d * (1/2 + 2^-25),  d = fl32(s + eps) >= 0.  For d in
+// [2^e, 2^(e+1)) the excess d * 2^-25 lies in [u/2, u), u = 2^(e-24) the
+// spacing of float32 values at d/2, so no float32 lies strictly between d/2
+// and the threshold: for a float32 |w| the test is  |w| > d/2  (d/2 exact),
+// and  |w| > RZ(d/2)  when d/2 falls below the normal range (RZ: rounded
+// toward zero).  One float32 compare per weight, no division.
 #include "common.hpp"
 
 namespace tmk {
 
 __global__ void zero_u64_kernel(unsigned long long* p) { *p = 0ull; }
 
-constexpr int kTernUnit = 1024;  // weights per wave iteration (4 loads x 64 lanes x 4)
-constexpr int kTernWaves = 16;   // waves per workgroup
+constexpr int kTernUnit = 1024;  // weights per wave iteration: 16 per lane
+constexpr int kTernWaves = 16;  // waves per workgroup
 
 // row_mult (optional, [N]): the code of row n divides by fl32(row_mult[n] * s)
 // + eps instead of s + eps (the appendix's asymmetric gate thresholds); the
 // stored scale is the absmean either way.
 // tau_in (optional, [N, K/g]): the caller's per-group thresholds replace the
 // absmean (a learned scale, Sec. 4); no scales are written then.
-template <int G>
+// MODE: 0 absmean, 1 absmean with row_mult, 2 tau_in (separate instances, so
+// the plain pass carries no registers for the other two)
+template <int G, int MODE>
 __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
     const float* __restrict__ W, int64_t total, int64_t K, float eps,
     const float* __restrict__ row_mult, const float* __restrict__ tau_in,
     uint32_t* __restrict__ codes,
     float* __restrict__ scales, uint16_t* __restrict__ scales_f16,
     unsigned long long* __restrict__ zero_count) {
-  constexpr int L = G / 4 < 64 ? G / 4 : 64;  // lanes holding one group within a load
+  constexpr int L = G / 16;  // lanes holding one group
+  static_assert(L >= 2 && L <= 32, "16 weights per lane, groups of 32 .. 512");
   __shared__ uint32_t wave_zeros[kTernWaves];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -47,63 +55,65 @@ __global__ __launch_bounds__(64 * kTernWaves) void ternarize_pack_kernel(
 
   for (int64_t u = (int64_t)blockIdx.x * kTernWaves + wave; u < nunits;
        u += (int64_t)gridDim.x * kTernWaves) {
+    // The unit's base is wave-uniform; offsets inside it are 32-bit.  The
+    // lane offset is made opaque per unit so that the compiler does not hoist
+    // every derived address out of the loop (registers held for the whole
+    // kernel would cost waves per SIMD).
     const int64_t base = u * kTernUnit;
-    // load i covers weights [base + 256 i, base + 256 i + 256); lane l holds 4 of them
-    float w[4][4];
-    bool ok[4];
-    double ps[4];
+    const int64_t rem = total - base;
+    const int lim = rem < kTernUnit ? (int)rem : kTernUnit;  // valid weights in the unit
+    int lo = 16 * lane;
+    asm volatile("" : "+v"(lo));
+    const bool ok = lo < lim;  // total % 16 == 0: a lane's 16 weights are all valid or none
+    const float* Wl = W + base + lo;
+    u32x4 v[4] = {};
+    if (ok) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = ld16(Wl + 4 * i);
+    }
+    // __uint_as_float, not __builtin_bit_cast: this compiler reads every
+    // element of a vector as its first one when bit-casting v.y, v.z, v.w
+    float w[16];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int64_t off = base + 256 * i + 4 * lane;
-      ok[i] = off < total;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (ok[i]) v = ld16(W + off);
-      // __uint_as_float, not __builtin_bit_cast: this compiler reads every
-      // element of a vector as its first one when bit-casting v.y, v.z, v.w
-      w[i][0] = __uint_as_float(v.x);
-      w[i][1] = __uint_as_float(v.y);
-      w[i][2] = __uint_as_float(v.z);
-      w[i][3] = __uint_as_float(v.w);
-      ps[i] = ((double)fabsf(w[i][0]) + (double)fabsf(w[i][1])) +
-              ((double)fabsf(w[i][2]) + (double)fabsf(w[i][3]));
+      w[4 * i + 0] = __uint_as_float(v[i].x);
+      w[4 * i + 1] = __uint_as_float(v[i].y);
+      w[4 * i + 2] = __uint_as_float(v[i].z);
+      w[4 * i + 3] = __uint_as_float(v[i].w);
     }
-    // group sums: butterfly over the L lanes of each group (float64, exact)
+    double ps = 0.0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ps[i] = group_sum_f64<L>(ps[i]);
-    if constexpr (G == 512) {  // a group spans two loads
-      ps[0] += ps[1];
-      ps[1] = ps[0];
-      ps[2] += ps[3];
-      ps[3] = ps[2];
-    }
+    for (int i = 0; i < 4; ++i)
+      ps += ((double)fabsf(w[4 * i]) + (double)fabsf(w[4 * i + 1])) +
+            ((double)fabsf(w[4 * i + 2]) + (double)fabsf(w[4 * i + 3]));
+    ps = group_sum_f64<L>(ps);  // float64, exact
 
+    float sc = (float)(ps / (double)G);
+    if constexpr (MODE == 2) sc = tau_in[(base + (ok ? lo : 0)) / G];
+    float tau = sc;
+    if constexpr (MODE == 1) {  // the threshold of this lane's row
+      const int64_t row = (base + (ok ? lo : 0)) / K;
+      tau = __fmul_rn(row_mult[row], sc);  // rounded on its own: no fused m * s + eps
+    }
+    const float d = __fadd_rn(tau, eps);
+    // d / 2 rounded toward zero, exactly: a plain halving when d is normal
+    // above 2^-125 (or inf, NaN), a truncating shift of the bits below
+    const uint32_t db = __float_as_uint(d);
+    const float thr = (db >> 23) >= 2u ? d * 0.5f : __uint_as_float(db >> 1);
+    // element j of the word: bits 2j (j even) or 16 + 2(j - 1)/2 (j odd);
+    // codes 01 = +1, 11 = -1
+    uint32_t word = 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float sc = (float)(ps[i] / (double)G);
-      if (tau_in) sc = tau_in[(ok[i] ? base + 256 * i + 4 * lane : 0) / G];  // uniform branch
-      float tau = sc;
-      if (row_mult) {  // (uniform branch) the threshold of this element's row
-        const int64_t off = base + 256 * i + 4 * lane;
-        const int64_t row = (ok[i] ? off : 0) / K;
-        tau = __fmul_rn(row_mult[row], sc);  // rounded on its own: no fused m * s + eps
-      }
-      const float d = __fadd_rn(tau, eps);
-      const double thr = (double)d * (0.5 + 0x1p-25);
-      uint32_t part = 0;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = 4 * (lane & 3) + j;  // element within its 16-weight word
-        const bool nz = (double)fabsf(w[i][j]) > thr;
-        const uint32_t code = nz ? ((__float_as_uint(w[i][j]) >> 31) ? 3u : 1u) : 0u;
-        part |= code << (2 * (e / 2) + 16 * (e % 2));
-        zeros += (nz || !ok[i]) ? 0u : 1u;
-      }
-      part |= lane_xchg<1>(part);
-      part |= lane_xchg<2>(part);
-      const int64_t off = base + 256 * i + 4 * lane;
-      if (ok[i] && (lane & 3) == 0) codes[off / 16] = part;
-      if (!tau_in && ok[i] && (lane % L) == 0 && (G != 512 || (i & 1) == 0)) {
-        const int64_t grp = off / G;
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t b = __float_as_uint(w[j]);
+      const uint32_t code = fabsf(w[j]) > thr ? (((b >> 30) & 2u) | 1u) : 0u;
+      word |= code << (2 * (j / 2) + 16 * (j % 2));
+    }
+    if (ok) {
+      codes[(base + lo) / 16] = word;
+      zeros += 16u - (uint32_t)__popc((word | (word >> 1)) & 0x55555555u);
+      if (MODE != 2 && (lane % L) == 0) {
+        const int64_t grp = (base + lo) / G;
         scales[grp] = sc;
         if (scales_f16) scales_f16[grp] = __builtin_bit_cast(uint16_t, (_Float16)sc);
       }
@@ -143,14 +153,29 @@ hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, fl
   if (blocks > 512) blocks = 512;
   const dim3 grid((unsigned)blocks), block(64 * kTernWaves);
   auto* cw = reinterpret_cast<uint32_t*>(codes);
+  const int mode = tau_in ? 2 : (row_mult ? 1 : 0);
+#define TM_TERN_CASE(GG, MM)                                                            \
+  hipLaunchKernelGGL((ternarize_pack_kernel<GG, MM>), grid, block, 0, stream, W, total, K, \
+                     eps, row_mult, tau_in, cw, scales, scales_f16, zc)
+#define TM_TERN_G(GG)                  \
+  case GG:                             \
+    if (mode == 0)                     \
+      TM_TERN_CASE(GG, 0);             \
+    else if (mode == 1)                \
+      TM_TERN_CASE(GG, 1);             \
+    else                               \
+      TM_TERN_CASE(GG, 2);             \
+    break;
   switch (g) {
-    case 32:  hipLaunchKernelGGL(ternarize_pack_kernel<32>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
-    case 64:  hipLaunchKernelGGL(ternarize_pack_kernel<64>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
-    case 128: hipLaunchKernelGGL(ternarize_pack_kernel<128>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
-    case 256: hipLaunchKernelGGL(ternarize_pack_kernel<256>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
-    case 512: hipLaunchKernelGGL(ternarize_pack_kernel<512>, grid, block, 0, stream, W, total, K, eps, row_mult, tau_in, cw, scales, scales_f16, zc); break;
+    TM_TERN_G(32)
+    TM_TERN_G(64)
+    TM_TERN_G(128)
+    TM_TERN_G(256)
+    TM_TERN_G(512)
     default: return hipErrorInvalidValue;
   }
+#undef TM_TERN_G
+#undef TM_TERN_CASE
   return hipGetLastError();
 }
 

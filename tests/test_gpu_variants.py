@@ -152,6 +152,37 @@ def test_given_thresholds_in_proj_and_ties():
     assert q[0, :4].tolist() == [0, 0, 1, -1] and np.all(q[1] == 1)
 
 
+def test_given_thresholds_tiny_and_huge():
+    # The kernel tests |w| > d/2 in float32, halving d exactly, or truncating
+    # its bits when d/2 falls below the normal range.  Thresholds across that
+    # edge (subnormal, the two smallest normal binades), ordinary and huge
+    # ones, each against the float32 neighbours of d/2: the float32 quotient
+    # of the definition decides.
+    f32 = np.float32
+    ds = [2.0**-149, 3 * 2.0**-149, 2.0**-140 + 2.0**-149, 2.0**-126, 1.5 * 2.0**-126,
+          2.0**-126 + 2.0**-149, 2.0**-125, 3 * 2.0**-125 + 2.0**-147, 0.3, 1.0, 3.0e38]
+    rows, taus = [], []
+    for d in ds:
+        d32 = f32(d)
+        assert float(d32) == d or d == 0.3 or d == 3.0e38
+        h = float(d32) / 2.0                          # exact in float64
+        lo = f32(h) if float(f32(h)) <= h else np.nextafter(f32(h), f32(0))
+        cand = [lo, np.nextafter(lo, f32(np.inf)), np.nextafter(lo, f32(0)),
+                np.nextafter(np.nextafter(lo, f32(np.inf)), f32(np.inf)), d32, f32(0)]
+        row = np.zeros(64, np.float32)  # K = 64: two groups of 32, the same threshold
+        vals = np.array(cand, np.float32)
+        row[:len(vals)] = vals
+        row[8:8 + len(vals)] = -vals
+        row[32:] = row[:32]
+        rows.append(row)
+        taus.append([d32, d32])
+    W = np.stack(rows)
+    tau = np.array(taus, np.float32)
+    q = check_given(W, tau, 32, 0.0, "tiny and huge thresholds")
+    # sanity: the definition gives both codes on every row
+    assert all(np.any(q[r] != 0) and np.any(q[r] == 0) for r in range(len(ds)))
+
+
 def test_given_thresholds_equal_the_absmean_call():
     # the absmean itself as the given threshold reproduces tm_ternarize_pack
     ops = _ops()
