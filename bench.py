@@ -56,11 +56,11 @@ def parse():
     ap.add_argument("--no-ceilings", action="store_true",
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
-                    help="comma list of optional sections to leave out: qat, variants "
-                         "(keeps a profiler trace to the kernels of interest)")
+                    help="comma list of optional sections to leave out: qat, variants, "
+                         "per_layer (keeps a profiler trace to the kernels of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
-    bad = args.skip - {"qat", "variants"}
+    bad = args.skip - {"qat", "variants", "per_layer"}
     if bad:
         ap.error(f"unknown --skip sections: {sorted(bad)}")
     return args
@@ -233,6 +233,10 @@ def main():
                 e0.elapsed_time(e1) / tokens)
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
 
+    # ---------------- decode in layer order: one launch per matrix ----------------
+    per_layer = (None if "per_layer" in args.skip
+                 else decode_per_layer(ops, dec, L, max(args.steps, 10)))
+
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
     qat_block_bf16 = (None if "qat" in args.skip
@@ -325,6 +329,7 @@ def main():
                            "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to back"},
         "kernels": kernels,
         "qat_block": qat_block,
+        "decode_per_layer": per_layer,
         "qat_block_bf16_out": qat_block_bf16,
         "variants": variants,
         "zero_ratio": None,
@@ -544,6 +549,66 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
                        f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
                        f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
     return base, par
+
+
+def decode_per_layer(ops, dec, L, tokens):
+    """Decode as a model runs it, layer by layer: in_proj of layer l, then its
+    out_proj, each launch carrying one matrix (4.4 MB or 2.1 MB of codes).
+    The SSM between the two projections is outside this library, so each GEMV
+    reads its input from the arena.  Timed with Python launches and as one
+    captured HIP graph of the 96 launches per token; the graph's outputs are
+    checked bit for bit against the eager ones."""
+    import torch
+
+    def token():
+        for layer in range(L):
+            for kind in ("in", "out"):
+                d = dec[kind]
+                sl = slice(layer, layer + 1)
+                ops.tgemv(d["x"][sl], d["codes"][sl], d["s16"][sl], d["cfg"].g, y=d["y"][sl])
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(2_000_000)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(tokens):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / tokens
+
+    eager_us = timed(token)
+    ref = {k: dec[k]["y"].clone() for k in ("in", "out")}
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        token()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph):
+        token()
+    for k in ("in", "out"):
+        dec[k]["y"].fill_(float("nan"))
+    graph_us = timed(graph.replay)
+    same = all(torch.equal(dec[k]["y"], ref[k]) for k in ("in", "out"))
+    nbytes = 0
+    for k in ("in", "out"):
+        c = dec[k]["cfg"]
+        B = dec[k]["x"].shape[1]
+        nbytes += L * (c.N * c.K / 4 + 2 * c.N * c.K / c.g + 2 * B * c.K + 4 * B * c.N)
+    del graph
+    return {"launches_per_token": 2 * L,
+            "us_per_token_eager": round(eager_us, 2),
+            "us_per_token_graph": round(graph_us, 2),
+            "GBps_graph": round(nbytes / (graph_us * 1e-6) / 1e9, 1),
+            "graph_outputs_equal_eager": bool(same),
+            "what": "48 x (in_proj 8512x2048, then out_proj 2048x4096), one tgemv launch per "
+                    "matrix in layer order, batch " + str(dec["in"]["x"].shape[1]) +
+                    "; the SSM between the projections is not part of this library"}
 
 
 def micro(args):

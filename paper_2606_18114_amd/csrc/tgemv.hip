@@ -53,6 +53,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "launchers.hpp"
 
 namespace tmk {
 
@@ -410,7 +411,13 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
 // row maxima are combined through LDS, and the pieces are split in place.
 // Otherwise the row maxima are taken by global loads over the whole row and
 // each part is split from global memory.
-template <int G, int WAVES, int RING, int SK, int NR, int NV, bool SW, bool XD>
+//
+// KS (split K across the waves, for launches with few row blocks): all waves
+// of the workgroup share its 32 rows, wave w takes slots w, w + WAVES, ...,
+// and the partial sums are added in LDS in wave order (deterministic) before
+// wave 0 stores y.  A single matrix of in_proj has only 67 blocks of 128
+// rows, out_proj 16, so without the split most CUs would idle.
+template <int G, int WAVES, int RING, int SK, int NR, int NV, bool SW, bool XD, bool KS>
 __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
     const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
@@ -430,7 +437,10 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   const int q = lane >> 4;
   const int64_t mat = blockIdx.y;
   const int nslot = (int)((K + SK - 1) / SK);
-  const int64_t rowb = (int64_t)blockIdx.x * (kGemvWaveRows * WAVES) + wave * kGemvWaveRows;
+  const int64_t rowb = KS ? (int64_t)blockIdx.x * kGemvWaveRows
+                          : (int64_t)blockIdx.x * (kGemvWaveRows * WAVES) + wave * kGemvWaveRows;
+  const int s0 = KS ? wave : 0;       // first slot of this wave
+  const int sstep = KS ? WAVES : 1;   // slot stride
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const uint32_t wlds = lds0 + wave * RING * Plan::kSlotBytes;
   const int R = 2 * B * H;
@@ -447,9 +457,10 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   plan.init(lane);
   const uint8_t* cmat = codes + mat * N * (K / 4);
   const uint16_t* smat = scales_f16 + mat * N * (K / G);
-  auto issue = [&](int s) {  // slot s (past the end: the last slot again) into buffer s % RING
+  auto issue = [&](int s) {  // slot s (past the end: the last slot again) into its ring buffer
     const int sc = s < nslot ? s : nslot - 1;
-    plan.issue(cmat, smat, N, K, rowb, (int64_t)sc * SK, wlds + (s % RING) * Plan::kSlotBytes);
+    plan.issue(cmat, smat, N, K, rowb, (int64_t)sc * SK,
+               wlds + ((s / sstep) % RING) * Plan::kSlotBytes);
   };
   const uint16_t* xm = x + mat * xms;
 
@@ -481,7 +492,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       gemv_dma16(xm + (int64_t)b * K, (uint32_t)(2 * e),
                  lds0 + xoff + 2 * (uint32_t)(b * KR + 512 * p));
     }
-    for (int p = 0; p < RING; ++p) issue(p);
+    for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");  // own x landed
     __syncthreads();
     // this thread's pieces (16 columns of one batch row, up to whole chunks)
@@ -538,7 +549,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
     __syncthreads();
   } else {
-    for (int p = 0; p < RING; ++p) issue(p);
+    for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
     // row maxima of |x| over all K, then the split exponents
     for (int b = 0; b < B; ++b) {
       float mx = 0.f;
@@ -582,7 +593,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
   };
 
-  int s = 0;
+  int s = s0;
   for (int64_t kp0 = 0; kp0 < K; kp0 += KP) {
     const int kpl = (int)(K - kp0 < KP ? K - kp0 : KP);
     if constexpr (!XD) {
@@ -591,15 +602,16 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       __syncthreads();
     }
     const int send = (int)((kp0 + kpl + SK - 1) / SK);
-    for (; s < send; ++s) {
+    for (; s < send; s += sstep) {
       // slot s landed (only the RING - 1 slots after it may still be in flight)
       asm volatile("s_waitcnt vmcnt(%0)" :: "n"((RING - 1) * Plan::kLoads) : "memory");
       SlotRegs<G, SK, H> sr;
-      sr.template fetch<SW>(smem + (wave * RING + s % RING) * Plan::kSlotBytes, l16, q);
+      sr.template fetch<SW>(smem + (wave * RING + (s / sstep) % RING) * Plan::kSlotBytes, l16,
+                            q);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the buffer is free again
       // (one slot in flight: nothing to issue past the end; deeper rings keep
       // their wait counts exact by reloading the last slot)
-      if (RING > 1 || s + RING < nslot) issue(s + RING);
+      if (RING > 1 || s + RING * sstep < nslot) issue(s + RING * sstep);
       const int64_t kcol = (int64_t)s * SK;
       const int cend = (int)((K - kcol) / 128 < CPS ? (K - kcol) / 128 : CPS);
       const bool tail64 = G < 128 && (K - kcol) % 128 != 0 && (K - kcol) < SK;
@@ -609,6 +621,32 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   }
   // loads issued past the end must land before the workgroup's LDS is released
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if constexpr (KS) {
+    // each wave parks its partial sums in its own slot buffer (free now),
+    // then wave 0 adds them in wave order
+    constexpr int kAcc = NR * kGemvBlocks * NV;
+    static_assert(kAcc * 64 * 4 <= RING * Plan::kSlotBytes, "partial sums fit the slot buffer");
+    float* mine = reinterpret_cast<float*>(smem + wave * RING * Plan::kSlotBytes);
+    int t = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+      for (int j = 0; j < kGemvBlocks; ++j)
+#pragma unroll
+        for (int i = 0; i < NV; ++i, ++t) mine[64 * t + lane] = acc[r][j][i];
+    __syncthreads();
+    if (wave != 0) return;
+    for (int w = 1; w < WAVES; ++w) {
+      const float* other = reinterpret_cast<const float*>(smem + w * RING * Plan::kSlotBytes);
+      t = 0;
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int j = 0; j < kGemvBlocks; ++j)
+#pragma unroll
+          for (int i = 0; i < NV; ++i, ++t) acc[r][j][i] += other[64 * t + lane];
+    }
+  }
   store_rows<NR, NV, H>(acc, xexp, B, N, rowb, l16, q, y + mat * yms);
 }
 
@@ -616,12 +654,11 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
 // Launch
 // ---------------------------------------------------------------------------
 
-template <int G>
-static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
-                           int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+template <int G, int WAVES, bool KS>
+static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
+                            int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int SK = kGemvSlotK;
-  constexpr int WAVES = kGemvWaves;
   constexpr int RING = kGemvRing;
   const int R = 2 * B * H;
   const int rmax = R < 64 ? R : 64;  // A rows of one pass
@@ -635,8 +672,8 @@ static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16
   // scales as 4-byte words: an even number of groups per row (so every row
   // and matrix starts 4-byte aligned) and two groups per slot
   const bool sw = (K / G) % 2 == 0 && SK / G >= 2 && ((uintptr_t)s16 & 3) == 0;
-  const dim3 grid((unsigned)((N + kGemvWaveRows * WAVES - 1) / (kGemvWaveRows * WAVES)),
-                  (unsigned)count);
+  constexpr int kRowsPerBlock = KS ? kGemvWaveRows : kGemvWaveRows * WAVES;
+  const dim3 grid((unsigned)((N + kRowsPerBlock - 1) / kRowsPerBlock), (unsigned)count);
   const dim3 block(64 * WAVES);
   auto lds_of = [&](int slot_bytes, int rows, bool with_raw) {
     size_t xa = (size_t)rows * (KP + kGemvXPad);
@@ -644,13 +681,13 @@ static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16
     return (size_t)WAVES * slot_bytes + xa + 128 + 4 * 16 * WAVES + 4 * 16;
   };
 #define TM_GEMV_LAUNCH(NR_, NV_, SW_, XD_, BP, B0)                                            \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, NV_, SW_, XD_>), grid, block,      \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, NV_, SW_, XD_, KS>), grid, block,  \
                      lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, 2 * (BP) * H, XD_), stream, \
                      x + (int64_t)(B0) * K, codes, s16, BP, N, K, KP, (int64_t)B * K,         \
                      (int64_t)B * N, y + (int64_t)(B0) * N)
   if (xd) {  // the common decode case: R <= 16
 #define TM_GEMV_XD(NV_, SW_)                                                                  \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, NV_, SW_, true>), grid, block,       \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, NV_, SW_, true, KS>), grid, block,   \
                      lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, R, true), stream, x,     \
                      codes, s16, B, N, K, KP, (int64_t)B * K, (int64_t)B * N, y)
     if constexpr (SK / G >= 2) {
@@ -674,15 +711,34 @@ static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16
   for (int b0 = 0; b0 < B; b0 += bmax) {
     const int bp = B - b0 < bmax ? B - b0 : bmax;
     const int rp = 2 * bp * H;
-    if (rp <= 16)
+    if (rp <= 16) {
       TM_GEMV_LAUNCH(1, 4, false, false, bp, b0);
-    else if (rp <= 32)
-      TM_GEMV_LAUNCH(2, 4, false, false, bp, b0);
-    else if constexpr (H >= 2)
-      TM_GEMV_LAUNCH(4, 4, false, false, bp, b0);
+    } else if constexpr (!KS) {  // the split form is only chosen for R <= 16
+      if (rp <= 32)
+        TM_GEMV_LAUNCH(2, 4, false, false, bp, b0);
+      else if constexpr (H >= 2)
+        TM_GEMV_LAUNCH(4, 4, false, false, bp, b0);
+    }
   }
 #undef TM_GEMV_LAUNCH
   return hipGetLastError();
+}
+
+// Few row blocks in all (a single matrix: one layer's projection) leave most
+// CUs idle, so the slots of each 32-row block are split across the waves of
+// its workgroup instead (eight waves once K has eight slots), for batches
+// whose A rows fit one 16-row operand.
+template <int G>
+static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
+                           int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+  const int64_t blocks = (int64_t)count * ((N + 127) / 128);
+  const int64_t nslot = (K + kGemvSlotK - 1) / kGemvSlotK;
+  const int R = 2 * B * (G < 128 ? 128 / G : 1);  // A rows: one 16-row operand when <= 16
+  if (blocks < 2 * (int64_t)current_cu_count() && nslot >= 2 && R <= 16) {
+    if (nslot >= 8) return launch_gw<G, 8, true>(x, codes, s16, count, B, N, K, y, stream);
+    return launch_gw<G, kGemvWaves, true>(x, codes, s16, count, B, N, K, y, stream);
+  }
+  return launch_gw<G, kGemvWaves, false>(x, codes, s16, count, B, N, K, y, stream);
 }
 
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,

@@ -483,6 +483,23 @@ def test_gemv_decode_shapes(B):
     gemv_case(2, B, synth.D_MODEL, synth.D_INNER, 128, seed=2000 + B, outliers=False)
 
 
+@pytest.mark.parametrize("B", [1, 2, 4])
+@pytest.mark.parametrize("N,K", [(synth.IN_PROJ_N, synth.D_MODEL), (synth.D_MODEL, synth.D_INNER),
+                                 (333, 2560), (64, 1024)])
+def test_gemv_single_matrix(N, K, B):
+    # one matrix per call, as a model decodes layer by layer: few row blocks,
+    # so the launcher splits each 32-row block's slots across the waves of
+    # its workgroup (8 waves when K has 8 slots; with K = 2560 the waves get
+    # 2 or 1 slots, with K = 1024 half of them none) and adds them in LDS
+    gemv_case(1, B, N, K, 128, seed=N + K + B, outliers=True)
+
+
+@pytest.mark.parametrize("g", [32, 64])
+def test_gemv_single_matrix_small_groups(g):
+    # g < 128: several groups per 128-column chunk (A rows 2 B H <= 16)
+    gemv_case(1, 2 if g == 32 else 4, 700, 2048, g, seed=g, outliers=True)
+
+
 @pytest.mark.parametrize("g", [32, 128])
 def test_gemv_activation_range(g):
     # batch rows: all zeros; magnitudes spread over 2^-40 .. 2^20; one
