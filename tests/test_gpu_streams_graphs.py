@@ -132,3 +132,42 @@ def test_graph_capture_and_replays():
     torch.cuda.synchronize()
     graph.replay()
     _compare(st.outputs(), ref2, "replay with new inputs")
+
+
+def test_graph_of_single_matrix_gemvs_in_layer_order():
+    # decode as a model runs it: one launch per matrix, layer by layer; these
+    # launches take the split-K form (partial sums added in LDS in a fixed
+    # order), so a captured graph must reproduce the eager outputs bit for bit
+    from paper_2606_18114_amd import ops
+    rng = np.random.default_rng(7)
+    layers = []
+    for N, K in ((1200, 2048), (640, 4096), (1200, 2048), (640, 4096)):
+        W = torch.from_numpy(synth.weights(rng, N, K, outliers=True)).cuda()
+        c, _, s16, _ = ops.ternarize_pack(W, 128, 1e-5)
+        x = _bf16(synth.activations(rng, 1, K)).view(1, 1, K)
+        layers.append((x, c.unsqueeze(0), s16.unsqueeze(0), torch.empty((1, 1, N), device="cuda")))
+
+    def run():
+        for x, c, s, y in layers:
+            ops.tgemv(x, c, s, 128, y=y)
+
+    run()
+    torch.cuda.synchronize()
+    ref = [y.clone() for *_, y in layers]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    for rep in range(3):
+        for *_, y in layers:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (*_, y) in enumerate(layers):
+            assert torch.equal(y, ref[i]), f"replay {rep}: layer {i} differs"
