@@ -28,7 +28,9 @@
 //
 // Work split: one workgroup of 4 waves per (matrix, 128-row block); each wave
 // owns 32 consecutive weight rows (two 16-row blocks) and walks the whole K
-// range in 512-column slots.
+// range in 512-column slots.  Launches with few row blocks (one layer's
+// matrix) use a split form instead: one workgroup per 32 rows, whose waves
+// share the slots and add their partial sums in LDS (see the kernel).
 //
 // Loads: a wave's slot (32 rows x 128 bytes of codes, plus the rows' float16
 // group scales) arrives in a wave-private LDS buffer by direct-to-LDS loads
