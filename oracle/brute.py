@@ -114,3 +114,34 @@ def group_code_dot(q, d, g):
                               for qq, dd in zip(qrow[j:j + g], drow[j:j + g])))
                     for j in range(0, len(qrow), g)])
     return out
+
+
+def f16(x):
+    """Round a real number (float or Fraction) to IEEE binary16, ties to even,
+    from the format's definition: 11 significant bits, exponents down to -14
+    with subnormals spaced 2**-24 below that, largest finite 65504, and
+    everything from 65520 (the midpoint to 2**16) up rounding to infinity."""
+    a = abs(Fraction(x))
+    neg = x < 0
+    if a == 0:
+        return -0.0 if neg else 0.0
+    if a >= 65520:
+        return float("-inf") if neg else float("inf")
+    e = a.numerator.bit_length() - a.denominator.bit_length()  # floor(log2 a) or one above
+    if Fraction(2) ** e > a:
+        e -= 1
+    e = max(e, -14)
+    spacing = Fraction(2) ** (e - 10)
+    m = a / spacing
+    r = math.floor(m)
+    if m - r > Fraction(1, 2) or (m - r == Fraction(1, 2) and r % 2 == 1):
+        r += 1
+    v = float(r * spacing)
+    return -v if neg else v
+
+
+def gemv(x, q, s16, g):
+    """y[b][n] = sum_k x[b][k] * s16[n][k//g] * q[n][k] (decode product with
+    float16 scales given as their values), exact-rounded fsum."""
+    return [[math.fsum(xb[k] * s16[n][k // g] * q[n][k] for k in range(len(xb)))
+             for n in range(len(q))] for xb in x]

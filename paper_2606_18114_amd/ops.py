@@ -1,10 +1,12 @@
 """Thin ctypes binding of ``libtmamba.so`` (declared in ``include/tmamba.h``).
 
-Argument marshalling only: every function checks tensor dtypes, devices and
-contiguity, allocates missing outputs with torch (the library itself
-allocates nothing), and passes raw device pointers plus the current HIP
-stream to the C ABI.  All arithmetic runs in the library's HIP kernels.
-There is no fallback: if the library is missing, every call raises.
+Argument marshalling only: every function checks the dtype, device,
+contiguity and exact shape of every tensor it is given (inputs and
+caller-supplied outputs: the C ABI sees only pointers, so a wrong size here
+would become an out-of-bounds access on the device), allocates missing
+outputs with torch (the library itself allocates nothing), and passes raw
+device pointers plus the current HIP stream to the C ABI.  All arithmetic
+runs in the library's HIP kernels.  There is no fallback: if the library is missing, every call raises.
 """
 
 from __future__ import annotations
@@ -95,10 +97,24 @@ def _need(t: torch.Tensor, name: str, dtypes, ndim: int) -> None:
         raise ValueError(f"{name} must be contiguous")
 
 
+def _shape(t: torch.Tensor, name: str, shape, device: torch.device) -> None:
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the other operands on {device}")
+
+
+def _groups(K: int, g: int) -> int:
+    """K / g for the shape checks; a K that g does not divide is left to the
+    library, which rejects it (TM_ESHAPE) before launching anything."""
+    return K // g if g > 0 and K % g == 0 else max(K // max(g, 1), 1)
+
+
 _BF16 = (torch.bfloat16, torch.int16, torch.uint16)
 _U8 = (torch.uint8,)
 _F32 = (torch.float32,)
 _F16 = (torch.float16, torch.int16, torch.uint16)
+_INT64 = (torch.int64,)
 
 
 def ternarize_pack(W: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
@@ -113,19 +129,29 @@ def ternarize_pack(W: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
     (``tm_ternarize_pack_thresh``); the stored scales stay the absmean."""
     _need(W, "W", _F32, 2)
     N, K = W.shape
+    dev = W.device
+    G = _groups(K, g)
     if row_mult is not None:
         _need(row_mult, "row_mult", _F32, 1)
-        if row_mult.shape[0] != N:
-            raise ValueError(f"row_mult has {row_mult.shape[0]} entries, W has {N} rows")
-    dev = W.device
+        _shape(row_mult, "row_mult", (N,), dev)
     if codes is None:
         codes = torch.empty((N, K // 4), dtype=torch.uint8, device=dev)
+    _need(codes, "codes", _U8, 2)
+    _shape(codes, "codes", (N, K // 4), dev)
     if scales is None:
-        scales = torch.empty((N, max(K // g, 1)), dtype=torch.float32, device=dev)
+        scales = torch.empty((N, G), dtype=torch.float32, device=dev)
+    _need(scales, "scales", _F32, 2)
+    _shape(scales, "scales", (N, G), dev)
     if scales_f16 is None and want_f16:
-        scales_f16 = torch.empty((N, max(K // g, 1)), dtype=torch.float16, device=dev)
+        scales_f16 = torch.empty((N, G), dtype=torch.float16, device=dev)
+    if scales_f16 is not None:
+        _need(scales_f16, "scales_f16", _F16, 2)
+        _shape(scales_f16, "scales_f16", (N, G), dev)
     if zero_count is None and want_zero_count:
         zero_count = torch.empty((1,), dtype=torch.int64, device=dev)
+    if zero_count is not None:
+        _need(zero_count, "zero_count", _INT64, 1)
+        _shape(zero_count, "zero_count", (1,), dev)
     if row_mult is None:
         st = lib().tm_ternarize_pack(_ptr(W), N, K, g, eps, _ptr(codes), _ptr(scales),
                                      _ptr(scales_f16), _ptr(zero_count), _stream())
@@ -146,12 +172,16 @@ def ternarize_codes(W: torch.Tensor, tau: torch.Tensor, g: int = 128, eps: float
     _need(W, "W", _F32, 2)
     _need(tau, "tau", _F32, 2)
     N, K = W.shape
-    if tau.shape != (N, K // g):
-        raise ValueError(f"tau has shape {tuple(tau.shape)}, expected {(N, K // g)}")
+    _shape(tau, "tau", (N, _groups(K, g)), W.device)
     if codes is None:
         codes = torch.empty((N, K // 4), dtype=torch.uint8, device=W.device)
+    _need(codes, "codes", _U8, 2)
+    _shape(codes, "codes", (N, K // 4), W.device)
     if zero_count is None and want_zero_count:
         zero_count = torch.empty((1,), dtype=torch.int64, device=W.device)
+    if zero_count is not None:
+        _need(zero_count, "zero_count", _INT64, 1)
+        _shape(zero_count, "zero_count", (1,), W.device)
     st = lib().tm_ternarize_codes(_ptr(W), N, K, g, eps, _ptr(tau), _ptr(codes),
                                   _ptr(zero_count), _stream())
     _check("tm_ternarize_codes", st)
@@ -165,10 +195,11 @@ def group_code_dot(codes: torch.Tensor, dW: torch.Tensor, g: int = 128,
     _need(codes, "codes", _U8, 2)
     _need(dW, "dW", _F32, 2)
     N, K = dW.shape
-    if codes.shape != (N, K // 4):
-        raise ValueError(f"codes has shape {tuple(codes.shape)}, expected {(N, K // 4)}")
+    _shape(codes, "codes", (N, K // 4), dW.device)
     if out is None:
-        out = torch.empty((N, max(K // g, 1)), dtype=torch.float32, device=dW.device)
+        out = torch.empty((N, _groups(K, g)), dtype=torch.float32, device=dW.device)
+    _need(out, "out", _F32, 2)
+    _shape(out, "out", (N, _groups(K, g)), dW.device)
     st = lib().tm_group_code_dot(_ptr(codes), _ptr(dW), N, K, g, _ptr(out), _stream())
     _check("tm_group_code_dot", st)
     return out
@@ -186,15 +217,17 @@ def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int
         raise TypeError(f"out_dtype must be float32 or bfloat16 (got {out_dtype})")
     M, K = X.shape
     N = codes.shape[0]
+    _shape(codes, "codes", (N, K // 4), X.device)
+    _shape(scales, "scales", (N, _groups(K, g)), X.device)
     if Y is None:
         Y = torch.empty((M, N), dtype=out_dtype, device=X.device)
+    _need(Y, "Y", _BF16 if out_dtype == torch.bfloat16 else _F32, 2)
+    _shape(Y, "Y", (M, N), X.device)
     if out_dtype == torch.bfloat16:
-        _need(Y, "Y", _BF16, 2)
         st = lib().tm_tgemm_fwd_bf16(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
                                      _stream())
         _check("tm_tgemm_fwd_bf16", st)
     else:
-        _need(Y, "Y", _F32, 2)
         st = lib().tm_tgemm_fwd(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
                                 _stream())
         _check("tm_tgemm_fwd", st)
@@ -209,8 +242,12 @@ def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g:
     _need(scales, "scales", _F32, 2)
     M, N = dY.shape
     K = codes.shape[1] * 4
+    _shape(codes, "codes", (N, K // 4), dY.device)
+    _shape(scales, "scales", (N, _groups(K, g)), dY.device)
     if dX is None:
         dX = torch.empty((M, K), dtype=torch.float32, device=dY.device)
+    _need(dX, "dX", _F32, 2)
+    _shape(dX, "dX", (M, K), dY.device)
     st = lib().tm_tgemm_bwd_dx(_ptr(dY), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(dX),
                                _stream())
     _check("tm_tgemm_bwd_dx", st)
@@ -224,10 +261,13 @@ def tgemm_bwd_dw_ste(dY: torch.Tensor, X: torch.Tensor, dW: Optional[torch.Tenso
     _need(X, "X", _BF16, 2)
     M, N = dY.shape
     K = X.shape[1]
+    _shape(X, "X", (M, K), dY.device)
     if dW is None:
         if accumulate:
             raise ValueError("accumulate=True needs an existing dW")
         dW = torch.empty((N, K), dtype=torch.float32, device=dY.device)
+    _need(dW, "dW", _F32, 2)
+    _shape(dW, "dW", (N, K), dY.device)
     st = lib().tm_tgemm_bwd_dw_ste(_ptr(dY), _ptr(X), M, N, K, _ptr(dW), int(accumulate),
                                    _stream())
     _check("tm_tgemm_bwd_dw_ste", st)
@@ -243,8 +283,12 @@ def tgemv(x: torch.Tensor, codes: torch.Tensor, scales_f16: torch.Tensor, g: int
     _need(scales_f16, "scales_f16", _F16, 3)
     count, B, K = x.shape
     N = codes.shape[1]
+    _shape(codes, "codes", (count, N, K // 4), x.device)
+    _shape(scales_f16, "scales_f16", (count, N, _groups(K, g)), x.device)
     if y is None:
         y = torch.empty((count, B, N), dtype=torch.float32, device=x.device)
+    _need(y, "y", _F32, 3)
+    _shape(y, "y", (count, B, N), x.device)
     st = lib().tm_tgemv(_ptr(x), _ptr(codes), _ptr(scales_f16), count, B, N, K, g, _ptr(y),
                         _stream())
     _check("tm_tgemv", st)

@@ -116,7 +116,8 @@ class TernaryLinear(torch.nn.Module):
     from the recomputed absmean, magnitude the parameter `scale`.
     "learnable": the parameter `scale` is both threshold and magnitude.  The
     parameter starts at the absmean of the weights (``reset_scale``, run on
-    the first call if not done before).  threshold_mult (float32 [out]) scales
+    the first call unless it was run before or the scale was loaded with
+    ``load_state_dict``).  threshold_mult (float32 [out]) scales
     each row's absmean threshold (e.g. 0.8 on the gate rows of in_proj).
     out_dtype: float32 (default) or bfloat16, the output rounded once as a
     bfloat16 model stores it; the incoming gradient then needs no cast.
@@ -150,6 +151,9 @@ class TernaryLinear(torch.nn.Module):
             self.scale = torch.nn.Parameter(
                 torch.zeros((out_features, in_features // g), dtype=torch.float32, device=device))
         self._scale_ready = scale_mode == "absmean"
+        # a scale that arrives through load_state_dict (a checkpoint, a resumed
+        # run) is the trained one: it must not be reset to the absmean
+        self.register_load_state_dict_pre_hook(TernaryLinear._mark_scale_loaded)
         self.register_buffer(
             "threshold_mult",
             None if threshold_mult is None
@@ -167,6 +171,11 @@ class TernaryLinear(torch.nn.Module):
         if m.scale is not None and weight.is_cuda:
             m.reset_scale()
         return m
+
+    @staticmethod
+    def _mark_scale_loaded(module, state_dict, prefix, *args) -> None:
+        if module.scale is not None and (prefix + "scale") in state_dict:
+            module._scale_ready = True
 
     @torch.no_grad()
     def reset_scale(self) -> None:

@@ -27,6 +27,28 @@ def test_layer_rejects_bad_shapes_and_cpu_tensors():
         layer(torch.zeros((4, 256), dtype=torch.bfloat16))  # no CPU fallback
 
 
+@pytest.mark.parametrize("mode", ["decoupled", "learnable"])
+def test_loaded_scale_is_not_reset(mode):
+    """A learned scale restored with load_state_dict (a checkpoint or a resumed
+    run) marks the layer initialised, so the first forward keeps it instead of
+    resetting it to the absmean; a fresh layer still starts uninitialised."""
+    from paper_2606_18114_amd.qat import TernaryLinear
+    trained = TernaryLinear(256, 64, g=128, scale_mode=mode)
+    with torch.no_grad():
+        trained.scale.copy_(torch.linspace(0.01, 0.05, trained.scale.numel()).view_as(
+            trained.scale))
+    trained._scale_ready = True
+    fresh = TernaryLinear(256, 64, g=128, scale_mode=mode)
+    assert not fresh._scale_ready
+    fresh.load_state_dict(trained.state_dict())
+    assert fresh._scale_ready
+    assert torch.equal(fresh.scale, trained.scale)
+    # nested under a prefix (a model holding the layer)
+    outer = torch.nn.Sequential(TernaryLinear(256, 64, g=128, scale_mode=mode))
+    outer.load_state_dict(torch.nn.Sequential(trained).state_dict())
+    assert outer[0]._scale_ready and torch.equal(outer[0].scale, trained.scale)
+
+
 def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(synth.f32_to_bf16_bits(a)).view(np.int16)).cuda() \
         .view(torch.bfloat16)
@@ -156,3 +178,22 @@ def test_bf16_output_layer():
     e_dw = O.rel_fro_error(layer.weight.grad.cpu().numpy(), O.gemm_bwd_dw(rb, xb))
     print(f"[qat bf16 out] y {e_y:.2e} dX {e_dx:.2e} dW {e_dw:.2e}", flush=True)
     assert e_y <= REL_BAR and e_dx <= REL_BAR and e_dw <= REL_DESIGN
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", ["decoupled", "learnable"])
+def test_reloaded_learned_layer_gives_the_same_outputs(mode):
+    from paper_2606_18114_amd.qat import TernaryLinear
+    torch.manual_seed(3)
+    layer = TernaryLinear(512, 256, g=128, scale_mode=mode, device="cuda")
+    x = _bf16(np.random.default_rng(3).standard_normal((32, 512)).astype(np.float32))
+    layer(x)                                   # initialises the scale from the absmean
+    with torch.no_grad():
+        layer.scale.mul_(1.37)                 # a "trained" scale, away from the absmean
+    y0 = layer(x).detach().clone()
+    fresh = TernaryLinear(512, 256, g=128, scale_mode=mode, device="cuda")
+    fresh.load_state_dict(layer.state_dict())
+    y1 = fresh(x).detach()
+    torch.cuda.synchronize()
+    assert torch.equal(fresh.scale, layer.scale)
+    assert torch.equal(y0, y1)
