@@ -177,14 +177,17 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
  *   scales_f16  uint16 [count, N, K/g]   in   float16 bits (2-byte aligned)
  *   count       1 .. 65535;  B  1 .. 16;  N * K / 4 <= 2^31 (bytes per matrix)
  *   y           float32 [count, B, N]    out  (16-byte aligned)
- * Each row of x is split into two FP8 terms, exact for elements within 2^14
- * of the row's largest magnitude (smaller ones err by at most 2^-22 of it);
- * the matrix cores add the products at slightly below float32 precision and
- * the float16 scale is applied in float32 per group.  Results are
- * deterministic for a given shape and count.  A launch with few row blocks
- * (fewer than two per CU, e.g. count = 1) splits K across the waves of a
- * workgroup and adds the parts in a fixed order, so its last bits can differ
- * from the same matrix inside a larger launch.
+ * Each 32-column block of a row of x is split into FP8 terms whose
+ * power-of-two scales are taken from the block itself (two magnitude
+ * classes of two terms each), so every element within 2^16 of its block's
+ * largest magnitude is represented exactly, and smaller ones err by less
+ * than 2^-19 of that maximum; an outlier affects only its own block.  The
+ * matrix cores add the exact products at float32-like precision and the
+ * float16 scale is applied in float32 per group.  x must be finite.
+ * Results are deterministic for a given shape and count.  A launch with few
+ * row blocks (fewer than two per CU, e.g. count = 1) splits K across the
+ * waves of a workgroup and adds the parts in a fixed order, so its last bits
+ * can differ from the same matrix inside a larger launch.
  */
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
                    const uint16_t* scales_f16, int32_t count, int32_t B,

@@ -14,17 +14,28 @@
 // against ~1.4 for a bfloat16 operand.
 //
 // Activations.  A bfloat16 value has 8 significant bits, an e4m3 value 4, so
-// x is split into two FP8 terms: with e = exponent of max|x| over the row
-// minus 7 (scaling the row maximum into [128, 256)),
+// each x is split into two FP8 terms at a power-of-two exponent e:
 //   t1 = fp8(x * 2^-e),  t2 = fp8((x * 2^-e - t1) * 16),
-// and x = (t1 + t2 / 16) * 2^e exactly for every element within 2^14 of the
-// row maximum (smaller ones err by at most 2^-22 of the row maximum).  The
-// two terms are two rows of the MFMA's A operand, so one instruction does
-// both; rows of other batch items (and, for g < 128, of the other groups
-// inside the 128 columns, each row holding zeros outside its group) fill the
-// remaining rows.  Rows are combined with their power-of-two factors at the
-// end.  The matrix core sums FP8 x FP4 products with somewhat less than
-// float32 precision: measured relative errors are 1e-7 .. 1e-5.
+// and x = (t1 + t2 / 16) * 2^e exactly whenever |x * 2^-e| >= 2^-6.  The
+// exponent is chosen per 32-column block of a row (the 32 values one MFMA
+// k block covers) and handed to the matrix core as the E8M0 scale of that
+// block, so an outlier only sets the exponent of its own block.
+//
+// The matrix core adds the 32 products of a block at about 13 bits below
+// the largest of them (measured: a product whose lowest bit lies further
+// down is truncated; sums across blocks are float32-accurate).  So each A
+// row of a block must keep its values within 2^8 of its largest one.  The
+// values of a block are therefore cut into two magnitude classes: "large"
+// values (|x| >= 2^(e-1), where e scales the block maximum into [128, 256))
+// are split at e, the others at the exponent of their own maximum.  Each
+// class and term is a row of the MFMA's A operand, four rows per batch
+// item, with scales 2^e and 2^(e-4) for the two terms.  Every value of at
+// least 2^-8 times the largest of its class is exact, which includes every
+// value within 2^16 of its block maximum; smaller ones err by less than
+// 2^-11 of the largest small value.  Blocks whose maximum lies under 2^-116
+// keep the exponent -123 that the scale range allows.  The other rows of the
+// operand hold other batch items and, for g < 128, the other groups inside
+// the 128 columns (each row zero outside its group).
 //
 // Work split: one workgroup of 4 waves per (matrix, 128-row block); each wave
 // owns 32 consecutive weight rows (two 16-row blocks) and walks the whole K
@@ -133,11 +144,17 @@ __device__ __forceinline__ i32x8 decode_fp4(u32x2 w) {
 // with an operand: with the result allocated over part of the B operand's
 // VGPRs, this instruction was measured to give wrong sums (the operand is
 // evidently still being read while the result is written).
-__device__ __forceinline__ f32x4 mfma_f8f4(i32x8 a, i32x8 b) {
-  // A: FP8 e4m3 (cbsz 0), B: FP4 e2m1 (blgp 4), unit scales (E8M0 127 = 2^0)
+// A: FP8 e4m3 (cbsz 0) scaled per lane by the E8M0 byte OPSEL of `escale`
+// (lane (row r, block q) holds row r's columns 32 q .. 32 q + 31 of the
+// chunk); B: FP4 e2m1 (blgp 4) with the scale 2^-1, since the codes are 2 q.
+template <int OPSEL>
+__device__ __forceinline__ f32x4 mfma_f8f4(i32x8 a, i32x8 b, int escale) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 4,
-                                                          0, 127, 0, 127);
+                                                          OPSEL, escale, 0, 126);
 }
+
+// A rows per batch item and group: large/small magnitude class x two terms
+constexpr int kTerms = 4;
 
 // Order of a 16-column piece of x in the MFMA's k order (see decode_fp4):
 // byte o of the piece holds column kFp4Col[o].
@@ -148,32 +165,72 @@ __device__ constexpr int kFp4Col[16] = {2, 6, 10, 14, 3, 7, 11, 15, 0, 4, 8, 12,
 // Pieces shared by both kernels
 // ---------------------------------------------------------------------------
 
-// Split 16 bfloat16 values (one code word's columns, bits in wv[0..7]) into
-// the two FP8 terms of row exponent e, in the MFMA's k order.
-__device__ __forceinline__ void split_piece(const uint32_t (&wv)[8], int e, u32x4& t1, u32x4& t2) {
-  uint32_t o1[4], o2[4];
+// Exponent that scales a block maximum into [128, 256), 0 for an all-zero
+// block, and at least -123 so that both terms' E8M0 scales (127 + e and
+// 127 + e - 4) stay in range.
+__device__ __forceinline__ int block_exp(float mx) {
+  const int e = mx > 0.f ? __builtin_amdgcn_frexp_expf(mx) - 8 : 0;
+  return e < -123 ? -123 : e;
+}
+
+// FP8 terms of four scaled values a[0..3] (byte j of the result: value j)
+__device__ __forceinline__ void fp8_terms(const float (&a)[4], uint32_t& p1out, uint32_t& p2out) {
+  int p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[0], a[1], 0, false);
+  p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[2], a[3], p1, true);
+  const float r0 = 16.f * (a[0] - __builtin_amdgcn_cvt_f32_fp8(p1, 0));
+  const float r1 = 16.f * (a[1] - __builtin_amdgcn_cvt_f32_fp8(p1, 1));
+  const float r2 = 16.f * (a[2] - __builtin_amdgcn_cvt_f32_fp8(p1, 2));
+  const float r3 = 16.f * (a[3] - __builtin_amdgcn_cvt_f32_fp8(p1, 3));
+  int p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
+  p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, p2, true);
+  p1out = (uint32_t)p1;
+  p2out = (uint32_t)p2;
+}
+
+// Split the 32-column block held by a lane pair (lane and lane ^ 1, each with
+// 16 bfloat16 values in wv; dead lanes pass zeros) into its four A rows in
+// the MFMA's k order: t[0], t[1] the large class's terms, t[2], t[3] the
+// small class's; e[u] is row u's scale exponent.  Both lanes of a pair must
+// call this together (the block maxima are exchanged between them).
+__device__ __forceinline__ void split_block(const uint32_t (&wv)[8], bool live, u32x4 (&t)[kTerms],
+                                            int (&e)[kTerms]) {
+  float v[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const uint32_t bits = (c & 1) ? (wv[c >> 1] & 0xFFFF0000u) : (wv[c >> 1] << 16);
+    v[c] = live ? __uint_as_float(bits) : 0.f;
+  }
+  float m = 0.f;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) m = fmaxf(m, fabsf(v[c]));
+  m = fmaxf(m, __shfl_xor(m, 1));
+  const int eb = block_exp(m);
+  const float thr = __builtin_ldexpf(1.f, eb - 1);  // large: within 2^8 of the maximum
+  float ms = 0.f;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) ms = fabsf(v[c]) < thr ? fmaxf(ms, fabsf(v[c])) : ms;
+  ms = fmaxf(ms, __shfl_xor(ms, 1));
+  const int es = block_exp(ms);
+  e[0] = eb;
+  e[1] = eb - 4;
+  e[2] = es;
+  e[3] = es - 4;
+  uint32_t o[kTerms][4];
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
-    float a[4];
+    float al[4], as[4];
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int c = kFp4Col[4 * d + jj];
-      const uint32_t bits = (c & 1) ? (wv[c >> 1] & 0xFFFF0000u) : (wv[c >> 1] << 16);
-      a[jj] = __builtin_ldexpf(__uint_as_float(bits), -e);
+      const float x = v[kFp4Col[4 * d + jj]];
+      const bool large = fabsf(x) >= thr;
+      al[jj] = large ? __builtin_ldexpf(x, -eb) : 0.f;
+      as[jj] = large ? 0.f : __builtin_ldexpf(x, -es);
     }
-    int p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[0], a[1], 0, false);
-    p1 = __builtin_amdgcn_cvt_pk_fp8_f32(a[2], a[3], p1, true);
-    const float r0 = 16.f * (a[0] - __builtin_amdgcn_cvt_f32_fp8(p1, 0));
-    const float r1 = 16.f * (a[1] - __builtin_amdgcn_cvt_f32_fp8(p1, 1));
-    const float r2 = 16.f * (a[2] - __builtin_amdgcn_cvt_f32_fp8(p1, 2));
-    const float r3 = 16.f * (a[3] - __builtin_amdgcn_cvt_f32_fp8(p1, 3));
-    int p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r0, r1, 0, false);
-    p2 = __builtin_amdgcn_cvt_pk_fp8_f32(r2, r3, p2, true);
-    o1[d] = (uint32_t)p1;
-    o2[d] = (uint32_t)p2;
+    fp8_terms(al, o[0][d], o[1][d]);
+    fp8_terms(as, o[2][d], o[3][d]);
   }
-  t1 = u32x4{o1[0], o1[1], o1[2], o1[3]};
-  t2 = u32x4{o2[0], o2[1], o2[2], o2[3]};
+#pragma unroll
+  for (int u = 0; u < kTerms; ++u) t[u] = u32x4{o[u][0], o[u][1], o[u][2], o[u][3]};
 }
 
 // max |x| of bfloat16 pairs
@@ -182,23 +239,39 @@ __device__ __forceinline__ float absmax2(float m, uint32_t w) {
   return fmaxf(m, fabsf(__uint_as_float(w & 0xFFFF0000u)));
 }
 
-// Exponent that scales a row maximum into [128, 256); 0 for an all-zero row.
-__device__ __forceinline__ int split_exp(float mx) {
-  return mx > 0.f ? __builtin_amdgcn_frexp_expf(mx) - 8 : 0;
-}
-
 // Write one split 16-column piece of batch row b at MFMA k offset koff of the
-// A rows (2b + t) H + hh: the piece's own group h gets the terms, the other
-// groups of the chunk zeros.
+// A rows (kTerms b + u) H + hh: the piece's own group h gets the terms, the
+// other groups of the chunk zeros.
 template <int H>
 __device__ __forceinline__ void put_piece(uint8_t* xs, int xstride, int b, int h, int koff,
-                                          u32x4 t1, u32x4 t2) {
+                                          const u32x4 (&t)[kTerms]) {
   const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int hh = 0; hh < H; ++hh) {
-    st16(xs + ((2 * b + 0) * H + hh) * xstride + koff, hh == h ? t1 : z);
-    st16(xs + ((2 * b + 1) * H + hh) * xstride + koff, hh == h ? t2 : z);
-  }
+  for (int u = 0; u < kTerms; ++u)
+#pragma unroll
+    for (int hh = 0; hh < H; ++hh)
+      st16(xs + ((kTerms * b + u) * H + hh) * xstride + koff, hh == h ? t[u] : z);
+}
+
+// Byte of 32-column block blk (of an x part) in an A row's exponent bytes:
+// one 32-bit word per (512-column slot, lane group q) holds the bytes of the
+// slot's four 128-column chunks, so a lane reads its scales for a whole slot
+// with one load and the MFMA picks the chunk's byte.
+__device__ __forceinline__ int exp_index(int blk) {
+  return (blk >> 4) * 16 + (blk & 3) * 4 + ((blk >> 2) & 3);
+}
+
+// E8M0 scale bytes of block blk for the A rows of batch row b (group h gets
+// 127 + e[u]; the other groups' rows, which are zero there, get 2^0)
+template <int H>
+__device__ __forceinline__ void put_exps(uint8_t* es, int estride, int b, int h, int blk,
+                                         const int (&e)[kTerms]) {
+  const int idx = exp_index(blk);
+#pragma unroll
+  for (int u = 0; u < kTerms; ++u)
+#pragma unroll
+    for (int hh = 0; hh < H; ++hh)
+      es[((kTerms * b + u) * H + hh) * estride + idx] = (uint8_t)(hh == h ? 127 + e[u] : 127);
 }
 
 // MFMA k offset of the first byte of the 16-column piece at column col
@@ -208,47 +281,34 @@ __device__ __forceinline__ int piece_koff(int col) {
   return (col - cic) + 32 * (cic / 32) + 16 * ((cic / 16) % 2);
 }
 
-// Combine the A rows of each batch item and store y for the wave's rows
-// rowb .. rowb + 31.  Lane (row l16, group q) holds D rows 16 r + 4 q + i =
-// (2 b + t) H + h; term t carries 2^(e_b - 4 t), and the FP4 codes are 2 q,
-// hence the extra -1.
-template <int NR, int NV, int H>
-__device__ __forceinline__ void store_rows(const float (&acc)[NR][kGemvBlocks][NV],
-                                           const int* xexp, int B, int64_t N, int64_t rowb,
-                                           int l16, int q, float* ym) {
+// Store y for the wave's rows rowb .. rowb + 31.  Lane (row l16, group q)
+// holds, per group hh, the scaled sum of its D rows 16 r + 4 q + i with
+// i % H == hh; D row (kTerms b + u) H + hh belongs to batch item b.
+template <int NR, int H>
+__device__ __forceinline__ void store_rows(const float (&acc)[NR][kGemvBlocks][H], int B,
+                                           int64_t N, int64_t rowb, int l16, int q, float* ym) {
 #pragma unroll
   for (int j = 0; j < kGemvBlocks; ++j) {
     const int64_t n = rowb + 16 * j + l16;
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
-      float part[4];
+      float v = acc[r][j][0];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int gr = 16 * r + 4 * q + i;
-        const int bt = gr / H;  // 2 b + t
-        const int b = bt >> 1, t = bt & 1;
-        part[i] = (i < NV && b < B) ? __builtin_ldexpf(acc[r][j][i < NV ? i : 0],
-                                                       xexp[b] - 1 - 4 * t)
-                                    : 0.f;
-      }
+      for (int hh = 1; hh < H; ++hh) v += acc[r][j][hh];
       if constexpr (H == 1) {
-        // rows 2b, 2b+1 are i = 0, 1 (and 2, 3) of one lane
-#pragma unroll
-        for (int i = 0; i < NV; i += 2) {
-          const int b = (16 * r + 4 * q + i) / 2;
-          if (n < N && b < B) ym[(int64_t)b * N + n] = part[i] + part[i + 1];
-        }
-      } else if constexpr (H == 2) {
-        // rows 4b .. 4b+3 are i = 0..3 of one lane
-        const int b = (16 * r + 4 * q) / 4;
-        const float v = (part[0] + part[1]) + (part[2] + part[3]);
+        // rows 4b .. 4b+3 are lane group q's four rows
+        const int b = 4 * r + q;
         if (n < N && b < B) ym[(int64_t)b * N + n] = v;
+      } else if constexpr (H == 2) {
+        // rows 8b .. 8b+7: lane groups q = 2(b%2) and q + 1
+        v += __shfl_xor(v, 16);
+        const int b = 2 * r + (q >> 1);
+        if ((q & 1) == 0 && n < N && b < B) ym[(int64_t)b * N + n] = v;
       } else {
-        // rows 8b .. 8b+7: term 0 on lane group q = 2(b%2), term 1 on q + 1
-        const float v = (part[0] + part[1]) + (part[2] + part[3]);
-        const float o = __shfl_xor(v, 16);
-        const int b = (16 * r + 4 * q) / 8;
-        if ((q & 1) == 0 && n < N && b < B) ym[(int64_t)b * N + n] = v + o;
+        // rows 16b .. 16b+15: all four lane groups of operand r
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (q == 0 && n < N && r < B) ym[(int64_t)r * N + n] = v;
       }
     }
   }
@@ -343,17 +403,44 @@ struct SlotRegs {
   }
 };
 
+// acc[r][j][hh] += (group hh's float16 scale) x (the sum of the chunk's D
+// rows of group hh): lane row i of a lane group is group i % H, and the
+// rows of one group in a lane are the terms of one batch item.
+template <int NR, int H, int CPS>
+__device__ __forceinline__ void scale_add(const f32x4 (&pb)[NR][kGemvBlocks],
+                                          const float (&sv)[kGemvBlocks][CPS][H], int c,
+                                          float (&acc)[NR][kGemvBlocks][H]) {
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+#pragma unroll
+    for (int j = 0; j < kGemvBlocks; ++j)
+#pragma unroll
+      for (int hh = 0; hh < H; ++hh) {
+        float t = pb[r][j][hh];
+#pragma unroll
+        for (int i = hh + H; i < 4; i += H) t += pb[r][j][i];
+        acc[r][j][hh] += sv[j][c][hh] * t;
+      }
+}
+
 // One slot of a wave from registers: cend full 128-column chunks plus a final
-// 64-column chunk when tail64, with the A rows at part column kb0.  Adds the
+// 64-column chunk when tail64, with the A rows at part column kb0 (a
+// multiple of the slot width) and their exponent words at ebase.  Adds the
 // scaled partial sums into acc.
-template <int G, int SK, int NR, int NV, int H>
+template <int G, int SK, int NR, int H>
 __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs<G, SK, H>& sr,
                                              const int (&abase)[NR],
-                                             const uint32_t (&amask)[NR], uint32_t kb0,
-                                             int cend, bool tail64, int q,
-                                             float (&acc)[NR][kGemvBlocks][NV]) {
+                                             const uint32_t (&amask)[NR],
+                                             const int (&ebase)[NR], uint32_t kb0, int cend,
+                                             bool tail64, int q,
+                                             float (&acc)[NR][kGemvBlocks][H]) {
   constexpr int CPS = SK / 128;
   constexpr int NB = kGemvBlocks;
+  static_assert(CPS <= 4, "one exponent word covers four chunks");
+  int esc[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+    esc[r] = *reinterpret_cast<const int*>(smem + ebase[r] + (kb0 / 512) * 16 + 4 * q);
   // partial sums alternate between two buffers: chunk c - 1 is scaled after
   // the MFMAs of chunk c are issued, so the vector ALUs never wait on them
   f32x4 pb[2][NR][NB];
@@ -373,25 +460,11 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
       const i32x8 aop = {(int)a0.x, (int)a0.y, (int)a0.z, (int)a0.w,
                          (int)a1.x, (int)a1.y, (int)a1.z, (int)a1.w};
 #pragma unroll
-      for (int j = 0; j < NB; ++j) pb[buf][r][j] = mfma_f8f4(aop, bop[j]);
+      for (int j = 0; j < NB; ++j) pb[buf][r][j] = mfma_f8f4<c>(aop, bop[j], esc[r]);
     }
-    if (c > 0) {
-#pragma unroll
-      for (int r = 0; r < NR; ++r)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int i = 0; i < NV; ++i)
-            acc[r][j][i] += sr.sv[j][c - 1][i % H] * pb[buf ^ 1][r][j][i];
-    }
-    if (c == CPS - 1 || c + 1 > cend || (c + 1 == cend && !tail64)) {  // the slot's last chunk
-#pragma unroll
-      for (int r = 0; r < NR; ++r)
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int i = 0; i < NV; ++i) acc[r][j][i] += sr.sv[j][c][i % H] * pb[buf][r][j][i];
-    }
+    if constexpr (c > 0) scale_add<NR, H, CPS>(pb[buf ^ 1], sr.sv, c - 1, acc);
+    if (c == CPS - 1 || c + 1 > cend || (c + 1 == cend && !tail64))  // the slot's last chunk
+      scale_add<NR, H, CPS>(pb[buf], sr.sv, c, acc);
   });
 }
 
@@ -400,26 +473,25 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
 // ---------------------------------------------------------------------------
 //
 // One workgroup per (matrix, 128-row block); each of its 4 waves owns 32 rows
-// and walks K in 512-column slots.  The split x (FP8 A rows) is staged in LDS
-// in parts of KP columns (a multiple of the slot width) that fit the LDS
-// budget, with up to NR = 4 A operands of 16 rows per chunk (the launcher
-// splits larger batches; x and y rows of matrix m start at m * xms and
-// m * yms).
+// and walks K in 512-column slots.  The split x (FP8 A rows and their E8M0
+// exponent bytes) is staged in LDS in parts of KP columns (a multiple of the
+// slot width) that fit the LDS budget, with up to NR = 4 A operands of 16
+// rows per chunk (the launcher splits larger batches; x and y rows of matrix
+// m start at m * xms and m * yms).
 //
 // XD (x by direct-to-LDS loads, one part only): the raw bfloat16 x of the
 // matrix is fetched into the A-row area by direct-to-LDS loads issued before
 // the first slot's codes, so both arrive within one memory latency; every
-// thread then takes its (at most two) 16-column pieces into registers, the
-// row maxima are combined through LDS, and the pieces are split in place.
-// Otherwise the row maxima are taken by global loads over the whole row and
-// each part is split from global memory.
+// thread then takes its (at most two) 16-column pieces into registers and,
+// once all raw pieces are read, splits them in place.  Otherwise each part
+// is split from global memory.
 //
 // KS (split K across the waves, for launches with few row blocks): all waves
 // of the workgroup share its 32 rows, wave w takes slots w, w + WAVES, ...,
 // and the partial sums are added in LDS in wave order (deterministic) before
 // wave 0 stores y.  A single matrix of in_proj has only 67 blocks of 128
 // rows, out_proj 16, so without the split most CUs would idle.
-template <int G, int WAVES, int RING, int SK, int NR, int NV, bool SW, bool XD, bool KS>
+template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS>
 __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
     const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
@@ -428,10 +500,9 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int CPS = SK / 128;
   constexpr int kXPieces = 2;  // XD: 16-column x pieces per thread
-  static_assert(NV == 4 || (NV == 2 && H == 1 && NR == 1), "two D rows only for B = 1, g >= 128");
   extern __shared__ __attribute__((aligned(1024))) uint8_t smem[];
   // [waves][codes | scales] | A rows [R][KP + pad] (XD: raw x first) |
-  // zero pad [128] | row maxima [WAVES][16] float | exponents [16] int
+  // exponent bytes [R][KP / 32] | zero pad [128]
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -445,15 +516,16 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   const int sstep = KS ? WAVES : 1;   // slot stride
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const uint32_t wlds = lds0 + wave * RING * Plan::kSlotBytes;
-  const int R = 2 * B * H;
+  const int R = kTerms * B * H;
   const int xstride = (int)KP + kGemvXPad;
+  const int estride = (int)(KP / 32);
   const int xoff = WAVES * RING * Plan::kSlotBytes;
   uint8_t* xs = smem + xoff;
   const int64_t KR = (K + 511) / 512 * 512;  // XD: raw x row length
   const int xarea = XD && B * KR * 2 > R * xstride ? (int)(B * KR * 2) : R * xstride;
-  const int zoff = xoff + xarea;
-  float* xmax = reinterpret_cast<float*>(smem + zoff + 128);
-  int* xexp = reinterpret_cast<int*>(smem + zoff + 128 + 4 * 16 * WAVES);
+  const int eoff = xoff + xarea;
+  uint8_t* es = smem + eoff;
+  const int zoff = eoff + (R * estride + 15) / 16 * 16;
 
   Plan plan;
   plan.init(lane);
@@ -466,28 +538,43 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   };
   const uint16_t* xm = x + mat * xms;
 
-  int abase[NR];
+  // operand rows past R read the zero pad (and row 0's exponents, any valid
+  // scale: their values are zero)
+  int abase[NR], ebase[NR];
   uint32_t amask[NR];
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     const int gr = 16 * r + l16;
     abase[r] = gr < R ? xoff + gr * xstride : zoff;
     amask[r] = gr < R ? 0xFFFFFFFFu : 0u;
+    ebase[r] = eoff + (gr < R ? gr : 0) * estride;
   }
-  float acc[NR][kGemvBlocks][NV];
+  float acc[NR][kGemvBlocks][H];
 #pragma unroll
   for (int r = 0; r < NR; ++r)
 #pragma unroll
     for (int j = 0; j < kGemvBlocks; ++j)
 #pragma unroll
-      for (int i = 0; i < NV; ++i) acc[r][j][i] = 0.f;
+      for (int i = 0; i < H; ++i) acc[r][j][i] = 0.f;
+
+  // split piece i (16 columns) of an x part whose pieces per row are
+  // `pieces`; the lane pair i, i ^ 1 holds one 32-column block
+  auto put_split = [&](int i, int pieces, int64_t kpl, const uint32_t (&wv)[8]) {
+    const int b = i / pieces, col = 16 * (i % pieces);
+    const bool live = col < kpl;
+    u32x4 t[kTerms];
+    int e[kTerms];
+    split_block(wv, live, t, e);
+    const int h = live ? (G < 128 ? (col % 128) / G : 0) : -1;
+    put_piece<H>(xs, xstride, b, h, piece_koff(col), t);
+    if ((i & 1) == 0) put_exps<H>(es, estride, b, h, col / 32, e);
+  };
 
   if constexpr (XD) {
     // raw x (row b, columns 512 p .. 512 p + 511 per load; a load past K
     // re-reads the row's last 16 bytes into the row's pad), then the codes
     const int xl = B * (int)(KR / 512);
-    int mine = 0;
-    for (int pi = wave; pi < xl; pi += WAVES, ++mine) {
+    for (int pi = wave; pi < xl; pi += WAVES) {
       const int b = pi / (int)(KR / 512), p = pi % (int)(KR / 512);
       int64_t e = 512 * (int64_t)p + 8 * lane;
       e = e < K - 8 ? e : K - 8;
@@ -501,7 +588,6 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
     const int pieces = (int)((K + 127) / 128 * 8);
     const uint16_t* xraw = reinterpret_cast<const uint16_t*>(xs);
     uint32_t wv[kXPieces][8];
-    float mx[kXPieces];
 #pragma unroll
     for (int m = 0; m < kXPieces; ++m) {
       const int i = threadIdx.x + 64 * WAVES * m;
@@ -512,64 +598,18 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       const u32x4 v1 = *reinterpret_cast<const u32x4*>(xraw + e + 8);
       wv[m][0] = v0.x; wv[m][1] = v0.y; wv[m][2] = v0.z; wv[m][3] = v0.w;
       wv[m][4] = v1.x; wv[m][5] = v1.y; wv[m][6] = v1.z; wv[m][7] = v1.w;
-      float t = 0.f;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) t = absmax2(t, wv[m][k]);
-      mx[m] = live ? t : 0.f;
     }
-    for (int b = 0; b < B; ++b) {
-      float t = 0.f;
-#pragma unroll
-      for (int m = 0; m < kXPieces; ++m)
-        if ((threadIdx.x + 64 * WAVES * m) / pieces == b) t = fmaxf(t, mx[m]);
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) t = fmaxf(t, __shfl_xor(t, o));
-      if (lane == 0) xmax[16 * wave + b] = t;
-    }
-    __syncthreads();  // maxima visible; every raw piece has been read
+    __syncthreads();  // every raw piece has been read: the A rows overwrite them
 #pragma unroll
     for (int m = 0; m < kXPieces; ++m) {
       const int i = threadIdx.x + 64 * WAVES * m;
-      const int b = i / pieces, col = 16 * (i % pieces);
-      if (b >= B) continue;
-      float t = 0.f;
-      for (int w = 0; w < WAVES; ++w) t = fmaxf(t, xmax[16 * w + b]);
-      u32x4 t1 = {0u, 0u, 0u, 0u}, t2 = {0u, 0u, 0u, 0u};
-      int h = -1;  // pieces past K (half a chunk, g < 128) are zeros
-      if (col < K) {
-        split_piece(wv[m], split_exp(t), t1, t2);
-        h = G < 128 ? (col % 128) / G : 0;
-      }
-      put_piece<H>(xs, xstride, b, h, piece_koff(col), t1, t2);
-    }
-    if (threadIdx.x < (unsigned)B) {
-      float t = 0.f;
-      for (int w = 0; w < WAVES; ++w) t = fmaxf(t, xmax[16 * w + threadIdx.x]);
-      xexp[threadIdx.x] = split_exp(t);
+      if (i / pieces < B) put_split(i, pieces, K, wv[m]);  // a lane pair shares its row
     }
     for (int i = threadIdx.x; i < 128 / 16; i += 64 * WAVES)
       st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
     __syncthreads();
   } else {
     for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
-    // row maxima of |x| over all K, then the split exponents
-    for (int b = 0; b < B; ++b) {
-      float mx = 0.f;
-      for (int64_t e = 8 * (int64_t)threadIdx.x; e < K; e += 8 * 64 * WAVES) {
-        const u32x4 v = ld16(xm + (int64_t)b * K + e);
-        mx = absmax2(absmax2(absmax2(absmax2(mx, v.x), v.y), v.z), v.w);
-      }
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-      if (lane == 0) xmax[16 * wave + b] = mx;
-    }
-    __syncthreads();
-    if (threadIdx.x < (unsigned)B) {
-      float mx = 0.f;
-      for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, xmax[16 * w + threadIdx.x]);
-      xexp[threadIdx.x] = split_exp(mx);
-    }
-    __syncthreads();
   }
 
   // part [kp0, kp0 + kpl) of x -> A rows; pieces past kpl up to the end of
@@ -577,19 +617,15 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   auto stage_x = [&](int64_t kp0, int kpl) {
     const int pieces = (kpl + 127) / 128 * 8;
     for (int i = threadIdx.x; i < B * pieces; i += 64 * WAVES) {
-      const int b = i / pieces, u = i % pieces;
-      const int col = 16 * u;
-      if (col >= kpl) {
-        put_piece<H>(xs, xstride, b, -1, piece_koff(col), u32x4{0u, 0u, 0u, 0u},
-                     u32x4{0u, 0u, 0u, 0u});
-        continue;
+      const int b = i / pieces, col = 16 * (i % pieces);
+      uint32_t wv[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+      if (col < kpl) {
+        const u32x4 v0 = ld16(xm + (int64_t)b * K + kp0 + col);
+        const u32x4 v1 = ld16(xm + (int64_t)b * K + kp0 + col + 8);
+        wv[0] = v0.x; wv[1] = v0.y; wv[2] = v0.z; wv[3] = v0.w;
+        wv[4] = v1.x; wv[5] = v1.y; wv[6] = v1.z; wv[7] = v1.w;
       }
-      const u32x4 v0 = ld16(xm + (int64_t)b * K + kp0 + col);
-      const u32x4 v1 = ld16(xm + (int64_t)b * K + kp0 + col + 8);
-      const uint32_t wv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-      u32x4 t1, t2;
-      split_piece(wv, xexp[b], t1, t2);
-      put_piece<H>(xs, xstride, b, G < 128 ? (col % 128) / G : 0, piece_koff(col), t1, t2);
+      put_split(i, pieces, kpl, wv);
     }
     for (int i = threadIdx.x; i < 128 / 16; i += 64 * WAVES)
       st16(smem + zoff + 16 * i, u32x4{0u, 0u, 0u, 0u});
@@ -617,8 +653,8 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
       const int64_t kcol = (int64_t)s * SK;
       const int cend = (int)((K - kcol) / 128 < CPS ? (K - kcol) / 128 : CPS);
       const bool tail64 = G < 128 && (K - kcol) % 128 != 0 && (K - kcol) < SK;
-      slot_compute<G, SK, NR, NV, H>(smem, sr, abase, amask, (uint32_t)(kcol - kp0), cend,
-                                     tail64, q, acc);
+      slot_compute<G, SK, NR, H>(smem, sr, abase, amask, ebase, (uint32_t)(kcol - kp0), cend,
+                                 tail64, q, acc);
     }
   }
   // loads issued past the end must land before the workgroup's LDS is released
@@ -626,7 +662,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   if constexpr (KS) {
     // each wave parks its partial sums in its own slot buffer (free now),
     // then wave 0 adds them in wave order
-    constexpr int kAcc = NR * kGemvBlocks * NV;
+    constexpr int kAcc = NR * kGemvBlocks * H;
     static_assert(kAcc * 64 * 4 <= RING * Plan::kSlotBytes, "partial sums fit the slot buffer");
     float* mine = reinterpret_cast<float*>(smem + wave * RING * Plan::kSlotBytes);
     int t = 0;
@@ -635,7 +671,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
 #pragma unroll
       for (int j = 0; j < kGemvBlocks; ++j)
 #pragma unroll
-        for (int i = 0; i < NV; ++i, ++t) mine[64 * t + lane] = acc[r][j][i];
+        for (int i = 0; i < H; ++i, ++t) mine[64 * t + lane] = acc[r][j][i];
     __syncthreads();
     if (wave != 0) return;
     for (int w = 1; w < WAVES; ++w) {
@@ -646,10 +682,10 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
 #pragma unroll
         for (int j = 0; j < kGemvBlocks; ++j)
 #pragma unroll
-          for (int i = 0; i < NV; ++i, ++t) acc[r][j][i] += other[64 * t + lane];
+          for (int i = 0; i < H; ++i, ++t) acc[r][j][i] += other[64 * t + lane];
     }
   }
-  store_rows<NR, NV, H>(acc, xexp, B, N, rowb, l16, q, y + mat * yms);
+  store_rows<NR, H>(acc, B, N, rowb, l16, q, y + mat * yms);
 }
 
 // ---------------------------------------------------------------------------
@@ -662,7 +698,7 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int SK = kGemvSlotK;
   constexpr int RING = kGemvRing;
-  const int R = 2 * B * H;
+  const int R = kTerms * B * H;
   const int rmax = R < 64 ? R : 64;  // A rows of one pass
   int budget = kGemvXBytes;
   if (budget < rmax * (SK + kGemvXPad)) budget = rmax * (SK + kGemvXPad);
@@ -680,46 +716,41 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
   auto lds_of = [&](int slot_bytes, int rows, bool with_raw) {
     size_t xa = (size_t)rows * (KP + kGemvXPad);
     if (with_raw && (size_t)B * KR * 2 > xa) xa = (size_t)B * KR * 2;
-    return (size_t)WAVES * slot_bytes + xa + 128 + 4 * 16 * WAVES + 4 * 16;
+    const size_t ea = ((size_t)rows * (KP / 32) + 15) / 16 * 16;
+    return (size_t)WAVES * slot_bytes + xa + ea + 128;
   };
-#define TM_GEMV_LAUNCH(NR_, NV_, SW_, XD_, BP, B0)                                            \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, NV_, SW_, XD_, KS>), grid, block,  \
-                     lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, 2 * (BP) * H, XD_), stream, \
-                     x + (int64_t)(B0) * K, codes, s16, BP, N, K, KP, (int64_t)B * K,         \
+#define TM_GEMV_LAUNCH(NR_, SW_, BP, B0)                                                      \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, SW_, false, KS>), grid, block,     \
+                     lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, kTerms * (BP) * H, false), \
+                     stream, x + (int64_t)(B0) * K, codes, s16, BP, N, K, KP, (int64_t)B * K,  \
                      (int64_t)B * N, y + (int64_t)(B0) * N)
   if (xd) {  // the common decode case: R <= 16
-#define TM_GEMV_XD(NV_, SW_)                                                                  \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, NV_, SW_, true, KS>), grid, block,   \
+#define TM_GEMV_XD(SW_)                                                                       \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, SW_, true, KS>), grid, block,        \
                      lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, R, true), stream, x,     \
                      codes, s16, B, N, K, KP, (int64_t)B * K, (int64_t)B * N, y)
     if constexpr (SK / G >= 2) {
       if (sw) {
-        if (R <= 2 && H == 1)
-          TM_GEMV_XD(H == 1 ? 2 : 4, true);
-        else
-          TM_GEMV_XD(4, true);
+        TM_GEMV_XD(true);
         return hipGetLastError();
       }
     }
-    if (R <= 2 && H == 1)
-      TM_GEMV_XD(H == 1 ? 2 : 4, false);
-    else
-      TM_GEMV_XD(4, false);
+    TM_GEMV_XD(false);
 #undef TM_GEMV_XD
     return hipGetLastError();
   }
-  // at most 64 A rows per launch: batches beyond 64 / (2 H) go in passes
-  const int bmax = 64 / (2 * H);
+  // at most 64 A rows per launch: batches beyond 64 / (kTerms H) go in passes
+  const int bmax = 64 / (kTerms * H);
   for (int b0 = 0; b0 < B; b0 += bmax) {
     const int bp = B - b0 < bmax ? B - b0 : bmax;
-    const int rp = 2 * bp * H;
+    const int rp = kTerms * bp * H;
     if (rp <= 16) {
-      TM_GEMV_LAUNCH(1, 4, false, false, bp, b0);
+      TM_GEMV_LAUNCH(1, false, bp, b0);
     } else if constexpr (!KS) {  // the split form is only chosen for R <= 16
       if (rp <= 32)
-        TM_GEMV_LAUNCH(2, 4, false, false, bp, b0);
-      else if constexpr (H >= 2)
-        TM_GEMV_LAUNCH(4, 4, false, false, bp, b0);
+        TM_GEMV_LAUNCH(2, false, bp, b0);
+      else
+        TM_GEMV_LAUNCH(4, false, bp, b0);
     }
   }
 #undef TM_GEMV_LAUNCH
@@ -735,7 +766,7 @@ static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16
                            int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
   const int64_t blocks = (int64_t)count * ((N + 127) / 128);
   const int64_t nslot = (K + kGemvSlotK - 1) / kGemvSlotK;
-  const int R = 2 * B * (G < 128 ? 128 / G : 1);  // A rows: one 16-row operand when <= 16
+  const int R = kTerms * B * (G < 128 ? 128 / G : 1);  // A rows: one 16-row operand when <= 16
   if (blocks < 2 * (int64_t)current_cu_count() && nslot >= 2 && R <= 16) {
     if (nslot >= 8) return launch_gw<G, 8, true>(x, codes, s16, count, B, N, K, y, stream);
     return launch_gw<G, kGemvWaves, true>(x, codes, s16, count, B, N, K, y, stream);

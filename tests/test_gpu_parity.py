@@ -59,7 +59,7 @@ def host_codes(codes_t, K):
     return O.unpack(host(codes_t), K)
 
 
-def check_ternarize(W, g, eps, label):
+def check_ternarize(W, g, eps, label, random_weights=True):
     ops = _ops()
     print(f"[ternarize] {label} N={W.shape[0]} K={W.shape[1]} g={g} eps={eps}", flush=True)
     c, s, s16, z = ops.ternarize_pack(dev_f32(W), g, eps)
@@ -79,9 +79,11 @@ def check_ternarize(W, g, eps, label):
     band = O.boundary_mask(W, s64, g, eps)
     diff = q_gpu != q_ref
     assert not np.any(diff & ~band), f"{int((diff & ~band).sum())} codes differ off the boundary"
-    # the band that excuses code differences stays small: about 6e-7 (Gaussian)
-    # to 9e-7 (with outliers) of the elements, ~15 of the in_proj matrix
-    assert int(band.sum()) <= 4e-6 * W.size + 16, int(band.sum())
+    # on random weights the band that excuses code differences stays small:
+    # about 6e-7 (Gaussian) to 9e-7 (with outliers) of the elements, ~15 of
+    # the in_proj matrix (hand-made edge cases put whole groups on it)
+    if random_weights:
+        assert int(band.sum()) <= 4e-6 * W.size + 16, int(band.sum())
     # zero count: exact on the GPU's own codes, and close to the oracle's
     assert z_gpu == O.zero_count(q_gpu)
     _, _, q_orc, z_orc = O.ternarize(W, g, eps)
@@ -124,12 +126,13 @@ def test_ternarize_edge_cases():
     W[5, :4] = [1.5, -0.5, 0.25, -1.75]                   # exact ties at eps=0:
     W[5, 4:g] = np.where(np.arange(4, g) % 2, 1.0, -1.0)  # sum |w| = 32, s = 1
     for eps in (0.0, 1e-5):
-        c, s, s16, q, sg = check_ternarize(W, g, eps, f"edge cases eps={eps}")
+        c, s, s16, q, sg = check_ternarize(W, g, eps, f"edge cases eps={eps}",
+                                           random_weights=False)
         assert not q[0].any() and sg[0].tolist() == [0, 0, 0, 0]
         assert np.all(q[1, :g] == 1) and q[2, 5] == -1 and np.count_nonzero(q[2]) == 1
         assert not q[4].any()
     # at eps = 0 the tie W = -0.5 (s = 1) must round to 0, W = 1.5 to +1
-    _, _, _, q, _ = check_ternarize(W, g, 0.0, "ties")
+    _, _, _, q, _ = check_ternarize(W, g, 0.0, "ties", random_weights=False)
     assert q[5, :4].tolist() == [1, 0, 0, -1]
 
 
@@ -552,3 +555,48 @@ def test_gemv_decode_full_stack(B):
         err = O.rel_fro_error(y[layer], ref)
         print(f"  layer {layer} rel fro err {err:.3e}", flush=True)
         assert err <= REL_DESIGN
+
+
+@pytest.mark.parametrize("g", [32, 128])
+@pytest.mark.parametrize("B", [1, 4])
+@pytest.mark.parametrize("count", [1, 3])
+def test_gemv_activation_outliers_per_output(g, B, count):
+    """One activation outlier of 2^10, 2^13 or 2^16 (batch row b gets 2^(10+3b)
+    at column 517, the last row none) among N(0, 1) values.  Each output is
+    checked on its own: outputs whose weight row has code 0 on the outlier
+    column see none of it, so an activation split that loses the small values
+    next to the outlier shows up there, which a Frobenius norm over the whole
+    vector (dominated by the outlier's products) would hide.  count = 1 runs
+    the single-matrix launch (K split across waves), count = 3 the batched one."""
+    ops = _ops()
+    rng = np.random.default_rng(500 + g + 7 * B + count)
+    N, K, col = 256, 2048, 517
+    codes, s16s, qs, s16h = [], [], [], []
+    for _ in range(count):
+        W = synth.weights(rng, N, K, True)
+        c, s, s16, _ = ops.ternarize_pack(dev_f32(W), g, 1e-5)
+        codes.append(c)
+        s16s.append(s16)
+        qs.append(host_codes(c, K))
+        s16h.append(host(s16))
+    xf = rng.standard_normal((count, B, K)).astype(np.float32)
+    for b in range(min(B, 3)):
+        xf[:, b, col] = np.float32(2.0 ** (10 + 3 * b)) * (1 if b % 2 == 0 else -1)
+    xb = synth.f32_to_bf16_bits(xf)
+    print(f"[gemv outliers] g={g} B={B} count={count}", flush=True)
+    y = host(ops.tgemv(dev_bf16(xb), torch.stack(codes), torch.stack(s16s), g))
+    worst_rel, worst_abs = 0.0, 0.0
+    for m in range(count):
+        ref = O.gemv(xb[m], qs[m], s16h[m], g)
+        mag = O.gemv(np.abs(O.bf16_bits_to_f64(xb[m])), np.abs(qs[m]), s16h[m], g)
+        err = np.abs(y[m] - ref)
+        # every output: error against the sum of its products' magnitudes
+        worst_abs = max(worst_abs, float((err / mag).max()))
+        # outputs without the outlier's product and without heavy cancellation:
+        # relative error of the output itself
+        sel = (qs[m][:, col] == 0)[None, :] & (np.abs(ref) >= 1e-2 * mag)
+        worst_rel = max(worst_rel, float((err[sel] / np.abs(ref[sel])).max()))
+    print(f"  max |err| / sum|x w| {worst_abs:.2e}, max rel err (no outlier product) "
+          f"{worst_rel:.2e}", flush=True)
+    assert worst_abs <= 1e-6
+    assert worst_rel <= 1e-4
