@@ -51,7 +51,7 @@ def hipcc() -> str:
 
 
 COMMON_FLAGS = [
-    "-O3", "-std=c++17", "-fPIC", "-Wall",
+    "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Werror",
     f"--offload-arch={ARCH}",
     # packed float32 instructions are kept out of the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

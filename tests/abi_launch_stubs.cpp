@@ -1,0 +1,44 @@
+// Host-only stand-ins for the kernel launchers, linked with abi.cpp into a
+// sanitizer build of the C ABI's argument checks.  The checks run before any
+// launch, and the tests that use this build pass only arguments the checks
+// reject, so reaching a stub is itself a failure: each one aborts.
+#include <cstdio>
+#include <cstdlib>
+
+#include "../paper_2606_18114_amd/csrc/launchers.hpp"
+
+namespace tmk {
+
+[[noreturn]] static void reached(const char* name) {
+  std::fprintf(stderr, "launcher %s reached in the host-only build\n", name);
+  std::abort();
+}
+
+hipError_t launch_ternarize_pack(const float*, int64_t, int64_t, int, float, const float*,
+                                 const float*, uint8_t*, float*, uint16_t*, uint64_t*,
+                                 hipStream_t) {
+  reached("ternarize_pack");
+}
+hipError_t launch_group_code_dot(const uint8_t*, const float*, int64_t, int64_t, int, float*,
+                                 hipStream_t) {
+  reached("group_code_dot");
+}
+hipError_t launch_tgemm_fwd(const uint16_t*, const uint8_t*, const float*, int64_t, int64_t,
+                            int64_t, int, void*, bool, hipStream_t) {
+  reached("tgemm_fwd");
+}
+hipError_t launch_tgemm_bwd_dx(const uint16_t*, const uint8_t*, const float*, int64_t, int64_t,
+                               int64_t, int, float*, hipStream_t) {
+  reached("tgemm_bwd_dx");
+}
+hipError_t launch_tgemm_bwd_dw(const uint16_t*, const uint16_t*, int64_t, int64_t, int64_t,
+                               float*, int, hipStream_t) {
+  reached("tgemm_bwd_dw");
+}
+hipError_t launch_fill_zero_f32(float*, int64_t, hipStream_t) { reached("fill_zero_f32"); }
+hipError_t launch_tgemv(const uint16_t*, const uint8_t*, const uint16_t*, int, int, int64_t,
+                        int64_t, int, float*, hipStream_t) {
+  reached("tgemv");
+}
+
+}  // namespace tmk

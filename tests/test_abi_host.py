@@ -19,6 +19,16 @@ P = 0x7F0000000000  # a 4 KiB-aligned fake device address, never dereferenced
 
 @pytest.fixture(scope="module")
 def L():
+    # TM_ABI_TEST_LIB: a host-only sanitizer build of the same C ABI
+    # (tests/test_abi_sanitized.py), loaded with the binding's signatures
+    alt = os.environ.get("TM_ABI_TEST_LIB")
+    if alt:
+        lib = ctypes.CDLL(alt)
+        for name, (res, args) in ops.SIGNATURES.items():
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        return lib
     if not os.path.exists(ops.lib_path()):
         from paper_2606_18114_amd import build
         build.build(verbose=False)

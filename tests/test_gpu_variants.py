@@ -323,13 +323,3 @@ def test_layer_learned_scales_move_under_sgd():
         print(f"[layer sgd] {mode}: loss {losses[0]:.4f} -> {losses[-1]:.4f}, "
               f"scale moved {moved:.3f}", flush=True)
         assert min(losses[1:]) < losses[0] and moved > 0.01
-
-
-def test_collapse_probe_runs():
-    from paper_2606_18114_amd import collapse_probe
-    for mode in ("absmean", "decoupled", "learnable"):
-        traj = collapse_probe.run(mode, steps=4, lr=1e-3, wd=0.0, N=256, K=256, tokens=64,
-                                  seed=0, log_every=2)
-        assert [e["step"] for e in traj] == [0, 2, 4]
-        assert all(0.0 < e["zero_ratio"] < 1.0 for e in traj)
-        assert ("mean_scale" in traj[0]) == (mode != "absmean")
