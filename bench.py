@@ -11,9 +11,14 @@ come from HIP events recorded on the stream the kernels run on.
 The headline `value` is the in_proj forward ternary GEMM in TFLOP/s
 (2*M*N*K algorithmic flops over the kernel's mean duration); every other
 kernel is reported beside it.  The decode GEMV is also timed the way a server
-runs it, tokens back to back (batch 1 and 4), after the step loop; that
-figure is `roofline_tgemv` (inside the step the GEMV follows the training
-kernels' output writes, whose write-back from the caches competes with it).
+runs it, tokens back to back (batch 1 and 4), after the step loop, warm (one
+weight arena) and cold (tokens cycling over copies of the arenas, >= 1.1 GiB
+in all, so nothing is left in the 256 MB memory-side cache); the cold batch-1
+figure is `roofline_tgemv`.  The HBM-bound ternarizers are reported cold and
+warm the same way (`cold_vs_warm`).  `small_configs` has the single linear
+layer's latency and the out_proj forward, `group_sweep` the group sizes 32 ..
+512 on in_proj with 2048 tokens, `codes_vs_oracle` the in_proj codes against
+the oracle's (boundary-band elements and mismatches on and off the band).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
     python bench.py --sweep-g     # group-size workload: one JSON line per g
@@ -57,7 +62,8 @@ def parse():
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants, "
-                         "per_layer (keeps a profiler trace to the kernels of interest)")
+                         "per_layer, small, sweep (keeps a profiler trace to the kernels "
+                         "of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
     bad = args.skip - {"qat", "variants", "per_layer"}
@@ -232,6 +238,9 @@ def main():
                 float(np.mean([e[1].elapsed_time(e[2]) for e in ev])),
                 e0.elapsed_time(e1) / tokens)
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
+    cold = cold_figures(ops, dec, W, dW, codes, scales, g, eps, max(args.steps // 4, 3))
+    small = None if "small" in args.skip else small_configs(ops, dev, args.steps)
+    sweep = None if "sweep" in args.skip else group_sweep(ops, dev, max(args.steps // 2, 5))
 
     # ---------------- decode in layer order: one launch per matrix ----------------
     per_layer = (None if "per_layer" in args.skip
@@ -288,7 +297,12 @@ def main():
             "bytes_per_token": nb,
             "per_kernel_events": {"in_proj_us": round(t_in_ms * 1e3, 2),
                                   "out_proj_us": round(t_out_ms * 1e3, 2)}}
+    for b in serve:
+        ck = cold.get(f"decode_B{b}")
+        if ck:
+            decode_serving[f"B{b}"]["cold"] = ck
     srv = decode_serving[f"B{B}"]
+    srv_cold = srv.get("cold", srv)
 
     fwd = kernels["tgemm_fwd"]
     t_in, t_out = measured_traffic("tgemv_in_proj"), measured_traffic("tgemv_out_proj")
@@ -313,9 +327,11 @@ def main():
                         "(in_proj 8512x2048 + out_proj 2048x4096, 2-bit codes + fp16 scales)",
             "M": M, "N": N, "K": K, "g": g, "eps": eps, "decode_layers": L, "decode_batch": B,
         },
-        "tgemv_GBps": srv["GBps"],
-        "tgemv_frac_hbm": srv["frac_hbm"],
-        "tgemv_us_per_token": srv["us_per_token"],
+        "tgemv_GBps": srv_cold["GBps"],
+        "tgemv_frac_hbm": srv_cold["frac_hbm"],
+        "tgemv_us_per_token": srv_cold["us_per_token"],
+        "tgemv_warm": {"GBps": srv["GBps"], "frac_hbm": srv["frac_hbm"],
+                       "us_per_token": srv["us_per_token"]},
         "tgemv_in_step": {"GBps": round(dec_gbps, 1), "frac_hbm": round(dec_gbps / PEAK_HBM_GBPS, 4),
                           "us_per_token": round(dec_ms * 1e3, 2)},
         "decode_serving": decode_serving,
@@ -323,15 +339,20 @@ def main():
                      "unit": "TFLOP/s", "frac": fwd["frac"],
                      "traffic": measured_traffic("tgemm_fwd"),
                      "kernel": "tgemm_fwd (in_proj)", "algorithmic_per_launch": fl},
-        "roofline_tgemv": {"bound": "hbm", "achieved": srv["GBps"], "peak": PEAK_HBM_GBPS,
-                           "unit": "GB/s", "frac": srv["frac_hbm"],
+        "roofline_tgemv": {"bound": "hbm", "achieved": srv_cold["GBps"], "peak": PEAK_HBM_GBPS,
+                           "unit": "GB/s", "frac": srv_cold["frac_hbm"],
                            "traffic": dec_traffic, "algorithmic_per_token": dec_bytes,
-                           "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to back"},
+                           "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to "
+                                     "back, weights rotated over >= 1.1 GiB of copies (cold)",
+                           "warm": {"achieved": srv["GBps"], "frac": srv["frac_hbm"]}},
         "kernels": kernels,
         "qat_block": qat_block,
         "decode_per_layer": per_layer,
         "qat_block_bf16_out": qat_block_bf16,
         "variants": variants,
+        "cold_vs_warm": {k: v for k, v in cold.items() if not k.startswith("decode_")},
+        "small_configs": small,
+        "group_sweep": sweep,
         "zero_ratio": None,
     }
     out["zero_ratio"] = round(int(zc.item()) / (N * K), 5)
@@ -351,24 +372,124 @@ def main():
         out["roofline"]["frac_of_measured"] = round(
             fwd["achieved"] / c["mfma_bf16_loop_random_TFLOPs"], 4)
         out["roofline_tgemv"]["frac_of_measured"] = round(
-            srv["GBps"] / c["hbm_read_stream_1GiB_GBps"], 4)
+            srv_cold["GBps"] / c["hbm_read_stream_1GiB_GBps"], 4)
         out["roofline_tgemv"]["frac_of_measured_decode_pattern"] = round(
-            srv["GBps"] / c["hbm_read_stream_decode_pattern_GBps"], 4)
+            srv_cold["GBps"] / c["hbm_read_stream_decode_pattern_GBps"], 4)
 
     # ---------------- CPU oracle baseline (bounded sample) ----------------
     # The oracle's outputs of that step are also the reference for a sampled
     # end-to-end parity check of this run's GPU outputs (the GPU codes may
     # differ from the oracle's on rounding-boundary elements only).
     if not args.no_cpu_baseline:
-        gpu_out = None if args.no_parity else dict(Y=Y, dX=dX, dW=dW)
-        out["cpu_baseline"], par = cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out)
+        gpu_out = None if args.no_parity else dict(Y=Y, dX=dX, dW=dW, codes=codes)
+        out["cpu_baseline"], par, band = cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out)
         if par is not None:
             out["parity_rel_fro"] = {k: float(f"{v:.3e}") for k, v in par.items()}
-            out["parity_ok"] = max(par.values()) <= 2e-3
+            out["codes_vs_oracle"] = band
+            out["parity_ok"] = (max(par.values()) <= 2e-3 and band["mismatch_off_band"] == 0)
             if not out["parity_ok"]:
                 log(f"PARITY FAILURE: {par}")
 
     print(json.dumps(out), flush=True)
+
+
+ROTATE_BYTES = 1.1 * 2 ** 30   # cold figures rotate over this much distinct input
+
+
+def cold_figures(ops, dec, W, dW, codes, scales, g, eps, reps):
+    """HBM-bound calls with their inputs rotated over >= 1.1 GiB of distinct
+    copies, so no call finds its input in the 256 MB memory-side cache or the
+    L2 (the "cold" figures; the warm ones repeat one input):
+      * the decode token (48 in_proj + 48 out_proj matrices), B = 1 and 4,
+        cycling over copies of both arenas, tokens back to back under one
+        event pair;
+      * ternarize_pack, the threshold-multiplier and given-threshold
+        ternarizers, cycling over copies of the in_proj W;
+      * the group-magnitude gradient, cycling over copies of dW.
+    Returns per-call microseconds and GB/s."""
+    import torch
+    dev = W.device
+    res = {}
+    # decode arenas
+    tok_bytes = sum(d["codes"].numel() + 2 * d["s16"].numel() for d in dec.values())
+    nsets = int(np.ceil(ROTATE_BYTES / tok_bytes))
+    sets = [{k: (d["codes"], d["s16"]) for k, d in dec.items()}]
+    for _ in range(nsets - 1):
+        sets.append({k: (d["codes"].clone(), d["s16"].clone()) for k, d in dec.items()})
+    for batch, (xk, yk) in ((1, ("x", "y")), (4, ("x4", "y4"))):
+        if dec["in"][xk].shape[1] != batch:
+            continue
+
+        def token(t):
+            for kind in ("in", "out"):
+                d = dec[kind]
+                c, sc = sets[t % nsets][kind]
+                ops.tgemv(d[xk], c, sc, d["cfg"].g, y=d[yk])
+        for t in range(2 * nsets):
+            token(t)
+        torch.cuda.synchronize()
+        ntok = max(reps, 5) * nsets
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for t in range(ntok):
+            token(t)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / ntok
+        nb = sum(L * (c.N * c.K / 4 + 2 * c.N * c.K / c.g + 2 * batch * c.K + 4 * batch * c.N)
+                 for c, L in ((dec[k]["cfg"], dec[k]["codes"].shape[0]) for k in ("in", "out")))
+        res[f"decode_B{batch}"] = {"us_per_token": round(us, 2),
+                                   "GBps": round(nb / (us * 1e-6) / 1e9, 1),
+                                   "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                                   "copies": nsets}
+    del sets
+    # W and dW copies
+    N, K = W.shape
+    ncp = int(np.ceil(ROTATE_BYTES / (N * K * 4)))
+    Ws = [W] + [W.clone() for _ in range(ncp - 1)]
+    dWs = [dW] + [dW.clone() for _ in range(ncp - 1)]
+    mult = torch.ones((N,), dtype=torch.float32, device=dev)
+    mult[:4096] = 0.8
+    c2, s2 = torch.empty_like(codes), torch.empty_like(scales)
+    s16 = torch.empty(scales.shape, dtype=torch.float16, device=dev)
+    zc = torch.empty((1,), dtype=torch.int64, device=dev)
+    ds = torch.empty_like(scales)
+    calls = {
+        "ternarize_pack": (lambda i: ops.ternarize_pack(Ws[i], g, eps, codes=c2, scales=s2,
+                                                        scales_f16=s16, zero_count=zc),
+                           N * K * (4 + 0.25 + 4 / g + 2 / g)),
+        "ternarize_pack_thresh": (lambda i: ops.ternarize_pack(Ws[i], g, eps, codes=c2, scales=s2,
+                                                               zero_count=zc, want_f16=False,
+                                                               row_mult=mult),
+                                  N * K * (4 + 0.25) + N * K / g * 4 + N * 4),
+        "ternarize_codes": (lambda i: ops.ternarize_codes(Ws[i], scales, g, eps, codes=c2,
+                                                          zero_count=zc),
+                            N * K * (4 + 0.25) + N * K / g * 4),
+        "group_code_dot": (lambda i: ops.group_code_dot(codes, dWs[i], g, out=ds),
+                           N * K * (4 + 0.25) + N * K / g * 4),
+    }
+    for name, (fn, nbytes) in calls.items():
+        out = {}
+        for mode, pick in (("cold", lambda i: i % ncp), ("warm", lambda i: 0)):
+            for i in range(ncp):
+                fn(pick(i))
+            torch.cuda.synchronize()
+            n = max(reps, 5) * ncp
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(2_000_000)
+            e0.record()
+            for i in range(n):
+                fn(pick(i))
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n
+            out[mode] = {"us": round(us, 2), "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                         "frac_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)}
+        out["copies"] = ncp
+        res[name] = out
+    del Ws, dWs
+    return res
 
 
 def variants_step(args, ops, W, scales, codes, dW, g, eps):
@@ -479,10 +600,12 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
     to the host before timing).  `value` is the oracle's forward-GEMM TFLOP/s,
     the unit of the headline.
 
-    Returns (baseline, parity): after the timing, 64 sampled rows of the
-    GPU's Y and dX, 64 rows of dW and the last in_proj decode output are
-    compared with the oracle's (relative Frobenius errors), unless gpu_out
-    is None."""
+    Returns (baseline, parity, codes): after the timing, 64 sampled rows of
+    the GPU's Y and dX, 64 rows of dW and the last in_proj decode output are
+    compared with the oracle's (relative Frobenius errors), and the GPU's
+    in_proj codes with the oracle's over the whole matrix: elements within
+    1e-6 of the rounding boundary, and mismatches on and off that band
+    (unless gpu_out is None)."""
     import torch
     from oracle import ternary as O
     try:
@@ -497,7 +620,7 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
             for kind in ("in", "out")}
     t = {}
     t0 = time.perf_counter()
-    _, s32, q, _ = O.ternarize(W_h, g, eps)
+    s64, s32, q, z_orc = O.ternarize(W_h, g, eps)
     t["ternarize"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     Y_ref = O.gemm_fwd(X_h, q, s32, g)
@@ -518,7 +641,7 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
             gemv_bytes += c.N * c.K / 4 + 2 * c.N * c.K / c.g
             nmat += 1
     t["gemv"] = time.perf_counter() - t0
-    par = None
+    par = codes_cmp = None
     if gpu_out is not None:
         dev = gpu_out["Y"].device
         rows = np.sort(np.random.default_rng(123).choice(M, 64, replace=False))
@@ -530,6 +653,12 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
             "dw": O.rel_fro_error(gpu_out["dW"][ci].cpu().numpy(), dW_ref[cols]),
             "tgemv": O.rel_fro_error(dec["in"]["y"][-1].cpu().numpy(), y_in_last),
         }
+        band = O.boundary_mask(W_h, s64, g, eps)
+        diff = O.unpack(gpu_out["codes"].cpu().numpy(), K) != q
+        codes_cmp = {"elements": int(q.size), "boundary_elements": int(band.sum()),
+                     "mismatch_on_band": int((diff & band).sum()),
+                     "mismatch_off_band": int((diff & ~band).sum()),
+                     "zero_count_oracle": int(z_orc)}
     del Y_ref, dX_ref, dW_ref
     fl = 2.0 * M * N * K
     total = sum(t.values())
@@ -548,7 +677,7 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
                        f"float64 fwd {t['fwd']:.2f}s, dX {t['dx']:.2f}s, dW {t['dw']:.2f}s "
                        f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
                        f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
-    return base, par
+    return base, par, codes_cmp
 
 
 def decode_per_layer(ops, dec, L, tokens):
@@ -719,17 +848,15 @@ def measure_ceilings():
     return res
 
 
-def sweep_g(args):
+def group_sweep(ops, dev, reps):
     """Group-size workload: the in_proj weights (8512 x 2048, with outliers)
     ternarized and applied to 2048 x 2048 bf16 activations for g = 32 .. 512.
-    One JSON line per g: zero ratio and NRMSE of the quantizer, ternarize
-    GB/s and forward TFLOP/s.  (Parity at every g is the tests' job.)"""
+    Per g: zero ratio (the kernel's count) and NRMSE of the quantizer,
+    ternarize GB/s and forward TFLOP/s.  (Parity at every g is the tests'
+    job, at this full shape included.)"""
     import torch
-    from paper_2606_18114_amd import ops, synth
+    from paper_2606_18114_amd import synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     N, K, M = synth.IN_PROJ_N, synth.D_MODEL, 2048
     W_h = synth.layer_weight(synth.C3, synth.SEED_W)
     X_h = synth.layer_acts(M, K, synth.SEED_X)
@@ -738,7 +865,7 @@ def sweep_g(args):
     Y = torch.empty((M, N), dtype=torch.float32, device=dev)
     eye = torch.eye(K, dtype=torch.bfloat16, device=dev)
     w_norm = float(torch.linalg.vector_norm(W.double()))
-    reps = max(args.steps, 5)
+    rows = []
     for g in synth.C5_GROUPS:
         codes = torch.empty((N, K // 4), dtype=torch.uint8, device=dev)
         scales = torch.empty((N, K // g), dtype=torch.float32, device=dev)
@@ -765,12 +892,110 @@ def sweep_g(args):
         z = int(zc.item())
         tern_bytes = N * K * (4 + 0.25 + 4 / g)
         fl = 2.0 * M * N * K
-        print(json.dumps({
-            "workload": f"group sweep: in_proj W {N}x{K} (1% Laplace outliers), X bf16 {M}x{K}",
+        rows.append({
             "g": g, "zero_ratio": round(z / (N * K), 5), "nrmse": round(nrmse, 5),
-            "ternarize_ms": round(t_tern, 4), "ternarize_GBps": round(tern_bytes / t_tern / 1e6, 1),
+            "ternarize_ms": round(t_tern, 4),
+            "ternarize_GBps": round(tern_bytes / t_tern / 1e6, 1),
             "fwd_ms": round(t_fwd, 4), "fwd_TFLOPs": round(fl / t_fwd / 1e9, 1),
-            "fwd_frac_mfma": round(fl / t_fwd / 1e9 / PEAK_BF16_TFLOPS, 4)}), flush=True)
+            "fwd_frac_mfma": round(fl / t_fwd / 1e9 / PEAK_BF16_TFLOPS, 4)})
+    return {"workload": f"group sweep: in_proj W {N}x{K} (1% Laplace outliers), "
+                        f"X bf16 {M}x{K}, warm", "rows": rows}
+
+
+def small_configs(ops, dev, reps):
+    """The single linear layer (W 256 x 512, X 16 x 512, g = 128) as a latency:
+    ternarize + forward per call, both launched back to back and timed with
+    one event pair around many calls; and the out_proj forward (W 2048 x 4096,
+    X 4096 x 4096) as a throughput."""
+    import torch
+    from paper_2606_18114_amd import synth
+
+    def bf16(bits):
+        return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    res = {}
+    # single linear: latency of one ternarize + forward
+    c1 = synth.C1
+    W_h, X_h = synth.single_linear_inputs(c1)
+    W, X = torch.from_numpy(W_h).to(dev), bf16(X_h)
+    codes = torch.empty((c1.N, c1.K // 4), dtype=torch.uint8, device=dev)
+    scales = torch.empty((c1.N, c1.K // c1.g), dtype=torch.float32, device=dev)
+    zc = torch.empty((1,), dtype=torch.int64, device=dev)
+    Y = torch.empty((c1.M, c1.N), dtype=torch.float32, device=dev)
+
+    def c1_call():
+        ops.ternarize_pack(W, c1.g, c1.eps, codes=codes, scales=scales, zero_count=zc,
+                           want_f16=False)
+        ops.tgemm_fwd(X, codes, scales, c1.g, Y=Y)
+
+    def per_call_us(fn, n):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    n = max(reps, 50) * 4
+    t_c1 = per_call_us(c1_call, n)
+    t_fwd = per_call_us(lambda: ops.tgemm_fwd(X, codes, scales, c1.g, Y=Y), n)
+    t_tern = per_call_us(lambda: ops.ternarize_pack(W, c1.g, c1.eps, codes=codes, scales=scales,
+                                                    zero_count=zc, want_f16=False), n)
+    # a captured graph of the two calls: the launch cost a serving loop pays
+    gr = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        c1_call()
+        with torch.cuda.graph(gr, stream=side):
+            c1_call()
+    torch.cuda.current_stream().wait_stream(side)
+    t_graph = per_call_us(gr.replay, n)
+    fl1 = 2.0 * c1.M * c1.N * c1.K
+    res["single_linear"] = {
+        "workload": "single ternary linear: W fp32 256x512, X bf16 16x512, g=128",
+        "us_ternarize_plus_fwd": round(t_c1, 2), "us_fwd": round(t_fwd, 2),
+        "us_ternarize": round(t_tern, 2), "us_graph_replay": round(t_graph, 2),
+        "fwd_GFLOPs": round(fl1 / (t_fwd * 1e-6) / 1e9, 2)}
+    # out_proj: forward throughput
+    c2 = synth.C2
+    W2 = torch.from_numpy(synth.layer_weight(c2, synth.SEED_W)).to(dev)
+    X2 = bf16(synth.layer_acts(c2.M, c2.K, synth.SEED_X))
+    codes2 = torch.empty((c2.N, c2.K // 4), dtype=torch.uint8, device=dev)
+    scales2 = torch.empty((c2.N, c2.K // c2.g), dtype=torch.float32, device=dev)
+    Y2 = torch.empty((c2.M, c2.N), dtype=torch.float32, device=dev)
+    tern2 = lambda: ops.ternarize_pack(W2, c2.g, c2.eps, codes=codes2, scales=scales2,
+                                       zero_count=zc, want_f16=False)
+    tern2()
+    t_fwd2 = per_call_us(lambda: ops.tgemm_fwd(X2, codes2, scales2, c2.g, Y=Y2), max(reps, 20))
+    t_tern2 = per_call_us(tern2, max(reps, 20))
+    fl2 = 2.0 * c2.M * c2.N * c2.K
+    tb2 = c2.N * c2.K * (4 + 0.25 + 4 / c2.g)
+    res["out_proj"] = {
+        "workload": "out_proj: W fp32 2048x4096, X bf16 4096x4096, g=128, fp32 out",
+        "fwd_us": round(t_fwd2, 2), "fwd_TFLOPs": round(fl2 / (t_fwd2 * 1e-6) / 1e12, 1),
+        "fwd_frac_mfma": round(fl2 / (t_fwd2 * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "ternarize_us": round(t_tern2, 2),
+        "ternarize_GBps_warm": round(tb2 / (t_tern2 * 1e-6) / 1e9, 1)}
+    return res
+
+
+def sweep_g(args):
+    """--sweep-g: the group-size workload alone, one JSON line per g."""
+    import torch
+    from paper_2606_18114_amd import ops
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sw = group_sweep(ops, dev, max(args.steps, 5))
+    for row in sw["rows"]:
+        print(json.dumps(dict(workload=sw["workload"], **row)), flush=True)
 
 
 if __name__ == "__main__":

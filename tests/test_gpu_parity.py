@@ -227,6 +227,26 @@ def test_fwd_in_proj_full_sampled_rows():
     assert err <= REL_DESIGN
 
 
+@pytest.mark.parametrize("g", synth.C5_GROUPS)
+def test_group_sweep_full_shape(g):
+    """The group-size workload at its full shape: the in_proj weights
+    (8512 x 2048 with outliers, seed 0) and X 2048 x 2048 (seed 1), for every
+    g.  Codes bit-exact off the boundary band, scales within 1e-6, the
+    whole forward output within the design bar of the float64 reference on
+    the GPU's codes, and within the contract end to end on the oracle's."""
+    ops = _ops()
+    cfg = synth.c5(g)
+    W = synth.layer_weight(synth.C3, synth.SEED_W)
+    X = synth.layer_acts(cfg.M, cfg.K, synth.SEED_X)
+    c, s, _, q, sg = check_ternarize(W, g, cfg.eps, f"group sweep full shape g={g}")
+    Y = host(ops.tgemm_fwd(dev_bf16(X), c, s, g))
+    err = O.rel_fro_error(Y, O.gemm_fwd(X, q, sg, g))
+    _, s32, q_o, _ = O.ternarize(W, g, cfg.eps)
+    err2 = O.rel_fro_error(Y, O.gemm_fwd(X, q_o, s32, g))
+    print(f"  fwd rel fro err {err:.3e} (oracle codes {err2:.3e})", flush=True)
+    assert err <= REL_DESIGN and err2 <= REL_BAR
+
+
 def test_fwd_exact_cases():
     """Selections and small integers are exact: one-hot tokens pick columns of
     What, integer tokens with power-of-two scales give exact integer sums."""
