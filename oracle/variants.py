@@ -15,10 +15,14 @@ The paper's appendix (Decoupled Quantization Ablations) and Sec. 4
   an independent, learnable magnitude alpha_g scales them, What = alpha_g * q.
   Its gradient is d alpha_g = sum_i q_i * dWhat_i over the group's elements
   (the codes do not depend on alpha).
-* Learnable scale: s_g itself an nn.Parameter.  Its magnitude path has the
-  same gradient, sum_i q_i * dWhat_i; the threshold path through the rounding
-  is cut by the hard forward quantization (the straight-through estimator of
-  Sec. 3.1 passes gradients to W only), which is the reading taken here.
+* Learnable scale: s_g itself an nn.Parameter.  Two readings of its
+  gradient are kept.  (a) Magnitude only: sum_i q_i * dWhat_i, the threshold
+  path through the rounding cut by the hard forward quantization.  (b) The
+  straight-through estimator applied to the rounding alone (round passes
+  the gradient unchanged, clip keeps its derivative), which is what a PyTorch
+  layer computing s * ste(round(clip(w / (s + eps)))) gives: the threshold
+  term feeds back into s and the weights' gradient is clip-masked
+  (``scale_ste_grad``).
 
 Readings: the multiplied threshold is rounded to
 float32 once (fl32(m * s)), then eps is added in float32, then the quotient is
@@ -32,7 +36,8 @@ import numpy as np
 
 from . import ternary as T
 
-__all__ = ["ternary_codes_thresh", "boundary_mask_thresh", "group_code_dot"]
+__all__ = ["ternary_codes_thresh", "boundary_mask_thresh", "group_code_dot",
+           "scale_ste_grad"]
 
 
 def ternary_codes_thresh(W: np.ndarray, s32: np.ndarray, g: int, eps: float,
@@ -69,3 +74,38 @@ def group_code_dot(q: np.ndarray, dWhat: np.ndarray, g: int) -> np.ndarray:
     if d.shape != (N, K) or K % g:
         raise ValueError("oracle: q and dWhat must be [N, K] with K % g == 0")
     return (q * d).reshape(N, K // g, g).sum(axis=2)
+
+
+def scale_ste_grad(W: np.ndarray, q: np.ndarray, s32: np.ndarray, dWhat: np.ndarray, g: int,
+                   eps: float):
+    """Gradients of a learnable scale s (Sec. 4) and of the latent weights
+    when only the rounding is straight-through:
+
+        x = clip(w / (s + eps), -1, 1),  q = round(x),  What = s * q,
+        d What / d s = q - m * s * w / (s + eps)^2,
+        d What / d w = m * s / (s + eps),
+
+    with m = 1 where the float32 quotient |w| / fl32(s + eps) is at most 1
+    (clip passes the gradient on its closed range) and 0 elsewhere; s + eps
+    is the float32 sum the codes are decided with.  Returns (ds [N, K/g],
+    dw [N, K]) in float64: ds[n, j] = sum over group j of dWhat * dWhat/ds,
+    dw = dWhat * dWhat/dw.  q are the layer's codes (ternarized against s)."""
+    W = np.asarray(W, dtype=np.float32)
+    N, K = W.shape
+    if K % g:
+        raise ValueError("oracle: K must be a multiple of g")
+    s32 = np.asarray(s32, dtype=np.float32).reshape(N, K // g)
+    if not np.all(np.isfinite(s32)) or np.any(s32 <= 0):
+        raise ValueError("oracle: a learnable scale must be finite and > 0")
+    d32 = (s32 + np.float32(eps)).astype(np.float32)
+    d_full = np.repeat(d32, g, axis=1)
+    quot = (np.abs(W) / d_full).astype(np.float32)          # float32 quotient
+    m = (quot <= np.float32(1.0)).astype(np.float64)
+    s64 = np.repeat(s32.astype(np.float64), g, axis=1)
+    d64 = d_full.astype(np.float64)
+    dwh = np.asarray(dWhat, dtype=np.float64)
+    qf = np.asarray(q, dtype=np.float64)
+    terms = dwh * (qf - m * s64 * W.astype(np.float64) / (d64 * d64))
+    ds = terms.reshape(N, K // g, g).sum(axis=2)
+    dw = dwh * m * s64 / d64
+    return ds, dw

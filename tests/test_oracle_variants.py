@@ -123,3 +123,99 @@ def test_planted_variant_mistakes_are_caught(ex, mutant, monkeypatch):
         monkeypatch.setattr(V, "ternary_codes_thresh", wrong)
         with pytest.raises(AssertionError):
             _check_twin(32, 5e-3)  # an eps comparable to the scales
+
+
+# --------------------------------------------------------------------------
+# Learnable scale with the straight-through rounding (scale_ste_grad)
+# --------------------------------------------------------------------------
+
+def _ste_case(ex, case):
+    e = ex["scale_ste_grad"]
+    W = np.array([e["W"]], np.float32)
+    s = np.array([[case["s"]]], np.float32)
+    q = T.ternary_codes(W, s, 4, case["eps"])
+    return W, s, q, np.array([e["dWhat"]])
+
+
+def test_hand_scale_ste_grad(ex):
+    for case in ex["scale_ste_grad"]["cases"]:
+        W, s, q, dwh = _ste_case(ex, case)
+        assert q[0].tolist() == case["q"], case["why"]
+        ds, dw = V.scale_ste_grad(W, q, s, dwh, 4, case["eps"])
+        assert ds[0, 0] == case["ds"], case["why"]
+        assert dw[0].tolist() == case["dw"], case["why"]
+
+
+@pytest.mark.parametrize("g,eps", [(32, 0.0), (128, 1e-5), (64, 3e-3)])
+def test_scale_ste_grad_is_pytorch_autograd(g, eps):
+    """CPU autograd of the layer written the usual PyTorch way, in float64:
+    x = clamp(w / (s + eps), -1, 1); q = x + (round(x) - x).detach();
+    What = s * q.  Weights and scales are drawn so that no quotient lies
+    within 1e-9 of a rounding or clip boundary, where float32 and float64
+    decisions could differ."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(60 + g)
+    N, K = 6, 512
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    s32 = (np.abs(W).reshape(N, K // g, g).mean(axis=2) * rng.uniform(0.6, 1.6, (N, K // g))
+           ).astype(np.float32)
+    d = np.repeat((s32 + np.float32(eps)).astype(np.float64), g, axis=1)
+    x = np.abs(W.astype(np.float64)) / d
+    assert np.min(np.abs(x - 0.5)) > 1e-9 and np.min(np.abs(x - 1.0)) > 1e-9
+    G = rng.standard_normal((N, K))
+    wt = torch.tensor(W.astype(np.float64), requires_grad=True)
+    st = torch.tensor(s32.astype(np.float64), requires_grad=True)
+    sf = st.repeat_interleave(g, dim=1)
+    # s + eps as the float32 layer forms it: the float32 rounding of the sum is
+    # added as a constant, so d(s + eps)/ds stays exactly 1 in float64
+    d32 = (s32 + np.float32(eps)).astype(np.float32).astype(np.float64)
+    delta = torch.from_numpy(np.repeat(d32 - s32.astype(np.float64), g, axis=1))
+    dt = sf + delta
+    xt = torch.clamp(wt / dt, -1.0, 1.0)
+    qt = xt + (torch.round(xt) - xt).detach()
+    (sf * qt * torch.from_numpy(G)).sum().backward()
+    q = T.ternary_codes(W, s32, g, eps)
+    assert np.array_equal(q, torch.round(xt).detach().numpy().astype(np.int8))
+    ds, dw = V.scale_ste_grad(W, q, s32, G, g, eps)
+    np.testing.assert_allclose(ds, st.grad.numpy(), rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(dw, wt.grad.numpy(), rtol=1e-9, atol=1e-15)
+    # the magnitude-only reading differs by the threshold term
+    assert not np.allclose(V.group_code_dot(q, G, g), ds, rtol=1e-3)
+
+
+_ORIG_STE = V.scale_ste_grad
+
+
+@pytest.mark.parametrize("mutant", ["magnitude_only", "threshold_sign", "no_mask",
+                                    "strict_mask", "no_eps_in_factor", "unmasked_dw"])
+def test_planted_scale_ste_mistakes_are_caught(ex, mutant, monkeypatch):
+    def mutated(W, q, s32, dWhat, g, eps):
+        ds, dw = _ORIG_STE(W, q, s32, dWhat, g, eps)
+        N, K = np.asarray(W).shape
+        s64 = np.repeat(np.asarray(s32, np.float64).reshape(N, K // g), g, axis=1)
+        d64 = np.repeat((np.asarray(s32, np.float32) + np.float32(eps)).astype(np.float64)
+                        .reshape(N, K // g), g, axis=1)
+        w = np.asarray(W, np.float64)
+        m = (np.abs(np.asarray(W, np.float32)) / d64.astype(np.float32) <= 1).astype(float)
+        dwh = np.asarray(dWhat, np.float64)
+        qf = np.asarray(q, np.float64)
+        if mutant == "magnitude_only":
+            return V.group_code_dot(q, dWhat, g), dw
+        if mutant == "threshold_sign":
+            t = dwh * (qf + m * s64 * w / d64 ** 2)
+        elif mutant == "no_mask":
+            t = dwh * (qf - s64 * w / d64 ** 2)
+        elif mutant == "strict_mask":
+            ms = (np.abs(np.asarray(W, np.float32)) / d64.astype(np.float32) < 1).astype(float)
+            t = dwh * (qf - ms * s64 * w / d64 ** 2)
+            return t.reshape(N, K // g, g).sum(axis=2), dwh * ms * s64 / d64
+        elif mutant == "no_eps_in_factor":
+            t = dwh * (qf - m * w / s64)
+            return t.reshape(N, K // g, g).sum(axis=2), dwh * m
+        elif mutant == "unmasked_dw":
+            return ds, dwh * s64 / d64
+        return t.reshape(N, K // g, g).sum(axis=2), dw
+
+    monkeypatch.setattr(V, "scale_ste_grad", mutated)
+    with pytest.raises(AssertionError):
+        test_hand_scale_ste_grad(ex)
