@@ -496,8 +496,10 @@ def variants_step(args, ops, W, scales, codes, dW, g, eps):
     """The entry points of the scale variants, timed on the in_proj shapes:
     ternarize with 0.8 x absmean thresholds on rows 0-4095 (the appendix's
     gate setting), codes against given thresholds (a learned scale; the
-    absmean is passed), and the group-magnitude gradient sum q * dW over
-    the step's dW.  All three are single HBM passes over W or dW."""
+    absmean is passed), the group-magnitude gradient sum q * dW over the
+    step's dW, and the learnable-scale gradient with the rounding
+    straight-through (the absmean as the learned scale).  All are single HBM
+    passes."""
     import torch
     N, K = W.shape
     dev = W.device
@@ -507,6 +509,7 @@ def variants_step(args, ops, W, scales, codes, dW, g, eps):
     s2 = torch.empty_like(scales)
     zc = torch.empty((1,), dtype=torch.int64, device=dev)
     ds = torch.empty_like(scales)
+    dWm = torch.empty_like(dW)
     calls = {
         "ternarize_pack_thresh": (
             lambda: ops.ternarize_pack(W, g, eps, codes=c2, scales=s2, zero_count=zc,
@@ -518,6 +521,12 @@ def variants_step(args, ops, W, scales, codes, dW, g, eps):
         "group_code_dot": (
             lambda: ops.group_code_dot(codes, dW, g, out=ds),
             N * K * (4 + 0.25) + N * K / g * 4),
+        # learnable scale, rounding straight-through: reads W, the codes, s and
+        # dWhat, writes ds and the clip-masked dW (here not in place, so that
+        # the step's dW stays as it is)
+        "scale_ste_grad": (
+            lambda: ops.scale_ste_grad(W, codes, scales, dW, g, eps, ds=ds, dW=dWm),
+            N * K * (4 + 4 + 0.25 + 4) + N * K / g * 8),
     }
     steps = max(args.steps, 10)
     res = {}

@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 3
+#define TM_ABI_VERSION 4
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -247,6 +247,34 @@ tm_status tm_ternarize_codes(const float* W, int64_t N, int64_t K, int32_t g, fl
  */
 tm_status tm_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, int64_t K,
                             int32_t g, float* out, tm_stream stream);
+
+/*
+ * tm_scale_ste_grad — gradients of a learnable scale (Sec. 4: s_g an
+ * nn.Parameter) and of the latent weights when only the rounding is
+ * straight-through (Sec. 3.1's estimator applied to round, clip keeping its
+ * derivative), i.e. what a layer computing s * ste(round(clip(w / (s + eps))))
+ * receives:
+ *   ds[n, j] = sum_{i < g} dWhat[n, i'] * (q[n, i'] - m[n, i'] * s * w / d^2),
+ *   dW[n, k] = dWhat[n, k] * m[n, k] * s / d,         i' = j*g + i,
+ * with d = fl32(s[n, k/g] + eps) and m = 1 where the float32 quotient
+ * |W| / d is at most 1 (the clip's closed range), else 0.  Unlike
+ * tm_group_code_dot (magnitude path only), the threshold term feeds back
+ * into s, and the weights' gradient is clip-masked.
+ *   W       float32 [N, K]    in   latent weights (16-byte aligned)
+ *   codes   uint8 [N, K/4]    in   the codes of the forward call, i.e.
+ *                                  tm_ternarize_codes against tau = s
+ *   scale   float32 [N, K/g]  in   the learned s (4-byte aligned); each value
+ *                                  finite and > 0 (not checked: device data)
+ *   dWhat   float32 [N, K]    in   gradient w.r.t. the dequantized weights
+ *                                  (tm_tgemm_bwd_dw_ste's output)
+ *   eps     float32, finite, >= 0
+ *   ds      float32 [N, K/g]  out  terms and sums in float64, rounded once
+ *   dW      float32 [N, K]    out  or NULL (not written); may be dWhat
+ *                                  itself (in place), no other overlap
+ */
+tm_status tm_scale_ste_grad(const float* W, const uint8_t* codes, const float* scale,
+                            const float* dWhat, int64_t N, int64_t K, int32_t g, float eps,
+                            float* ds, float* dW, tm_stream stream);
 
 #ifdef __cplusplus
 }

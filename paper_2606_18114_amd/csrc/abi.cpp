@@ -164,6 +164,31 @@ tm_status tm_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, in
 }
 
 
+tm_status tm_scale_ste_grad(const float* W, const uint8_t* codes, const float* scale,
+                            const float* dWhat, int64_t N, int64_t K, int32_t g, float eps,
+                            float* ds, float* dW, tm_stream stream) {
+  if (!W || !codes || !scale || !dWhat || !ds) return TM_EINVAL;
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t wb, cb, sb;
+  if (!bytes_of(N, K, 4, &wb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb))
+    return TM_ESHAPE;
+  if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scale, 4) || !aligned(dWhat, 16) ||
+      !aligned(ds, 4) || !aligned(dW, 16))
+    return TM_EALIGN;
+  const Span o = span(ds, sb), w = span(dW, dW ? wb : 0), g_in = span(dWhat, wb);
+  const Span ins[3] = {span(W, wb), span(codes, cb), span(scale, sb)};
+  for (const Span& in : ins)
+    if (overlap(in, o) || overlap(in, w)) return TM_EINVAL;
+  if (overlap(o, g_in) || overlap(o, w)) return TM_EINVAL;
+  // dW may be dWhat itself (in place), but no other overlap of the two
+  if (dW && static_cast<const void*>(dW) != static_cast<const void*>(dWhat) && overlap(w, g_in))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_scale_ste_grad(W, codes, scale, dWhat, N, K, g, eps, ds, dW,
+                                               to_hip(stream)));
+}
+
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales, int64_t M,
                        int64_t N, int64_t K, int32_t g, float* Y, tm_stream stream) {
   return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 4, stream);

@@ -34,6 +34,11 @@ hipError_t launch_ternarize_pack(const float* W, int64_t N, int64_t K, int g, fl
 // out[n, j] = sum over group j of row n of q * dW (float64 sums, float32 out)
 hipError_t launch_group_code_dot(const uint8_t* codes, const float* dW, int64_t N, int64_t K,
                                  int g, float* out, hipStream_t stream);
+// ds[n, j] = sum over group j of dWhat * (q - m w s/d^2), dw = dWhat m s/d
+// (d = fl32(s + eps), m the float32 clip mask); dw may be NULL or dWhat
+hipError_t launch_scale_ste_grad(const float* W, const uint8_t* codes, const float* scale,
+                                 const float* dWhat, int64_t N, int64_t K, int g, float eps,
+                                 float* ds, float* dw, hipStream_t stream);
 // Y: float32 [M, N], or bfloat16 bits [M, N] when bf16_out
 hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int g, void* Y, bool bf16_out,

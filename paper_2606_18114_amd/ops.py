@@ -40,6 +40,8 @@ SIGNATURES = {
     "tm_group_code_dot": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P]),
     "tm_ternarize_codes": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P]),
     "tm_tgemm_fwd_bf16": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_scale_ste_grad": (ctypes.c_int,
+                          [_P, _P, _P, _P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P]),
 }
 
 
@@ -203,6 +205,39 @@ def group_code_dot(codes: torch.Tensor, dW: torch.Tensor, g: int = 128,
     st = lib().tm_group_code_dot(_ptr(codes), _ptr(dW), N, K, g, _ptr(out), _stream())
     _check("tm_group_code_dot", st)
     return out
+
+
+def scale_ste_grad(W: torch.Tensor, codes: torch.Tensor, scale: torch.Tensor,
+                   dWhat: torch.Tensor, g: int = 128, eps: float = 1e-5, *,
+                   ds: Optional[torch.Tensor] = None, dW: Optional[torch.Tensor] = None,
+                   want_dW: bool = True, in_place: bool = False):
+    """Learnable-scale gradients with the rounding straight-through:
+    (ds float32 [N, K/g], dW float32 [N, K] or None).  in_place=True writes
+    dW over dWhat."""
+    _need(W, "W", _F32, 2)
+    _need(codes, "codes", _U8, 2)
+    _need(scale, "scale", _F32, 2)
+    _need(dWhat, "dWhat", _F32, 2)
+    N, K = W.shape
+    G = _groups(K, g)
+    _shape(codes, "codes", (N, K // 4), W.device)
+    _shape(scale, "scale", (N, G), W.device)
+    _shape(dWhat, "dWhat", (N, K), W.device)
+    if ds is None:
+        ds = torch.empty((N, G), dtype=torch.float32, device=W.device)
+    _need(ds, "ds", _F32, 2)
+    _shape(ds, "ds", (N, G), W.device)
+    if in_place:
+        dW = dWhat
+    elif dW is None and want_dW:
+        dW = torch.empty((N, K), dtype=torch.float32, device=W.device)
+    if dW is not None:
+        _need(dW, "dW", _F32, 2)
+        _shape(dW, "dW", (N, K), W.device)
+    st = lib().tm_scale_ste_grad(_ptr(W), _ptr(codes), _ptr(scale), _ptr(dWhat), N, K, g, eps,
+                                 _ptr(ds), _ptr(dW), _stream())
+    _check("tm_scale_ste_grad", st)
+    return ds, dW
 
 
 def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,

@@ -36,7 +36,7 @@ import torch
 from . import ops
 
 
-SCALE_MODES = ("absmean", "decoupled", "learnable")
+SCALE_MODES = ("absmean", "decoupled", "learnable", "learnable_ste")
 
 
 class TernaryLinearFn(torch.autograd.Function):
@@ -48,8 +48,12 @@ class TernaryLinearFn(torch.autograd.Function):
     Quantization Ablations).  mode "learnable": `scale` is the learned s_g of
     Sec. 4, used as the rounding threshold and as the magnitude.  `row_mult`
     (float32 [out] or None) multiplies each row's absmean threshold.
-    The gradient of a learned magnitude is sum_group q * dWhat; the hard
-    forward rounding passes nothing back through the threshold.
+    In "decoupled" and "learnable" the gradient of the learned scale is
+    sum_group q * dWhat (the hard forward rounding passes nothing back
+    through the threshold) and the weights get dWhat.  "learnable_ste" has
+    the same forward as "learnable", with only the rounding straight-through:
+    the scale also receives the threshold term, and the weights' gradient is
+    clip-masked (``tm_scale_ste_grad``).
     """
 
     @staticmethod
@@ -67,7 +71,7 @@ class TernaryLinearFn(torch.autograd.Function):
         x2 = x2.contiguous()
         w = weight.detach().contiguous()
         want_zc = zero_count is not None
-        if mode == "learnable":
+        if mode in ("learnable", "learnable_ste"):
             mag = scale.detach().contiguous()
             codes, _ = ops.ternarize_codes(w, mag, g, eps, zero_count=zero_count,
                                            want_zero_count=want_zc)
@@ -77,8 +81,10 @@ class TernaryLinearFn(torch.autograd.Function):
                                                       row_mult=row_mult)
             mag = absmean if mode == "absmean" else scale.detach().contiguous()
         y = ops.tgemm_fwd(x2, codes, mag, g, out_dtype=out_dtype)
-        ctx.save_for_backward(x2, codes, mag)
+        ctx.save_for_backward(x2, codes, mag, w if mode == "learnable_ste" else None)
         ctx.g = g
+        ctx.eps = eps
+        ctx.ste_scale = mode == "learnable_ste"
         ctx.lead = lead
         ctx.x_dtype = x.dtype
         ctx.learned = mode != "absmean"
@@ -86,7 +92,7 @@ class TernaryLinearFn(torch.autograd.Function):
 
     @staticmethod
     def backward(ctx, gy: torch.Tensor):
-        x2, codes, mag = ctx.saved_tensors
+        x2, codes, mag, w = ctx.saved_tensors
         N = codes.shape[0]
         dy = gy.reshape(-1, N)
         if dy.dtype != torch.bfloat16:
@@ -99,10 +105,21 @@ class TernaryLinearFn(torch.autograd.Function):
         want_scale = ctx.learned and ctx.needs_input_grad[2]
         if ctx.needs_input_grad[1] or want_scale:
             dw_hat = ops.tgemm_bwd_dw_ste(dy, x2)   # gradient w.r.t. the dequantized weights
-            if want_scale:
-                dscale = ops.group_code_dot(codes, dw_hat, ctx.g)
-            if ctx.needs_input_grad[1]:
-                dw = dw_hat
+            if ctx.ste_scale:
+                # scale gradient with the threshold term; the weights' gradient
+                # clip-masked, written over dWhat
+                dscale, dw_m = ops.scale_ste_grad(w, codes, mag, dw_hat, ctx.g, ctx.eps,
+                                                  in_place=ctx.needs_input_grad[1],
+                                                  want_dW=ctx.needs_input_grad[1])
+                if ctx.needs_input_grad[1]:
+                    dw = dw_m
+                if not want_scale:
+                    dscale = None
+            else:
+                if want_scale:
+                    dscale = ops.group_code_dot(codes, dw_hat, ctx.g)
+                if ctx.needs_input_grad[1]:
+                    dw = dw_hat
         return dx, dw, dscale, None, None, None, None, None, None
 
 
@@ -114,8 +131,10 @@ class TernaryLinear(torch.nn.Module):
     scale_mode "absmean" (the paper's layer): the scale is recomputed from
     the weights on every call and is not a parameter.  "decoupled": codes
     from the recomputed absmean, magnitude the parameter `scale`.
-    "learnable": the parameter `scale` is both threshold and magnitude.  The
-    parameter starts at the absmean of the weights (``reset_scale``, run on
+    "learnable": the parameter `scale` is both threshold and magnitude;
+    "learnable_ste": the same with only the rounding straight-through (the
+    scale's gradient keeps the threshold term, the weights' is clip-masked).
+    The parameter starts at the absmean of the weights (``reset_scale``, run on
     the first call unless it was run before or the scale was loaded with
     ``load_state_dict``).  threshold_mult (float32 [out]) scales
     each row's absmean threshold (e.g. 0.8 on the gate rows of in_proj).
@@ -136,7 +155,7 @@ class TernaryLinear(torch.nn.Module):
         if scale_mode not in SCALE_MODES:
             raise ValueError(f"scale_mode must be one of {SCALE_MODES}")
         if threshold_mult is not None:
-            if scale_mode == "learnable":
+            if scale_mode in ("learnable", "learnable_ste"):
                 raise ValueError("a learnable scale is its own threshold: no threshold_mult")
             if threshold_mult.shape != (out_features,):
                 raise ValueError(f"threshold_mult must have shape ({out_features},)")
@@ -210,7 +229,7 @@ class TernaryLinear(torch.nn.Module):
             codes, _, s16, _ = ops.ternarize_pack(w, self.g, self.eps, want_zero_count=False,
                                                   row_mult=self.threshold_mult)
             return codes, s16
-        if self.scale_mode == "learnable":
+        if self.scale_mode in ("learnable", "learnable_ste"):
             codes, _ = ops.ternarize_codes(w, self.scale.detach().contiguous(), self.g, self.eps,
                                            want_zero_count=False)
         else:

@@ -23,6 +23,10 @@ hipError_t launch_group_code_dot(const uint8_t*, const float*, int64_t, int64_t,
                                  hipStream_t) {
   reached("group_code_dot");
 }
+hipError_t launch_scale_ste_grad(const float*, const uint8_t*, const float*, const float*,
+                                 int64_t, int64_t, int, float, float*, float*, hipStream_t) {
+  reached("scale_ste_grad");
+}
 hipError_t launch_tgemm_fwd(const uint16_t*, const uint8_t*, const float*, int64_t, int64_t,
                             int64_t, int, void*, bool, hipStream_t) {
   reached("tgemm_fwd");

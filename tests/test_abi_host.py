@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 3
+    assert L.tm_abi_version() == 4
 
 
 def test_status_strings(L):
@@ -143,6 +143,31 @@ def test_group_code_dot_validation(L):
     assert gcd(L, out=P + 2 ** 26 + 2) == EALIGN
     assert gcd(L, out=P + 256) == EINVAL                 # overlaps the codes
     assert gcd(L, out=P + 2 ** 24 + 1024) == EINVAL      # overlaps dW
+
+
+def ssg(L, W=P, codes=P + 2 ** 22, scale=P + 2 ** 23, dWhat=P + 2 ** 24, N=8, K=256, g=128,
+        eps=1e-5, ds=P + 2 ** 25, dW=P + 2 ** 26):
+    return L.tm_scale_ste_grad(W, codes, scale, dWhat, N, K, g, eps, ds, dW, None)
+
+
+def test_scale_ste_grad_validation(L):
+    for kw in ("W", "codes", "scale", "dWhat", "ds"):
+        assert ssg(L, **{kw: 0}) == EINVAL, kw
+    assert ssg(L, eps=-1.0) == EINVAL
+    assert ssg(L, eps=float("nan")) == EINVAL
+    assert ssg(L, N=0) == ESHAPE
+    assert ssg(L, K=96, g=32) == ESHAPE
+    assert ssg(L, g=16) == ESHAPE
+    assert ssg(L, N=2 ** 40, K=2 ** 20) == ESHAPE
+    assert ssg(L, W=P + 4) == EALIGN
+    assert ssg(L, dWhat=P + 2 ** 24 + 8) == EALIGN
+    assert ssg(L, dW=P + 2 ** 26 + 4) == EALIGN
+    assert ssg(L, ds=P + 2 ** 25 + 2) == EALIGN
+    assert ssg(L, ds=P + 64) == EINVAL                    # ds overlaps W
+    assert ssg(L, ds=P + 2 ** 24 + 64) == EINVAL          # ds overlaps dWhat
+    assert ssg(L, dW=P + 2 ** 22) == EINVAL               # dW overlaps the codes
+    assert ssg(L, dW=P + 2 ** 24 + 16) == EINVAL          # partly over dWhat
+    assert ssg(L, dW=P + 2 ** 25 - 4 * 1024) == EINVAL    # dW [8, 256] (8 KiB) reaches ds
 
 
 def fwd(L, X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):

@@ -5,6 +5,8 @@
 * tm_ternarize_codes: codes against caller-given thresholds (the learned
   scale of Sec. 4);
 * tm_group_code_dot: the gradient of a per-group magnitude, sum q * dWhat;
+* tm_scale_ste_grad: a learnable scale's gradient with the rounding
+  straight-through (threshold term, clip-masked weight gradient);
 * TernaryLinear in its decoupled and learnable modes and with threshold
   multipliers, forward and backward.
 
@@ -243,6 +245,80 @@ def test_group_dot_special_cases():
 
 
 # --------------------------------------------------------------------------
+# learnable scale with the rounding straight-through
+# --------------------------------------------------------------------------
+
+def check_ssg(W, s, dWhat, g, eps, label):
+    ops = _ops()
+    N, K = W.shape
+    print(f"[scale ste grad] {label} N={N} K={K} g={g} eps={eps}", flush=True)
+    Wd, sd, gd = dev(W), dev(s), dev(dWhat)
+    codes, _ = ops.ternarize_codes(Wd, sd, g, eps)
+    q = O.unpack(host(codes), K)
+    assert np.array_equal(q, O.ternary_codes(W, s, g, eps))   # same float32 decisions
+    ds, dw = ops.scale_ste_grad(Wd, codes, sd, gd, g, eps)
+    ds, dw = host(ds), host(dw)
+    ds_ref, dw_ref = V.scale_ste_grad(W, q, s, dWhat, g, eps)
+    d = np.repeat((s + np.float32(eps)).astype(np.float32).astype(np.float64), g, axis=1)
+    sf = np.repeat(s.astype(np.float64), g, axis=1)
+    mag = (np.abs(dWhat.astype(np.float64)) * (np.abs(q) + np.abs(W) * sf / d ** 2)).reshape(
+        N, K // g, g).sum(2)
+    bound = 2.0 ** -24 * np.abs(ds_ref) + 4.0 * g * 2.0 ** -53 * mag + 1e-300
+    err = np.abs(ds.astype(np.float64) - ds_ref)
+    assert np.all(err <= bound), f"ds: max err / bound {np.max(err / bound):.3f}"
+    # dw: one float32 rounding of a float64 product
+    assert np.all(np.abs(dw.astype(np.float64) - dw_ref) <= 2.0 ** -24 * np.abs(dw_ref))
+    # in place over dWhat gives the same bits
+    gi = gd.clone()
+    ds2, dw2 = ops.scale_ste_grad(Wd, codes, sd, gi, g, eps, in_place=True)
+    assert dw2.data_ptr() == gi.data_ptr()
+    assert np.array_equal(host(ds2), ds) and np.array_equal(host(gi), dw)
+    # scale only
+    ds3, none = ops.scale_ste_grad(Wd, codes, sd, gd, g, eps, want_dW=False)
+    assert none is None and np.array_equal(host(ds3), ds)
+    masked = int((dw_ref == 0).sum() - (dWhat == 0).sum())
+    print(f"  clip-masked elements {masked}, max ds err / bound {np.max(err / bound):.3f}",
+          flush=True)
+    return q, ds, dw
+
+
+@pytest.mark.parametrize("g", synth.C5_GROUPS)
+@pytest.mark.parametrize("eps", [0.0, 1e-5])
+def test_scale_ste_grad_ragged(g, eps):
+    rng = np.random.default_rng(700 + g)
+    N, K = 301, 1024
+    W = synth.weights(rng, N, K, outliers=True)
+    s = (O.group_scales_f32(W, g) * rng.uniform(0.6, 1.6, (N, K // g))).astype(np.float32)
+    dWhat = (rng.standard_normal((N, K)) * np.exp(rng.uniform(-6, 6, (N, 1)))).astype(np.float32)
+    check_ssg(W, s, dWhat, g, eps, "301x1024 outliers, scales 0.6..1.6 x absmean")
+
+
+def test_scale_ste_grad_in_proj_full():
+    rng = np.random.default_rng(43)
+    W = synth.layer_weight(synth.C3, synth.SEED_W)
+    s = O.group_scales_f32(W, 128) * np.float32(1.2)
+    dWhat = rng.standard_normal(W.shape, dtype=np.float32) * np.float32(1e-3)
+    check_ssg(W, s.astype(np.float32), dWhat, 128, 1e-5, "in_proj 8512x2048")
+
+
+def test_scale_ste_grad_bounds_and_ties():
+    """Weights exactly on the clip bound (|w| = s, eps = 0: m = 1), one float32
+    step above it (m = 0), exact rounding ties (|w| = s/2: code 0) and zeros."""
+    g = 32
+    N, K = 4, 128
+    s = np.full((N, K // g), 0.75, np.float32)
+    W = np.zeros((N, K), np.float32)
+    W[0, :] = 0.75
+    W[1, :] = np.nextafter(np.float32(0.75), np.float32(1))
+    W[2, ::2], W[2, 1::2] = 0.375, -0.375
+    dWhat = np.linspace(-1, 1, N * K).astype(np.float32).reshape(N, K)
+    q, ds, dw = check_ssg(W, s, dWhat, g, 0.0, "bounds and ties")
+    assert np.all(q[0] == 1) and np.all(q[1] == 1) and np.all(q[2] == 0) and np.all(q[3] == 0)
+    assert np.array_equal(dw[0], dWhat[0]) and not dw[1].any()   # closed clip range
+    assert np.array_equal(dw[2], dWhat[2]) and np.array_equal(dw[3], dWhat[3])
+
+
+# --------------------------------------------------------------------------
 # TernaryLinear variants
 # --------------------------------------------------------------------------
 
@@ -251,7 +327,8 @@ def _bits(t):
 
 
 @pytest.mark.parametrize("mode,mult", [("absmean", True), ("decoupled", False),
-                                       ("decoupled", True), ("learnable", False)])
+                                       ("decoupled", True), ("learnable", False),
+                                       ("learnable_ste", False)])
 def test_layer_variants_forward_backward(mode, mult):
     from paper_2606_18114_amd.qat import TernaryLinear
     rng = np.random.default_rng(51)
@@ -272,7 +349,7 @@ def test_layer_variants_forward_backward(mode, mult):
     (y * r).sum().backward()
     torch.cuda.synchronize()
 
-    if mode == "learnable":
+    if mode in ("learnable", "learnable_ste"):
         mag = host(layer.scale)
         q = O.ternary_codes(W, mag, g, eps)
     else:
@@ -289,6 +366,9 @@ def test_layer_variants_forward_backward(mode, mult):
     e_y = O.rel_fro_error(host(y).reshape(-1, N), O.gemm_fwd(xb, q, mag, g))
     e_dx = O.rel_fro_error(host(x.grad.float()).reshape(-1, K), O.gemm_bwd_dx(rb, q, mag, g))
     dw_ref = O.gemm_bwd_dw(rb, xb)
+    dw_hat = dw_ref
+    if mode == "learnable_ste":
+        ds_ste, dw_ref = V.scale_ste_grad(W, q, mag, dw_hat, g, eps)
     e_dw = O.rel_fro_error(host(layer.weight.grad), dw_ref)
     print(f"  y {e_y:.2e} dX {e_dx:.2e} dW {e_dw:.2e}", flush=True)
     assert e_y <= REL_DESIGN and e_dx <= REL_BAR and e_dw <= REL_DESIGN
@@ -296,7 +376,8 @@ def test_layer_variants_forward_backward(mode, mult):
         assert [n for n, _ in layer.named_parameters()] == ["weight"]
     else:
         ds = host(layer.scale.grad)
-        e_ds = O.rel_fro_error(ds, V.group_code_dot(q, dw_ref, g))
+        ds_ref = ds_ste if mode == "learnable_ste" else V.group_code_dot(q, dw_hat, g)
+        e_ds = O.rel_fro_error(ds, ds_ref)
         print(f"  d scale {e_ds:.2e}", flush=True)
         assert e_ds <= REL_DESIGN
 
