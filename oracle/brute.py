@@ -145,3 +145,9 @@ def gemv(x, q, s16, g):
     float16 scales given as their values), exact-rounded fsum."""
     return [[math.fsum(xb[k] * s16[n][k // g] * q[n][k] for k in range(len(xb)))
              for n in range(len(q))] for xb in x]
+
+
+def dense_gemv(x, W):
+    """y[b][n] = sum_k x[b][k] * W[n][k], exact-rounded fsum (float values)."""
+    return [[math.fsum(xb[k] * W[n][k] for k in range(len(xb))) for n in range(len(W))]
+            for xb in x]

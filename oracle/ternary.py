@@ -57,6 +57,7 @@ __all__ = [
     "gemm_bwd_dx",
     "gemm_bwd_dw",
     "gemv",
+    "dense_gemv",
     "nrmse",
     "rel_fro_error",
     "ternarize",
@@ -246,6 +247,17 @@ def gemv(x: np.ndarray, q: np.ndarray, s16: np.ndarray, g: int) -> np.ndarray:
     """y[B, N] = x[B, K] . (q * s16)^T for decode, with float16 scales."""
     xf = bf16_bits_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, np.float64)
     return xf @ dequantize(q, np.asarray(s16).astype(np.float64), g).T
+
+
+def dense_gemv(x: np.ndarray, W16: np.ndarray) -> np.ndarray:
+    """y[B, N] = x[B, K] . W16[N, K]^T in float64: the decode product of a
+    layer kept in FP16 (Sec. 7, layer-selective quantization: the first and
+    last blocks stay unquantized).  x may be bf16 bits; W16 is float16."""
+    xf = bf16_bits_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, np.float64)
+    W = np.asarray(W16)
+    if W.dtype != np.float16:
+        raise ValueError("oracle: the kept layers' weights are float16")
+    return xf @ W.astype(np.float64).T
 
 
 # --------------------------------------------------------------------------

@@ -284,3 +284,66 @@ def test_planted_error_measure_mistakes_are_caught(dec, mutant, monkeypatch):
     monkeypatch.setattr(O, "rel_fro_error", {"no_sqrt": no_sqrt, "relative_to_got": rel_got,
                                              "max_abs": max_abs}[mutant])
     assert _caught(test_rel_fro_error_cases, dec), f"mutant {mutant} escaped"
+
+
+# --------------------------------------------------------------------------
+# Dense FP16 decode product (the layers kept unquantized)
+# --------------------------------------------------------------------------
+
+def _dense_case(dec):
+    c = dec["dense_gemv"]
+    W16 = np.array([[_f(v) for v in r] for r in c["W16"]], np.float16)
+    x = np.array([[_f(v) for v in r] for r in c["x"]], np.float64)
+    y = np.array([[_f(v) for v in r] for r in c["y"]])
+    return W16, x, y
+
+
+def test_hand_dense_gemv(dec):
+    """Float16 subnormal, largest and smallest normal weights, exact in float64."""
+    W16, x, y = _dense_case(dec)
+    assert np.array_equal(W16.astype(np.float64),
+                          np.array([[_f(v) for v in r] for r in dec["dense_gemv"]["W16"]]))
+    np.testing.assert_array_equal(O.dense_gemv(x, W16), y)
+    assert brute.dense_gemv(x.tolist(), W16.astype(float).tolist()) == y.tolist()
+    xb = synth.f32_to_bf16_bits(x.astype(np.float32))
+    np.testing.assert_array_equal(O.dense_gemv(xb, W16), y)
+
+
+def test_dense_gemv_against_twin_random():
+    rng = np.random.default_rng(77)
+    W16 = (rng.standard_normal((7, 192)) * 0.02).astype(np.float16)
+    x = synth.activations(rng, 3, 192)
+    twin = np.array(brute.dense_gemv(O.bf16_bits_to_f64(x).tolist(), W16.astype(float).tolist()))
+    np.testing.assert_allclose(O.dense_gemv(x, W16), twin, rtol=1e-12, atol=1e-15)
+    # one-hot rows select weight columns exactly
+    eye = np.eye(192)[:5]
+    np.testing.assert_array_equal(O.dense_gemv(eye, W16), W16.astype(np.float64)[:, :5].T)
+    with pytest.raises(ValueError):
+        O.dense_gemv(x, W16.astype(np.float32))
+
+
+_ORIG_DENSE = O.dense_gemv
+
+
+@pytest.mark.parametrize("mutant", ["no_transpose", "batch_rows_swapped", "weights_bf16",
+                                    "x_as_float16"])
+def test_planted_dense_mistakes_are_caught(dec, mutant, monkeypatch):
+    if mutant == "no_transpose":
+        monkeypatch.setattr(O, "dense_gemv", lambda x, W: (
+            O.bf16_bits_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, float))
+            @ np.asarray(W, np.float64))
+    elif mutant == "batch_rows_swapped":
+        monkeypatch.setattr(O, "dense_gemv", lambda x, W: _ORIG_DENSE(x, W)[::-1])
+    elif mutant == "weights_bf16":
+        def wbf(x, W):
+            Wb = O.bf16_bits_to_f64(synth.f32_to_bf16_bits(np.asarray(W, np.float32)))
+            xf = O.bf16_bits_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, float)
+            return xf @ Wb.T
+        monkeypatch.setattr(O, "dense_gemv", wbf)
+    elif mutant == "x_as_float16":
+        def xf16(x, W):
+            xf = O.bf16_bits_to_f64(x) if x.dtype == np.uint16 else np.asarray(x, float)
+            with np.errstate(over="ignore"):
+                return xf.astype(np.float16).astype(np.float64) @ np.asarray(W, np.float64).T
+        monkeypatch.setattr(O, "dense_gemv", xf16)
+    assert _caught(test_hand_dense_gemv, dec), f"mutant {mutant} escaped"
