@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 4
+#define TM_ABI_VERSION 5
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -192,6 +192,23 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
                    const uint16_t* scales_f16, int32_t count, int32_t B,
                    int64_t N, int64_t K, int32_t g, float* y, tm_stream stream);
+
+/*
+ * tm_dgemv — decode-time product of a layer kept in FP16 (Sec. 7,
+ * layer-selective quantization: the first and last blocks are not
+ * ternarized), strided-batched like tm_tgemv:
+ *   y[c, b, n] = sum_k x[c, b, k] * W16[c, n, k]
+ *
+ *   x      bf16 [count, B, K]     in   (16-byte aligned)
+ *   W16    float16 bits [count, N, K]  in   (16-byte aligned)
+ *   count  1 .. 65535;  B  1 .. 8;  K % 64 == 0 and B * K <= 16384
+ *   y      float32 [count, B, N]  out  (4-byte aligned)
+ * Each product of a float16 weight and the float32 value of a bfloat16
+ * activation is exact; they are summed with float32 fused multiply-adds and
+ * a float32 butterfly across lanes, in a fixed order (deterministic).
+ */
+tm_status tm_dgemv(const uint16_t* x, const uint16_t* W16, int32_t count, int32_t B, int64_t N,
+                   int64_t K, float* y, tm_stream stream);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

@@ -33,6 +33,7 @@ SOURCES = [
     "tgemm_bwd_dx.hip",
     "tgemm_bwd_dw.hip",
     "tgemv.hip",
+    "dgemv.hip",
     "group_code_dot.hip",
 ]
 

@@ -236,6 +236,22 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X, int64_t M, 
   return hip_status(tmk::launch_tgemm_bwd_dw(dY, X, M, N, K, dW, accumulate, to_hip(stream)));
 }
 
+tm_status tm_dgemv(const uint16_t* x, const uint16_t* W16, int32_t count, int32_t B, int64_t N,
+                   int64_t K, float* y, tm_stream stream) {
+  if (!x || !W16 || !y) return TM_EINVAL;
+  if (count < 1 || count > 65535 || B < 1 || B > 8 || N < 1) return TM_ESHAPE;
+  if (K < 64 || K % 64 != 0 || (int64_t)B * K > 16384) return TM_ESHAPE;
+  int64_t xb, wb, yb;
+  if (!bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of((int64_t)count * N, K, 2, &wb) ||
+      !bytes_of((int64_t)count * B, N, 4, &yb))
+    return TM_ESHAPE;
+  if ((N + 7) / 8 > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(x, 16) || !aligned(W16, 16) || !aligned(y, 4)) return TM_EALIGN;
+  const Span o = span(y, yb);
+  if (overlap(o, span(x, xb)) || overlap(o, span(W16, wb))) return TM_EINVAL;
+  return hip_status(tmk::launch_dgemv(x, W16, count, B, N, K, y, to_hip(stream)));
+}
+
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
                    int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
                    tm_stream stream) {

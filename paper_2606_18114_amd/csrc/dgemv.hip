@@ -1,0 +1,158 @@
+// Decode product of a layer kept in FP16 (layer-selective quantization,
+// paper Sec. 7: the first and last blocks stay unquantized):
+//   y[c, b, n] = sum_k x[c, b, k] * W[c, n, k],  W float16, x bfloat16,
+// strided-batched over `count` same-shape matrices, float32 out.
+//
+// HBM bound: 2 bytes per weight against 1/4 + 2/g for a ternary matrix, so a
+// kept in_proj layer streams 34.9 MB where its ternary form streams 4.6 MB.
+// Each lane streams 16-byte pieces (8 weights) of its wave's rows, R rows at
+// a time with SEG pieces of each row in flight (R * SEG = 16 loads of 16
+// bytes per lane, issued together), and multiplies them on the vector ALUs
+// in float32: a float16 weight times the float32 value of its bfloat16
+// activation is exact, and the products are summed by fused multiply-adds.
+// x is staged once per workgroup in LDS as float32 [B][K]; one 32-byte LDS
+// read per lane and chunk serves all R rows.  The per-lane partial sums of a
+// row meet in a butterfly over the wave.
+#include "common.hpp"
+#include "launchers.hpp"
+
+namespace tmk {
+
+constexpr int kDgWaves = 4;
+constexpr int kDgChunk = 512;  // columns one wave load covers (64 lanes x 8)
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  v += __uint_as_float(lane_xchg<1>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<2>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<4>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<8>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<16>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<32>(__float_as_uint(v)));
+  return v;
+}
+
+__device__ __forceinline__ float half_lo(uint32_t w) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu));
+}
+__device__ __forceinline__ float half_hi(uint32_t w) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16));
+}
+
+// Grid: (ceil(N / (R * kDgWaves)), count); wave w of workgroup i owns rows
+// (i * kDgWaves + w) * R .. + R - 1.  LDS: B * K floats.
+template <int BMAX, int R, int SEG>
+__global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ W, int B, int64_t N,
+    int64_t K, float* __restrict__ y) {
+  extern __shared__ __attribute__((aligned(16))) float xs[];
+  const int64_t mat = blockIdx.y;
+  const uint16_t* xm = x + mat * (int64_t)B * K;
+  const uint16_t* Wm = W + mat * N * K;
+  float* ym = y + mat * (int64_t)B * N;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+
+  // x -> float32 in LDS (8 values per thread and step; K % 8 == 0)
+  for (int64_t i = threadIdx.x; i < (int64_t)B * K / 8; i += 64 * kDgWaves) {
+    const u32x4 v = ld16(xm + 8 * i);
+    const uint32_t a[4] = {v.x, v.y, v.z, v.w};
+    float f[8];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      f[2 * t] = __uint_as_float(a[t] << 16);
+      f[2 * t + 1] = __uint_as_float(a[t] & 0xFFFF0000u);
+    }
+    st16(xs + 8 * i, u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                           __float_as_uint(f[3])});
+    st16(xs + 8 * i + 4, u32x4{__float_as_uint(f[4]), __float_as_uint(f[5]),
+                               __float_as_uint(f[6]), __float_as_uint(f[7])});
+  }
+  __syncthreads();
+
+  const int64_t row0 = ((int64_t)blockIdx.x * kDgWaves + wave) * R;
+  float acc[R][BMAX];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b) acc[r][b] = 0.f;
+
+  for (int64_t k0 = 0; k0 < K; k0 += (int64_t)kDgChunk * SEG) {
+    // all loads of this pass first (rows past N and columns past K re-read
+    // an in-bounds piece and are not used)
+    u32x4 wv[R][SEG];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t n = row0 + r < N ? row0 + r : N - 1;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        int64_t col = k0 + (int64_t)kDgChunk * j + 8 * lane;
+        col = col < K ? col : K - 8;
+        wv[r][j] = ld16(Wm + n * K + col);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) {
+      const int64_t col = k0 + (int64_t)kDgChunk * j + 8 * lane;
+      if (col >= K) continue;
+#pragma unroll
+      for (int b = 0; b < BMAX; ++b) {
+        if (b >= B) break;
+        const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col);
+        const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col + 4);
+        const float xv[8] = {__uint_as_float(x0.x), __uint_as_float(x0.y),
+                             __uint_as_float(x0.z), __uint_as_float(x0.w),
+                             __uint_as_float(x1.x), __uint_as_float(x1.y),
+                             __uint_as_float(x1.z), __uint_as_float(x1.w)};
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const uint32_t wa[4] = {wv[r][j].x, wv[r][j].y, wv[r][j].z, wv[r][j].w};
+          float a = acc[r][b];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            a = __builtin_fmaf(half_lo(wa[t]), xv[2 * t], a);
+            a = __builtin_fmaf(half_hi(wa[t]), xv[2 * t + 1], a);
+          }
+          acc[r][b] = a;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b) acc[r][b] = wave_sum_f32(acc[r][b]);
+  // lane r * BMAX + b stores row r, batch row b
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int b = 0; b < BMAX; ++b)
+      if (lane == r * BMAX + b && b < B && row0 + r < N) ym[(int64_t)b * N + row0 + r] = acc[r][b];
+}
+
+template <int BMAX>
+static hipError_t launch_dgemv_b(const uint16_t* x, const uint16_t* W, int count, int B,
+                                 int64_t N, int64_t K, float* y, hipStream_t stream) {
+  const size_t lds = (size_t)B * K * sizeof(float);
+  // four rows per wave, or two when the launch has few rows per CU
+  const int64_t blocks4 = (N + 4 * kDgWaves - 1) / (4 * kDgWaves) * count;
+  if (blocks4 >= 2 * (int64_t)current_cu_count()) {
+    const dim3 grid((unsigned)((N + 4 * kDgWaves - 1) / (4 * kDgWaves)), (unsigned)count);
+    hipLaunchKernelGGL((dgemv_kernel<BMAX, 4, 4>), grid, dim3(64 * kDgWaves), lds, stream, x, W,
+                       B, N, K, y);
+  } else {
+    const dim3 grid((unsigned)((N + 2 * kDgWaves - 1) / (2 * kDgWaves)), (unsigned)count);
+    hipLaunchKernelGGL((dgemv_kernel<BMAX, 2, 8>), grid, dim3(64 * kDgWaves), lds, stream, x, W,
+                       B, N, K, y);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W, int count, int B, int64_t N,
+                        int64_t K, float* y, hipStream_t stream) {
+  if (B <= 1) return launch_dgemv_b<1>(x, W, count, B, N, K, y, stream);
+  if (B <= 2) return launch_dgemv_b<2>(x, W, count, B, N, K, y, stream);
+  if (B <= 4) return launch_dgemv_b<4>(x, W, count, B, N, K, y, stream);
+  return launch_dgemv_b<8>(x, W, count, B, N, K, y, stream);
+}
+
+}  // namespace tmk

@@ -52,5 +52,8 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
 hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
+// y[c, b, n] = sum_k x[c, b, k] * W16[c, n, k] (dense float16 weights)
+hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W16, int count, int B, int64_t N,
+                        int64_t K, float* y, hipStream_t stream);
 
 }  // namespace tmk

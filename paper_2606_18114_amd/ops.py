@@ -40,6 +40,7 @@ SIGNATURES = {
     "tm_group_code_dot": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P]),
     "tm_ternarize_codes": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P]),
     "tm_tgemm_fwd_bf16": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_dgemv": (ctypes.c_int, [_P, _P, _I32, _I32, _I64, _I64, _P, _P]),
     "tm_scale_ste_grad": (ctypes.c_int,
                           [_P, _P, _P, _P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P]),
 }
@@ -327,4 +328,21 @@ def tgemv(x: torch.Tensor, codes: torch.Tensor, scales_f16: torch.Tensor, g: int
     st = lib().tm_tgemv(_ptr(x), _ptr(codes), _ptr(scales_f16), count, B, N, K, g, _ptr(y),
                         _stream())
     _check("tm_tgemv", st)
+    return y
+
+
+def dgemv(x: torch.Tensor, W16: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Dense decode product of layers kept in FP16: x bf16 [count, B, K],
+    W16 float16 [count, N, K] -> y float32 [count, B, N]."""
+    _need(x, "x", _BF16, 3)
+    _need(W16, "W16", _F16, 3)
+    count, B, K = x.shape
+    N = W16.shape[1]
+    _shape(W16, "W16", (count, N, K), x.device)
+    if y is None:
+        y = torch.empty((count, B, N), dtype=torch.float32, device=x.device)
+    _need(y, "y", _F32, 3)
+    _shape(y, "y", (count, B, N), x.device)
+    st = lib().tm_dgemv(_ptr(x), _ptr(W16), count, B, N, K, _ptr(y), _stream())
+    _check("tm_dgemv", st)
     return y

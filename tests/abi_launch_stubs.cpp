@@ -45,4 +45,9 @@ hipError_t launch_tgemv(const uint16_t*, const uint8_t*, const uint16_t*, int, i
   reached("tgemv");
 }
 
+hipError_t launch_dgemv(const uint16_t*, const uint16_t*, int, int, int64_t, int64_t, float*,
+                        hipStream_t) {
+  reached("dgemv");
+}
+
 }  // namespace tmk

@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 4
+    assert L.tm_abi_version() == 5
 
 
 def test_status_strings(L):
@@ -168,6 +168,27 @@ def test_scale_ste_grad_validation(L):
     assert ssg(L, dW=P + 2 ** 22) == EINVAL               # dW overlaps the codes
     assert ssg(L, dW=P + 2 ** 24 + 16) == EINVAL          # partly over dWhat
     assert ssg(L, dW=P + 2 ** 25 - 4 * 1024) == EINVAL    # dW [8, 256] (8 KiB) reaches ds
+
+
+def dg(L, x=P, W=P + 2 ** 24, count=2, B=1, N=300, K=2048, y=P + 2 ** 28):
+    return L.tm_dgemv(x, W, count, B, N, K, y, None)
+
+
+def test_dgemv_validation(L):
+    for kw in ("x", "W", "y"):
+        assert dg(L, **{kw: 0}) == EINVAL, kw
+    assert dg(L, count=0) == ESHAPE
+    assert dg(L, count=65536) == ESHAPE
+    assert dg(L, B=0) == ESHAPE
+    assert dg(L, B=9) == ESHAPE
+    assert dg(L, N=0) == ESHAPE
+    assert dg(L, K=2000) == ESHAPE
+    assert dg(L, B=5, K=4096) == ESHAPE          # x staging beyond 64 KiB of LDS
+    assert dg(L, x=P + 8) == EALIGN
+    assert dg(L, W=P + 2 ** 24 + 8) == EALIGN
+    assert dg(L, y=P + 2 ** 28 + 2) == EALIGN
+    assert dg(L, y=P + 2048) == EINVAL           # y overlaps x
+    assert dg(L, y=P + 2 ** 24 + 4096) == EINVAL  # y overlaps W
 
 
 def fwd(L, X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):

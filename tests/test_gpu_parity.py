@@ -620,3 +620,77 @@ def test_gemv_activation_outliers_per_output(g, B, count):
           f"{worst_rel:.2e}", flush=True)
     assert worst_abs <= 1e-6
     assert worst_rel <= 1e-4
+
+
+# --------------------------------------------------------------------------
+# dense FP16 decode product (layers kept unquantized)
+# --------------------------------------------------------------------------
+
+def dgemv_case(count, B, N, K, seed, label="", W16=None, xb=None, fro_bar=1e-6):
+    ops = _ops()
+    print(f"[dgemv] {label} count={count} B={B} N={N} K={K} seed={seed}", flush=True)
+    rng = np.random.default_rng(seed)
+    if W16 is None:
+        W16 = (rng.standard_normal((count, N, K)) * 0.02).astype(np.float16)
+    if xb is None:
+        xb = synth.activations(rng, count * B, K).reshape(count, B, K)
+    Wt = torch.from_numpy(W16.view(np.int16)).cuda().view(torch.float16)
+    y = host(ops.dgemv(dev_bf16(xb), Wt))
+    worst_fro, worst_out = 0.0, 0.0
+    for m in range(count):
+        ref = O.dense_gemv(xb[m], W16[m])
+        mag = O.dense_gemv(np.abs(O.bf16_bits_to_f64(xb[m])), np.abs(W16[m]))
+        worst_fro = max(worst_fro, O.rel_fro_error(y[m], ref))
+        worst_out = max(worst_out, float((np.abs(y[m] - ref) / np.maximum(mag, 1e-300)).max()))
+    print(f"  rel fro err {worst_fro:.3e}, max |err| / sum|x w| {worst_out:.3e}", flush=True)
+    assert worst_fro <= fro_bar and worst_out <= 1e-5
+    return y
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 4, 8])
+def test_dgemv_ragged(B):
+    # N not a multiple of the rows per workgroup, K not a multiple of the
+    # 512-column wave load (a partial last chunk), several matrices
+    dgemv_case(3, B, 300, 576 if B < 8 else 1600, seed=40 + B, label="ragged")
+
+
+@pytest.mark.parametrize("K", [64, 2048])
+def test_dgemv_single_matrix_few_rows(K):
+    dgemv_case(1, 1, 37, K, seed=K, label="one matrix")
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_dgemv_kept_layer_shapes(B):
+    # the four kept layers' in_proj (8512 x 2048) and out_proj (2048 x 4096)
+    dgemv_case(4, B, synth.IN_PROJ_N, synth.D_MODEL, seed=900 + B, label="kept in_proj")
+    dgemv_case(4, B, synth.D_MODEL, synth.D_INNER, seed=910 + B, label="kept out_proj")
+
+
+def test_dgemv_float16_range():
+    """Subnormal, largest and smallest normal float16 weights, activations
+    over 2^-30 .. 2^14, a zero row and a one-hot row."""
+    rng = np.random.default_rng(5)
+    N, K = 64, 1024
+    W16 = (rng.standard_normal((1, N, K)) * 0.02).astype(np.float16)
+    W16[0, 0, :] = np.float16(2.0 ** -24)
+    W16[0, 1, ::2], W16[0, 1, 1::2] = np.float16(65504.0), np.float16(-65504.0)
+    W16[0, 2, :] = np.float16(2.0 ** -14)
+    xf = np.zeros((1, 4, K), np.float32)
+    xf[0, 1] = rng.standard_normal(K) * np.exp2(rng.integers(-30, 15, K))
+    xf[0, 2, 333] = 1.0
+    xf[0, 3] = rng.standard_normal(K)
+    xb = synth.f32_to_bf16_bits(xf)
+    # the +-65504 row cancels heavily, so its own relative error is larger;
+    # every output stays within 1e-5 of the sum of its products' magnitudes
+    y = dgemv_case(1, 4, N, K, seed=5, label="float16 range", W16=W16, xb=xb, fro_bar=REL_DESIGN)
+    assert np.all(y[0, 0] == 0.0)
+    assert np.array_equal(y[0, 2], W16[0, :, 333].astype(np.float32))
+
+
+def test_dgemv_deterministic():
+    ops = _ops()
+    rng = np.random.default_rng(8)
+    W16 = torch.from_numpy((rng.standard_normal((2, 500, 2048)) * 0.02).astype(np.float16)).cuda()
+    x = dev_bf16(synth.activations(rng, 2, 2048).reshape(2, 1, 2048))
+    a, b = host(ops.dgemv(x, W16)), host(ops.dgemv(x, W16))
+    assert np.array_equal(a, b)
