@@ -62,11 +62,11 @@ def parse():
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants, "
-                         "per_layer, small, sweep (keeps a profiler trace to the kernels "
+                         "per_layer, small, sweep, mixed (keeps a profiler trace to the kernels "
                          "of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
-    bad = args.skip - {"qat", "variants", "per_layer"}
+    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed"}
     if bad:
         ap.error(f"unknown --skip sections: {sorted(bad)}")
     return args
@@ -245,6 +245,7 @@ def main():
     # ---------------- decode in layer order: one launch per matrix ----------------
     per_layer = (None if "per_layer" in args.skip
                  else decode_per_layer(ops, dec, L, max(args.steps, 10)))
+    mixed = None if "mixed" in args.skip else decode_mixed_stack(dev, max(args.steps // 4, 3))
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
@@ -348,6 +349,7 @@ def main():
         "kernels": kernels,
         "qat_block": qat_block,
         "decode_per_layer": per_layer,
+        "decode_mixed_fp16_blocks": mixed,
         "qat_block_bf16_out": qat_block_bf16,
         "variants": variants,
         "cold_vs_warm": {k: v for k, v in cold.items() if not k.startswith("decode_")},
@@ -687,6 +689,56 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
                        f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
                        f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
     return base, par, codes_cmp
+
+
+def decode_mixed_stack(dev, tokens, batch=1):
+    """Layer-selective quantization (Sec. 7, Table 10): the 48-layer decode
+    token with the first two and last two blocks kept in FP16 (2 bytes per
+    weight, tm_dgemv) and the other 44 ternary (tm_tgemv): four launches per
+    token (ternary and FP16 arenas of each projection kind).  Warm (one set
+    of arenas) and cold (tokens cycling over copies, >= 1.1 GiB)."""
+    import torch
+    from paper_2606_18114_amd import synth
+    from paper_2606_18114_amd.stack import DecodeStack, keep_first_last
+
+    cfg = {"in": synth.DECODE_IN, "out": synth.DECODE_OUT}
+    L = synth.N_LAYERS
+    keep = keep_first_last(L, 2)
+    st = DecodeStack(
+        lambda k, l: torch.from_numpy(synth.layer_weight(cfg[k], synth.decode_seed(f"{k}_w", l))
+                                      ).to(dev),
+        L, {k: (c.N, c.K) for k, c in cfg.items()}, keep=keep, g=128, eps=1e-5, batch=batch,
+        device=dev)
+    for k, c in cfg.items():
+        xs = np.stack([synth.layer_acts(batch, c.K, synth.decode_seed(f"{k}_x", l))
+                       for l in range(L)])
+        st.set_inputs(k, torch.from_numpy(xs.view(np.int16)).to(dev).view(torch.bfloat16))
+    nb = st.bytes_per_token()
+    copies = [None] + [st.arena_copy() for _ in range(int(np.ceil(ROTATE_BYTES / nb)) - 1)]
+    res = {"kept_layers": keep, "bytes_per_token": nb, "batch": batch,
+           "launches_per_token": 4}
+    for mode in ("warm", "cold"):
+        pick = (lambda t: None) if mode == "warm" else (lambda t: copies[t % len(copies)])
+        for t in range(2 * len(copies)):
+            st.token(arenas=pick(t))
+        torch.cuda.synchronize()
+        n = max(tokens, 5) * len(copies)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for t in range(n):
+            st.token(arenas=pick(t))
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / n
+        res[mode] = {"us_per_token": round(us, 2), "GBps": round(nb / (us * 1e-6) / 1e9, 1),
+                     "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)}
+    res["copies_cold"] = len(copies)
+    res["what"] = ("48 layers (in_proj 8512x2048 + out_proj 2048x4096), layers 0, 1, 46, 47 "
+                   "in float16, the rest 2-bit codes + fp16 scales, batch 1, all layers of a "
+                   "kind per launch")
+    del copies, st
+    return res
 
 
 def decode_per_layer(ops, dec, L, tokens):
