@@ -151,3 +151,44 @@ def dense_gemv(x, W):
     """y[b][n] = sum_k x[b][k] * W[n][k], exact-rounded fsum (float values)."""
     return [[math.fsum(xb[k] * W[n][k] for k in range(len(xb))) for n in range(len(W))]
             for xb in x]
+
+
+def mixer_step(zxbcdt, conv_state, ssm_state, conv_w, conv_b, dt_bias, A_log, D, norm_w,
+               eps, headdim, d_state):
+    """One Mamba-2 mixer decode step in plain loops over lists (a second
+    formulation of ``oracle/mamba.py``): per token, the convolution window of
+    each channel, the per-head decay and input terms, the per-element state
+    recurrence, the readout, the gate and the root-mean-square scale."""
+    nheads = len(A_log)
+    d_inner = nheads * headdim
+    conv_dim = d_inner + 2 * d_state
+    sp = lambda v: v if v > 20 else math.log1p(math.exp(v))
+    si = lambda v: v / (1.0 + math.exp(-v))
+    outs, conv_new, ssm_new = [], [], []
+    for b, row in enumerate(zxbcdt):
+        z = row[:d_inner]
+        xbc = row[d_inner:d_inner + conv_dim]
+        dt = row[d_inner + conv_dim:]
+        u, cs = [], []
+        for c in range(conv_dim):
+            win = list(conv_state[b][c][1:]) + [xbc[c]]
+            cs.append(win)
+            u.append(si(math.fsum(win[t] * conv_w[c][t] for t in range(len(win))) + conv_b[c]))
+        conv_new.append(cs)
+        Bv, Cv = u[d_inner:d_inner + d_state], u[d_inner + d_state:]
+        y, st_b = [], []
+        for h in range(nheads):
+            d = sp(dt[h] + dt_bias[h])
+            a = math.exp(-d * math.exp(A_log[h]))
+            st_h = []
+            for p in range(headdim):
+                xv = u[h * headdim + p]
+                new = [a * ssm_state[b][h][p][n] + d * xv * Bv[n] for n in range(d_state)]
+                st_h.append(new)
+                y.append(math.fsum(new[n] * Cv[n] for n in range(d_state)) + D[h] * xv)
+            st_b.append(st_h)
+        ssm_new.append(st_b)
+        g = [y[i] * si(z[i]) for i in range(d_inner)]
+        r = 1.0 / math.sqrt(math.fsum(v * v for v in g) / d_inner + eps)
+        outs.append([g[i] * r * norm_w[i] for i in range(d_inner)])
+    return outs, conv_new, ssm_new
