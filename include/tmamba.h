@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 5
+#define TM_ABI_VERSION 7
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -209,6 +209,59 @@ tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
  */
 tm_status tm_dgemv(const uint16_t* x, const uint16_t* W16, int32_t count, int32_t B, int64_t N,
                    int64_t K, float* y, tm_stream stream);
+
+/*
+ * tm_residual_rmsnorm — the Mamba-2 block wrapper around the mixer in
+ * decode: the residual stream takes the previous layer's out_proj output,
+ * and the pre-norm gives the next layer's in_proj input:
+ *   residual[b] += y[b]   (skipped when y is NULL);
+ *   x[b, i] = bf16(residual[b, i] / sqrt(mean_i(residual[b, i]^2) + eps) * w[i]).
+ *   residual  float32 [B, D]  in/out;  y  float32 [B, D] in or NULL
+ *   w         float32 [D];  eps float32, finite, >= 0
+ *   x         bfloat16 bits [B, D]  out
+ *   B 1 .. 65535;  arrays must not overlap
+ */
+tm_status tm_residual_rmsnorm(float* residual, const float* y, int32_t B, int64_t D,
+                              const float* w, float eps, uint16_t* x, tm_stream stream);
+
+/*
+ * tm_mixer_step — one Mamba-2 mixer decode step between in_proj and
+ * out_proj, the part of a decoding layer kept in FP16 (Sec. 3.2: the
+ * convolution, SSM parameters and state are not ternarized; Sec. 8:
+ * batch-1 decode).  Per token b, with d_inner = nheads * 64, d_state = 128,
+ * conv_dim = d_inner + 2 d_state and zxbcdt[b] = [z | xBC | dt] (in_proj's
+ * output, widths d_inner | conv_dim | nheads):
+ *   u = SiLU(conv step of xBC: window = the 3 previous inputs and xBC,
+ *            u[c] = conv_b[c] + sum_t window[t] conv_w[c, t]);
+ *   x, B, C = u[:d_inner], u[d_inner:d_inner+128], u[d_inner+128:];
+ *   dt' = softplus(dt + dt_bias[h]);  a = exp(-dt' exp(A_log[h]));
+ *   S[h,p,n] <- a S[h,p,n] + dt' x[h,p] B[n];  y = S C + D[h] x;
+ *   g = y * SiLU(z);  out[b] = bf16(g / sqrt(mean(g^2) + eps) * norm_w).
+ *
+ *   zxbcdt      float32 [B, 2 d_inner + 2 d_state + nheads]   in
+ *   B 1 .. 65535;  nheads 1 .. 4096;  headdim == 64;  d_state == 128
+ *   conv_state  float16 [B, conv_dim, 4]   in/out: a ring of the last 4
+ *               inputs per channel; slot (pos + j) % 4 holds the j-th
+ *               oldest, j = 0 .. 3 (pos = 0: slots in time order)
+ *   conv_pos    int32 [1]   in/out: pos, advanced by one (mod 4) per call
+ *   ssm_state   float16 [B, nheads, 64, 128]  in/out (16-byte aligned);
+ *               updated in float32 and rounded once to float16
+ *   conv_w      float32 [conv_dim, 4] (oldest tap first);  conv_b [conv_dim]
+ *   dt_bias, A_log, D  float32 [nheads];  norm_w  float32 [d_inner]
+ *   eps         float32, finite, >= 0
+ *   workspace   float32 [B * (d_inner + nheads)]  scratch owned by the caller
+ *   out         bfloat16 bits [B, d_inner]  out: out_proj's input
+ * Two launches on `stream` (the step, then the normalization, which also
+ * advances conv_pos).  The state arrays, conv_pos, workspace and out must
+ * not overlap each other or the inputs; calls that share state must not
+ * run concurrently.
+ */
+tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                        int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                        uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                        const float* dt_bias, const float* A_log, const float* D,
+                        const float* norm_w, float eps, float* workspace, uint16_t* out,
+                        tm_stream stream);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

@@ -34,7 +34,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["split_in_proj", "conv_step", "ssm_step", "gated_rmsnorm", "mixer_step",
-           "softplus", "silu"]
+           "softplus", "silu", "rmsnorm"]
 
 
 def softplus(v: np.ndarray) -> np.ndarray:
@@ -111,3 +111,10 @@ def mixer_step(zxbcdt, conv_state, ssm_state, conv_w, conv_b, dt_bias, A_log, D,
     y, ssm_new = ssm_step(ssm_state, x, Bv, Cv, dt, dt_bias, A_log, D)
     out = gated_rmsnorm(y.reshape(-1, d_inner), z, norm_w, eps)
     return out, conv_new, ssm_new
+
+
+def rmsnorm(residual: np.ndarray, w: np.ndarray, eps: float) -> np.ndarray:
+    """The block's pre-norm: residual / sqrt(mean(residual^2) + eps) * w, per token
+    (the next layer's in_proj input before its bfloat16 rounding)."""
+    r = np.asarray(residual, np.float64)
+    return r / np.sqrt((r * r).mean(axis=-1, keepdims=True) + eps) * np.asarray(w, np.float64)[None]

@@ -34,6 +34,7 @@ SOURCES = [
     "tgemm_bwd_dw.hip",
     "tgemv.hip",
     "dgemv.hip",
+    "mixer.hip",
     "group_code_dot.hip",
 ]
 

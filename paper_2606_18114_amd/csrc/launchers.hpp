@@ -56,4 +56,17 @@ hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t*
 hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W16, int count, int B, int64_t N,
                         int64_t K, float* y, hipStream_t stream);
 
+// one Mamba-2 mixer decode step (headdim 64, d_state 128): conv ring step,
+// float16 SSM update, gated RMSNorm -> bfloat16 out; workspace holds
+// B * (d_inner + nheads) floats
+hipError_t launch_mixer_step(const float* zxbcdt, int B, int nheads, uint16_t* conv_state,
+                             int* conv_pos, uint16_t* ssm_state, const float* conv_w,
+                             const float* conv_b, const float* dt_bias, const float* A_log,
+                             const float* D, const float* norm_w, float eps, float* workspace,
+                             uint16_t* out, hipStream_t stream);
+
+// residual += y (y may be null); x = bf16(rmsnorm(residual) * w), B rows of D
+hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,
+                                   const float* w, float eps, uint16_t* x, hipStream_t stream);
+
 }  // namespace tmk

@@ -1,0 +1,201 @@
+// One Mamba-2 mixer decode step between in_proj and out_proj: the part of a
+// decoding layer the paper keeps in FP16 (Sec. 3.2; batch-1 decode, Sec. 8).
+//
+// Kernel 1, one workgroup per (head, batch row):
+//   * causal depthwise convolution step (d_conv = 4) over the head's 64 x
+//     channels and the 2 x d_state B/C channels shared by all heads, SiLU;
+//   * dt' = softplus(dt + dt_bias), decay a = exp(-dt' exp(A_log));
+//   * state[p, n] <- a state[p, n] + dt' x[p] B[n]  (float16 state, float32
+//     arithmetic, rounded once to float16 when stored);
+//   * y[p] = sum_n state[p, n] C[n] + D x[p];  g = y * SiLU(z);
+//   * g (float32) and the head's sum of g^2 go to the workspace.
+// Kernel 2, one workgroup per batch row: the gated RMSNorm over all d_inner
+// channels, out = bf16(g / sqrt(mean(g^2) + eps) * w), the bfloat16 input
+// of out_proj; and the convolution ring position advances.
+//
+// Convolution state: a ring of 4 float16 slots per channel; the window of a
+// step, oldest first, is slots (pos + 1 .. pos + 3) % 4 and the new input,
+// which then overwrites slot pos (the oldest).  Every workgroup reads the
+// B/C channels' window, so no workgroup may shift it in place while others
+// still read: the ring writes only the slot nobody reads, and the position
+// moves on in kernel 2, after every workgroup of kernel 1 is done.
+#include "common.hpp"
+#include "launchers.hpp"
+
+namespace tmk {
+
+constexpr int kMxP = 64;    // headdim
+constexpr int kMxN = 128;   // d_state
+constexpr int kMxThreads = 256;
+
+__device__ __forceinline__ float mx_silu(float v) { return v / (1.f + expf(-v)); }
+__device__ __forceinline__ float mx_softplus(float v) { return v > 20.f ? v : log1pf(expf(v)); }
+
+__device__ __forceinline__ float h2f(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+__device__ __forceinline__ uint16_t f2h(float f) {  // round to nearest even
+  return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// grid (nheads, B); layout: zxbcdt [B, Z] with Z = 2 d_inner + 2 N + nheads,
+// conv [B, conv_dim, 4] float16 ring, ssm [B, nheads, P, N] float16,
+// gated [B, d_inner] and partial [B, nheads] float32
+__global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
+    const float* __restrict__ zxbcdt, int nheads, uint16_t* __restrict__ conv,
+    const int* __restrict__ conv_pos, uint16_t* __restrict__ ssm,
+    const float* __restrict__ conv_w, const float* __restrict__ conv_b,
+    const float* __restrict__ dt_bias, const float* __restrict__ A_log,
+    const float* __restrict__ Dp, float* __restrict__ gated, float* __restrict__ partial) {
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int d_inner = nheads * kMxP;
+  const int conv_dim = d_inner + 2 * kMxN;
+  const int64_t Z = (int64_t)2 * d_inner + 2 * kMxN + nheads;
+  const float* row = zxbcdt + (int64_t)b * Z;
+  const int pos = conv_pos[0] & 3;
+  __shared__ float u[kMxP + 2 * kMxN];  // x of the head, then B, then C (after SiLU)
+  __shared__ float wsum[kMxThreads / 64];
+
+  // convolution: local channel i < 64 is x channel 64 h + i, then the B/C
+  // channels d_inner + (i - 64)
+  for (int i = tid; i < kMxP + 2 * kMxN; i += kMxThreads) {
+    const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
+    const float xin = row[d_inner + c];
+    uint16_t* cs = conv + ((int64_t)b * conv_dim + c) * 4;
+    const float* w = conv_w + (int64_t)c * 4;
+    float acc = conv_b[c];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(h2f(cs[(pos + 1 + j) & 3]), w[j], acc);
+    acc = __builtin_fmaf(xin, w[3], acc);
+    u[i] = mx_silu(acc);
+    // the slot nobody reads; the shared B/C channels are written by head 0
+    if (i < kMxP || h == 0) cs[pos] = f2h(xin);
+  }
+  __syncthreads();
+
+  const float dtp = mx_softplus(row[2 * d_inner + 2 * kMxN + h] + dt_bias[h]);
+  const float a = expf(-dtp * expf(A_log[h]));
+  // thread t: channel p = t / 4, states n = 32 (t % 4) .. + 31
+  const int p = tid >> 2, q = tid & 3;
+  const float xp = u[p];
+  const float dx = dtp * xp;
+  uint16_t* sp = ssm + (((int64_t)b * nheads + h) * kMxP + p) * kMxN + 32 * q;
+  float y = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const u32x4 v = ld16(sp + 8 * k);
+    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int n0 = 32 * q + 8 * k + 2 * t;
+      const float s0 = __builtin_fmaf(a, h2f((uint16_t)(wv[t] & 0xFFFFu)), dx * u[kMxP + n0]);
+      const float s1 = __builtin_fmaf(a, h2f((uint16_t)(wv[t] >> 16)), dx * u[kMxP + n0 + 1]);
+      y = __builtin_fmaf(s0, u[kMxP + kMxN + n0], y);
+      y = __builtin_fmaf(s1, u[kMxP + kMxN + n0 + 1], y);
+      o[t] = (uint32_t)f2h(s0) | ((uint32_t)f2h(s1) << 16);
+    }
+    st16(sp + 8 * k, u32x4{o[0], o[1], o[2], o[3]});
+  }
+  // the four threads of a channel (lanes 4p' .. 4p' + 3 of the wave)
+  y += __uint_as_float(lane_xchg<1>(__float_as_uint(y)));
+  y += __uint_as_float(lane_xchg<2>(__float_as_uint(y)));
+  y = __builtin_fmaf(Dp[h], xp, y);
+  const float g = y * mx_silu(row[h * kMxP + p]);
+  if (q == 0) gated[(int64_t)b * d_inner + h * kMxP + p] = g;
+  // sum of g^2 over the head's 64 channels: each channel counted once (q = 0)
+  float sq = q == 0 ? g * g : 0.f;
+  sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<2>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<4>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<8>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<16>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<32>(__float_as_uint(sq)));
+  if ((tid & 63) == 0) wsum[tid >> 6] = sq;
+  __syncthreads();
+  if (tid == 0)
+    partial[(int64_t)b * nheads + h] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+}
+
+// grid (B); out[b, i] = bf16(g[b, i] * rsqrt(sum_h partial[b, h] / d_inner + eps) * w[i])
+__global__ __launch_bounds__(kMxThreads) void mixer_norm_kernel(
+    const float* __restrict__ gated, const float* __restrict__ partial, int nheads,
+    const float* __restrict__ norm_w, float eps, uint16_t* __restrict__ out,
+    int* __restrict__ conv_pos) {
+  const int b = blockIdx.x;
+  const int d_inner = nheads * kMxP;
+  __shared__ float r_sh;
+  if (threadIdx.x == 0) {
+    float s = 0.f;
+    for (int h = 0; h < nheads; ++h) s += partial[(int64_t)b * nheads + h];  // fixed order
+    r_sh = 1.f / sqrtf(s / (float)d_inner + eps);
+  }
+  __syncthreads();
+  const float r = r_sh;
+  for (int i = threadIdx.x; i < d_inner; i += kMxThreads) {
+    const float v = gated[(int64_t)b * d_inner + i] * r * norm_w[i];
+    const uint32_t bits = __float_as_uint(v);
+    out[(int64_t)b * d_inner + i] = (uint16_t)((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16);
+  }
+  if (b == 0 && threadIdx.x == 0) conv_pos[0] = (conv_pos[0] + 1) & 3;
+}
+
+// grid (B): residual[b] += y[b] (y may be null), then
+// x[b, i] = bf16(residual[b, i] / sqrt(mean(residual[b]^2) + eps) * w[i])
+__global__ __launch_bounds__(kMxThreads) void residual_rmsnorm_kernel(
+    float* __restrict__ residual, const float* __restrict__ y, int64_t D,
+    const float* __restrict__ w, float eps, uint16_t* __restrict__ x) {
+  const int b = blockIdx.x;
+  float* r = residual + (int64_t)b * D;
+  const float* yy = y ? y + (int64_t)b * D : nullptr;
+  __shared__ float wsum[kMxThreads / 64];
+  float sq = 0.f;
+  for (int64_t i = threadIdx.x; i < D; i += kMxThreads) {
+    float v = r[i];
+    if (yy) {
+      v += yy[i];
+      r[i] = v;
+    }
+    sq = __builtin_fmaf(v, v, sq);
+  }
+  sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<2>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<4>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<8>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<16>(__float_as_uint(sq)));
+  sq += __uint_as_float(lane_xchg<32>(__float_as_uint(sq)));
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
+  __syncthreads();
+  const float scale = 1.f / sqrtf(((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) / (float)D + eps);
+  for (int64_t i = threadIdx.x; i < D; i += kMxThreads) {
+    const uint32_t bits = __float_as_uint(r[i] * scale * w[i]);
+    x[(int64_t)b * D + i] = (uint16_t)((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16);
+  }
+}
+
+hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,
+                                   const float* w, float eps, uint16_t* x, hipStream_t stream) {
+  hipLaunchKernelGGL(residual_rmsnorm_kernel, dim3((unsigned)B), dim3(kMxThreads), 0, stream,
+                     residual, y, D, w, eps, x);
+  return hipGetLastError();
+}
+
+hipError_t launch_mixer_step(const float* zxbcdt, int B, int nheads, uint16_t* conv_state,
+                             int* conv_pos, uint16_t* ssm_state, const float* conv_w,
+                             const float* conv_b, const float* dt_bias, const float* A_log,
+                             const float* D, const float* norm_w, float eps, float* workspace,
+                             uint16_t* out, hipStream_t stream) {
+  float* gated = workspace;
+  float* partial = workspace + (int64_t)B * nheads * kMxP;
+  hipLaunchKernelGGL(mixer_ssm_kernel, dim3((unsigned)nheads, (unsigned)B), dim3(kMxThreads), 0,
+                     stream, zxbcdt, nheads, conv_state, conv_pos, ssm_state, conv_w, conv_b,
+                     dt_bias, A_log, D, gated, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mixer_norm_kernel, dim3((unsigned)B), dim3(kMxThreads), 0, stream, gated,
+                     partial, nheads, norm_w, eps, out, conv_pos);
+  return hipGetLastError();
+}
+
+}  // namespace tmk

@@ -41,6 +41,9 @@ SIGNATURES = {
     "tm_ternarize_codes": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P]),
     "tm_tgemm_fwd_bf16": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
     "tm_dgemv": (ctypes.c_int, [_P, _P, _I32, _I32, _I64, _I64, _P, _P]),
+    "tm_residual_rmsnorm": (ctypes.c_int, [_P, _P, _I32, _I64, _P, ctypes.c_float, _P, _P]),
+    "tm_mixer_step": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
+                                     _P, ctypes.c_float, _P, _P, _P]),
     "tm_scale_ste_grad": (ctypes.c_int,
                           [_P, _P, _P, _P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P]),
 }
@@ -346,3 +349,73 @@ def dgemv(x: torch.Tensor, W16: torch.Tensor, y: Optional[torch.Tensor] = None) 
     st = lib().tm_dgemv(_ptr(x), _ptr(W16), count, B, N, K, _ptr(y), _stream())
     _check("tm_dgemv", st)
     return y
+
+
+MIXER_HEADDIM = 64
+MIXER_DSTATE = 128
+
+
+def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.Tensor,
+               ssm_state: torch.Tensor, conv_w: torch.Tensor, conv_b: torch.Tensor,
+               dt_bias: torch.Tensor, A_log: torch.Tensor, D: torch.Tensor,
+               norm_w: torch.Tensor, eps: float = 1e-5, *,
+               workspace: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One Mamba-2 mixer decode step between the projections (tm_mixer_step):
+    zxbcdt float32 [B, Z] -> out bfloat16 [B, d_inner]; conv_state (float16
+    ring [B, conv_dim, 4]), conv_pos (int32 [1]) and ssm_state (float16
+    [B, nheads, 64, 128]) are updated in place."""
+    _need(zxbcdt, "zxbcdt", _F32, 2)
+    B = zxbcdt.shape[0]
+    _need(A_log, "A_log", _F32, 1)
+    H = A_log.shape[0]
+    P, N = MIXER_HEADDIM, MIXER_DSTATE
+    di, cd = H * P, H * P + 2 * N
+    dev = zxbcdt.device
+    _shape(zxbcdt, "zxbcdt", (B, 2 * di + 2 * N + H), dev)
+    _need(conv_state, "conv_state", _F16, 3)
+    _shape(conv_state, "conv_state", (B, cd, 4), dev)
+    _need(conv_pos, "conv_pos", (torch.int32,), 1)
+    _shape(conv_pos, "conv_pos", (1,), dev)
+    _need(ssm_state, "ssm_state", _F16, 4)
+    _shape(ssm_state, "ssm_state", (B, H, P, N), dev)
+    for t, name, shp in ((conv_w, "conv_w", (cd, 4)), (conv_b, "conv_b", (cd,)),
+                         (dt_bias, "dt_bias", (H,)), (D, "D", (H,)), (norm_w, "norm_w", (di,))):
+        _need(t, name, _F32, len(shp))
+        _shape(t, name, shp, dev)
+    if workspace is None:
+        workspace = torch.empty((B * (di + H),), dtype=torch.float32, device=dev)
+    _need(workspace, "workspace", _F32, 1)
+    if workspace.numel() < B * (di + H):
+        raise ValueError(f"workspace holds {workspace.numel()} floats, needs {B * (di + H)}")
+    if out is None:
+        out = torch.empty((B, di), dtype=torch.bfloat16, device=dev)
+    _need(out, "out", _BF16, 2)
+    _shape(out, "out", (B, di), dev)
+    st = lib().tm_mixer_step(_ptr(zxbcdt), B, H, P, N, _ptr(conv_state), _ptr(conv_pos),
+                             _ptr(ssm_state), _ptr(conv_w), _ptr(conv_b), _ptr(dt_bias),
+                             _ptr(A_log), _ptr(D), _ptr(norm_w), eps, _ptr(workspace), _ptr(out),
+                             _stream())
+    _check("tm_mixer_step", st)
+    return out
+
+
+def residual_rmsnorm(residual: torch.Tensor, y: Optional[torch.Tensor], w: torch.Tensor,
+                     eps: float = 1e-5, x: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """residual float32 [B, D] += y (if given); returns x = bf16(rmsnorm(residual) * w)."""
+    _need(residual, "residual", _F32, 2)
+    B, D = residual.shape
+    dev = residual.device
+    if y is not None:
+        _need(y, "y", _F32, 2)
+        _shape(y, "y", (B, D), dev)
+    _need(w, "w", _F32, 1)
+    _shape(w, "w", (D,), dev)
+    if x is None:
+        x = torch.empty((B, D), dtype=torch.bfloat16, device=dev)
+    _need(x, "x", _BF16, 2)
+    _shape(x, "x", (B, D), dev)
+    st = lib().tm_residual_rmsnorm(_ptr(residual), _ptr(y), B, D, _ptr(w), eps, _ptr(x),
+                                   _stream())
+    _check("tm_residual_rmsnorm", st)
+    return x

@@ -12,6 +12,9 @@ quality lost to ternarization).
   2-bit codes + float16 group scales for the ternary layers and float16
   weights for the kept ones, and one decode token over them
   (``tm_tgemv`` for the ternary layers, ``tm_dgemv`` for the kept ones).
+* ``Mamba2Decoder``: decode in layer order through whole Mamba-2 blocks
+  (pre-norm, in_proj, the FP16 mixer step of Sec. 3.2, out_proj), one token
+  capturable as a HIP graph (Sec. 8: batch-1 decode).
 
 Only argument marshalling and packing happen here; every product runs in
 the library's kernels.
@@ -151,3 +154,151 @@ class DecodeStack:
 
 
 __all__ = ["keep_first_last", "quantize_projections", "DecodeStack", "PROJECTIONS"]
+
+
+class Mamba2Decoder:
+    """Batch-B decode through L Mamba-2 blocks in layer order, every step on
+    the library's kernels:
+
+        x   = rmsnorm(residual += y_prev) * w_pre[l]      tm_residual_rmsnorm
+        zx  = in_proj(x)                                  tm_tgemv / tm_dgemv (kept)
+        m   = mixer step (conv, FP16 SSM, gated norm)     tm_mixer_step
+        y   = out_proj(m)                                 tm_tgemv / tm_dgemv (kept)
+
+    and after the last layer the residual takes y and the final norm gives
+    ``x_out`` (the lm head is outside).  Five to six launches per layer, all
+    on the current stream with fixed buffers, so a token can be captured once
+    as a HIP graph (``capture``) and replayed.
+
+    weight(kind, l) -> float32 [N, K] master weights (kind "in": [Z, d_model],
+    "out": [d_model, d_inner]); mixer(l) -> dict of float32 arrays conv_w,
+    conv_b, dt_bias, A_log, D, norm_w (see ops.mixer_step); pre_norm(l) ->
+    float32 [d_model].  Layers in ``keep`` stay in float16 (Sec. 7).
+    """
+
+    def __init__(self, weight: Callable[[str, int], torch.Tensor], mixer: Callable[[int], dict],
+                 pre_norm: Callable[[int], torch.Tensor], n_layers: int, d_model: int,
+                 nheads: int, keep: Iterable[int] = (), g: int = 128, eps: float = 1e-5,
+                 batch: int = 1, device: Optional[torch.device] = None):
+        dev = device or torch.device("cuda")
+        self.L, self.B, self.g, self.eps = n_layers, batch, g, eps
+        self.keep = set(keep)
+        self.d_model, self.nheads = d_model, nheads
+        P, N = ops.MIXER_HEADDIM, ops.MIXER_DSTATE
+        self.d_inner = nheads * P
+        self.Z = 2 * self.d_inner + 2 * N + nheads
+        conv_dim = self.d_inner + 2 * N
+        self.layers = []
+        for l in range(n_layers):
+            lay = {}
+            for kind, (n, k) in (("in", (self.Z, d_model)), ("out", (d_model, self.d_inner))):
+                w = weight(kind, l).contiguous()
+                if tuple(w.shape) != (n, k):
+                    raise ValueError(f"layer {l} {kind}_proj has shape {tuple(w.shape)}")
+                if l in self.keep:
+                    lay[kind] = ("dense", w.to(torch.float16)[None].contiguous())
+                else:
+                    codes = torch.empty((1, n, k // 4), dtype=torch.uint8, device=dev)
+                    s16 = torch.empty((1, n, k // g), dtype=torch.float16, device=dev)
+                    ops.ternarize_pack(w, g, eps, codes=codes[0], scales_f16=s16[0],
+                                       want_zero_count=False)
+                    lay[kind] = ("ternary", codes, s16)
+            prm = mixer(l)
+            lay["mixer"] = {k: (v if isinstance(v, torch.Tensor) else torch.from_numpy(v))
+                            .to(dev, torch.float32).contiguous() for k, v in prm.items()}
+            lay["pre"] = pre_norm(l).to(dev, torch.float32).contiguous()
+            lay["conv"] = torch.zeros((batch, conv_dim, 4), dtype=torch.float16, device=dev)
+            lay["pos"] = torch.zeros((1,), dtype=torch.int32, device=dev)
+            lay["ssm"] = torch.zeros((batch, nheads, P, N), dtype=torch.float16, device=dev)
+            self.layers.append(lay)
+        self.final_norm = torch.ones((d_model,), dtype=torch.float32, device=dev)
+        # token buffers (reused by every layer: the layers run one after another)
+        self.emb = torch.zeros((batch, d_model), dtype=torch.float32, device=dev)
+        self.residual = torch.zeros((batch, d_model), dtype=torch.float32, device=dev)
+        self.x = torch.empty((1, batch, d_model), dtype=torch.bfloat16, device=dev)
+        self.zx = torch.empty((1, batch, self.Z), dtype=torch.float32, device=dev)
+        self.m = torch.empty((1, batch, self.d_inner), dtype=torch.bfloat16, device=dev)
+        self.y = torch.empty((1, batch, d_model), dtype=torch.float32, device=dev)
+        self.ws = torch.empty((batch * (self.d_inner + nheads),), dtype=torch.float32,
+                              device=dev)
+        self.x_out = torch.empty((batch, d_model), dtype=torch.bfloat16, device=dev)
+        self.graph = None
+
+    def set_states(self, l: int, conv: torch.Tensor, ssm: torch.Tensor, pos: int = 0) -> None:
+        """Layer l's convolution ring (float16 [B, conv_dim, 4], slot (pos + j) % 4
+        the j-th oldest) and SSM state (float16 [B, nheads, 64, 128])."""
+        lay = self.layers[l]
+        lay["conv"].copy_(conv)
+        lay["ssm"].copy_(ssm)
+        lay["pos"].fill_(pos)
+
+    def _proj(self, lay, kind, x, y) -> None:
+        p = lay[kind]
+        if p[0] == "dense":
+            ops.dgemv(x, p[1], y=y)
+        else:
+            ops.tgemv(x, p[1], p[2], self.g, y=y)
+
+    def layer_step(self, l: int) -> None:
+        """Layer l of a token: pre-norm (taking the previous layer's output
+        into the residual), in_proj, mixer step, out_proj into ``y``."""
+        lay = self.layers[l]
+        if l == 0:
+            self.residual.copy_(self.emb)
+        ops.residual_rmsnorm(self.residual, None if l == 0 else self.y[0], lay["pre"], self.eps,
+                             x=self.x[0])
+        self._proj(lay, "in", self.x, self.zx)
+        mp = lay["mixer"]
+        ops.mixer_step(self.zx[0], lay["conv"], lay["pos"], lay["ssm"], mp["conv_w"],
+                       mp["conv_b"], mp["dt_bias"], mp["A_log"], mp["D"], mp["norm_w"], self.eps,
+                       workspace=self.ws, out=self.m[0])
+        self._proj(lay, "out", self.m, self.y)
+
+    def token(self) -> torch.Tensor:
+        """One decode token from ``emb`` (float32 [B, d_model]) through every
+        layer; returns ``x_out`` = final norm of the residual (bfloat16)."""
+        for l in range(self.L):
+            self.layer_step(l)
+        ops.residual_rmsnorm(self.residual, self.y[0], self.final_norm, self.eps, x=self.x_out)
+        return self.x_out
+
+    def capture(self) -> None:
+        """Record one token (all layers) as a HIP graph on a side stream."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            with torch.cuda.graph(self.graph, stream=side):
+                self.token()
+        torch.cuda.current_stream().wait_stream(side)
+
+    def replay(self) -> torch.Tensor:
+        if self.graph is None:
+            raise RuntimeError("capture() first")
+        self.graph.replay()
+        return self.x_out
+
+    def launches_per_token(self) -> int:
+        return 5 * self.L + 1 + 1   # pre-norm, in_proj, mixer (2), out_proj per layer; copy, final norm
+
+    def bytes_per_token(self) -> float:
+        """Algorithmic HBM bytes of one token: packed or float16 projection
+        weights, both SSM/conv state passes (read + write), mixer parameters
+        and the activations, per batch of B tokens."""
+        total = 0.0
+        P, N = ops.MIXER_HEADDIM, ops.MIXER_DSTATE
+        for l, lay in enumerate(self.layers):
+            for kind in ("in", "out"):
+                p = lay[kind]
+                total += p[1].numel() * p[1].element_size()
+                if p[0] == "ternary":
+                    total += p[2].numel() * 2
+            total += 2 * self.B * self.nheads * P * N * 2          # SSM state read + write
+            total += self.B * (self.d_inner + 2 * N) * 4 * 2       # conv ring read, new slot
+            total += sum(v.numel() * 4 for v in lay["mixer"].values()) + self.d_model * 4
+            total += self.B * (4 * self.Z + 2 * self.Z + 4 * self.d_inner + 2 * self.d_inner
+                               + 12 * self.d_model)                # activations, roughly
+        return total
+
+
+__all__.append("Mamba2Decoder")

@@ -109,3 +109,38 @@ DECODE_OUT = Config("decode_out_proj", D_MODEL, D_INNER, 1, 128, False)
 
 def decode_seed(kind: str, layer: int) -> int:
     return {"in_w": 1000, "out_w": 2000, "in_x": 3000, "out_x": 4000}[kind] + layer
+
+
+# Mamba-2 mixer parameters and states for the decode step between the
+# projections (64 heads of 64 channels, d_state 128, d_conv 4):
+#   conv taps and bias U(-1/2, 1/2); step sizes dt log-uniform in
+#   [1e-3, 1e-1] stored as dt_bias = softplus^-1(dt); A_log = log U(1, 16);
+#   D = 1; norm weight 1 + N(0, 0.1); conv state N(0, 1) and SSM state
+#   N(0, 0.5), both rounded to float16.
+HEADDIM, D_STATE, D_CONV = 64, 128, 4
+
+
+def mixer_params(rng: np.random.Generator, nheads: int):
+    d_inner = nheads * HEADDIM
+    conv_dim = d_inner + 2 * D_STATE
+    dt = np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), nheads))
+    return dict(
+        conv_w=rng.uniform(-0.5, 0.5, (conv_dim, D_CONV)).astype(np.float32),
+        conv_b=rng.uniform(-0.5, 0.5, conv_dim).astype(np.float32),
+        dt_bias=(dt + np.log(-np.expm1(-dt))).astype(np.float32),
+        A_log=np.log(rng.uniform(1.0, 16.0, nheads)).astype(np.float32),
+        D=np.ones(nheads, np.float32),
+        norm_w=(1.0 + 0.1 * rng.standard_normal(d_inner)).astype(np.float32))
+
+
+def mixer_states(rng: np.random.Generator, B: int, nheads: int):
+    d_inner = nheads * HEADDIM
+    conv_dim = d_inner + 2 * D_STATE
+    return (rng.standard_normal((B, conv_dim, D_CONV)).astype(np.float16),
+            (0.5 * rng.standard_normal((B, nheads, HEADDIM, D_STATE))).astype(np.float16))
+
+
+def in_proj_out(rng: np.random.Generator, B: int, nheads: int) -> np.ndarray:
+    """A float32 stand-in for in_proj's output [B, 2 d_inner + 2 d_state + nheads]."""
+    d_inner = nheads * HEADDIM
+    return rng.standard_normal((B, 2 * d_inner + 2 * D_STATE + nheads)).astype(np.float32)

@@ -50,4 +50,15 @@ hipError_t launch_dgemv(const uint16_t*, const uint16_t*, int, int, int64_t, int
   reached("dgemv");
 }
 
+hipError_t launch_mixer_step(const float*, int, int, uint16_t*, int*, uint16_t*, const float*,
+                             const float*, const float*, const float*, const float*, const float*,
+                             float, float*, uint16_t*, hipStream_t) {
+  reached("mixer_step");
+}
+
+hipError_t launch_residual_rmsnorm(float*, const float*, int, int64_t, const float*, float,
+                                   uint16_t*, hipStream_t) {
+  reached("residual_rmsnorm");
+}
+
 }  // namespace tmk

@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 5
+    assert L.tm_abi_version() == 7
 
 
 def test_status_strings(L):
@@ -189,6 +189,47 @@ def test_dgemv_validation(L):
     assert dg(L, y=P + 2 ** 28 + 2) == EALIGN
     assert dg(L, y=P + 2048) == EINVAL           # y overlaps x
     assert dg(L, y=P + 2 ** 24 + 4096) == EINVAL  # y overlaps W
+
+
+def mx(L, z=P, B=1, H=64, hd=64, ds=128, cs=P + 2 ** 20, pos=P + 2 ** 21, ss=P + 2 ** 22,
+       cw=P + 2 ** 24, cb=P + 2 ** 25, dtb=P + 2 ** 26, al=P + 2 ** 26 + 4096,
+       D=P + 2 ** 26 + 8192, nw=P + 2 ** 27, eps=1e-5, ws=P + 2 ** 28, out=P + 2 ** 29):
+    return L.tm_mixer_step(z, B, H, hd, ds, cs, pos, ss, cw, cb, dtb, al, D, nw, eps, ws, out,
+                           None)
+
+
+def test_mixer_step_validation(L):
+    for kw in ("z", "cs", "pos", "ss", "cw", "cb", "dtb", "al", "D", "nw", "ws", "out"):
+        assert mx(L, **{kw: 0}) == EINVAL, kw
+    assert mx(L, eps=-1.0) == EINVAL
+    assert mx(L, B=0) == ESHAPE
+    assert mx(L, H=0) == ESHAPE
+    assert mx(L, hd=32) == ESHAPE
+    assert mx(L, ds=64) == ESHAPE
+    assert mx(L, ss=P + 2 ** 22 + 8) == EALIGN
+    assert mx(L, pos=P + 2 ** 21 + 2) == EALIGN
+    assert mx(L, out=P + 2 ** 29 + 1) == EALIGN
+    assert mx(L, ss=P + 2 ** 20 + 64) == EINVAL           # SSM state over the conv state
+    assert mx(L, out=P + 2 ** 22) == EINVAL               # out over the SSM state
+    assert mx(L, ws=P + 16) == EINVAL                     # workspace over zxbcdt
+    assert mx(L, pos=P + 2 ** 24 + 64) == EINVAL          # conv_pos inside conv_w
+
+
+def rn(L, r=P, y=P + 2 ** 20, B=2, D=2048, w=P + 2 ** 21, eps=1e-5, x=P + 2 ** 22):
+    return L.tm_residual_rmsnorm(r, y, B, D, w, eps, x, None)
+
+
+def test_residual_rmsnorm_validation(L):
+    for kw in ("r", "w", "x"):
+        assert rn(L, **{kw: 0}) == EINVAL, kw
+    assert rn(L, eps=float("inf")) == EINVAL
+    assert rn(L, B=0) == ESHAPE
+    assert rn(L, D=0) == ESHAPE
+    assert rn(L, r=P + 2) == EALIGN
+    assert rn(L, x=P + 2 ** 22 + 1) == EALIGN
+    assert rn(L, x=P + 64) == EINVAL          # x over the residual
+    assert rn(L, y=P + 4096) == EINVAL        # y over the residual
+    assert rn(L, w=P + 2 ** 22 + 64) == EINVAL  # w over x
 
 
 def fwd(L, X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128, Y=P + 2 ** 26):

@@ -196,3 +196,15 @@ def test_planted_mixer_mistakes_are_caught(mutant, monkeypatch):
         except AssertionError:
             caught = True
     assert caught, f"mutant {mutant} escaped the pins"
+
+
+def test_rmsnorm_closed_forms():
+    # a constant row c: every output is sign(c) * w (eps = 0)
+    w = np.array([0.5, 2.0, -1.0, 3.0])
+    np.testing.assert_allclose(MB.rmsnorm(np.full((1, 4), -7.5), w, 0.0), [-w], rtol=1e-15)
+    # [3, 4, 0, 0]: mean square 25/4, scale 2/5
+    np.testing.assert_allclose(MB.rmsnorm(np.array([[3.0, 4.0, 0.0, 0.0]]), np.ones(4), 0.0),
+                               [[1.2, 1.6, 0.0, 0.0]], rtol=1e-15)
+    # eps enters under the root: [1, 1] with eps 3 -> 1/2
+    np.testing.assert_allclose(MB.rmsnorm(np.ones((1, 2)), np.ones(2), 3.0), [[0.5, 0.5]],
+                               rtol=1e-15)
