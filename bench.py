@@ -62,11 +62,11 @@ def parse():
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants, "
-                         "per_layer, small, sweep, mixed (keeps a profiler trace to the kernels "
+                         "per_layer, small, sweep, mixed, blocks (keeps a profiler trace to the kernels "
                          "of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
-    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed"}
+    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed", "blocks"}
     if bad:
         ap.error(f"unknown --skip sections: {sorted(bad)}")
     return args
@@ -246,6 +246,12 @@ def main():
     per_layer = (None if "per_layer" in args.skip
                  else decode_per_layer(ops, dec, L, max(args.steps, 10)))
     mixed = None if "mixed" in args.skip else decode_mixed_stack(dev, max(args.steps // 4, 3))
+    blocks = None
+    if "blocks" not in args.skip:
+        from paper_2606_18114_amd.stack import keep_first_last
+        blocks = {"all_ternary": decode_mamba2_blocks(dev, args.steps),
+                  "first_last_2_fp16": decode_mamba2_blocks(
+                      dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2))}
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
@@ -350,6 +356,7 @@ def main():
         "qat_block": qat_block,
         "decode_per_layer": per_layer,
         "decode_mixed_fp16_blocks": mixed,
+        "decode_mamba2_blocks_layer_order": blocks,
         "qat_block_bf16_out": qat_block_bf16,
         "variants": variants,
         "cold_vs_warm": {k: v for k, v in cold.items() if not k.startswith("decode_")},
@@ -689,6 +696,62 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
                        f"({fl / 1e9:.0f} GFLOP each); batch-1 decode token over {nmat} matrices "
                        f"{t['gemv']:.2f}s ({gemv_bytes / t['gemv'] / 1e9:.3f} GB/s of packed weights)")}
     return base, par, codes_cmp
+
+
+def decode_mamba2_blocks(dev, tokens, keep=(), batch=1):
+    """Decode as a model runs it: 48 whole Mamba-2 blocks in layer order, each
+    pre-norm -> in_proj -> mixer step (convolution, FP16 SSM state update,
+    gated RMSNorm) -> out_proj, then the final norm: 5 launches per layer plus
+    2, timed eagerly (one Python call per launch) and as one captured HIP
+    graph per token.  States persist from token to token."""
+    import torch
+    from paper_2606_18114_amd import synth
+    from paper_2606_18114_amd.stack import Mamba2Decoder
+
+    cfg = {"in": synth.DECODE_IN, "out": synth.DECODE_OUT}
+    L, H = synth.N_LAYERS, synth.D_INNER // synth.HEADDIM
+    rng = np.random.default_rng(5000)
+    mix = [synth.mixer_params(rng, H) for _ in range(L)]
+    dec = Mamba2Decoder(
+        lambda k, l: torch.from_numpy(synth.layer_weight(cfg[k], synth.decode_seed(f"{k}_w", l))
+                                      ).to(dev),
+        lambda l: mix[l], lambda l: torch.ones(synth.D_MODEL), L, synth.D_MODEL, H,
+        keep=keep, g=128, batch=batch, device=dev)
+    for l in range(L):
+        conv, ssm = synth.mixer_states(rng, batch, H)
+        dec.set_states(l, torch.from_numpy(conv).to(dev), torch.from_numpy(ssm).to(dev))
+    dec.emb.copy_(torch.from_numpy(rng.standard_normal((batch, synth.D_MODEL))
+                                   .astype(np.float32)).to(dev))
+
+    def timed(fn, n):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    n = max(tokens, 10)
+    us_eager = timed(dec.token, n)
+    dec.capture()
+    us_graph = timed(dec.replay, n)
+    nb = dec.bytes_per_token()
+    res = {"layers": L, "kept_fp16_layers": sorted(dec.keep), "batch": batch,
+           "launches_per_token": dec.launches_per_token(), "bytes_per_token": nb,
+           "us_per_token_eager": round(us_eager, 2), "us_per_token_graph": round(us_graph, 2),
+           "GBps_graph": round(nb / (us_graph * 1e-6) / 1e9, 1),
+           "frac_hbm_graph": round(nb / (us_graph * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+           "what": "48 Mamba-2 1.3B blocks in layer order (pre-norm, in_proj 8512x2048, "
+                   "conv + FP16 SSM state + gated RMSNorm, out_proj 2048x4096) + final norm, "
+                   "one token, states carried over"}
+    del dec
+    torch.cuda.empty_cache()
+    return res
 
 
 def decode_mixed_stack(dev, tokens, batch=1):

@@ -250,11 +250,14 @@ tm_status tm_residual_rmsnorm(float* residual, const float* y, int32_t B, int64_
  *   dt_bias, A_log, D  float32 [nheads];  norm_w  float32 [d_inner]
  *   eps         float32, finite, >= 0
  *   workspace   float32 [B * (d_inner + nheads)]  scratch owned by the caller
+ *               (4-byte aligned): the gated values and per-head sums of
+ *               squares between the two launches
  *   out         bfloat16 bits [B, d_inner]  out: out_proj's input
- * Two launches on `stream` (the step, then the normalization, which also
- * advances conv_pos).  The state arrays, conv_pos, workspace and out must
- * not overlap each other or the inputs; calls that share state must not
- * run concurrently.
+ * Two launches on `stream`: the step (a workgroup per head and token), then
+ * the normalization (a workgroup per token), which also advances conv_pos.
+ * The state arrays, conv_pos, workspace and out must not overlap each other
+ * or the inputs; calls that share state or workspace must not run
+ * concurrently.
  */
 tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
                         int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,

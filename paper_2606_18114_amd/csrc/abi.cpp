@@ -73,6 +73,45 @@ tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float
       tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, es == 2, to_hip(stream)));
 }
 
+// argument checks of the mixer step; workspace NULL: the library's own
+// scratch array (no overlap check needed: no caller array can overlap it)
+tm_status mixer_checked(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                        int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                        uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                        const float* dt_bias, const float* A_log, const float* D,
+                        const float* norm_w, float eps, float* workspace, uint16_t* out) {
+  if (!zxbcdt || !conv_state || !conv_pos || !ssm_state || !conv_w || !conv_b || !dt_bias ||
+      !A_log || !D || !norm_w || !out)
+    return TM_EINVAL;
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (B < 1 || B > 65535 || nheads < 1 || nheads > 4096 || headdim != 64 || d_state != 128)
+    return TM_ESHAPE;
+  const int64_t di = (int64_t)nheads * headdim, cd = di + 2 * (int64_t)d_state;
+  const int64_t zw = 2 * di + 2 * (int64_t)d_state + nheads;
+  int64_t zb, cb, sb, wb, ob;
+  if (!bytes_of(B, zw, 4, &zb) || !bytes_of((int64_t)B * cd, 4, 2, &cb) ||
+      !bytes_of((int64_t)B * nheads * headdim, d_state, 2, &sb) ||
+      !bytes_of(B, di + nheads, 4, &wb) || !bytes_of(B, di, 2, &ob))
+    return TM_ESHAPE;
+  if (!aligned(zxbcdt, 4) || !aligned(conv_state, 2) || !aligned(conv_pos, 4) ||
+      !aligned(ssm_state, 16) || !aligned(conv_w, 4) || !aligned(conv_b, 4) ||
+      !aligned(dt_bias, 4) || !aligned(A_log, 4) || !aligned(D, 4) || !aligned(norm_w, 4) ||
+      !aligned(workspace, 4) || !aligned(out, 2))
+    return TM_EALIGN;
+  const Span outs[5] = {span(conv_state, cb), span(conv_pos, 4), span(ssm_state, sb),
+                        span(workspace, workspace ? wb : 0), span(out, ob)};
+  const Span ins[7] = {span(zxbcdt, zb), span(conv_w, cd * 16), span(conv_b, cd * 4),
+                       span(dt_bias, (int64_t)nheads * 4), span(A_log, (int64_t)nheads * 4),
+                       span(D, (int64_t)nheads * 4), span(norm_w, di * 4)};
+  for (int i = 0; i < 5; ++i) {
+    for (int j = i + 1; j < 5; ++j)
+      if (overlap(outs[i], outs[j])) return TM_EINVAL;
+    for (const Span& in : ins)
+      if (overlap(outs[i], in)) return TM_EINVAL;
+  }
+  return TM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -274,60 +313,14 @@ tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                         const float* dt_bias, const float* A_log, const float* D,
                         const float* norm_w, float eps, float* workspace, uint16_t* out,
                         tm_stream stream) {
-  if (!zxbcdt || !conv_state || !conv_pos || !ssm_state || !conv_w || !conv_b || !dt_bias ||
-      !A_log || !D || !norm_w || !workspace || !out)
-    return TM_EINVAL;
-  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
-  if (B < 1 || B > 65535 || nheads < 1 || nheads > 4096 || headdim != 64 || d_state != 128)
-    return TM_ESHAPE;
-  const int64_t di = (int64_t)nheads * headdim, cd = di + 2 * (int64_t)d_state;
-  const int64_t zw = 2 * di + 2 * (int64_t)d_state + nheads;
-  int64_t zb, cb, sb, wb, ob;
-  if (!bytes_of(B, zw, 4, &zb) || !bytes_of((int64_t)B * cd, 4, 2, &cb) ||
-      !bytes_of((int64_t)B * nheads * headdim, d_state, 2, &sb) ||
-      !bytes_of(B, di + nheads, 4, &wb) || !bytes_of(B, di, 2, &ob))
-    return TM_ESHAPE;
-  if (!aligned(zxbcdt, 4) || !aligned(conv_state, 2) || !aligned(conv_pos, 4) ||
-      !aligned(ssm_state, 16) || !aligned(conv_w, 4) || !aligned(conv_b, 4) ||
-      !aligned(dt_bias, 4) || !aligned(A_log, 4) || !aligned(D, 4) || !aligned(norm_w, 4) ||
-      !aligned(workspace, 4) || !aligned(out, 2))
-    return TM_EALIGN;
-  const Span outs[5] = {span(conv_state, cb), span(conv_pos, 4), span(ssm_state, sb),
-                        span(workspace, wb), span(out, ob)};
-  const Span ins[7] = {span(zxbcdt, zb), span(conv_w, cd * 16), span(conv_b, cd * 4),
-                       span(dt_bias, (int64_t)nheads * 4), span(A_log, (int64_t)nheads * 4),
-                       span(D, (int64_t)nheads * 4), span(norm_w, di * 4)};
-  for (int i = 0; i < 5; ++i) {
-    for (int j = i + 1; j < 5; ++j)
-      if (overlap(outs[i], outs[j])) return TM_EINVAL;
-    for (const Span& in : ins)
-      if (overlap(outs[i], in)) return TM_EINVAL;
-  }
+  if (!workspace) return TM_EINVAL;
+  if (tm_status st = mixer_checked(zxbcdt, B, nheads, headdim, d_state, conv_state, conv_pos,
+                                   ssm_state, conv_w, conv_b, dt_bias, A_log, D, norm_w, eps,
+                                   workspace, out))
+    return st;
   return hip_status(tmk::launch_mixer_step(zxbcdt, B, nheads, conv_state, conv_pos, ssm_state,
                                            conv_w, conv_b, dt_bias, A_log, D, norm_w, eps,
                                            workspace, out, to_hip(stream)));
-}
-
-tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
-                   int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
-                   tm_stream stream) {
-  if (!x || !codes || !scales_f16 || !y) return TM_EINVAL;
-  if (count < 1 || count > 65535 || B < 1 || B > 16 || N < 1) return TM_ESHAPE;
-  if (tm_status st = shape_kg(K, g)) return st;
-  int64_t cbm, sbm, xb, cb, sb, yb, ybm;
-  if (!bytes_of(N, K / 4, 1, &cbm) || !bytes_of(N, K / g, 2, &sbm) ||
-      !bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of(count, cbm, 1, &cb) ||
-      !bytes_of(count, sbm, 1, &sb) || !bytes_of((int64_t)B, N, 4, &ybm) ||
-      !bytes_of(count, ybm, 1, &yb))
-    return TM_ESHAPE;
-  if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
-  if (cbm > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside one matrix
-  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
-    return TM_EALIGN;
-  const Span o = span(y, yb);
-  if (overlap(o, span(x, xb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales_f16, sb)))
-    return TM_EINVAL;
-  return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
 }
 
 }  // extern "C"

@@ -9,9 +9,12 @@
 //     arithmetic, rounded once to float16 when stored);
 //   * y[p] = sum_n state[p, n] C[n] + D x[p];  g = y * SiLU(z);
 //   * g (float32) and the head's sum of g^2 go to the workspace.
+// The head's SSM state is loaded at the start, so its memory latency
+// overlaps the convolution.
 // Kernel 2, one workgroup per batch row: the gated RMSNorm over all d_inner
 // channels, out = bf16(g / sqrt(mean(g^2) + eps) * w), the bfloat16 input
-// of out_proj; and the convolution ring position advances.
+// of out_proj (the per-head partial sums meet in a wave butterfly); and the
+// convolution ring position advances.
 //
 // Convolution state: a ring of 4 float16 slots per channel; the window of a
 // step, oldest first, is slots (pos + 1 .. pos + 3) % 4 and the new input,
@@ -56,6 +59,13 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   const int pos = conv_pos[0] & 3;
   __shared__ float u[kMxP + 2 * kMxN];  // x of the head, then B, then C (after SiLU)
   __shared__ float wsum[kMxThreads / 64];
+  // thread t: channel p = t / 4, states n = 32 (t % 4) .. + 31; its 64 bytes
+  // of state are loaded first
+  const int p = tid >> 2, q = tid & 3;
+  uint16_t* sp = ssm + (((int64_t)b * nheads + h) * kMxP + p) * kMxN + 32 * q;
+  u32x4 sv[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) sv[k] = ld16(sp + 8 * k);
 
   // convolution: local channel i < 64 is x channel 64 h + i, then the B/C
   // channels d_inner + (i - 64)
@@ -76,16 +86,12 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
 
   const float dtp = mx_softplus(row[2 * d_inner + 2 * kMxN + h] + dt_bias[h]);
   const float a = expf(-dtp * expf(A_log[h]));
-  // thread t: channel p = t / 4, states n = 32 (t % 4) .. + 31
-  const int p = tid >> 2, q = tid & 3;
   const float xp = u[p];
   const float dx = dtp * xp;
-  uint16_t* sp = ssm + (((int64_t)b * nheads + h) * kMxP + p) * kMxN + 32 * q;
   float y = 0.f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const u32x4 v = ld16(sp + 8 * k);
-    const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+    const uint32_t wv[4] = {sv[k].x, sv[k].y, sv[k].z, sv[k].w};
     uint32_t o[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
@@ -118,27 +124,32 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
     partial[(int64_t)b * nheads + h] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
 }
 
-// grid (B); out[b, i] = bf16(g[b, i] * rsqrt(sum_h partial[b, h] / d_inner + eps) * w[i])
+// grid (B); out[b, i] = bf16(g[b, i] / sqrt(sum_h partial[b, h] / d_inner + eps) * w[i])
 __global__ __launch_bounds__(kMxThreads) void mixer_norm_kernel(
     const float* __restrict__ gated, const float* __restrict__ partial, int nheads,
     const float* __restrict__ norm_w, float eps, uint16_t* __restrict__ out,
     int* __restrict__ conv_pos) {
   const int b = blockIdx.x;
+  const int tid = threadIdx.x;
   const int d_inner = nheads * kMxP;
-  __shared__ float r_sh;
-  if (threadIdx.x == 0) {
-    float s = 0.f;
-    for (int h = 0; h < nheads; ++h) s += partial[(int64_t)b * nheads + h];  // fixed order
-    r_sh = 1.f / sqrtf(s / (float)d_inner + eps);
-  }
+  __shared__ float wsum[kMxThreads / 64];
+  float s2 = 0.f;
+  for (int h = tid; h < nheads; h += kMxThreads) s2 += partial[(int64_t)b * nheads + h];
+  s2 += __uint_as_float(lane_xchg<1>(__float_as_uint(s2)));
+  s2 += __uint_as_float(lane_xchg<2>(__float_as_uint(s2)));
+  s2 += __uint_as_float(lane_xchg<4>(__float_as_uint(s2)));
+  s2 += __uint_as_float(lane_xchg<8>(__float_as_uint(s2)));
+  s2 += __uint_as_float(lane_xchg<16>(__float_as_uint(s2)));
+  s2 += __uint_as_float(lane_xchg<32>(__float_as_uint(s2)));
+  if ((tid & 63) == 0) wsum[tid >> 6] = s2;
   __syncthreads();
-  const float r = r_sh;
-  for (int i = threadIdx.x; i < d_inner; i += kMxThreads) {
+  const float r = 1.f / sqrtf(((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) / (float)d_inner + eps);
+  for (int i = tid; i < d_inner; i += kMxThreads) {
     const float v = gated[(int64_t)b * d_inner + i] * r * norm_w[i];
     const uint32_t bits = __float_as_uint(v);
     out[(int64_t)b * d_inner + i] = (uint16_t)((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16);
   }
-  if (b == 0 && threadIdx.x == 0) conv_pos[0] = (conv_pos[0] + 1) & 3;
+  if (b == 0 && tid == 0) conv_pos[0] = (conv_pos[0] + 1) & 3;
 }
 
 // grid (B): residual[b] += y[b] (y may be null), then
@@ -146,18 +157,31 @@ __global__ __launch_bounds__(kMxThreads) void mixer_norm_kernel(
 __global__ __launch_bounds__(kMxThreads) void residual_rmsnorm_kernel(
     float* __restrict__ residual, const float* __restrict__ y, int64_t D,
     const float* __restrict__ w, float eps, uint16_t* __restrict__ x) {
+  constexpr int kReg = 16;  // values kept in registers per thread (D <= 4096)
   const int b = blockIdx.x;
   float* r = residual + (int64_t)b * D;
   const float* yy = y ? y + (int64_t)b * D : nullptr;
   __shared__ float wsum[kMxThreads / 64];
+  float v[kReg];
   float sq = 0.f;
-  for (int64_t i = threadIdx.x; i < D; i += kMxThreads) {
-    float v = r[i];
+#pragma unroll
+  for (int j = 0; j < kReg; ++j) {
+    const int64_t i = threadIdx.x + (int64_t)j * kMxThreads;
+    v[j] = i < D ? r[i] + (yy ? yy[i] : 0.f) : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < kReg; ++j) {
+    const int64_t i = threadIdx.x + (int64_t)j * kMxThreads;
+    if (yy && i < D) r[i] = v[j];
+    sq = __builtin_fmaf(v[j], v[j], sq);
+  }
+  for (int64_t i = threadIdx.x + (int64_t)kReg * kMxThreads; i < D; i += kMxThreads) {
+    float t = r[i];
     if (yy) {
-      v += yy[i];
-      r[i] = v;
+      t += yy[i];
+      r[i] = t;
     }
-    sq = __builtin_fmaf(v, v, sq);
+    sq = __builtin_fmaf(t, t, sq);
   }
   sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
   sq += __uint_as_float(lane_xchg<2>(__float_as_uint(sq)));
@@ -168,10 +192,16 @@ __global__ __launch_bounds__(kMxThreads) void residual_rmsnorm_kernel(
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
   __syncthreads();
   const float scale = 1.f / sqrtf(((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) / (float)D + eps);
-  for (int64_t i = threadIdx.x; i < D; i += kMxThreads) {
-    const uint32_t bits = __float_as_uint(r[i] * scale * w[i]);
+  auto put = [&](int64_t i, float t) {
+    const uint32_t bits = __float_as_uint(t * scale * w[i]);
     x[(int64_t)b * D + i] = (uint16_t)((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16);
+  };
+#pragma unroll
+  for (int j = 0; j < kReg; ++j) {
+    const int64_t i = threadIdx.x + (int64_t)j * kMxThreads;
+    if (i < D) put(i, v[j]);
   }
+  for (int64_t i = threadIdx.x + (int64_t)kReg * kMxThreads; i < D; i += kMxThreads) put(i, r[i]);
 }
 
 hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,

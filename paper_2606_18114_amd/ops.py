@@ -355,6 +355,12 @@ MIXER_HEADDIM = 64
 MIXER_DSTATE = 128
 
 
+def mixer_workspace(B: int, nheads: int, device) -> torch.Tensor:
+    """Scratch for mixer_step: the gated values and per-head sums of squares."""
+    return torch.empty((B * (nheads * MIXER_HEADDIM + nheads),), dtype=torch.float32,
+                       device=device)
+
+
 def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.Tensor,
                ssm_state: torch.Tensor, conv_w: torch.Tensor, conv_b: torch.Tensor,
                dt_bias: torch.Tensor, A_log: torch.Tensor, D: torch.Tensor,
@@ -384,7 +390,7 @@ def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.T
         _need(t, name, _F32, len(shp))
         _shape(t, name, shp, dev)
     if workspace is None:
-        workspace = torch.empty((B * (di + H),), dtype=torch.float32, device=dev)
+        workspace = mixer_workspace(B, H, dev)
     _need(workspace, "workspace", _F32, 1)
     if workspace.numel() < B * (di + H):
         raise ValueError(f"workspace holds {workspace.numel()} floats, needs {B * (di + H)}")

@@ -166,7 +166,7 @@ class Mamba2Decoder:
         y   = out_proj(m)                                 tm_tgemv / tm_dgemv (kept)
 
     and after the last layer the residual takes y and the final norm gives
-    ``x_out`` (the lm head is outside).  Five to six launches per layer, all
+    ``x_out`` (the lm head is outside).  Five launches per layer, all
     on the current stream with fixed buffers, so a token can be captured once
     as a HIP graph (``capture``) and replayed.
 
@@ -219,8 +219,7 @@ class Mamba2Decoder:
         self.zx = torch.empty((1, batch, self.Z), dtype=torch.float32, device=dev)
         self.m = torch.empty((1, batch, self.d_inner), dtype=torch.bfloat16, device=dev)
         self.y = torch.empty((1, batch, d_model), dtype=torch.float32, device=dev)
-        self.ws = torch.empty((batch * (self.d_inner + nheads),), dtype=torch.float32,
-                              device=dev)
+        self.ws = ops.mixer_workspace(batch, nheads, dev)
         self.x_out = torch.empty((batch, d_model), dtype=torch.bfloat16, device=dev)
         self.graph = None
 
