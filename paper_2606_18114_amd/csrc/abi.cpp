@@ -323,4 +323,26 @@ tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                                            workspace, out, to_hip(stream)));
 }
 
+tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
+                   int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
+                   tm_stream stream) {
+  if (!x || !codes || !scales_f16 || !y) return TM_EINVAL;
+  if (count < 1 || count > 65535 || B < 1 || B > 16 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t cbm, sbm, xb, cb, sb, yb, ybm;
+  if (!bytes_of(N, K / 4, 1, &cbm) || !bytes_of(N, K / g, 2, &sbm) ||
+      !bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of(count, cbm, 1, &cb) ||
+      !bytes_of(count, sbm, 1, &sb) || !bytes_of((int64_t)B, N, 4, &ybm) ||
+      !bytes_of(count, ybm, 1, &yb))
+    return TM_ESHAPE;
+  if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
+  if (cbm > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside one matrix
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
+    return TM_EALIGN;
+  const Span o = span(y, yb);
+  if (overlap(o, span(x, xb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales_f16, sb)))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
+}
+
 }  // extern "C"
