@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 7
+#define TM_ABI_VERSION 8
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -265,6 +265,26 @@ tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                         const float* dt_bias, const float* A_log, const float* D,
                         const float* norm_w, float eps, float* workspace, uint16_t* out,
                         tm_stream stream);
+
+/*
+ * tm_mixer_step_noalloc — tm_mixer_step for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses
+ * that forbid hipMalloc): the same computation and kernels, with the
+ * workspace taken from a file-scope device array of the library instead of
+ * an argument.  That array holds B * (d_inner + nheads) <= 16 * (8192 + 128)
+ * floats (larger calls return TM_ESHAPE); each GPU the library runs on has
+ * its own copy, kept until the process ends, whose address is looked up
+ * once per device on the first call.  The call allocates nothing.  Every
+ * call on a GPU shares that GPU's array: calls on one GPU that overlap in
+ * time (different streams, host threads) race on it and must be serialized
+ * by the caller.  All other arguments, checks and results as tm_mixer_step.
+ */
+tm_status tm_mixer_step_noalloc(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                                int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                                uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                                const float* dt_bias, const float* A_log, const float* D,
+                                const float* norm_w, float eps, uint16_t* out,
+                                tm_stream stream);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

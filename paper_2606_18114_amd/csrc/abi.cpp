@@ -323,6 +323,23 @@ tm_status tm_mixer_step(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                                            workspace, out, to_hip(stream)));
 }
 
+tm_status tm_mixer_step_noalloc(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                                int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                                uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                                const float* dt_bias, const float* A_log, const float* D,
+                                const float* norm_w, float eps, uint16_t* out,
+                                tm_stream stream) {
+  if (tm_status st = mixer_checked(zxbcdt, B, nheads, headdim, d_state, conv_state, conv_pos,
+                                   ssm_state, conv_w, conv_b, dt_bias, A_log, D, norm_w, eps,
+                                   nullptr, out))
+    return st;
+  if ((int64_t)B * ((int64_t)nheads * headdim + nheads) > tmk::mixer_scratch_floats())
+    return TM_ESHAPE;
+  return hip_status(tmk::launch_mixer_step_noalloc(zxbcdt, B, nheads, conv_state, conv_pos,
+                                                   ssm_state, conv_w, conv_b, dt_bias, A_log, D,
+                                                   norm_w, eps, out, to_hip(stream)));
+}
+
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
                    int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
                    tm_stream stream) {

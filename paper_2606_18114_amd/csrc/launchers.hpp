@@ -65,6 +65,15 @@ hipError_t launch_mixer_step(const float* zxbcdt, int B, int nheads, uint16_t* c
                              const float* D, const float* norm_w, float eps, float* workspace,
                              uint16_t* out, hipStream_t stream);
 
+// the same with the workspace in a file-scope device array of
+// mixer_scratch_floats() floats (hipErrorInvalidValue when it does not fit)
+int64_t mixer_scratch_floats();
+hipError_t launch_mixer_step_noalloc(const float* zxbcdt, int B, int nheads,
+                                     uint16_t* conv_state, int* conv_pos, uint16_t* ssm_state,
+                                     const float* conv_w, const float* conv_b,
+                                     const float* dt_bias, const float* A_log, const float* D,
+                                     const float* norm_w, float eps, uint16_t* out,
+                                     hipStream_t stream);
 // residual += y (y may be null); x = bf16(rmsnorm(residual) * w), B rows of D
 hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,
                                    const float* w, float eps, uint16_t* x, hipStream_t stream);

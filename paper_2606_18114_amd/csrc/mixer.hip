@@ -22,6 +22,8 @@
 // B/C channels' window, so no workgroup may shift it in place while others
 // still read: the ring writes only the slot nobody reads, and the position
 // moves on in kernel 2, after every workgroup of kernel 1 is done.
+#include <atomic>
+
 #include "common.hpp"
 #include "launchers.hpp"
 
@@ -226,6 +228,40 @@ hipError_t launch_mixer_step(const float* zxbcdt, int B, int nheads, uint16_t* c
   hipLaunchKernelGGL(mixer_norm_kernel, dim3((unsigned)B), dim3(kMxThreads), 0, stream, gated,
                      partial, nheads, norm_w, eps, out, conv_pos);
   return hipGetLastError();
+}
+
+// Allocation-free variant: the workspace is a file-scope device array (one
+// copy per GPU, kept until the process ends).  Host code never passes the
+// array's name to a kernel: its device address is looked up once per device
+// with hipGetSymbolAddress (with that device current) and cached.
+constexpr int64_t kMixerScratchFloats = 16 * (8192 + 128);  // B * (d_inner + nheads) <= this
+static __device__ __align__(256) float scratch[kMixerScratchFloats];
+
+int64_t mixer_scratch_floats() { return kMixerScratchFloats; }
+
+hipError_t launch_mixer_step_noalloc(const float* zxbcdt, int B, int nheads,
+                                     uint16_t* conv_state, int* conv_pos, uint16_t* ssm_state,
+                                     const float* conv_w, const float* conv_b,
+                                     const float* dt_bias, const float* A_log, const float* D,
+                                     const float* norm_w, float eps, uint16_t* out,
+                                     hipStream_t stream) {
+  if ((int64_t)B * (nheads * kMxP + nheads) > kMixerScratchFloats) return hipErrorInvalidValue;
+  constexpr int kMaxDev = 64;
+  static std::atomic<float*> ptrs[kMaxDev];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+  float* ws = ptrs[dev].load(std::memory_order_acquire);
+  if (ws == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    ws = static_cast<float*>(p);
+    ptrs[dev].store(ws, std::memory_order_release);
+  }
+  return launch_mixer_step(zxbcdt, B, nheads, conv_state, conv_pos, ssm_state, conv_w, conv_b,
+                           dt_bias, A_log, D, norm_w, eps, ws, out, stream);
 }
 
 }  // namespace tmk

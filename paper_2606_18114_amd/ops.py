@@ -42,6 +42,8 @@ SIGNATURES = {
     "tm_tgemm_fwd_bf16": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
     "tm_dgemv": (ctypes.c_int, [_P, _P, _I32, _I32, _I64, _I64, _P, _P]),
     "tm_residual_rmsnorm": (ctypes.c_int, [_P, _P, _I32, _I64, _P, ctypes.c_float, _P, _P]),
+    "tm_mixer_step_noalloc": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P,
+                                             _P, _P, _P, ctypes.c_float, _P, _P]),
     "tm_mixer_step": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                      _P, ctypes.c_float, _P, _P, _P]),
     "tm_scale_ste_grad": (ctypes.c_int,
@@ -366,11 +368,12 @@ def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.T
                dt_bias: torch.Tensor, A_log: torch.Tensor, D: torch.Tensor,
                norm_w: torch.Tensor, eps: float = 1e-5, *,
                workspace: Optional[torch.Tensor] = None,
-               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+               out: Optional[torch.Tensor] = None, noalloc: bool = False) -> torch.Tensor:
     """One Mamba-2 mixer decode step between the projections (tm_mixer_step):
     zxbcdt float32 [B, Z] -> out bfloat16 [B, d_inner]; conv_state (float16
     ring [B, conv_dim, 4]), conv_pos (int32 [1]) and ssm_state (float16
-    [B, nheads, 64, 128]) are updated in place."""
+    [B, nheads, 64, 128]) are updated in place.  noalloc=True calls
+    tm_mixer_step_noalloc (the library's own scratch array, no workspace)."""
     _need(zxbcdt, "zxbcdt", _F32, 2)
     B = zxbcdt.shape[0]
     _need(A_log, "A_log", _F32, 1)
@@ -389,15 +392,24 @@ def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.T
                          (dt_bias, "dt_bias", (H,)), (D, "D", (H,)), (norm_w, "norm_w", (di,))):
         _need(t, name, _F32, len(shp))
         _shape(t, name, shp, dev)
+    if out is None:
+        out = torch.empty((B, di), dtype=torch.bfloat16, device=dev)
+    _need(out, "out", _BF16, 2)
+    _shape(out, "out", (B, di), dev)
+    if noalloc:
+        if workspace is not None:
+            raise ValueError("noalloc=True takes no workspace")
+        st = lib().tm_mixer_step_noalloc(_ptr(zxbcdt), B, H, P, N, _ptr(conv_state),
+                                         _ptr(conv_pos), _ptr(ssm_state), _ptr(conv_w),
+                                         _ptr(conv_b), _ptr(dt_bias), _ptr(A_log), _ptr(D),
+                                         _ptr(norm_w), eps, _ptr(out), _stream())
+        _check("tm_mixer_step_noalloc", st)
+        return out
     if workspace is None:
         workspace = mixer_workspace(B, H, dev)
     _need(workspace, "workspace", _F32, 1)
     if workspace.numel() < B * (di + H):
         raise ValueError(f"workspace holds {workspace.numel()} floats, needs {B * (di + H)}")
-    if out is None:
-        out = torch.empty((B, di), dtype=torch.bfloat16, device=dev)
-    _need(out, "out", _BF16, 2)
-    _shape(out, "out", (B, di), dev)
     st = lib().tm_mixer_step(_ptr(zxbcdt), B, H, P, N, _ptr(conv_state), _ptr(conv_pos),
                              _ptr(ssm_state), _ptr(conv_w), _ptr(conv_b), _ptr(dt_bias),
                              _ptr(A_log), _ptr(D), _ptr(norm_w), eps, _ptr(workspace), _ptr(out),

@@ -56,6 +56,12 @@ hipError_t launch_mixer_step(const float*, int, int, uint16_t*, int*, uint16_t*,
   reached("mixer_step");
 }
 
+int64_t mixer_scratch_floats() { return 16 * (8192 + 128); }
+hipError_t launch_mixer_step_noalloc(const float*, int, int, uint16_t*, int*, uint16_t*,
+                                     const float*, const float*, const float*, const float*,
+                                     const float*, const float*, float, uint16_t*, hipStream_t) {
+  reached("mixer_step_noalloc");
+}
 hipError_t launch_residual_rmsnorm(float*, const float*, int, int64_t, const float*, float,
                                    uint16_t*, hipStream_t) {
   reached("residual_rmsnorm");

@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 7
+    assert L.tm_abi_version() == 8
 
 
 def test_status_strings(L):
@@ -196,6 +196,26 @@ def mx(L, z=P, B=1, H=64, hd=64, ds=128, cs=P + 2 ** 20, pos=P + 2 ** 21, ss=P +
        D=P + 2 ** 26 + 8192, nw=P + 2 ** 27, eps=1e-5, ws=P + 2 ** 28, out=P + 2 ** 29):
     return L.tm_mixer_step(z, B, H, hd, ds, cs, pos, ss, cw, cb, dtb, al, D, nw, eps, ws, out,
                            None)
+
+
+def test_mixer_step_noalloc_validation(L):
+    def na(**kw):
+        S = 2 ** 27   # arrays far apart, so that only the size check can fail
+        a = dict(z=P, B=1, H=64, hd=64, ds=128, cs=P + S, pos=P + 2 * S, ss=P + 3 * S,
+                 cw=P + 4 * S, cb=P + 5 * S, dtb=P + 6 * S, al=P + 7 * S, D=P + 8 * S,
+                 nw=P + 9 * S, eps=1e-5, out=P + 10 * S)
+        a.update(kw)
+        return L.tm_mixer_step_noalloc(a["z"], a["B"], a["H"], a["hd"], a["ds"], a["cs"],
+                                       a["pos"], a["ss"], a["cw"], a["cb"], a["dtb"], a["al"],
+                                       a["D"], a["nw"], a["eps"], a["out"], None)
+    assert na(z=0) == EINVAL
+    assert na(out=0) == EINVAL
+    assert na(hd=32) == ESHAPE
+    # the scratch array holds 16 * (8192 + 128) = 133120 floats
+    assert na(B=33) == ESHAPE          # 33 * (4096 + 64) = 137280 floats
+    assert na(B=1, H=2049) == ESHAPE   # 2049 * 65 = 133185 floats
+    assert na(ss=P + 3 * 2 ** 27 + 8) == EALIGN
+    assert na(out=P + 3 * 2 ** 27) == EINVAL    # out over the SSM state
 
 
 def test_mixer_step_validation(L):
