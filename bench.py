@@ -377,6 +377,7 @@ def main():
     # ---------------- measured ceilings (context for the fractions) ----------------
     if not args.no_ceilings:
         c = measure_ceilings()
+        out["base3_packing_probe"] = c.pop("base3_packing_probe", None)
         out["measured_ceilings"] = dict(c, what=MICRO_WHAT)
         out["roofline"]["frac_of_measured"] = round(
             fwd["achieved"] / c["mfma_bf16_loop_random_TFLOPs"], 4)
@@ -895,6 +896,8 @@ def measure_ceilings():
                                   ctypes.c_void_p]
     lib.tmm_read_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                     ctypes.c_void_p]
+    lib.tmm_decode_stream.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                      ctypes.c_void_p, ctypes.c_void_p]
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -962,6 +965,38 @@ def measure_ceilings():
     sec = timed(lambda: [token() for _ in range(tokens)], reps=3, warm=1)
     res["hbm_read_stream_decode_pattern_GBps"] = round(sum(sizes) * tokens / sec / 1e9, 1)
     del pat
+    # base-3 packing against the 2-bit format: the 48 in_proj matrices' codes
+    # streamed and decoded into the matrix-core operand nibbles (five codes
+    # per byte from a table, or the 2-bit shift-and-mask), in copies rotated
+    # over > 1 GiB so that both stream from HBM
+    c = synth.DECODE_IN
+    codes = synth.N_LAYERS * c.N * c.K
+    b3 = {}
+    for fmt, per_byte in ((2, 4), (3, 5)):
+        nb = -(-codes // per_byte)
+        nb += (-nb) % 16384
+        copies = [torch.randint(0, 243 if fmt == 3 else 256, (nb,), dtype=torch.uint8,
+                                device=dev, generator=gen) for _ in range(-(-(1 << 30) // nb) + 1)]
+
+        def run(f):
+            for b in copies:
+                check(lib.tmm_decode_stream(b.data_ptr(), b.numel(), f, words.data_ptr(), st))
+
+        def plain():
+            for b in copies:
+                check(lib.tmm_read_stream(b.data_ptr(), b.numel(), words.data_ptr(), st))
+        sec = timed(lambda: run(fmt), reps=3, warm=1) / len(copies)
+        sec_read = timed(plain, reps=3, warm=1) / len(copies)
+        b3[f"format{fmt}"] = {"bytes": nb, "bits_per_code": round(8.0 * nb / codes, 3),
+                              "decode_us": round(sec * 1e6, 2), "read_only_us": round(sec_read * 1e6, 2),
+                              "Gcodes_per_s": round(codes / sec / 1e9, 1)}
+        del copies
+    b3["base3_vs_2bit_time"] = round(b3["format3"]["decode_us"] / b3["format2"]["decode_us"], 3)
+    b3["what"] = ("codes of the 48 in_proj layers (8512 x 2048 each) streamed from HBM and "
+                  "decoded to the FP4 operand nibbles: format 2 = the 2-bit codes, format 3 = "
+                  "base-3 packing (5 codes per byte, 1.6 bits); decode_us per pass, read_only_us "
+                  "the same bytes without the decode")
+    res["base3_packing_probe"] = b3
     M, N, K = 16384, 8512, 2048
     X = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
     Wt = (torch.randn((N, K), generator=gen, device=dev) * 0.02).to(torch.bfloat16).t().contiguous()

@@ -15,6 +15,14 @@
 //     be dropped.  Of the access patterns tried (grid-stride 16-byte pieces,
 //     4 KiB or 16 KiB per wave, 32 rows x 128 bytes at a 512-byte pitch) the
 //     contiguous chunks were fastest.  `bytes` must be a multiple of 16 KiB.
+//   tmm_decode_stream: the same stream, with every 16-byte piece of packed
+//     ternary codes decoded into the FP4 operand nibbles (2q: 0100, 1100,
+//     0000) the decode GEMV hands to the matrix cores: format 2 is the 2-bit
+//     code format (64 codes per piece, one 64-bit shift and four ANDs per 32
+//     codes), format 3 base-3 packing (five codes per byte, 80 per piece,
+//     one LDS table read per byte giving its five nibbles, placed into the
+//     nibble stream by shifts).  It measures what decoding costs per code
+//     against the bytes a format saves.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -89,6 +97,68 @@ __global__ __launch_bounds__(kThreads) void read_stream_kernel(const mu32x4* __r
   out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
 }
 
+// keeps a decoded operand word alive (as the matrix-core operand would) at
+// no instruction cost, so the decode cannot be folded away
+__device__ __forceinline__ void sink(uint32_t v) { asm volatile("" ::"v"(v)); }
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void decode_stream_kernel(const mu32x4* __restrict__ buf,
+                                                                 int64_t chunks,
+                                                                 uint32_t* __restrict__ out) {
+  __shared__ uint32_t lut[256];  // base 3: byte -> its five codes' FP4 nibbles
+  if constexpr (FMT == 3) {
+    for (int b = threadIdx.x; b < 256; b += kThreads) {
+      uint32_t t = 0, v = (uint32_t)b;
+      for (int i = 0; i < 5; ++i) {
+        const uint32_t c = v % 3u;  // code + 1
+        v /= 3u;
+        t |= (c == 2u ? 0x4u : c == 0u ? 0xCu : 0u) << (4 * i);
+      }
+      lut[b] = b < 243 ? t : 0u;
+    }
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int64_t nwaves = (int64_t)gridDim.x * (kThreads / 64);
+  uint32_t acc = 0;
+  for (int64_t ch = wave; ch < chunks; ch += nwaves) {
+    const mu32x4* p = buf + ch * 1024 + lane;
+    mu32x4 v[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = p[64 * j];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t w[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+      acc ^= w[0];
+      if constexpr (FMT == 2) {
+        constexpr uint32_t kNib = 0xCCCCCCCCu;
+#pragma unroll
+        for (int k = 0; k < 4; k += 2) {
+          const uint64_t ww = ((uint64_t)w[k + 1] << 32) | w[k];
+          const uint64_t sh = ww << 2;
+          sink(w[k] & kNib);
+          sink((uint32_t)sh & kNib);
+          sink(w[k + 1] & kNib);
+          sink((uint32_t)(sh >> 32) & kNib);
+        }
+      } else {
+        uint32_t o[10] = {};
+#pragma unroll
+        for (int b = 0; b < 16; ++b) {
+          const uint32_t t = lut[(w[b / 4] >> (8 * (b % 4))) & 0xFFu];
+          const int pos = 5 * b, d = pos / 8, sh = 4 * (pos % 8);
+          o[d] |= t << sh;
+          if (sh + 20 > 32) o[d + 1] |= t >> (32 - sh);
+        }
+#pragma unroll
+        for (int i = 0; i < 10; ++i) sink(o[i]);
+      }
+    }
+  }
+  out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
 int cu_count() {
   int dev = 0, v = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -129,6 +199,23 @@ int tmm_read_stream(const void* buf, int64_t bytes, uint32_t* out, void* stream)
   hipLaunchKernelGGL(read_stream_kernel, dim3(2 * cu_count()), dim3(kThreads), 0,
                      (hipStream_t)stream, reinterpret_cast<const mu32x4*>(buf), bytes / 16384,
                      out);
+  return (int)hipGetLastError();
+}
+
+// The read stream with each piece decoded as packed ternary codes: format 2
+// (2-bit codes) or 3 (base-3, five codes per byte).  Same contract as
+// tmm_read_stream.
+int tmm_decode_stream(const void* buf, int64_t bytes, int format, uint32_t* out, void* stream) {
+  if (!buf || !out || bytes <= 0 || bytes % 16384 != 0 || (format != 2 && format != 3) ||
+      reinterpret_cast<uintptr_t>(buf) % 16 != 0)
+    return (int)hipErrorInvalidValue;
+  const auto* b = reinterpret_cast<const mu32x4*>(buf);
+  if (format == 2)
+    hipLaunchKernelGGL(decode_stream_kernel<2>, dim3(2 * cu_count()), dim3(kThreads), 0,
+                       (hipStream_t)stream, b, bytes / 16384, out);
+  else
+    hipLaunchKernelGGL(decode_stream_kernel<3>, dim3(2 * cu_count()), dim3(kThreads), 0,
+                       (hipStream_t)stream, b, bytes / 16384, out);
   return (int)hipGetLastError();
 }
 
