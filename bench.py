@@ -62,11 +62,11 @@ def parse():
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants, "
-                         "per_layer, small, sweep, mixed, blocks (keeps a profiler trace to the kernels "
-                         "of interest)")
+                         "per_layer, small, sweep, mixed, blocks, cold (keeps a profiler trace to the "
+                         "kernels of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
-    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed", "blocks"}
+    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed", "blocks", "cold"}
     if bad:
         ap.error(f"unknown --skip sections: {sorted(bad)}")
     return args
@@ -238,7 +238,8 @@ def main():
                 float(np.mean([e[1].elapsed_time(e[2]) for e in ev])),
                 e0.elapsed_time(e1) / tokens)
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
-    cold = cold_figures(ops, dec, W, dW, codes, scales, g, eps, max(args.steps // 4, 3))
+    cold = ({} if "cold" in args.skip
+            else cold_figures(ops, dec, W, dW, codes, scales, g, eps, max(args.steps // 4, 3)))
     small = None if "small" in args.skip else small_configs(ops, dev, args.steps)
     sweep = None if "sweep" in args.skip else group_sweep(ops, dev, max(args.steps // 2, 5))
 
@@ -350,7 +351,8 @@ def main():
                            "unit": "GB/s", "frac": srv_cold["frac_hbm"],
                            "traffic": dec_traffic, "algorithmic_per_token": dec_bytes,
                            "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to "
-                                     "back, weights rotated over >= 1.1 GiB of copies (cold)",
+                                     "back, " + ("weights rotated over >= 1.1 GiB of copies (cold)"
+                                                 if "cold" in srv else "one weight arena (warm)"),
                            "warm": {"achieved": srv["GBps"], "frac": srv["frac_hbm"]}},
         "kernels": kernels,
         "qat_block": qat_block,
