@@ -251,8 +251,10 @@ def main():
     if "blocks" not in args.skip:
         from paper_2606_18114_amd.stack import keep_first_last
         blocks = {"all_ternary": decode_mamba2_blocks(dev, args.steps),
+                  "all_ternary_unfused": decode_mamba2_blocks(dev, args.steps, fused=False),
                   "first_last_2_fp16": decode_mamba2_blocks(
-                      dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2))}
+                      dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2)),
+                  "all_ternary_B4": decode_mamba2_blocks(dev, args.steps, batch=4)}
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
@@ -701,12 +703,14 @@ def cpu_baseline(W_h, X_h, dY_h, g, eps, dec, gpu_out=None):
     return base, par, codes_cmp
 
 
-def decode_mamba2_blocks(dev, tokens, keep=(), batch=1):
+def decode_mamba2_blocks(dev, tokens, keep=(), batch=1, fused=True):
     """Decode as a model runs it: 48 whole Mamba-2 blocks in layer order, each
     pre-norm -> in_proj -> mixer step (convolution, FP16 SSM state update,
-    gated RMSNorm) -> out_proj, then the final norm: 5 launches per layer plus
-    2, timed eagerly (one Python call per launch) and as one captured HIP
-    graph per token.  States persist from token to token."""
+    gated RMSNorm) -> out_proj, then the final norm.  Fused: 3 launches per
+    layer (the norms inside the projections' staging, the residual add in
+    out_proj's store); unfused: 5.  Timed eagerly (one Python call per
+    launch) and as one captured HIP graph per token; states persist from
+    token to token."""
     import torch
     from paper_2606_18114_amd import synth
     from paper_2606_18114_amd.stack import Mamba2Decoder
@@ -719,7 +723,7 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1):
         lambda k, l: torch.from_numpy(synth.layer_weight(cfg[k], synth.decode_seed(f"{k}_w", l))
                                       ).to(dev),
         lambda l: mix[l], lambda l: torch.ones(synth.D_MODEL), L, synth.D_MODEL, H,
-        keep=keep, g=128, batch=batch, device=dev)
+        keep=keep, g=128, batch=batch, device=dev, fused=fused)
     for l in range(L):
         conv, ssm = synth.mixer_states(rng, batch, H)
         dec.set_states(l, torch.from_numpy(conv).to(dev), torch.from_numpy(ssm).to(dev))
@@ -745,6 +749,7 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1):
     us_graph = timed(dec.replay, n)
     nb = dec.bytes_per_token()
     res = {"layers": L, "kept_fp16_layers": sorted(dec.keep), "batch": batch,
+           "fused": dec.fused,
            "launches_per_token": dec.launches_per_token(), "bytes_per_token": nb,
            "us_per_token_eager": round(us_eager, 2), "us_per_token_graph": round(us_graph, 2),
            "GBps_graph": round(nb / (us_graph * 1e-6) / 1e9, 1),

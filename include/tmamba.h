@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 8
+#define TM_ABI_VERSION 9
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -285,6 +285,64 @@ tm_status tm_mixer_step_noalloc(const float* zxbcdt, int32_t B, int32_t nheads, 
                                 const float* dt_bias, const float* A_log, const float* D,
                                 const float* norm_w, float eps, uint16_t* out,
                                 tm_stream stream);
+
+/*
+ * The fused decode block (Sec. 8, batch-1 decode: a token streams each
+ * layer's weights once; Sec. 3.2: the state update between the projections
+ * stays FP16).  A Mamba-2 block in layer order runs three launches:
+ *   zx  = tm_tgemv_rms(residual, w_pre)           pre-norm + in_proj
+ *   g   = tm_mixer_gate(zx, states)               conv + SSM step + gate
+ *   residual += tm_tgemv_rms(g, norm_w, acc = 1)  gated norm + out_proj
+ * (tm_dgemv_rms for a layer kept in FP16).  The normalizations are folded
+ * into the products' activation staging: every workgroup normalizes the
+ * whole source row itself, so no launch exists only to normalize.
+ *
+ * tm_tgemv_rms — one packed matrix applied to normalized float32 rows:
+ *   x[b, k] = bf16(src[b, k] / sqrt(mean_k(src[b, k]^2) + eps) * norm_w[k]);
+ *   y[b, n] = sum_k x[b, k] q[n, k] s16[n, k/g]   (accumulate 0), or
+ *   y[b, n] += that sum                           (accumulate 1).
+ *   src         float32 [B, K]   in   (16-byte aligned)
+ *   norm_w      float32 [K]      in   (16-byte aligned)
+ *   eps         float32, finite, >= 0
+ *   codes, scales_f16, g   as tm_tgemv with count = 1
+ *   B  1 .. 16 with 4 B (128 / g if g < 128, else 1) <= 16 and
+ *      B * ceil(K / 128) * 8 <= 512 (1024 when K > 3584): the shapes whose
+ *      rows one workgroup stages at once (TM_ESHAPE otherwise)
+ *   y           float32 [B, N]   out or in/out (16-byte aligned)
+ * x is split and multiplied as in tm_tgemv.  The row sums of squares are
+ * taken in a fixed order (deterministic results).  y must not overlap the
+ * inputs.
+ */
+tm_status tm_tgemv_rms(const float* src, const float* norm_w, float eps, const uint8_t* codes,
+                       const uint16_t* scales_f16, int32_t B, int64_t N, int64_t K, int32_t g,
+                       float* y, int32_t accumulate, tm_stream stream);
+
+/*
+ * tm_dgemv_rms — tm_tgemv_rms for one matrix kept in FP16 (Sec. 7):
+ * x as there, y[b, n] (+)= sum_k x[b, k] W16[n, k], summed as tm_dgemv.
+ *   src float32 [B, K], norm_w float32 [K] (16-byte aligned); W16 as tm_dgemv
+ *   B 1 .. 8;  K % 64 == 0 and B * K <= 16384;  y float32 [B, N] (4-byte aligned)
+ */
+tm_status tm_dgemv_rms(const float* src, const float* norm_w, float eps, const uint16_t* W16,
+                       int32_t B, int64_t N, int64_t K, float* y, int32_t accumulate,
+                       tm_stream stream);
+
+/*
+ * tm_mixer_gate — tm_mixer_step up to the gated values, in one launch:
+ *   gated[b] = g = y * SiLU(z)   (float32 [B, d_inner], not normalized)
+ * with the same convolution, state update and arguments as tm_mixer_step
+ * (no norm_w, eps or workspace).  The convolution ring position advances
+ * inside the launch: conv_pos[0] & 3 is the position; every workgroup adds
+ * 4 once it has read it and the last one stores the next position, so
+ * between calls conv_pos[0] holds just the position, as for tm_mixer_step
+ * (either call continues the other's ring).  gated must not overlap the
+ * other arrays.
+ */
+tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                        int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                        uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                        const float* dt_bias, const float* A_log, const float* D, float* gated,
+                        tm_stream stream);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

@@ -75,15 +75,18 @@ tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float
 
 // argument checks of the mixer step; workspace NULL: the library's own
 // scratch array (no overlap check needed: no caller array can overlap it)
+// gate_only: the gated float32 output of tm_mixer_gate in place of the
+// normalized bfloat16 one (no norm_w, eps or workspace)
 tm_status mixer_checked(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
                         int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
                         uint16_t* ssm_state, const float* conv_w, const float* conv_b,
                         const float* dt_bias, const float* A_log, const float* D,
-                        const float* norm_w, float eps, float* workspace, uint16_t* out) {
+                        const float* norm_w, float eps, float* workspace, const void* out,
+                        bool gate_only = false) {
   if (!zxbcdt || !conv_state || !conv_pos || !ssm_state || !conv_w || !conv_b || !dt_bias ||
-      !A_log || !D || !norm_w || !out)
+      !A_log || !D || (!gate_only && !norm_w) || !out)
     return TM_EINVAL;
-  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (!gate_only && (!(eps >= 0.0f) || !std::isfinite(eps))) return TM_EINVAL;
   if (B < 1 || B > 65535 || nheads < 1 || nheads > 4096 || headdim != 64 || d_state != 128)
     return TM_ESHAPE;
   const int64_t di = (int64_t)nheads * headdim, cd = di + 2 * (int64_t)d_state;
@@ -91,18 +94,18 @@ tm_status mixer_checked(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
   int64_t zb, cb, sb, wb, ob;
   if (!bytes_of(B, zw, 4, &zb) || !bytes_of((int64_t)B * cd, 4, 2, &cb) ||
       !bytes_of((int64_t)B * nheads * headdim, d_state, 2, &sb) ||
-      !bytes_of(B, di + nheads, 4, &wb) || !bytes_of(B, di, 2, &ob))
+      !bytes_of(B, di + nheads, 4, &wb) || !bytes_of(B, di, gate_only ? 4 : 2, &ob))
     return TM_ESHAPE;
   if (!aligned(zxbcdt, 4) || !aligned(conv_state, 2) || !aligned(conv_pos, 4) ||
       !aligned(ssm_state, 16) || !aligned(conv_w, 4) || !aligned(conv_b, 4) ||
       !aligned(dt_bias, 4) || !aligned(A_log, 4) || !aligned(D, 4) || !aligned(norm_w, 4) ||
-      !aligned(workspace, 4) || !aligned(out, 2))
+      !aligned(workspace, 4) || !aligned(out, gate_only ? 4 : 2))
     return TM_EALIGN;
   const Span outs[5] = {span(conv_state, cb), span(conv_pos, 4), span(ssm_state, sb),
                         span(workspace, workspace ? wb : 0), span(out, ob)};
   const Span ins[7] = {span(zxbcdt, zb), span(conv_w, cd * 16), span(conv_b, cd * 4),
                        span(dt_bias, (int64_t)nheads * 4), span(A_log, (int64_t)nheads * 4),
-                       span(D, (int64_t)nheads * 4), span(norm_w, di * 4)};
+                       span(D, (int64_t)nheads * 4), span(norm_w, norm_w ? di * 4 : 0)};
   for (int i = 0; i < 5; ++i) {
     for (int j = i + 1; j < 5; ++j)
       if (overlap(outs[i], outs[j])) return TM_EINVAL;
@@ -360,6 +363,69 @@ tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scal
   if (overlap(o, span(x, xb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales_f16, sb)))
     return TM_EINVAL;
   return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
+}
+
+tm_status tm_tgemv_rms(const float* src, const float* norm_w, float eps, const uint8_t* codes,
+                       const uint16_t* scales_f16, int32_t B, int64_t N, int64_t K, int32_t g,
+                       float* y, int32_t accumulate, tm_stream stream) {
+  if (!src || !norm_w || !codes || !scales_f16 || !y) return TM_EINVAL;
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (accumulate != 0 && accumulate != 1) return TM_EINVAL;
+  if (B < 1 || B > 16 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  if (!tmk::tgemv_rms_fits(B, K, g)) return TM_ESHAPE;
+  int64_t xb, wb, cb, sb, yb;
+  if (!bytes_of(B, K, 4, &xb) || !bytes_of(1, K, 4, &wb) || !bytes_of(N, K / 4, 1, &cb) ||
+      !bytes_of(N, K / g, 2, &sb) || !bytes_of(B, N, 4, &yb))
+    return TM_ESHAPE;
+  if ((N + 31) / 32 > kMaxGridBlocks) return TM_ESHAPE;
+  if (cb > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside the matrix
+  if (!aligned(src, 16) || !aligned(norm_w, 16) || !aligned(codes, 16) ||
+      !aligned(scales_f16, 2) || !aligned(y, 16))
+    return TM_EALIGN;
+  const Span o = span(y, yb);
+  if (overlap(o, span(src, xb)) || overlap(o, span(norm_w, wb)) || overlap(o, span(codes, cb)) ||
+      overlap(o, span(scales_f16, sb)))
+    return TM_EINVAL;
+  return hip_status(tmk::launch_tgemv_rms(src, norm_w, eps, codes, scales_f16, B, N, K, g, y,
+                                          accumulate, to_hip(stream)));
+}
+
+tm_status tm_dgemv_rms(const float* src, const float* norm_w, float eps, const uint16_t* W16,
+                       int32_t B, int64_t N, int64_t K, float* y, int32_t accumulate,
+                       tm_stream stream) {
+  if (!src || !norm_w || !W16 || !y) return TM_EINVAL;
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return TM_EINVAL;
+  if (accumulate != 0 && accumulate != 1) return TM_EINVAL;
+  if (B < 1 || B > 8 || N < 1) return TM_ESHAPE;
+  if (K < 64 || K % 64 != 0 || (int64_t)B * K > 16384) return TM_ESHAPE;
+  int64_t xb, wb, mb, yb;
+  if (!bytes_of(B, K, 4, &xb) || !bytes_of(1, K, 4, &wb) || !bytes_of(N, K, 2, &mb) ||
+      !bytes_of(B, N, 4, &yb))
+    return TM_ESHAPE;
+  if ((N + 7) / 8 > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(src, 16) || !aligned(norm_w, 16) || !aligned(W16, 16) || !aligned(y, 4))
+    return TM_EALIGN;
+  const Span o = span(y, yb);
+  if (overlap(o, span(src, xb)) || overlap(o, span(norm_w, wb)) || overlap(o, span(W16, mb)))
+    return TM_EINVAL;
+  return hip_status(
+      tmk::launch_dgemv_rms(src, norm_w, eps, W16, B, N, K, y, accumulate, to_hip(stream)));
+}
+
+tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t headdim,
+                        int32_t d_state, uint16_t* conv_state, int32_t* conv_pos,
+                        uint16_t* ssm_state, const float* conv_w, const float* conv_b,
+                        const float* dt_bias, const float* A_log, const float* D, float* gated,
+                        tm_stream stream) {
+  if (tm_status st = mixer_checked(zxbcdt, B, nheads, headdim, d_state, conv_state, conv_pos,
+                                   ssm_state, conv_w, conv_b, dt_bias, A_log, D, nullptr, 0.f,
+                                   nullptr, gated, true))
+    return st;
+  if ((int64_t)B * nheads >= (int64_t(1) << 29)) return TM_ESHAPE;  // the arrival count fits
+  return hip_status(tmk::launch_mixer_gate(zxbcdt, B, nheads, conv_state, conv_pos, ssm_state,
+                                           conv_w, conv_b, dt_bias, A_log, D, gated,
+                                           to_hip(stream)));
 }
 
 }  // extern "C"

@@ -39,11 +39,15 @@ __device__ __forceinline__ float half_hi(uint32_t w) {
 }
 
 // Grid: (ceil(N / (R * kDgWaves)), count); wave w of workgroup i owns rows
-// (i * kDgWaves + w) * R .. + R - 1.  LDS: B * K floats.
-template <int BMAX, int R, int SEG>
+// (i * kDgWaves + w) * R .. + R - 1.  LDS: B * K floats (+ B row factors).
+// RMS (one matrix; a decoding block's normalization fused into the staging):
+// x[b, k] = bf16(xr[b, k] / sqrt(mean_k xr[b, k]^2 + eps) * nw[k]), the row
+// sums taken by one wave per row in a fixed order.  accum: y += instead of =.
+template <int BMAX, int R, int SEG, bool RMS>
 __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ W, int B, int64_t N,
-    int64_t K, float* __restrict__ y) {
+    int64_t K, float* __restrict__ y, const float* __restrict__ xr,
+    const float* __restrict__ nw, float eps, int accum) {
   extern __shared__ __attribute__((aligned(16))) float xs[];
   const int64_t mat = blockIdx.y;
   const uint16_t* xm = x + mat * (int64_t)B * K;
@@ -52,8 +56,38 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 
+  if constexpr (RMS) {
+    float* rfac = xs + (int64_t)B * K;
+    for (int b = wave; b < B; b += kDgWaves) {
+      float sq = 0.f;
+      for (int64_t k = 4 * lane; k < K; k += 256) {
+        const u32x4 v = ld16(xr + (int64_t)b * K + k);
+        sq = __builtin_fmaf(__uint_as_float(v.x), __uint_as_float(v.x), sq);
+        sq = __builtin_fmaf(__uint_as_float(v.y), __uint_as_float(v.y), sq);
+        sq = __builtin_fmaf(__uint_as_float(v.z), __uint_as_float(v.z), sq);
+        sq = __builtin_fmaf(__uint_as_float(v.w), __uint_as_float(v.w), sq);
+      }
+      sq = wave_sum_f32(sq);
+      if (lane == 0) rfac[b] = 1.f / sqrtf(sq / (float)K + eps);
+    }
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < (int64_t)B * K / 4; i += 64 * kDgWaves) {
+      const int64_t b = 4 * i / K, k = 4 * i % K;
+      const u32x4 v = ld16(xr + 4 * i);
+      const u32x4 w = ld16(nw + k);
+      const float r = rfac[b];
+      const uint32_t a[4] = {v.x, v.y, v.z, v.w}, c[4] = {w.x, w.y, w.z, w.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const uint32_t bits = __float_as_uint(__uint_as_float(a[t]) * r * __uint_as_float(c[t]));
+        o[t] = ((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16) << 16;  // bf16, nearest even
+      }
+      st16(xs + 4 * i, u32x4{o[0], o[1], o[2], o[3]});
+    }
+  }
   // x -> float32 in LDS (8 values per thread and step; K % 8 == 0)
-  for (int64_t i = threadIdx.x; i < (int64_t)B * K / 8; i += 64 * kDgWaves) {
+  for (int64_t i = threadIdx.x; !RMS && i < (int64_t)B * K / 8; i += 64 * kDgWaves) {
     const u32x4 v = ld16(xm + 8 * i);
     const uint32_t a[4] = {v.x, v.y, v.z, v.w};
     float f[8];
@@ -126,33 +160,50 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int b = 0; b < BMAX; ++b)
-      if (lane == r * BMAX + b && b < B && row0 + r < N) ym[(int64_t)b * N + row0 + r] = acc[r][b];
+      if (lane == r * BMAX + b && b < B && row0 + r < N) {
+        float* o = ym + (int64_t)b * N + row0 + r;
+        *o = accum ? *o + acc[r][b] : acc[r][b];
+      }
 }
 
-template <int BMAX>
+template <int BMAX, bool RMS>
 static hipError_t launch_dgemv_b(const uint16_t* x, const uint16_t* W, int count, int B,
-                                 int64_t N, int64_t K, float* y, hipStream_t stream) {
-  const size_t lds = (size_t)B * K * sizeof(float);
+                                 int64_t N, int64_t K, float* y, hipStream_t stream,
+                                 const float* xr, const float* nw, float eps, int accum) {
+  const size_t lds = ((size_t)B * K + (RMS ? 16 : 0)) * sizeof(float);
   // four rows per wave, or two when the launch has few rows per CU
   const int64_t blocks4 = (N + 4 * kDgWaves - 1) / (4 * kDgWaves) * count;
   if (blocks4 >= 2 * (int64_t)current_cu_count()) {
     const dim3 grid((unsigned)((N + 4 * kDgWaves - 1) / (4 * kDgWaves)), (unsigned)count);
-    hipLaunchKernelGGL((dgemv_kernel<BMAX, 4, 4>), grid, dim3(64 * kDgWaves), lds, stream, x, W,
-                       B, N, K, y);
+    hipLaunchKernelGGL((dgemv_kernel<BMAX, 4, 4, RMS>), grid, dim3(64 * kDgWaves), lds, stream, x,
+                       W, B, N, K, y, xr, nw, eps, accum);
   } else {
     const dim3 grid((unsigned)((N + 2 * kDgWaves - 1) / (2 * kDgWaves)), (unsigned)count);
-    hipLaunchKernelGGL((dgemv_kernel<BMAX, 2, 8>), grid, dim3(64 * kDgWaves), lds, stream, x, W,
-                       B, N, K, y);
+    hipLaunchKernelGGL((dgemv_kernel<BMAX, 2, 8, RMS>), grid, dim3(64 * kDgWaves), lds, stream, x,
+                       W, B, N, K, y, xr, nw, eps, accum);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W, int count, int B, int64_t N,
+template <bool RMS>
+static hipError_t launch_dgemv_any(const uint16_t* x, const uint16_t* W16, int count, int B,
+                                   int64_t N, int64_t K, float* y, hipStream_t stream,
+                                   const float* xr, const float* nw, float eps, int accum) {
+  if (B <= 1) return launch_dgemv_b<1, RMS>(x, W16, count, B, N, K, y, stream, xr, nw, eps, accum);
+  if (B <= 2) return launch_dgemv_b<2, RMS>(x, W16, count, B, N, K, y, stream, xr, nw, eps, accum);
+  if (B <= 4) return launch_dgemv_b<4, RMS>(x, W16, count, B, N, K, y, stream, xr, nw, eps, accum);
+  return launch_dgemv_b<8, RMS>(x, W16, count, B, N, K, y, stream, xr, nw, eps, accum);
+}
+
+hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W16, int count, int B, int64_t N,
                         int64_t K, float* y, hipStream_t stream) {
-  if (B <= 1) return launch_dgemv_b<1>(x, W, count, B, N, K, y, stream);
-  if (B <= 2) return launch_dgemv_b<2>(x, W, count, B, N, K, y, stream);
-  if (B <= 4) return launch_dgemv_b<4>(x, W, count, B, N, K, y, stream);
-  return launch_dgemv_b<8>(x, W, count, B, N, K, y, stream);
+  return launch_dgemv_any<false>(x, W16, count, B, N, K, y, stream, nullptr, nullptr, 0.f, 0);
+}
+
+hipError_t launch_dgemv_rms(const float* src, const float* nw, float eps, const uint16_t* W16,
+                            int B, int64_t N, int64_t K, float* y, int accum,
+                            hipStream_t stream) {
+  return launch_dgemv_any<true>(nullptr, W16, 1, B, N, K, y, stream, src, nw, eps, accum);
 }
 
 }  // namespace tmk

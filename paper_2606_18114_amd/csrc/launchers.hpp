@@ -52,9 +52,27 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
 hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
+// Fused decode projection: x = bf16(src / sqrt(mean(src^2) + eps) * nw) per
+// batch row, y = (or +=, accum) x times the ternary matrix.  Shapes the
+// kernel stages in one part (tgemv_rms_fits) only.
+// (4 A rows per batch item and group, 512-column slots; 8 waves once K has
+// eight slots, else 4; at most two 16-column pieces per thread)
+inline bool tgemv_rms_fits(int B, int64_t K, int g) {
+  const int H = g < 128 ? 128 / g : 1;
+  const int64_t pieces = (K + 127) / 128 * 8;
+  const int waves = (K + 511) / 512 >= 8 ? 8 : 4;
+  return 4 * B * H <= 16 && B * pieces <= 2 * 64 * waves;
+}
+hipError_t launch_tgemv_rms(const float* src, const float* nw, float eps, const uint8_t* codes,
+                            const uint16_t* s16, int B, int64_t N, int64_t K, int g, float* y,
+                            int accum, hipStream_t stream);
 // y[c, b, n] = sum_k x[c, b, k] * W16[c, n, k] (dense float16 weights)
 hipError_t launch_dgemv(const uint16_t* x, const uint16_t* W16, int count, int B, int64_t N,
                         int64_t K, float* y, hipStream_t stream);
+// the fused form of launch_tgemv_rms for one dense float16 matrix
+hipError_t launch_dgemv_rms(const float* src, const float* nw, float eps, const uint16_t* W16,
+                            int B, int64_t N, int64_t K, float* y, int accum,
+                            hipStream_t stream);
 
 // one Mamba-2 mixer decode step (headdim 64, d_state 128): conv ring step,
 // float16 SSM update, gated RMSNorm -> bfloat16 out; workspace holds
@@ -74,6 +92,14 @@ hipError_t launch_mixer_step_noalloc(const float* zxbcdt, int B, int nheads,
                                      const float* dt_bias, const float* A_log, const float* D,
                                      const float* norm_w, float eps, uint16_t* out,
                                      hipStream_t stream);
+// the step up to the gated output g = y * SiLU(z) (float32 [B, d_inner], not
+// normalized: the fused out_proj normalizes it), one launch; the conv ring
+// position advances when the last workgroup is done
+hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* conv_state,
+                             int* conv_pos, uint16_t* ssm_state, const float* conv_w,
+                             const float* conv_b, const float* dt_bias, const float* A_log,
+                             const float* D, float* gated, hipStream_t stream);
+
 // residual += y (y may be null); x = bf16(rmsnorm(residual) * w), B rows of D
 hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,
                                    const float* w, float eps, uint16_t* x, hipStream_t stream);

@@ -11,6 +11,7 @@
 //   * g (float32) and the head's sum of g^2 go to the workspace.
 // The head's SSM state is loaded at the start, so its memory latency
 // overlaps the convolution.
+// (The fused decode runs kernel 1 alone and normalizes g in out_proj.)
 // Kernel 2, one workgroup per batch row: the gated RMSNorm over all d_inner
 // channels, out = bf16(g / sqrt(mean(g^2) + eps) * w), the bfloat16 input
 // of out_proj (the per-head partial sums meet in a wave butterfly); and the
@@ -45,10 +46,17 @@ __device__ __forceinline__ uint16_t f2h(float f) {  // round to nearest even
 
 // grid (nheads, B); layout: zxbcdt [B, Z] with Z = 2 d_inner + 2 N + nheads,
 // conv [B, conv_dim, 4] float16 ring, ssm [B, nheads, P, N] float16,
-// gated [B, d_inner] and partial [B, nheads] float32
+// gated [B, d_inner] and partial [B, nheads] float32.
+// GATE (the fused decode's form): no partial sums (the fused out_proj takes
+// its own), and the ring position advances here: every workgroup adds 4 to
+// the position word once it has read the position (the word's low two
+// bits), and the last one to arrive stores the next position with a zero
+// count.  Until then the low bits stay the position, so every read of it
+// is right, and no workgroup reads after the last one arrived.
+template <bool GATE>
 __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
     const float* __restrict__ zxbcdt, int nheads, uint16_t* __restrict__ conv,
-    const int* __restrict__ conv_pos, uint16_t* __restrict__ ssm,
+    int* __restrict__ conv_pos, uint16_t* __restrict__ ssm,
     const float* __restrict__ conv_w, const float* __restrict__ conv_b,
     const float* __restrict__ dt_bias, const float* __restrict__ A_log,
     const float* __restrict__ Dp, float* __restrict__ gated, float* __restrict__ partial) {
@@ -112,6 +120,15 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   y = __builtin_fmaf(Dp[h], xp, y);
   const float g = y * mx_silu(row[h * kMxP + p]);
   if (q == 0) gated[(int64_t)b * d_inner + h * kMxP + p] = g;
+  if constexpr (GATE) {
+    // every thread read the position before the barrier after the convolution
+    if (tid == 0) {
+      const int total = (int)(gridDim.x * gridDim.y);
+      const int old = atomicAdd(conv_pos, 4);
+      if ((old >> 2) == total - 1) atomicExch(conv_pos, (old + 1) & 3);
+    }
+    return;
+  }
   // sum of g^2 over the head's 64 channels: each channel counted once (q = 0)
   float sq = q == 0 ? g * g : 0.f;
   sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
@@ -220,13 +237,23 @@ hipError_t launch_mixer_step(const float* zxbcdt, int B, int nheads, uint16_t* c
                              uint16_t* out, hipStream_t stream) {
   float* gated = workspace;
   float* partial = workspace + (int64_t)B * nheads * kMxP;
-  hipLaunchKernelGGL(mixer_ssm_kernel, dim3((unsigned)nheads, (unsigned)B), dim3(kMxThreads), 0,
-                     stream, zxbcdt, nheads, conv_state, conv_pos, ssm_state, conv_w, conv_b,
-                     dt_bias, A_log, D, gated, partial);
+  hipLaunchKernelGGL(mixer_ssm_kernel<false>, dim3((unsigned)nheads, (unsigned)B),
+                     dim3(kMxThreads), 0, stream, zxbcdt, nheads, conv_state, conv_pos,
+                     ssm_state, conv_w, conv_b, dt_bias, A_log, D, gated, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(mixer_norm_kernel, dim3((unsigned)B), dim3(kMxThreads), 0, stream, gated,
                      partial, nheads, norm_w, eps, out, conv_pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* conv_state,
+                             int* conv_pos, uint16_t* ssm_state, const float* conv_w,
+                             const float* conv_b, const float* dt_bias, const float* A_log,
+                             const float* D, float* gated, hipStream_t stream) {
+  hipLaunchKernelGGL(mixer_ssm_kernel<true>, dim3((unsigned)nheads, (unsigned)B),
+                     dim3(kMxThreads), 0, stream, zxbcdt, nheads, conv_state, conv_pos,
+                     ssm_state, conv_w, conv_b, dt_bias, A_log, D, gated, nullptr);
   return hipGetLastError();
 }
 

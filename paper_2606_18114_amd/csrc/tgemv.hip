@@ -286,7 +286,14 @@ __device__ __forceinline__ int piece_koff(int col) {
 // i % H == hh; D row (kTerms b + u) H + hh belongs to batch item b.
 template <int NR, int H>
 __device__ __forceinline__ void store_rows(const float (&acc)[NR][kGemvBlocks][H], int B,
-                                           int64_t N, int64_t rowb, int l16, int q, float* ym) {
+                                           int64_t N, int64_t rowb, int l16, int q, float* ym,
+                                           bool accum) {
+  auto put = [&](int64_t at, float v) {
+    if (accum)
+      ym[at] += v;  // each element has one owner lane: a plain read-modify-write
+    else
+      ym[at] = v;
+  };
 #pragma unroll
   for (int j = 0; j < kGemvBlocks; ++j) {
     const int64_t n = rowb + 16 * j + l16;
@@ -298,17 +305,17 @@ __device__ __forceinline__ void store_rows(const float (&acc)[NR][kGemvBlocks][H
       if constexpr (H == 1) {
         // rows 4b .. 4b+3 are lane group q's four rows
         const int b = 4 * r + q;
-        if (n < N && b < B) ym[(int64_t)b * N + n] = v;
+        if (n < N && b < B) put((int64_t)b * N + n, v);
       } else if constexpr (H == 2) {
         // rows 8b .. 8b+7: lane groups q = 2(b%2) and q + 1
         v += __shfl_xor(v, 16);
         const int b = 2 * r + (q >> 1);
-        if ((q & 1) == 0 && n < N && b < B) ym[(int64_t)b * N + n] = v;
+        if ((q & 1) == 0 && n < N && b < B) put((int64_t)b * N + n, v);
       } else {
         // rows 16b .. 16b+15: all four lane groups of operand r
         v += __shfl_xor(v, 16);
         v += __shfl_xor(v, 32);
-        if (q == 0 && n < N && r < B) ym[(int64_t)r * N + n] = v;
+        if (q == 0 && n < N && r < B) put((int64_t)r * N + n, v);
       }
     }
   }
@@ -491,11 +498,21 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
 // and the partial sums are added in LDS in wave order (deterministic) before
 // wave 0 stores y.  A single matrix of in_proj has only 67 blocks of 128
 // rows, out_proj 16, so without the split most CUs would idle.
-template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS>
+//
+// RMS (XD only; a decoding block's normalization fused into the staging):
+// x is not given; each batch row b of the float32 source xr is normalized,
+//   x[b, k] = bf16(xr[b, k] / sqrt(mean_k xr[b, k]^2 + eps) * nw[k]),
+// by every workgroup for itself: the source rows and the weight arrive by
+// direct-to-LDS loads like the raw x, the sums of squares are taken per
+// 16-column piece and then per row in a fixed order (deterministic).
+// accum: y += the product instead of y = (each element has one owner lane).
+template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS, bool RMS>
 __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
     const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
-    int64_t xms, int64_t yms, float* __restrict__ y) {
+    int64_t xms, int64_t yms, float* __restrict__ y, const float* __restrict__ xr,
+    const float* __restrict__ nw, float eps, int accum) {
+  static_assert(!RMS || XD, "the fused normalization stages x directly");
   using Plan = SlotPlan<G, SK, SW>;
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int CPS = SK / 128;
@@ -522,10 +539,17 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   const int xoff = WAVES * RING * Plan::kSlotBytes;
   uint8_t* xs = smem + xoff;
   const int64_t KR = (K + 511) / 512 * 512;  // XD: raw x row length
-  const int xarea = XD && B * KR * 2 > R * xstride ? (int)(B * KR * 2) : R * xstride;
+  constexpr int kRawBytes = RMS ? 4 : 2;     // XD: bytes per raw x value
+  const int xarea = XD && B * KR * kRawBytes > R * xstride ? (int)(B * KR * kRawBytes)
+                                                           : R * xstride;
   const int eoff = xoff + xarea;
   uint8_t* es = smem + eoff;
   const int zoff = eoff + (R * estride + 15) / 16 * 16;
+  // RMS: norm weight [KR] | per-piece sums of squares [2 x 64 WAVES] | row factors [4]
+  const int woff = zoff + 128;
+  float* wls = reinterpret_cast<float*>(smem + woff);
+  float* part = wls + KR;
+  float* rfac = part + 2 * 64 * WAVES;
 
   Plan plan;
   plan.init(lane);
@@ -571,33 +595,104 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   };
 
   if constexpr (XD) {
-    // raw x (row b, columns 512 p .. 512 p + 511 per load; a load past K
-    // re-reads the row's last 16 bytes into the row's pad), then the codes
-    const int xl = B * (int)(KR / 512);
-    for (int pi = wave; pi < xl; pi += WAVES) {
-      const int b = pi / (int)(KR / 512), p = pi % (int)(KR / 512);
-      int64_t e = 512 * (int64_t)p + 8 * lane;
-      e = e < K - 8 ? e : K - 8;
-      gemv_dma16(xm + (int64_t)b * K, (uint32_t)(2 * e),
-                 lds0 + xoff + 2 * (uint32_t)(b * KR + 512 * p));
+    if constexpr (RMS) {
+      // float32 source rows b < B, then the norm weight as row B (columns
+      // 256 p .. 256 p + 255 per load; a load past K re-reads the row's
+      // last 16 bytes into the row's pad)
+      const int per = (int)(KR / 256);
+      const float* xrm = xr + mat * xms;
+      for (int pi = wave; pi < (B + 1) * per; pi += WAVES) {
+        const int b = pi / per, p = pi % per;
+        int64_t e = 256 * (int64_t)p + 4 * lane;
+        e = e < K - 4 ? e : K - 4;
+        if (b < B)
+          gemv_dma16(xrm + (int64_t)b * K, (uint32_t)(4 * e),
+                     lds0 + xoff + 4 * (uint32_t)(b * KR + 256 * p));
+        else
+          gemv_dma16(nw, (uint32_t)(4 * e), lds0 + woff + 4 * (uint32_t)(256 * p));
+      }
+    } else {
+      // raw x (row b, columns 512 p .. 512 p + 511 per load; a load past K
+      // re-reads the row's last 16 bytes into the row's pad), then the codes
+      const int xl = B * (int)(KR / 512);
+      for (int pi = wave; pi < xl; pi += WAVES) {
+        const int b = pi / (int)(KR / 512), p = pi % (int)(KR / 512);
+        int64_t e = 512 * (int64_t)p + 8 * lane;
+        e = e < K - 8 ? e : K - 8;
+        gemv_dma16(xm + (int64_t)b * K, (uint32_t)(2 * e),
+                   lds0 + xoff + 2 * (uint32_t)(b * KR + 512 * p));
+      }
     }
     for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");  // own x landed
     __syncthreads();
     // this thread's pieces (16 columns of one batch row, up to whole chunks)
     const int pieces = (int)((K + 127) / 128 * 8);
-    const uint16_t* xraw = reinterpret_cast<const uint16_t*>(xs);
     uint32_t wv[kXPieces][8];
+    if constexpr (RMS) {
+      const float* fraw = reinterpret_cast<const float*>(xs);
+      float v[kXPieces][16];
 #pragma unroll
-    for (int m = 0; m < kXPieces; ++m) {
-      const int i = threadIdx.x + 64 * WAVES * m;
-      const int b = i / pieces, col = 16 * (i % pieces);
-      const bool live = b < B && col < K;
-      const int e = live ? (int)(b * KR) + col : 0;
-      const u32x4 v0 = *reinterpret_cast<const u32x4*>(xraw + e);
-      const u32x4 v1 = *reinterpret_cast<const u32x4*>(xraw + e + 8);
-      wv[m][0] = v0.x; wv[m][1] = v0.y; wv[m][2] = v0.z; wv[m][3] = v0.w;
-      wv[m][4] = v1.x; wv[m][5] = v1.y; wv[m][6] = v1.z; wv[m][7] = v1.w;
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        const int b = i / pieces, col = 16 * (i % pieces);
+        const bool live = b < B && col < K;
+        const int e = live ? (int)(b * KR) + col : 0;
+        float sq = 0.f;
+#pragma unroll
+        for (int c = 0; c < 16; c += 4) {
+          const u32x4 t = *reinterpret_cast<const u32x4*>(fraw + e + c);
+          v[m][c] = live ? __uint_as_float(t.x) : 0.f;
+          v[m][c + 1] = live ? __uint_as_float(t.y) : 0.f;
+          v[m][c + 2] = live ? __uint_as_float(t.z) : 0.f;
+          v[m][c + 3] = live ? __uint_as_float(t.w) : 0.f;
+        }
+#pragma unroll
+        for (int c = 0; c < 16; ++c) sq = __builtin_fmaf(v[m][c], v[m][c], sq);
+        if (b < B) part[i] = sq;
+      }
+      __syncthreads();
+      if (wave < B) {  // row `wave`: its pieces' sums in a fixed order
+        float sq = 0.f;
+        for (int j = lane; j < pieces; j += 64) sq += part[wave * pieces + j];
+        sq += __shfl_xor(sq, 1);
+        sq += __shfl_xor(sq, 2);
+        sq += __shfl_xor(sq, 4);
+        sq += __shfl_xor(sq, 8);
+        sq += __shfl_xor(sq, 16);
+        sq += __shfl_xor(sq, 32);
+        if (lane == 0) rfac[wave] = 1.f / sqrtf(sq / (float)K + eps);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        const int b = i / pieces, col = 16 * (i % pieces);
+        const bool live = b < B && col < K;
+        const float r = live ? rfac[b] : 0.f;
+        const int wc = live ? col : 0;
+#pragma unroll
+        for (int c = 0; c < 16; c += 2) {
+          const uint32_t lo = __float_as_uint(v[m][c] * r * wls[wc + c]);
+          const uint32_t hi = __float_as_uint(v[m][c + 1] * r * wls[wc + c + 1]);
+          const uint32_t blo = (lo + 0x7FFFu + ((lo >> 16) & 1u)) >> 16;   // round to
+          const uint32_t bhi = (hi + 0x7FFFu + ((hi >> 16) & 1u)) >> 16;   // nearest even
+          wv[m][c / 2] = blo | (bhi << 16);
+        }
+      }
+    } else {
+      const uint16_t* xraw = reinterpret_cast<const uint16_t*>(xs);
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        const int b = i / pieces, col = 16 * (i % pieces);
+        const bool live = b < B && col < K;
+        const int e = live ? (int)(b * KR) + col : 0;
+        const u32x4 v0 = *reinterpret_cast<const u32x4*>(xraw + e);
+        const u32x4 v1 = *reinterpret_cast<const u32x4*>(xraw + e + 8);
+        wv[m][0] = v0.x; wv[m][1] = v0.y; wv[m][2] = v0.z; wv[m][3] = v0.w;
+        wv[m][4] = v1.x; wv[m][5] = v1.y; wv[m][6] = v1.z; wv[m][7] = v1.w;
+      }
     }
     __syncthreads();  // every raw piece has been read: the A rows overwrite them
 #pragma unroll
@@ -685,7 +780,7 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
           for (int i = 0; i < H; ++i, ++t) acc[r][j][i] += other[64 * t + lane];
     }
   }
-  store_rows<NR, H>(acc, B, N, rowb, l16, q, y + mat * yms);
+  store_rows<NR, H>(acc, B, N, rowb, l16, q, y + mat * yms, accum != 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -694,7 +789,9 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
 
 template <int G, int WAVES, bool KS>
 static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
-                            int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+                            int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream,
+                            const float* xr = nullptr, const float* nw = nullptr, float eps = 0.f,
+                            int accum = 0) {
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int SK = kGemvSlotK;
   constexpr int RING = kGemvRing;
@@ -719,16 +816,45 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
     const size_t ea = ((size_t)rows * (KP / 32) + 15) / 16 * 16;
     return (size_t)WAVES * slot_bytes + xa + ea + 128;
   };
+  if (xr) {  // fused normalization: x staged directly, one part over all of K
+    const int pieces = (int)((K + 127) / 128 * 8);
+    if (R > 16 || B * pieces > 2 * 64 * WAVES) return hipErrorInvalidValue;
+    KP = (K + SK - 1) / SK * SK;
+    const size_t xa = (size_t)R * (KP + kGemvXPad) > (size_t)B * KR * 4
+                          ? (size_t)R * (KP + kGemvXPad) : (size_t)B * KR * 4;
+    const size_t ea = ((size_t)R * (KP / 32) + 15) / 16 * 16;
+    const size_t aux = (size_t)KR * 4 + 2 * 64 * WAVES * 4 + 16;
+#define TM_GEMV_RMS(SW_)                                                                     \
+  do {                                                                                        \
+    const size_t lds = (size_t)WAVES * RING * SlotPlan<G, SK, SW_>::kSlotBytes + xa + ea + 128 + \
+                       aux;                                                                   \
+    if (lds > 160 * 1024) return hipErrorInvalidValue;                                        \
+    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, SW_, true, KS, true>), grid, block, \
+                       lds, stream, nullptr, codes, s16, B, N, K, KP, (int64_t)B * K,         \
+                       (int64_t)B * N, y, xr, nw, eps, accum);                                \
+  } while (0)
+    if constexpr (SK / G >= 2) {
+      if (sw) {
+        TM_GEMV_RMS(true);
+        return hipGetLastError();
+      }
+    }
+    TM_GEMV_RMS(false);
+#undef TM_GEMV_RMS
+    return hipGetLastError();
+  }
 #define TM_GEMV_LAUNCH(NR_, SW_, BP, B0)                                                      \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, SW_, false, KS>), grid, block,     \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, NR_, SW_, false, KS, false>), grid,     \
+                     block,                                                                   \
                      lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, kTerms * (BP) * H, false), \
                      stream, x + (int64_t)(B0) * K, codes, s16, BP, N, K, KP, (int64_t)B * K,  \
-                     (int64_t)B * N, y + (int64_t)(B0) * N)
+                     (int64_t)B * N, y + (int64_t)(B0) * N, nullptr, nullptr, 0.f, 0)
   if (xd) {  // the common decode case: R <= 16
 #define TM_GEMV_XD(SW_)                                                                       \
-  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, SW_, true, KS>), grid, block,        \
+  hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, SW_, true, KS, false>), grid, block, \
                      lds_of(RING * SlotPlan<G, SK, SW_>::kSlotBytes, R, true), stream, x,     \
-                     codes, s16, B, N, K, KP, (int64_t)B * K, (int64_t)B * N, y)
+                     codes, s16, B, N, K, KP, (int64_t)B * K, (int64_t)B * N, y, nullptr,      \
+                     nullptr, 0.f, 0)
     if constexpr (SK / G >= 2) {
       if (sw) {
         TM_GEMV_XD(true);
@@ -763,27 +889,48 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
 // whose A rows fit one 16-row operand.
 template <int G>
 static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
-                           int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream) {
+                           int count, int B, int64_t N, int64_t K, float* y, hipStream_t stream,
+                           const float* xr, const float* nw, float eps, int accum) {
   const int64_t blocks = (int64_t)count * ((N + 127) / 128);
   const int64_t nslot = (K + kGemvSlotK - 1) / kGemvSlotK;
   const int R = kTerms * B * (G < 128 ? 128 / G : 1);  // A rows: one 16-row operand when <= 16
-  if (blocks < 2 * (int64_t)current_cu_count() && nslot >= 2 && R <= 16) {
-    if (nslot >= 8) return launch_gw<G, 8, true>(x, codes, s16, count, B, N, K, y, stream);
-    return launch_gw<G, kGemvWaves, true>(x, codes, s16, count, B, N, K, y, stream);
+  // the fused form (one matrix) takes the split form whenever K has two slots
+  if ((xr || blocks < 2 * (int64_t)current_cu_count()) && nslot >= 2 && R <= 16) {
+    if (nslot >= 8)
+      return launch_gw<G, 8, true>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    return launch_gw<G, kGemvWaves, true>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps,
+                                          accum);
   }
-  return launch_gw<G, kGemvWaves, false>(x, codes, s16, count, B, N, K, y, stream);
+  return launch_gw<G, kGemvWaves, false>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps,
+                                         accum);
+}
+
+static hipError_t launch_any_g(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
+                               int count, int B, int64_t N, int64_t K, int g, float* y,
+                               hipStream_t stream, const float* xr, const float* nw, float eps,
+                               int accum) {
+  switch (g) {
+    case 32:  return launch_g<32>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    case 64:  return launch_g<64>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    case 128: return launch_g<128>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    case 256: return launch_g<256>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    case 512: return launch_g<512>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream) {
-  switch (g) {
-    case 32:  return launch_g<32>(x, codes, s16, count, B, N, K, y, stream);
-    case 64:  return launch_g<64>(x, codes, s16, count, B, N, K, y, stream);
-    case 128: return launch_g<128>(x, codes, s16, count, B, N, K, y, stream);
-    case 256: return launch_g<256>(x, codes, s16, count, B, N, K, y, stream);
-    case 512: return launch_g<512>(x, codes, s16, count, B, N, K, y, stream);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_any_g(x, codes, s16, count, B, N, K, g, y, stream, nullptr, nullptr, 0.f, 0);
+}
+
+static_assert(kTerms == 4 && kGemvSlotK == 512 && kGemvWaves == 4,
+              "tgemv_rms_fits (launchers.hpp) assumes this launch shape");
+
+hipError_t launch_tgemv_rms(const float* src, const float* nw, float eps, const uint8_t* codes,
+                            const uint16_t* s16, int B, int64_t N, int64_t K, int g, float* y,
+                            int accum, hipStream_t stream) {
+  return launch_any_g(nullptr, codes, s16, 1, B, N, K, g, y, stream, src, nw, eps, accum);
 }
 
 }  // namespace tmk

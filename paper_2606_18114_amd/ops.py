@@ -48,6 +48,11 @@ SIGNATURES = {
                                      _P, ctypes.c_float, _P, _P, _P]),
     "tm_scale_ste_grad": (ctypes.c_int,
                           [_P, _P, _P, _P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P]),
+    "tm_tgemv_rms": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _P, _I32, _I64, _I64, _I32, _P,
+                                    _I32, _P]),
+    "tm_dgemv_rms": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I32, _I64, _I64, _P, _I32, _P]),
+    "tm_mixer_gate": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
+                                     _P, _P]),
 }
 
 
@@ -353,8 +358,97 @@ def dgemv(x: torch.Tensor, W16: torch.Tensor, y: Optional[torch.Tensor] = None) 
     return y
 
 
+def _rms_args(src, norm_w, y, N):
+    _need(src, "src", _F32, 2)
+    B, K = src.shape
+    _need(norm_w, "norm_w", _F32, 1)
+    _shape(norm_w, "norm_w", (K,), src.device)
+    if y is None:
+        y = torch.empty((B, N), dtype=torch.float32, device=src.device)
+    _need(y, "y", _F32, 2)
+    _shape(y, "y", (B, N), src.device)
+    return B, K, y
+
+
+def tgemv_rms(src: torch.Tensor, codes: torch.Tensor, scales_f16: torch.Tensor, g: int,
+              norm_w: torch.Tensor, eps: float = 1e-5, y: Optional[torch.Tensor] = None,
+              accumulate: bool = False) -> torch.Tensor:
+    """Fused decode projection (tm_tgemv_rms): src float32 [B, K] is
+    normalized per row (RMSNorm with weight norm_w, rounded to bfloat16) and
+    multiplied by one packed matrix (codes uint8 [N, K/4], scales_f16
+    [N, K/g]); y float32 [B, N] = the product, or += it when accumulate."""
+    _need(codes, "codes", _U8, 2)
+    N = codes.shape[0]
+    B, K, y = _rms_args(src, norm_w, y, N)
+    _need(scales_f16, "scales_f16", _F16, 2)
+    _shape(codes, "codes", (N, K // 4), src.device)
+    _shape(scales_f16, "scales_f16", (N, _groups(K, g)), src.device)
+    st = lib().tm_tgemv_rms(_ptr(src), _ptr(norm_w), eps, _ptr(codes), _ptr(scales_f16), B, N, K,
+                            g, _ptr(y), int(bool(accumulate)), _stream())
+    _check("tm_tgemv_rms", st)
+    return y
+
+
+def dgemv_rms(src: torch.Tensor, W16: torch.Tensor, norm_w: torch.Tensor, eps: float = 1e-5,
+              y: Optional[torch.Tensor] = None, accumulate: bool = False) -> torch.Tensor:
+    """tgemv_rms for one matrix kept in float16: W16 float16 [N, K]."""
+    _need(W16, "W16", _F16, 2)
+    N = W16.shape[0]
+    B, K, y = _rms_args(src, norm_w, y, N)
+    _shape(W16, "W16", (N, K), src.device)
+    st = lib().tm_dgemv_rms(_ptr(src), _ptr(norm_w), eps, _ptr(W16), B, N, K, _ptr(y),
+                            int(bool(accumulate)), _stream())
+    _check("tm_dgemv_rms", st)
+    return y
+
+
 MIXER_HEADDIM = 64
 MIXER_DSTATE = 128
+
+
+def _mixer_args(zxbcdt, conv_state, conv_pos, ssm_state, A_log, params):
+    """Shape and dtype checks shared by mixer_step and mixer_gate; params:
+    (tensor, name) pairs of the per-channel and per-head parameters."""
+    _need(zxbcdt, "zxbcdt", _F32, 2)
+    B = zxbcdt.shape[0]
+    _need(A_log, "A_log", _F32, 1)
+    H = A_log.shape[0]
+    P, N = MIXER_HEADDIM, MIXER_DSTATE
+    di, cd = H * P, H * P + 2 * N
+    dev = zxbcdt.device
+    _shape(zxbcdt, "zxbcdt", (B, 2 * di + 2 * N + H), dev)
+    _need(conv_state, "conv_state", _F16, 3)
+    _shape(conv_state, "conv_state", (B, cd, 4), dev)
+    _need(conv_pos, "conv_pos", (torch.int32,), 1)
+    _shape(conv_pos, "conv_pos", (1,), dev)
+    _need(ssm_state, "ssm_state", _F16, 4)
+    _shape(ssm_state, "ssm_state", (B, H, P, N), dev)
+    shapes = {"conv_w": (cd, 4), "conv_b": (cd,), "dt_bias": (H,), "D": (H,), "norm_w": (di,)}
+    for t, name in params:
+        _need(t, name, _F32, len(shapes[name]))
+        _shape(t, name, shapes[name], dev)
+    return B, H, P, N, di, dev
+
+
+def mixer_gate(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.Tensor,
+               ssm_state: torch.Tensor, conv_w: torch.Tensor, conv_b: torch.Tensor,
+               dt_bias: torch.Tensor, A_log: torch.Tensor, D: torch.Tensor,
+               gated: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The mixer step up to the gated values (tm_mixer_gate): zxbcdt float32
+    [B, Z] -> gated float32 [B, d_inner] = y * SiLU(z), not normalized; the
+    states and conv_pos are updated in place as by mixer_step."""
+    B, H, P, N, di, dev = _mixer_args(
+        zxbcdt, conv_state, conv_pos, ssm_state, A_log,
+        ((conv_w, "conv_w"), (conv_b, "conv_b"), (dt_bias, "dt_bias"), (D, "D")))
+    if gated is None:
+        gated = torch.empty((B, di), dtype=torch.float32, device=dev)
+    _need(gated, "gated", _F32, 2)
+    _shape(gated, "gated", (B, di), dev)
+    st = lib().tm_mixer_gate(_ptr(zxbcdt), B, H, P, N, _ptr(conv_state), _ptr(conv_pos),
+                             _ptr(ssm_state), _ptr(conv_w), _ptr(conv_b), _ptr(dt_bias),
+                             _ptr(A_log), _ptr(D), _ptr(gated), _stream())
+    _check("tm_mixer_gate", st)
+    return gated
 
 
 def mixer_workspace(B: int, nheads: int, device) -> torch.Tensor:
@@ -374,24 +468,10 @@ def mixer_step(zxbcdt: torch.Tensor, conv_state: torch.Tensor, conv_pos: torch.T
     ring [B, conv_dim, 4]), conv_pos (int32 [1]) and ssm_state (float16
     [B, nheads, 64, 128]) are updated in place.  noalloc=True calls
     tm_mixer_step_noalloc (the library's own scratch array, no workspace)."""
-    _need(zxbcdt, "zxbcdt", _F32, 2)
-    B = zxbcdt.shape[0]
-    _need(A_log, "A_log", _F32, 1)
-    H = A_log.shape[0]
-    P, N = MIXER_HEADDIM, MIXER_DSTATE
-    di, cd = H * P, H * P + 2 * N
-    dev = zxbcdt.device
-    _shape(zxbcdt, "zxbcdt", (B, 2 * di + 2 * N + H), dev)
-    _need(conv_state, "conv_state", _F16, 3)
-    _shape(conv_state, "conv_state", (B, cd, 4), dev)
-    _need(conv_pos, "conv_pos", (torch.int32,), 1)
-    _shape(conv_pos, "conv_pos", (1,), dev)
-    _need(ssm_state, "ssm_state", _F16, 4)
-    _shape(ssm_state, "ssm_state", (B, H, P, N), dev)
-    for t, name, shp in ((conv_w, "conv_w", (cd, 4)), (conv_b, "conv_b", (cd,)),
-                         (dt_bias, "dt_bias", (H,)), (D, "D", (H,)), (norm_w, "norm_w", (di,))):
-        _need(t, name, _F32, len(shp))
-        _shape(t, name, shp, dev)
+    B, H, P, N, di, dev = _mixer_args(
+        zxbcdt, conv_state, conv_pos, ssm_state, A_log,
+        ((conv_w, "conv_w"), (conv_b, "conv_b"), (dt_bias, "dt_bias"), (D, "D"),
+         (norm_w, "norm_w")))
     if out is None:
         out = torch.empty((B, di), dtype=torch.bfloat16, device=dev)
     _need(out, "out", _BF16, 2)

@@ -156,30 +156,49 @@ class DecodeStack:
 __all__ = ["keep_first_last", "quantize_projections", "DecodeStack", "PROJECTIONS"]
 
 
+def rms_fused_fits(B: int, K: int, g: int) -> bool:
+    """Whether tm_tgemv_rms takes B rows of K columns at group size g (the
+    rule its declaration states: one workgroup stages all rows at once)."""
+    H = 128 // g if g < 128 else 1
+    pieces = (K + 127) // 128 * 8
+    waves = 8 if (K + 511) // 512 >= 8 else 4
+    return 4 * B * H <= 16 and B * pieces <= 2 * 64 * waves
+
+
 class Mamba2Decoder:
     """Batch-B decode through L Mamba-2 blocks in layer order, every step on
-    the library's kernels:
+    the library's kernels.  Fused (the default where the shapes allow it),
+    three launches per layer:
+
+        zx  = in_proj(rmsnorm(residual) * w_pre[l])       tm_tgemv_rms / tm_dgemv_rms
+        g   = mixer step up to the gate (conv, FP16 SSM)  tm_mixer_gate
+        residual += out_proj(rmsnorm(g) * norm_w[l])      tm_tgemv_rms / tm_dgemv_rms
+
+    or unfused, five (each normalization its own launch):
 
         x   = rmsnorm(residual += y_prev) * w_pre[l]      tm_residual_rmsnorm
         zx  = in_proj(x)                                  tm_tgemv / tm_dgemv (kept)
         m   = mixer step (conv, FP16 SSM, gated norm)     tm_mixer_step
         y   = out_proj(m)                                 tm_tgemv / tm_dgemv (kept)
 
-    and after the last layer the residual takes y and the final norm gives
-    ``x_out`` (the lm head is outside).  Five launches per layer, all
-    on the current stream with fixed buffers, so a token can be captured once
-    as a HIP graph (``capture``) and replayed.
+    After the last layer the final norm of the residual gives ``x_out`` (the
+    lm head is outside).  All launches go to the current stream with fixed
+    buffers, so a token can be captured once as a HIP graph (``capture``) and
+    replayed.
 
     weight(kind, l) -> float32 [N, K] master weights (kind "in": [Z, d_model],
     "out": [d_model, d_inner]); mixer(l) -> dict of float32 arrays conv_w,
     conv_b, dt_bias, A_log, D, norm_w (see ops.mixer_step); pre_norm(l) ->
     float32 [d_model].  Layers in ``keep`` stay in float16 (Sec. 7).
+    fused: None picks the fused form whenever every projection's shape
+    allows it (batch up to 4 at g >= 128 for the Mamba-2 1.3B shapes).
     """
 
     def __init__(self, weight: Callable[[str, int], torch.Tensor], mixer: Callable[[int], dict],
                  pre_norm: Callable[[int], torch.Tensor], n_layers: int, d_model: int,
                  nheads: int, keep: Iterable[int] = (), g: int = 128, eps: float = 1e-5,
-                 batch: int = 1, device: Optional[torch.device] = None):
+                 batch: int = 1, device: Optional[torch.device] = None,
+                 fused: Optional[bool] = None):
         dev = device or torch.device("cuda")
         self.L, self.B, self.g, self.eps = n_layers, batch, g, eps
         self.keep = set(keep)
@@ -188,6 +207,11 @@ class Mamba2Decoder:
         self.d_inner = nheads * P
         self.Z = 2 * self.d_inner + 2 * N + nheads
         conv_dim = self.d_inner + 2 * N
+        fits = all(rms_fused_fits(batch, k, g) if l not in self.keep else batch * k <= 16384
+                   for l in range(n_layers) for k in (d_model, self.d_inner))
+        if fused and not fits:
+            raise ValueError(f"batch {batch} does not fit the fused decode at g = {g}")
+        self.fused = fits if fused is None else bool(fused)
         self.layers = []
         for l in range(n_layers):
             lay = {}
@@ -219,6 +243,7 @@ class Mamba2Decoder:
         self.zx = torch.empty((1, batch, self.Z), dtype=torch.float32, device=dev)
         self.m = torch.empty((1, batch, self.d_inner), dtype=torch.bfloat16, device=dev)
         self.y = torch.empty((1, batch, d_model), dtype=torch.float32, device=dev)
+        self.gated = torch.empty((batch, self.d_inner), dtype=torch.float32, device=dev)
         self.ws = ops.mixer_workspace(batch, nheads, dev)
         self.x_out = torch.empty((batch, d_model), dtype=torch.bfloat16, device=dev)
         self.graph = None
@@ -238,16 +263,32 @@ class Mamba2Decoder:
         else:
             ops.tgemv(x, p[1], p[2], self.g, y=y)
 
+    def _proj_rms(self, lay, kind, src, norm_w, y, accumulate) -> None:
+        p = lay[kind]
+        if p[0] == "dense":
+            ops.dgemv_rms(src, p[1][0], norm_w, self.eps, y=y, accumulate=accumulate)
+        else:
+            ops.tgemv_rms(src, p[1][0], p[2][0], self.g, norm_w, self.eps, y=y,
+                          accumulate=accumulate)
+
     def layer_step(self, l: int) -> None:
-        """Layer l of a token: pre-norm (taking the previous layer's output
+        """Layer l of a token.  Fused: in_proj of the normalized residual,
+        the mixer up to the gate, out_proj of the normalized gate added into
+        the residual.  Unfused: pre-norm (taking the previous layer's output
         into the residual), in_proj, mixer step, out_proj into ``y``."""
         lay = self.layers[l]
         if l == 0:
             self.residual.copy_(self.emb)
+        mp = lay["mixer"]
+        if self.fused:
+            self._proj_rms(lay, "in", self.residual, lay["pre"], self.zx[0], False)
+            ops.mixer_gate(self.zx[0], lay["conv"], lay["pos"], lay["ssm"], mp["conv_w"],
+                           mp["conv_b"], mp["dt_bias"], mp["A_log"], mp["D"], gated=self.gated)
+            self._proj_rms(lay, "out", self.gated, mp["norm_w"], self.residual, True)
+            return
         ops.residual_rmsnorm(self.residual, None if l == 0 else self.y[0], lay["pre"], self.eps,
                              x=self.x[0])
         self._proj(lay, "in", self.x, self.zx)
-        mp = lay["mixer"]
         ops.mixer_step(self.zx[0], lay["conv"], lay["pos"], lay["ssm"], mp["conv_w"],
                        mp["conv_b"], mp["dt_bias"], mp["A_log"], mp["D"], mp["norm_w"], self.eps,
                        workspace=self.ws, out=self.m[0])
@@ -258,7 +299,8 @@ class Mamba2Decoder:
         layer; returns ``x_out`` = final norm of the residual (bfloat16)."""
         for l in range(self.L):
             self.layer_step(l)
-        ops.residual_rmsnorm(self.residual, self.y[0], self.final_norm, self.eps, x=self.x_out)
+        ops.residual_rmsnorm(self.residual, None if self.fused else self.y[0], self.final_norm,
+                             self.eps, x=self.x_out)
         return self.x_out
 
     def capture(self) -> None:
@@ -278,7 +320,9 @@ class Mamba2Decoder:
         return self.x_out
 
     def launches_per_token(self) -> int:
-        return 5 * self.L + 1 + 1   # pre-norm, in_proj, mixer (2), out_proj per layer; copy, final norm
+        # per layer: in_proj, mixer, out_proj (fused) or pre-norm, in_proj,
+        # mixer (2), out_proj; then the residual copy and the final norm
+        return (3 if self.fused else 5) * self.L + 2
 
     def bytes_per_token(self) -> float:
         """Algorithmic HBM bytes of one token: packed or float16 projection
@@ -300,4 +344,4 @@ class Mamba2Decoder:
         return total
 
 
-__all__.append("Mamba2Decoder")
+__all__ += ["Mamba2Decoder", "rms_fused_fits"]

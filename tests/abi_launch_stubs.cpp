@@ -50,6 +50,20 @@ hipError_t launch_dgemv(const uint16_t*, const uint16_t*, int, int, int64_t, int
   reached("dgemv");
 }
 
+hipError_t launch_tgemv_rms(const float*, const float*, float, const uint8_t*, const uint16_t*,
+                            int, int64_t, int64_t, int, float*, int, hipStream_t) {
+  reached("tgemv_rms");
+}
+hipError_t launch_dgemv_rms(const float*, const float*, float, const uint16_t*, int, int64_t,
+                            int64_t, float*, int, hipStream_t) {
+  reached("dgemv_rms");
+}
+hipError_t launch_mixer_gate(const float*, int, int, uint16_t*, int*, uint16_t*, const float*,
+                             const float*, const float*, const float*, const float*, float*,
+                             hipStream_t) {
+  reached("mixer_gate");
+}
+
 hipError_t launch_mixer_step(const float*, int, int, uint16_t*, int*, uint16_t*, const float*,
                              const float*, const float*, const float*, const float*, const float*,
                              float, float*, uint16_t*, hipStream_t) {

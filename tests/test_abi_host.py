@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 8
+    assert L.tm_abi_version() == 9
 
 
 def test_status_strings(L):
@@ -233,6 +233,69 @@ def test_mixer_step_validation(L):
     assert mx(L, out=P + 2 ** 22) == EINVAL               # out over the SSM state
     assert mx(L, ws=P + 16) == EINVAL                     # workspace over zxbcdt
     assert mx(L, pos=P + 2 ** 24 + 64) == EINVAL          # conv_pos inside conv_w
+
+
+def tr(L, src=P, nw=P + 2 ** 20, eps=1e-5, codes=P + 2 ** 21, s16=P + 2 ** 24, B=1, N=8512,
+       K=2048, g=128, y=P + 2 ** 25, acc=0):
+    return L.tm_tgemv_rms(src, nw, eps, codes, s16, B, N, K, g, y, acc, None)
+
+
+def test_tgemv_rms_validation(L):
+    for kw in ("src", "nw", "codes", "s16", "y"):
+        assert tr(L, **{kw: 0}) == EINVAL, kw
+    assert tr(L, eps=-1.0) == EINVAL
+    assert tr(L, eps=float("nan")) == EINVAL
+    assert tr(L, acc=2) == EINVAL
+    assert tr(L, B=0) == ESHAPE
+    assert tr(L, N=0) == ESHAPE
+    assert tr(L, K=2000) == ESHAPE
+    assert tr(L, g=100) == ESHAPE
+    assert tr(L, B=5) == ESHAPE                 # 20 A rows: more than one operand
+    assert tr(L, B=3, g=64) == ESHAPE           # 4 * 3 * 2 = 24 A rows
+    assert tr(L, B=4, K=3584) == ESHAPE         # 4 * 224 pieces > 512 (4 waves)
+    assert tr(L, src=P + 8) == EALIGN
+    assert tr(L, nw=P + 2 ** 20 + 4) == EALIGN
+    assert tr(L, y=P + 2 ** 25 + 4) == EALIGN
+    assert tr(L, y=P + 4096) == EINVAL          # y over src
+    assert tr(L, y=P + 2 ** 20) == EINVAL       # y over the norm weight
+    assert tr(L, y=P + 2 ** 21 + 2 ** 20) == EINVAL  # y over the codes
+
+
+def dr(L, src=P, nw=P + 2 ** 20, eps=1e-5, W=P + 2 ** 21, B=1, N=2048, K=4096,
+       y=P + 2 ** 26, acc=1):
+    return L.tm_dgemv_rms(src, nw, eps, W, B, N, K, y, acc, None)
+
+
+def test_dgemv_rms_validation(L):
+    for kw in ("src", "nw", "W", "y"):
+        assert dr(L, **{kw: 0}) == EINVAL, kw
+    assert dr(L, eps=float("inf")) == EINVAL
+    assert dr(L, acc=-1) == EINVAL
+    assert dr(L, B=0) == ESHAPE
+    assert dr(L, B=9, K=64) == ESHAPE
+    assert dr(L, K=1000) == ESHAPE
+    assert dr(L, B=5) == ESHAPE                 # 5 * 4096 > 16384
+    assert dr(L, src=P + 4) == EALIGN
+    assert dr(L, y=P + 2 ** 26 + 2) == EALIGN
+    assert dr(L, y=P + 2 ** 21 + 64) == EINVAL  # y over W
+    assert dr(L, y=P + 2 ** 20 + 4) == EINVAL   # y over the norm weight
+
+
+def mg(L, z=P, B=1, H=64, hd=64, ds=128, cs=P + 2 ** 20, pos=P + 2 ** 21, ss=P + 2 ** 22,
+       cw=P + 2 ** 24, cb=P + 2 ** 25, dtb=P + 2 ** 26, al=P + 2 ** 26 + 4096,
+       D=P + 2 ** 26 + 8192, gated=P + 2 ** 28):
+    return L.tm_mixer_gate(z, B, H, hd, ds, cs, pos, ss, cw, cb, dtb, al, D, gated, None)
+
+
+def test_mixer_gate_validation(L):
+    for kw in ("z", "cs", "pos", "ss", "cw", "cb", "dtb", "al", "D", "gated"):
+        assert mg(L, **{kw: 0}) == EINVAL, kw
+    assert mg(L, B=0) == ESHAPE
+    assert mg(L, hd=128) == ESHAPE
+    assert mg(L, gated=P + 2 ** 28 + 2) == EALIGN          # float32 output
+    assert mg(L, gated=P + 2 ** 22 + 64) == EINVAL         # gated over the SSM state
+    assert mg(L, gated=P + 8) == EINVAL                    # gated over zxbcdt
+    assert mg(L, pos=P + 2 ** 28 + 4) == EINVAL            # conv_pos inside gated
 
 
 def rn(L, r=P, y=P + 2 ** 20, B=2, D=2048, w=P + 2 ** 21, eps=1e-5, x=P + 2 ** 22):

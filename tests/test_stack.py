@@ -54,8 +54,10 @@ def test_quantize_projections_keeps_the_selected_blocks():
 @pytest.mark.parametrize("B", [1, 4])
 def test_mixed_stack_decode_token(B):
     """Six layers, the first and last kept in FP16: every layer's in_proj and
-    out_proj output against the oracle (ternary layers with the stack's own
-    codes and float16 scales, kept layers with their float16 weights)."""
+    out_proj output against the oracle (ternary layers ternarized by the
+    oracle, kept layers with their float16 weights).  The stack's codes equal
+    the oracle's off the rounding-boundary band; a band element whose code
+    differs widens that output's bar by its own product."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2606_18114_amd.stack import DecodeStack, keep_first_last
@@ -78,13 +80,27 @@ def test_mixed_stack_decode_token(B):
                 W16 = Ws[(k, l)].astype(np.float16)
                 assert np.array_equal(st.w16[k][st.keep.index(l)].cpu().numpy(), W16)
                 ref = O.dense_gemv(xs[k][l], W16)
+                err = O.rel_fro_error(y[l], ref)
+                assert err <= 1e-6, (k, l, err)
             else:
+                s64, s32, q, _ = O.ternarize(Ws[(k, l)], g, 1e-5)
+                s16 = O.scales_f16(s32)
                 t = st.tern.index(l)
-                q = O.unpack(st.codes[k][t].cpu().numpy(), K)
-                s16 = st.s16[k][t].cpu().numpy()
+                q_gpu = O.unpack(st.codes[k][t].cpu().numpy(), K)
+                band = O.boundary_mask(Ws[(k, l)], s64, g, 1e-5)
+                assert np.array_equal(q_gpu[~band], q[~band]), (k, l)
+                s16_gpu = st.s16[k][t].cpu().numpy()
+                ds = np.abs(s16_gpu.astype(np.float64) - s16.astype(np.float64))
+                assert np.all(ds <= np.spacing(s16).astype(np.float64)), (k, l)
                 ref = O.gemv(xs[k][l], q, s16, g)
-            err = O.rel_fro_error(y[l], ref)
-            assert err <= 1e-6, (k, l, err)
+                xa = np.abs(synth.bf16_bits_to_f32(xs[k][l]).astype(np.float64))
+                sw = np.abs(O.dequantize(np.ones_like(q), s16.astype(np.float64), g))
+                # a code off by up to 2 (band elements), a scale off by one step
+                moved = (q_gpu != q) * 2 * (sw + O.dequantize(np.ones_like(q), ds, g)) \
+                    + np.abs(O.dequantize(q, ds, g))
+                bar = 1e-6 * (xa @ np.abs(O.dequantize(q, s16.astype(np.float64), g)).T) \
+                    + xa @ moved.T + 1e-30
+                assert np.all(np.abs(y[l] - ref) <= bar), (k, l)
     # bytes: 4 ternary layers of codes + scales, 2 kept layers in float16
     exp = sum(4 * (N * K / 4 + 2 * N * K / g) + 2 * 2 * N * K + L * (2 * B * K + 4 * B * N)
               for N, K in shapes.values())
