@@ -240,9 +240,9 @@ tm_status tm_residual_rmsnorm(float* residual, const float* y, int32_t B, int64_
  *
  *   zxbcdt      float32 [B, 2 d_inner + 2 d_state + nheads]   in
  *   B 1 .. 65535;  nheads 1 .. 4096;  headdim == 64;  d_state == 128
- *   conv_state  float16 [B, conv_dim, 4]   in/out: a ring of the last 4
- *               inputs per channel; slot (pos + j) % 4 holds the j-th
- *               oldest, j = 0 .. 3 (pos = 0: slots in time order)
+ *   conv_state  float16 [B, conv_dim, 4]   in/out (8-byte aligned): a ring
+ *               of the last 4 inputs per channel; slot (pos + j) % 4 holds
+ *               the j-th oldest, j = 0 .. 3 (pos = 0: slots in time order)
  *   conv_pos    int32 [1]   in/out: pos, advanced by one (mod 4) per call
  *   ssm_state   float16 [B, nheads, 64, 128]  in/out (16-byte aligned);
  *               updated in float32 and rounded once to float16

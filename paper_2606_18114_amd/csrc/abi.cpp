@@ -96,7 +96,7 @@ tm_status mixer_checked(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
       !bytes_of((int64_t)B * nheads * headdim, d_state, 2, &sb) ||
       !bytes_of(B, di + nheads, 4, &wb) || !bytes_of(B, di, gate_only ? 4 : 2, &ob))
     return TM_ESHAPE;
-  if (!aligned(zxbcdt, 4) || !aligned(conv_state, 2) || !aligned(conv_pos, 4) ||
+  if (!aligned(zxbcdt, 4) || !aligned(conv_state, 8) || !aligned(conv_pos, 4) ||
       !aligned(ssm_state, 16) || !aligned(conv_w, 4) || !aligned(conv_b, 4) ||
       !aligned(dt_bias, 4) || !aligned(A_log, 4) || !aligned(D, 4) || !aligned(norm_w, 4) ||
       !aligned(workspace, 4) || !aligned(out, gate_only ? 4 : 2))

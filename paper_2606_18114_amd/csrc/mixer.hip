@@ -48,11 +48,13 @@ __device__ __forceinline__ uint16_t f2h(float f) {  // round to nearest even
 // conv [B, conv_dim, 4] float16 ring, ssm [B, nheads, P, N] float16,
 // gated [B, d_inner] and partial [B, nheads] float32.
 // GATE (the fused decode's form): no partial sums (the fused out_proj takes
-// its own), and the ring position advances here: every workgroup adds 4 to
-// the position word once it has read the position (the word's low two
-// bits), and the last one to arrive stores the next position with a zero
-// count.  Until then the low bits stay the position, so every read of it
-// is right, and no workgroup reads after the last one arrived.
+// its own), and the ring position advances here: every workgroup reads the
+// position word by adding 4 to it (one atomic, issued first, whose result
+// holds the position in its low two bits and the number of workgroups that
+// came before in the rest), and the last one to arrive stores the next
+// position with a zero count at its end.  No workgroup reads the word after
+// the last one has.  The ring slots of a channel are loaded all four at
+// once, before the position is known, and picked afterwards.
 template <bool GATE>
 __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
     const float* __restrict__ zxbcdt, int nheads, uint16_t* __restrict__ conv,
@@ -66,8 +68,9 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   const int conv_dim = d_inner + 2 * kMxN;
   const int64_t Z = (int64_t)2 * d_inner + 2 * kMxN + nheads;
   const float* row = zxbcdt + (int64_t)b * Z;
-  const int pos = conv_pos[0] & 3;
   __shared__ float u[kMxP + 2 * kMxN];  // x of the head, then B, then C (after SiLU)
+  __shared__ int pos_word;
+  if (GATE && tid == 0) pos_word = atomicAdd(conv_pos, 4);
   __shared__ float wsum[kMxThreads / 64];
   // thread t: channel p = t / 4, states n = 32 (t % 4) .. + 31; its 64 bytes
   // of state are loaded first
@@ -78,19 +81,44 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   for (int k = 0; k < 4; ++k) sv[k] = ld16(sp + 8 * k);
 
   // convolution: local channel i < 64 is x channel 64 h + i, then the B/C
-  // channels d_inner + (i - 64)
-  for (int i = tid; i < kMxP + 2 * kMxN; i += kMxThreads) {
+  // channels d_inner + (i - 64); a thread takes at most two channels
+  constexpr int kMxCh = (kMxP + 2 * kMxN + kMxThreads - 1) / kMxThreads;
+  uint32_t ring[kMxCh][2];
+  float xin[kMxCh];
+#pragma unroll
+  for (int t = 0; t < kMxCh; ++t) {
+    const int i = tid + t * kMxThreads;
+    if (i >= kMxP + 2 * kMxN) break;
     const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
-    const float xin = row[d_inner + c];
-    uint16_t* cs = conv + ((int64_t)b * conv_dim + c) * 4;
+    const u32x2 r2 = *reinterpret_cast<const u32x2*>(conv + ((int64_t)b * conv_dim + c) * 4);
+    ring[t][0] = r2.x;
+    ring[t][1] = r2.y;
+    xin[t] = row[d_inner + c];
+  }
+  int pos;
+  if constexpr (GATE) {
+    __syncthreads();  // the position word has arrived in LDS
+    pos = pos_word & 3;
+  } else {
+    pos = conv_pos[0] & 3;
+  }
+#pragma unroll
+  for (int t = 0; t < kMxCh; ++t) {
+    const int i = tid + t * kMxThreads;
+    if (i >= kMxP + 2 * kMxN) break;
+    const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
     const float* w = conv_w + (int64_t)c * 4;
+    auto slot = [&](int k) {  // float16 of ring slot k (0 .. 3)
+      const uint32_t wd = ring[t][k >> 1];
+      return h2f((uint16_t)((k & 1) ? wd >> 16 : wd & 0xFFFFu));
+    };
     float acc = conv_b[c];
 #pragma unroll
-    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(h2f(cs[(pos + 1 + j) & 3]), w[j], acc);
-    acc = __builtin_fmaf(xin, w[3], acc);
+    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(slot((pos + 1 + j) & 3), w[j], acc);
+    acc = __builtin_fmaf(xin[t], w[3], acc);
     u[i] = mx_silu(acc);
     // the slot nobody reads; the shared B/C channels are written by head 0
-    if (i < kMxP || h == 0) cs[pos] = f2h(xin);
+    if (i < kMxP || h == 0) conv[((int64_t)b * conv_dim + c) * 4 + pos] = f2h(xin[t]);
   }
   __syncthreads();
 
@@ -121,12 +149,8 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   const float g = y * mx_silu(row[h * kMxP + p]);
   if (q == 0) gated[(int64_t)b * d_inner + h * kMxP + p] = g;
   if constexpr (GATE) {
-    // every thread read the position before the barrier after the convolution
-    if (tid == 0) {
-      const int total = (int)(gridDim.x * gridDim.y);
-      const int old = atomicAdd(conv_pos, 4);
-      if ((old >> 2) == total - 1) atomicExch(conv_pos, (old + 1) & 3);
-    }
+    if (tid == 0 && (pos_word >> 2) == (int)(gridDim.x * gridDim.y) - 1)
+      atomicExch(conv_pos, (pos_word + 1) & 3);  // every other workgroup has read it
     return;
   }
   // sum of g^2 over the head's 64 channels: each channel counted once (q = 0)

@@ -671,10 +671,19 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
         const bool live = b < B && col < K;
         const float r = live ? rfac[b] : 0.f;
         const int wc = live ? col : 0;
+        float wk[16];  // the piece's weights, four 16-byte reads
+#pragma unroll
+        for (int c = 0; c < 16; c += 4) {
+          const u32x4 t = *reinterpret_cast<const u32x4*>(wls + wc + c);
+          wk[c] = __uint_as_float(t.x);
+          wk[c + 1] = __uint_as_float(t.y);
+          wk[c + 2] = __uint_as_float(t.z);
+          wk[c + 3] = __uint_as_float(t.w);
+        }
 #pragma unroll
         for (int c = 0; c < 16; c += 2) {
-          const uint32_t lo = __float_as_uint(v[m][c] * r * wls[wc + c]);
-          const uint32_t hi = __float_as_uint(v[m][c + 1] * r * wls[wc + c + 1]);
+          const uint32_t lo = __float_as_uint(v[m][c] * r * wk[c]);
+          const uint32_t hi = __float_as_uint(v[m][c + 1] * r * wk[c + 1]);
           const uint32_t blo = (lo + 0x7FFFu + ((lo >> 16) & 1u)) >> 16;   // round to
           const uint32_t bhi = (hi + 0x7FFFu + ((hi >> 16) & 1u)) >> 16;   // nearest even
           wv[m][c / 2] = blo | (bhi << 16);

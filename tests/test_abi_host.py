@@ -228,6 +228,7 @@ def test_mixer_step_validation(L):
     assert mx(L, ds=64) == ESHAPE
     assert mx(L, ss=P + 2 ** 22 + 8) == EALIGN
     assert mx(L, pos=P + 2 ** 21 + 2) == EALIGN
+    assert mx(L, cs=P + 2 ** 20 + 4) == EALIGN            # conv ring: 8-byte aligned
     assert mx(L, out=P + 2 ** 29 + 1) == EALIGN
     assert mx(L, ss=P + 2 ** 20 + 64) == EINVAL           # SSM state over the conv state
     assert mx(L, out=P + 2 ** 22) == EINVAL               # out over the SSM state

@@ -406,7 +406,7 @@ def test_bwd_dx_exact_unit_scales():
     # |W| = 0.5 on every element: s = 0.5 exactly, codes = sign
     W = np.where(q == 0, 0.5, q * 0.5).astype(np.float32)
     c, s, _, qo, s32, _ = oracle_packed(W, g, 0.0)
-    assert np.array_equal(qo, q) and np.all(s32 == 0.5)
+    assert np.array_equal(qo, np.where(q == 0, 1, q)) and np.all(s32 == 0.5)   # sign of W
     dYi = synth.f32_to_bf16_bits(rng.integers(-4, 5, size=(M, N)).astype(np.float32))
     dX = host(ops.tgemm_bwd_dx(dev_bf16(dYi), c, s, g))
     np.testing.assert_array_equal(dX, O.gemm_bwd_dx(dYi, qo, s32, g))
