@@ -502,8 +502,8 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
 // RMS (XD only; a decoding block's normalization fused into the staging):
 // x is not given; each batch row b of the float32 source xr is normalized,
 //   x[b, k] = bf16(xr[b, k] / sqrt(mean_k xr[b, k]^2 + eps) * nw[k]),
-// by every workgroup for itself: the source rows and the weight arrive by
-// direct-to-LDS loads like the raw x, the sums of squares are taken per
+// by every workgroup for itself: each thread loads its pieces of the source
+// rows and of the weight into registers, the sums of squares are taken per
 // 16-column piece and then per row in a fixed order (deterministic).
 // accum: y += the product instead of y = (each element has one owner lane).
 template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS, bool RMS>
@@ -539,16 +539,12 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   const int xoff = WAVES * RING * Plan::kSlotBytes;
   uint8_t* xs = smem + xoff;
   const int64_t KR = (K + 511) / 512 * 512;  // XD: raw x row length
-  constexpr int kRawBytes = RMS ? 4 : 2;     // XD: bytes per raw x value
-  const int xarea = XD && B * KR * kRawBytes > R * xstride ? (int)(B * KR * kRawBytes)
-                                                           : R * xstride;
+  const int xarea = XD && !RMS && B * KR * 2 > R * xstride ? (int)(B * KR * 2) : R * xstride;
   const int eoff = xoff + xarea;
   uint8_t* es = smem + eoff;
   const int zoff = eoff + (R * estride + 15) / 16 * 16;
-  // RMS: norm weight [KR] | per-piece sums of squares [2 x 64 WAVES] | row factors [4]
-  const int woff = zoff + 128;
-  float* wls = reinterpret_cast<float*>(smem + woff);
-  float* part = wls + KR;
+  // RMS: per-piece sums of squares [2 x 64 WAVES] | row factors [4]
+  float* part = reinterpret_cast<float*>(smem + zoff + 128);
   float* rfac = part + 2 * 64 * WAVES;
 
   Plan plan;
@@ -595,21 +591,87 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   };
 
   if constexpr (XD) {
+    // this thread's pieces (16 columns of one batch row, up to whole chunks)
+    const int pieces = (int)((K + 127) / 128 * 8);
+    uint32_t wv[kXPieces][8];
     if constexpr (RMS) {
-      // float32 source rows b < B, then the norm weight as row B (columns
-      // 256 p .. 256 p + 255 per load; a load past K re-reads the row's
-      // last 16 bytes into the row's pad)
-      const int per = (int)(KR / 256);
+      // the pieces of the source rows and the norm weight straight into
+      // registers, issued before the slots' direct-to-LDS loads (the
+      // compiler's own waits for them then also cover those slots)
       const float* xrm = xr + mat * xms;
-      for (int pi = wave; pi < (B + 1) * per; pi += WAVES) {
-        const int b = pi / per, p = pi % per;
-        int64_t e = 256 * (int64_t)p + 4 * lane;
-        e = e < K - 4 ? e : K - 4;
-        if (b < B)
-          gemv_dma16(xrm + (int64_t)b * K, (uint32_t)(4 * e),
-                     lds0 + xoff + 4 * (uint32_t)(b * KR + 256 * p));
-        else
-          gemv_dma16(nw, (uint32_t)(4 * e), lds0 + woff + 4 * (uint32_t)(256 * p));
+      float v[kXPieces][16], wk[kXPieces][16];
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        const int b = i / pieces, col = 16 * (i % pieces);
+        const bool live = b < B && col < K;
+#pragma unroll
+        for (int c = 0; c < 16; c += 4) {
+          u32x4 t = {0u, 0u, 0u, 0u}, u = {0u, 0u, 0u, 0u};
+          if (live) {
+            t = ld16(xrm + (int64_t)b * K + col + c);
+            u = ld16(nw + col + c);
+          }
+          v[m][c] = __uint_as_float(t.x);
+          v[m][c + 1] = __uint_as_float(t.y);
+          v[m][c + 2] = __uint_as_float(t.z);
+          v[m][c + 3] = __uint_as_float(t.w);
+          wk[m][c] = __uint_as_float(u.x);
+          wk[m][c + 1] = __uint_as_float(u.y);
+          wk[m][c + 2] = __uint_as_float(u.z);
+          wk[m][c + 3] = __uint_as_float(u.w);
+        }
+      }
+      for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        float sq = 0.f;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) sq = __builtin_fmaf(v[m][c], v[m][c], sq);
+        if (i / pieces < B) part[i] = sq;
+      }
+      asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");
+      __syncthreads();
+      // row factors: the pieces' sums in a fixed order, then across a wave;
+      // one row: every wave takes it itself (no second barrier); more: wave
+      // b takes row b and hands it over in LDS
+      auto row_factor = [&](int b) {
+        float sq = 0.f;
+        for (int j = lane; j < pieces; j += 64) sq += part[b * pieces + j];
+        sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
+        sq += __uint_as_float(lane_xchg<2>(__float_as_uint(sq)));
+        sq += __uint_as_float(lane_xchg<4>(__float_as_uint(sq)));
+        sq += __uint_as_float(lane_xchg<8>(__float_as_uint(sq)));
+        sq += __uint_as_float(lane_xchg<16>(__float_as_uint(sq)));
+        sq += __uint_as_float(lane_xchg<32>(__float_as_uint(sq)));
+        return 1.f / sqrtf(sq / (float)K + eps);
+      };
+      float rf[4] = {0.f, 0.f, 0.f, 0.f};
+      if (B == 1) {
+        rf[0] = row_factor(0);
+      } else {
+        if (wave < B) {
+          const float r = row_factor(wave);
+          if (lane == 0) rfac[wave] = r;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int b = 0; b < 4; ++b) rf[b] = b < B ? rfac[b] : 0.f;
+      }
+#pragma unroll
+      for (int m = 0; m < kXPieces; ++m) {
+        const int i = threadIdx.x + 64 * WAVES * m;
+        const int b = i / pieces;
+        const float r = b == 0 ? rf[0] : b == 1 ? rf[1] : b == 2 ? rf[2] : rf[3];
+#pragma unroll
+        for (int c = 0; c < 16; c += 2) {   // dead pieces hold zeros
+          const uint32_t lo = __float_as_uint(v[m][c] * r * wk[m][c]);
+          const uint32_t hi = __float_as_uint(v[m][c + 1] * r * wk[m][c + 1]);
+          const uint32_t blo = (lo + 0x7FFFu + ((lo >> 16) & 1u)) >> 16;   // round to
+          const uint32_t bhi = (hi + 0x7FFFu + ((hi >> 16) & 1u)) >> 16;   // nearest even
+          wv[m][c / 2] = blo | (bhi << 16);
+        }
       }
     } else {
       // raw x (row b, columns 512 p .. 512 p + 511 per load; a load past K
@@ -622,74 +684,9 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
         gemv_dma16(xm + (int64_t)b * K, (uint32_t)(2 * e),
                    lds0 + xoff + 2 * (uint32_t)(b * KR + 512 * p));
       }
-    }
-    for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
-    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");  // own x landed
-    __syncthreads();
-    // this thread's pieces (16 columns of one batch row, up to whole chunks)
-    const int pieces = (int)((K + 127) / 128 * 8);
-    uint32_t wv[kXPieces][8];
-    if constexpr (RMS) {
-      const float* fraw = reinterpret_cast<const float*>(xs);
-      float v[kXPieces][16];
-#pragma unroll
-      for (int m = 0; m < kXPieces; ++m) {
-        const int i = threadIdx.x + 64 * WAVES * m;
-        const int b = i / pieces, col = 16 * (i % pieces);
-        const bool live = b < B && col < K;
-        const int e = live ? (int)(b * KR) + col : 0;
-        float sq = 0.f;
-#pragma unroll
-        for (int c = 0; c < 16; c += 4) {
-          const u32x4 t = *reinterpret_cast<const u32x4*>(fraw + e + c);
-          v[m][c] = live ? __uint_as_float(t.x) : 0.f;
-          v[m][c + 1] = live ? __uint_as_float(t.y) : 0.f;
-          v[m][c + 2] = live ? __uint_as_float(t.z) : 0.f;
-          v[m][c + 3] = live ? __uint_as_float(t.w) : 0.f;
-        }
-#pragma unroll
-        for (int c = 0; c < 16; ++c) sq = __builtin_fmaf(v[m][c], v[m][c], sq);
-        if (b < B) part[i] = sq;
-      }
+      for (int p = 0; p < RING; ++p) issue(s0 + p * sstep);
+      asm volatile("s_waitcnt vmcnt(%0)" :: "n"(RING * Plan::kLoads) : "memory");  // own x landed
       __syncthreads();
-      if (wave < B) {  // row `wave`: its pieces' sums in a fixed order
-        float sq = 0.f;
-        for (int j = lane; j < pieces; j += 64) sq += part[wave * pieces + j];
-        sq += __shfl_xor(sq, 1);
-        sq += __shfl_xor(sq, 2);
-        sq += __shfl_xor(sq, 4);
-        sq += __shfl_xor(sq, 8);
-        sq += __shfl_xor(sq, 16);
-        sq += __shfl_xor(sq, 32);
-        if (lane == 0) rfac[wave] = 1.f / sqrtf(sq / (float)K + eps);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int m = 0; m < kXPieces; ++m) {
-        const int i = threadIdx.x + 64 * WAVES * m;
-        const int b = i / pieces, col = 16 * (i % pieces);
-        const bool live = b < B && col < K;
-        const float r = live ? rfac[b] : 0.f;
-        const int wc = live ? col : 0;
-        float wk[16];  // the piece's weights, four 16-byte reads
-#pragma unroll
-        for (int c = 0; c < 16; c += 4) {
-          const u32x4 t = *reinterpret_cast<const u32x4*>(wls + wc + c);
-          wk[c] = __uint_as_float(t.x);
-          wk[c + 1] = __uint_as_float(t.y);
-          wk[c + 2] = __uint_as_float(t.z);
-          wk[c + 3] = __uint_as_float(t.w);
-        }
-#pragma unroll
-        for (int c = 0; c < 16; c += 2) {
-          const uint32_t lo = __float_as_uint(v[m][c] * r * wk[c]);
-          const uint32_t hi = __float_as_uint(v[m][c + 1] * r * wk[c + 1]);
-          const uint32_t blo = (lo + 0x7FFFu + ((lo >> 16) & 1u)) >> 16;   // round to
-          const uint32_t bhi = (hi + 0x7FFFu + ((hi >> 16) & 1u)) >> 16;   // nearest even
-          wv[m][c / 2] = blo | (bhi << 16);
-        }
-      }
-    } else {
       const uint16_t* xraw = reinterpret_cast<const uint16_t*>(xs);
 #pragma unroll
       for (int m = 0; m < kXPieces; ++m) {
@@ -829,10 +826,9 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
     const int pieces = (int)((K + 127) / 128 * 8);
     if (R > 16 || B * pieces > 2 * 64 * WAVES) return hipErrorInvalidValue;
     KP = (K + SK - 1) / SK * SK;
-    const size_t xa = (size_t)R * (KP + kGemvXPad) > (size_t)B * KR * 4
-                          ? (size_t)R * (KP + kGemvXPad) : (size_t)B * KR * 4;
+    const size_t xa = (size_t)R * (KP + kGemvXPad);
     const size_t ea = ((size_t)R * (KP / 32) + 15) / 16 * 16;
-    const size_t aux = (size_t)KR * 4 + 2 * 64 * WAVES * 4 + 16;
+    const size_t aux = 2 * 64 * WAVES * 4 + 16;
 #define TM_GEMV_RMS(SW_)                                                                     \
   do {                                                                                        \
     const size_t lds = (size_t)WAVES * RING * SlotPlan<G, SK, SW_>::kSlotBytes + xa + ea + 128 + \
