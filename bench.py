@@ -2,7 +2,8 @@
 
 A step is one pass of the whole path on synthetic Mamba-2 1.3B-shaped data:
   * in_proj QAT step (8512 x 2048 weights, 16384 tokens, g = 128):
-    ternarize_pack -> tgemm_fwd -> tgemm_bwd_dx -> tgemm_bwd_dw_ste;
+    ternarize_pack -> tgemm_fwd -> tgemm_bwd_dx (one float16 pass, its
+    prepass included) -> tgemm_bwd_dw_ste;
   * one decode token over all 48 layers: tgemv over the 48 packed in_proj
     matrices and over the 48 packed out_proj matrices (batch 1).
 All inputs are resident in HBM before the timed region.  Per-kernel times
@@ -62,11 +63,12 @@ def parse():
                     help="leave out the measured MFMA-loop and read-stream ceilings")
     ap.add_argument("--skip", default="",
                     help="comma list of optional sections to leave out: qat, variants, "
-                         "per_layer, small, sweep, mixed, blocks, cold (keeps a profiler trace to the "
+                         "per_layer, small, sweep, mixed, blocks, cold, dx_exact (keeps a profiler trace to the "
                          "kernels of interest)")
     args = ap.parse_args()
     args.skip = {x for x in args.skip.split(",") if x}
-    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed", "blocks", "cold"}
+    bad = args.skip - {"qat", "variants", "per_layer", "small", "sweep", "mixed", "blocks", "cold",
+                       "dx_exact"}
     if bad:
         ap.error(f"unknown --skip sections: {sorted(bad)}")
     return args
@@ -143,6 +145,7 @@ def main():
     Y = torch.empty((M, N), dtype=torch.float32, device=dev)
     dX = torch.empty((M, K), dtype=torch.float32, device=dev)
     dW = torch.empty((N, K), dtype=torch.float32, device=dev)
+    dx_ws = torch.empty(ops.dx_f16_workspace_bytes(M, N), dtype=torch.uint8, device=dev)
     log(f"in_proj inputs ready in {time.time() - t0:.1f}s")
 
     # ---------------- decode: 48 layers of packed weights ----------------
@@ -178,7 +181,7 @@ def main():
         ev[1].record()
         ops.tgemm_fwd(X, codes, scales, g, Y=Y)
         ev[2].record()
-        ops.tgemm_bwd_dx(dY, codes, scales, g, dX=dX)
+        ops.tgemm_bwd_dx(dY, codes, scales, g, dX=dX, workspace=dx_ws)
         ev[3].record()
         ops.tgemm_bwd_dw_ste(dY, X, dW=dW)
         ev[4].record()
@@ -205,6 +208,20 @@ def main():
 
     per = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in events]))
            for i, n in enumerate(names)}
+
+    # the two-pass dX (16 bits of every scale) on the same operands, for comparison
+    dx_exact_ms = None
+    if "dx_exact" not in args.skip:
+        for _ in range(2):
+            ops.tgemm_bwd_dx(dY, codes, scales, g, dX=dX, precision="exact")
+        ex = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(max(args.steps // 2, 3))]
+        for a, b in ex:
+            a.record()
+            ops.tgemm_bwd_dx(dY, codes, scales, g, dX=dX, precision="exact")
+            b.record()
+        torch.cuda.synchronize()
+        dx_exact_ms = float(np.mean([a.elapsed_time(b) for a, b in ex]))
 
     # ---------------- decode as a server runs it: tokens back to back ----------------
     def serving(batch, tokens):
@@ -292,6 +309,12 @@ def main():
             ach = amount / sec / 1e9
             kernels[n] = dict(ms=round(per[n], 4), bound="hbm", achieved=round(ach, 1),
                               unit="GB/s", frac=round(ach / PEAK_HBM_GBPS, 4))
+    if dx_exact_ms is not None:
+        ach = fl / (dx_exact_ms * 1e-3) / 1e12
+        kernels["tgemm_bwd_dx_exact"] = dict(
+            ms=round(dx_exact_ms, 4), bound="mfma", achieved=round(ach, 1), unit="TFLOP/s",
+            frac=round(ach / PEAK_BF16_TFLOPS, 4),
+            what="two bfloat16 passes (16 bits of every scale); not part of the step")
     # in the step (after the training kernels) ...
     dec_ms = per["tgemv_in_proj"] + per["tgemv_out_proj"]
     dec_bytes = gemv_bytes(dcfg_in) + gemv_bytes(dcfg_out)

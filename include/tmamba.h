@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 9
+#define TM_ABI_VERSION 10
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -148,6 +148,38 @@ tm_status tm_tgemm_fwd_bf16(const uint16_t* X, const uint8_t* codes,
 tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes,
                           const float* scales, int64_t M, int64_t N, int64_t K,
                           int32_t g, float* dX, tm_stream stream);
+
+/*
+ * tm_tgemm_bwd_dx_f16 — the same product (Sec. 3.1, straight-through
+ * backward w.r.t. the input) in one float16 pass on the matrix cores.
+ *
+ *   dY, codes, scales, dX   as for tm_tgemm_bwd_dx (same limits, N % 8 == 0)
+ *   workspace               device memory owned by the caller, at least
+ *                           tm_tgemm_bwd_dx_f16_workspace(M, N) bytes,
+ *                           256-byte aligned, overlapping no other argument;
+ *                           its contents are scratch (nothing need be set
+ *                           before the call, nothing is kept after it)
+ *   workspace_bytes         its size (TM_ESHAPE if too small)
+ * A prepass writes fp16(dY * 2^e[m]) into the workspace, with one power of
+ * two per row of dY that puts the row's largest magnitude in [2^14, 2^15)
+ * (every value within 2^28 of it converts exactly); the weight operand is
+ * q * fp16(s * 2^t) with one power of two for the tensor (largest |s| in
+ * [2^14, 2^15)); products are exact in float32, accumulated in float32, and
+ * scaled back by 2^-(e[m] + t) in the store.  Each dequantized weight so
+ * carries a relative error of at most 2^-11, which bounds every output by
+ * 2^-11 * sum_n |dY[m, n] q[n, k] s| plus float32 accumulation (about 2e-4
+ * relative Frobenius error on Gaussian weights).  Scales may have either
+ * sign; dY must be finite.  Cut tiles and atomics as for tm_tgemm_bwd_dx.
+ * Calls that share a workspace must not run concurrently.
+ */
+tm_status tm_tgemm_bwd_dx_f16(const uint16_t* dY, const uint8_t* codes,
+                              const float* scales, int64_t M, int64_t N,
+                              int64_t K, int32_t g, float* dX, void* workspace,
+                              int64_t workspace_bytes, tm_stream stream);
+
+/* Workspace bytes tm_tgemm_bwd_dx_f16 needs for an M x N dY (-1 if M or N
+ * is below 1 or the size overflows). */
+int64_t tm_tgemm_bwd_dx_f16_workspace(int64_t M, int64_t N);
 
 /*
  * tm_tgemm_bwd_dw_ste — Sec. 3.1 straight-through backward w.r.t. the latent

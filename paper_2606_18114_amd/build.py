@@ -31,6 +31,7 @@ SOURCES = [
     "ternarize_pack.hip",
     "tgemm_fwd.hip",
     "tgemm_bwd_dx.hip",
+    "tgemm_bwd_dx_f16.hip",
     "tgemm_bwd_dw.hip",
     "tgemv.hip",
     "dgemv.hip",

@@ -73,6 +73,37 @@ tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float
       tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, es == 2, to_hip(stream)));
 }
 
+// argument checks of both dX calls; workspace NULL: the two-pass call,
+// which takes none
+tm_status bwd_dx_checked(const uint16_t* dY, const uint8_t* codes, const float* scales,
+                         int64_t M, int64_t N, int64_t K, int32_t g, float* dX,
+                         const void* workspace, int64_t workspace_bytes) {
+  if (!dY || !codes || !scales || !dX) return TM_EINVAL;
+  if (M < 1 || N < 1 || N % 8 != 0) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  if (N > (int64_t(1) << 22) || K > (int64_t(1) << 26)) return TM_ESHAPE;
+  int64_t yb, cb, sb, xb;
+  if (!bytes_of(M, N, 2, &yb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
+      !bytes_of(M, K, 4, &xb))
+    return TM_ESHAPE;
+  if (((M + 255) / 256) * ((K + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
+  if (!aligned(dY, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(dX, 16))
+    return TM_EALIGN;
+  const Span o = span(dX, xb);
+  if (overlap(o, span(dY, yb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales, sb)))
+    return TM_EINVAL;
+  if (workspace) {
+    const int64_t need = tmk::dx_f16_workspace_bytes(M, N);
+    if (workspace_bytes < need) return TM_ESHAPE;
+    if (!aligned(workspace, 256)) return TM_EALIGN;
+    const Span w = span(workspace, need);
+    if (overlap(w, o) || overlap(w, span(dY, yb)) || overlap(w, span(codes, cb)) ||
+        overlap(w, span(scales, sb)))
+      return TM_EINVAL;
+  }
+  return TM_OK;
+}
+
 // argument checks of the mixer step; workspace NULL: the library's own
 // scratch array (no overlap check needed: no caller array can overlap it)
 // gate_only: the gated float32 output of tm_mixer_gate in place of the
@@ -245,21 +276,25 @@ tm_status tm_tgemm_fwd_bf16(const uint16_t* X, const uint8_t* codes, const float
 tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,
                           int64_t M, int64_t N, int64_t K, int32_t g, float* dX,
                           tm_stream stream) {
-  if (!dY || !codes || !scales || !dX) return TM_EINVAL;
-  if (M < 1 || N < 1 || N % 8 != 0) return TM_ESHAPE;
-  if (tm_status st = shape_kg(K, g)) return st;
-  if (N > (int64_t(1) << 22) || K > (int64_t(1) << 26)) return TM_ESHAPE;
-  int64_t yb, cb, sb, xb;
-  if (!bytes_of(M, N, 2, &yb) || !bytes_of(N, K / 4, 1, &cb) || !bytes_of(N, K / g, 4, &sb) ||
-      !bytes_of(M, K, 4, &xb))
-    return TM_ESHAPE;
-  if (((M + 255) / 256) * ((K + 255) / 256) > kMaxGridBlocks) return TM_ESHAPE;
-  if (!aligned(dY, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(dX, 16))
-    return TM_EALIGN;
-  const Span o = span(dX, xb);
-  if (overlap(o, span(dY, yb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales, sb)))
-    return TM_EINVAL;
+  if (tm_status st = bwd_dx_checked(dY, codes, scales, M, N, K, g, dX, nullptr, 0)) return st;
   return hip_status(tmk::launch_tgemm_bwd_dx(dY, codes, scales, M, N, K, g, dX, to_hip(stream)));
+}
+
+int64_t tm_tgemm_bwd_dx_f16_workspace(int64_t M, int64_t N) {
+  int64_t yb;
+  if (M < 1 || N < 1 || !bytes_of(M, N, 2, &yb)) return -1;
+  return tmk::dx_f16_workspace_bytes(M, N);
+}
+
+tm_status tm_tgemm_bwd_dx_f16(const uint16_t* dY, const uint8_t* codes, const float* scales,
+                              int64_t M, int64_t N, int64_t K, int32_t g, float* dX,
+                              void* workspace, int64_t workspace_bytes, tm_stream stream) {
+  if (!workspace) return TM_EINVAL;
+  if (tm_status st = bwd_dx_checked(dY, codes, scales, M, N, K, g, dX, workspace,
+                                    workspace_bytes))
+    return st;
+  return hip_status(tmk::launch_tgemm_bwd_dx_f16(dY, codes, scales, M, N, K, g, dX, workspace,
+                                                 to_hip(stream)));
 }
 
 tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,

@@ -46,6 +46,17 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
 hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,
                                int64_t M, int64_t N, int64_t K, int g, float* dX,
                                hipStream_t stream);
+// the one-pass float16 form: a prepass writes fp16(dY * 2^e[m]), the row
+// exponents and the scale maxima into workspace (dx_f16_workspace_bytes)
+// (the scale maxima come from kDxScaleParts waves of the prepass)
+constexpr int kDxScaleParts = 256;
+inline int64_t dx_f16_workspace_bytes(int64_t M, int64_t N) {
+  auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
+  return up(M * N * 2) + up(M * 4) + kDxScaleParts * 4;
+}
+hipError_t launch_tgemm_bwd_dx_f16(const uint16_t* dY, const uint8_t* codes, const float* scales,
+                                   int64_t M, int64_t N, int64_t K, int g, float* dX,
+                                   void* workspace, hipStream_t stream);
 hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M, int64_t N,
                                int64_t K, float* dW, int accumulate, hipStream_t stream);
 // dst[0 .. n) = 0 (float32), by a plain fill kernel

@@ -35,9 +35,7 @@
 // The direct-to-LDS loads are issued from inline assembly, so the compiler
 // neither tracks nor waits for them; each wave issues exactly seven per stage
 // and counts them itself (vector-memory operations retire in order).
-#include <type_traits>
-
-#include "common.hpp"
+#include "dx_common.hpp"
 #include "launchers.hpp"
 
 namespace tmk {
@@ -52,62 +50,6 @@ constexpr int kDxDec = 2 * kDxPlane;               // hi plane, then lo plane
 constexpr int kDxRingBase = 2 * kDxDec;            // planes first, then the ring
 constexpr int kDxLds = kDxRingBase + kDxRing * kDxSlot;  // 140 KiB
 constexpr int kDxLoads = 7;                        // direct-to-LDS loads per wave per stage
-
-typedef __attribute__((ext_vector_type(4))) short dx_s16x4;
-typedef __attribute__((address_space(3))) dx_s16x4 dx_lds_s16x4;
-typedef __attribute__((ext_vector_type(2))) short dx_s16x2;
-
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-// lane i: 16 bytes at base + voff -> LDS lds_base + 16 i (lds_base wave-uniform)
-__device__ __forceinline__ void dx_dma16(const void* base, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :: "v"(voff), "s"(base), "s"(lds_base) : "memory", "m0");
-}
-// lane i: 4 bytes at base + voff -> LDS lds_base + 4 i
-__device__ __forceinline__ void dx_dma4(const void* base, uint32_t voff, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
-               :: "v"(voff), "s"(base), "s"(lds_base) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-template <int kVm>
-__device__ __forceinline__ void dx_stage_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(kVm) : "memory");
-  __builtin_amdgcn_sched_barrier(0);
-}
-
-template <int I, int N, typename F>
-__device__ __forceinline__ void dx_static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    dx_static_for<I + 1, N>(f);
-  }
-}
-
-// byte offset of (weight row r, column c) inside a plane, c % 4 == 0.  The
-// 32-byte units of row r are XOR-permuted by f = (r%4) ^ 2 (r%4), which is
-// distinct modulo 4 and in its two upper bits over any four consecutive rows:
-// the four rows of a transpose read land in distinct 32-byte bank groups, and
-// so do the two column groups (units u and u + 1) read in the same cycle.
-__device__ __forceinline__ uint32_t dx_poff(int r, int c) {
-  const int f = (r & 3) ^ ((r & 3) << 1);
-  return (uint32_t)(r * 512 + 32 * ((c >> 4) ^ f) + 2 * (c & 15));
-}
-
-// byte offset of 16-byte unit u (columns 8u .. 8u+7) of dY row r in a stage;
-// the XOR ((r/2) % 4) ^ ((r/8) % 2) spreads any 8 (and any 16) consecutive
-// rows over distinct 16-byte bank groups
-__device__ __forceinline__ uint32_t dx_yoff(int r, int u) {
-  return (uint32_t)(r * 64 + 16 * (u ^ ((r >> 1) & 3) ^ ((r >> 3) & 1)));
-}
-
-// 0xFFFF in each 16-bit half whose bit 15 is set
-__device__ __forceinline__ uint32_t dx_halfmask(uint32_t y) {
-  const dx_s16x2 v = __builtin_bit_cast(dx_s16x2, y) >> (short)15;
-  return __builtin_bit_cast(uint32_t, v);
-}
 
 template <int G>
 __global__ __launch_bounds__(256) void tgemm_bwd_dx_kernel(
@@ -314,7 +256,8 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dx_kernel(
     };
     // Pair I of both words: w << (14 - 2 I) holds the two codes at bits
     // 14-15 / 30-31, w << (15 - 2 I) their low bits at bits 15 / 31; a
-    // nonzero code (low bit set) selects the scale, its high bit is the sign.
+    // nonzero code (low bit set) selects the scale, its high bit flips the
+    // sign (so negative scales work too).
     // vh / vl: [word 0 elements 0-7, 8-15, word 1 elements 0-7, 8-15]
     auto decode_pair = [&](auto i_tag, const DecIn& d, u32x4* vh, u32x4* vl) {
       constexpr int I = decltype(i_tag)::value;
@@ -322,10 +265,10 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dx_kernel(
       const uint32_t sg1 = (d.w.y << (14 - 2 * I)) & 0x80008000u;
       const uint32_t nz0 = dx_halfmask(d.w.x << (15 - 2 * I));
       const uint32_t nz1 = dx_halfmask(d.w.y << (15 - 2 * I));
-      vh[I / 4][I % 4] = (nz0 & d.hi2) | sg0;
-      vl[I / 4][I % 4] = (nz0 & d.lo2) | sg0;
-      vh[2 + I / 4][I % 4] = (nz1 & d.hi2) | sg1;
-      vl[2 + I / 4][I % 4] = (nz1 & d.lo2) | sg1;
+      vh[I / 4][I % 4] = (nz0 & d.hi2) ^ sg0;
+      vl[I / 4][I % 4] = (nz0 & d.lo2) ^ sg0;
+      vh[2 + I / 4][I % 4] = (nz1 & d.hi2) ^ sg1;
+      vl[2 + I / 4][I % 4] = (nz1 & d.lo2) ^ sg1;
     };
     // the same for one word (W = 0, 1) of pair I
     auto decode_word_pair = [&](auto i_tag, auto w_tag, const DecIn& d, u32x4* vh, u32x4* vl) {
@@ -334,8 +277,8 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dx_kernel(
       const uint32_t w = W ? d.w.y : d.w.x;
       const uint32_t sg = (w << (14 - 2 * I)) & 0x80008000u;
       const uint32_t nz = dx_halfmask(w << (15 - 2 * I));
-      vh[2 * W + I / 4][I % 4] = (nz & d.hi2) | sg;
-      vl[2 * W + I / 4][I % 4] = (nz & d.lo2) | sg;
+      vh[2 * W + I / 4][I % 4] = (nz & d.hi2) ^ sg;
+      vl[2 * W + I / 4][I % 4] = (nz & d.lo2) ^ sg;
     };
     // plane writes of register half H of both words (elements 8 H .. 8 H + 7,
     // or 8 (1 - H) .. for the lanes that decode swapped words)

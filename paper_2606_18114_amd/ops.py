@@ -33,6 +33,9 @@ SIGNATURES = {
     "tm_ternarize_pack": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P]),
     "tm_tgemm_fwd": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
     "tm_tgemm_bwd_dx": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_tgemm_bwd_dx_f16": (ctypes.c_int,
+                            [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P, _I64, _P]),
+    "tm_tgemm_bwd_dx_f16_workspace": (ctypes.c_int64, [_I64, _I64]),
     "tm_tgemm_bwd_dw_ste": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _I32, _P]),
     "tm_tgemv": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _I64, _I32, _P, _P]),
     "tm_ternarize_pack_thresh": (ctypes.c_int,
@@ -281,8 +284,15 @@ def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int
 
 
 def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
-                 dX: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """dX[M, K] = dY . (q * s) in float32."""
+                 dX: Optional[torch.Tensor] = None, *, precision: str = "f16",
+                 workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """dX[M, K] = dY . (q * s) in float32.
+
+    precision "f16" (``tm_tgemm_bwd_dx_f16``): one float16 pass, each
+    dequantized weight within 2^-11 relative; the workspace (uint8, at least
+    ``dx_f16_workspace_bytes(M, N)`` bytes) is allocated here when not given.
+    precision "exact" (``tm_tgemm_bwd_dx``): two bfloat16 passes carrying 16
+    bits of every scale."""
     _need(dY, "dY", _BF16, 2)
     _need(codes, "codes", _U8, 2)
     _need(scales, "scales", _F32, 2)
@@ -294,10 +304,33 @@ def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g:
         dX = torch.empty((M, K), dtype=torch.float32, device=dY.device)
     _need(dX, "dX", _F32, 2)
     _shape(dX, "dX", (M, K), dY.device)
-    st = lib().tm_tgemm_bwd_dx(_ptr(dY), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(dX),
-                               _stream())
-    _check("tm_tgemm_bwd_dx", st)
+    if precision == "exact":
+        st = lib().tm_tgemm_bwd_dx(_ptr(dY), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(dX),
+                                   _stream())
+        _check("tm_tgemm_bwd_dx", st)
+        return dX
+    if precision != "f16":
+        raise ValueError(f"precision must be 'f16' or 'exact' (got {precision!r})")
+    need = dx_f16_workspace_bytes(M, N)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dY.device)
+    _need(workspace, "workspace", _U8, 1)
+    if workspace.numel() < need:
+        raise ValueError(f"workspace has {workspace.numel()} bytes, {need} needed")
+    if workspace.device != dY.device:
+        raise ValueError(f"workspace is on {workspace.device}, the operands on {dY.device}")
+    st = lib().tm_tgemm_bwd_dx_f16(_ptr(dY), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(dX),
+                                   _ptr(workspace), workspace.numel(), _stream())
+    _check("tm_tgemm_bwd_dx_f16", st)
     return dX
+
+
+def dx_f16_workspace_bytes(M: int, N: int) -> int:
+    """Workspace bytes of the float16 dX call for an M x N gradient."""
+    n = int(lib().tm_tgemm_bwd_dx_f16_workspace(M, N))
+    if n < 0:
+        raise ValueError(f"no workspace size for M={M}, N={N}")
+    return n
 
 
 def tgemm_bwd_dw_ste(dY: torch.Tensor, X: torch.Tensor, dW: Optional[torch.Tensor] = None,

@@ -9,7 +9,9 @@ float32 latent weights, and on every forward call
     (``tm_tgemm_fwd``, float32 output);
 
 and its backward pass is the straight-through estimator: the gradient passes
-the quantizer unchanged, so ``dX = dY . (q s)`` (``tm_tgemm_bwd_dx``) and
+the quantizer unchanged, so ``dX = dY . (q s)`` (``tm_tgemm_bwd_dx_f16``:
+one float16 pass, each dequantized weight within 2^-11 relative; or the
+two-pass ``tm_tgemm_bwd_dx`` with ``dx_precision="exact"``) and
 ``dW = dY^T . X`` (``tm_tgemm_bwd_dw_ste``).  The incoming gradient is taken
 in bfloat16, the precision the backward kernels read.
 
@@ -60,7 +62,8 @@ class TernaryLinearFn(torch.autograd.Function):
     def forward(ctx, x: torch.Tensor, weight: torch.Tensor, scale: Optional[torch.Tensor],
                 g: int, eps: float, zero_count: Optional[torch.Tensor], mode: str,
                 row_mult: Optional[torch.Tensor],
-                out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
+                out_dtype: torch.dtype = torch.float32,
+                dx_precision: str = "f16") -> torch.Tensor:
         N, K = weight.shape
         if x.shape[-1] != K:
             raise ValueError(f"x has {x.shape[-1]} features, the layer takes {K}")
@@ -88,6 +91,7 @@ class TernaryLinearFn(torch.autograd.Function):
         ctx.lead = lead
         ctx.x_dtype = x.dtype
         ctx.learned = mode != "absmean"
+        ctx.dx_precision = dx_precision
         return y.reshape(*lead, N)
 
     @staticmethod
@@ -100,7 +104,7 @@ class TernaryLinearFn(torch.autograd.Function):
         dy = dy.contiguous()
         dx = dw = dscale = None
         if ctx.needs_input_grad[0]:
-            dx = ops.tgemm_bwd_dx(dy, codes, mag, ctx.g)
+            dx = ops.tgemm_bwd_dx(dy, codes, mag, ctx.g, precision=ctx.dx_precision)
             dx = dx.to(ctx.x_dtype).reshape(*ctx.lead, x2.shape[1])
         want_scale = ctx.learned and ctx.needs_input_grad[2]
         if ctx.needs_input_grad[1] or want_scale:
@@ -120,7 +124,7 @@ class TernaryLinearFn(torch.autograd.Function):
                     dscale = ops.group_code_dot(codes, dw_hat, ctx.g)
                 if ctx.needs_input_grad[1]:
                     dw = dw_hat
-        return dx, dw, dscale, None, None, None, None, None, None
+        return dx, dw, dscale, None, None, None, None, None, None, None
 
 
 class TernaryLinear(torch.nn.Module):
@@ -140,13 +144,18 @@ class TernaryLinear(torch.nn.Module):
     each row's absmean threshold (e.g. 0.8 on the gate rows of in_proj).
     out_dtype: float32 (default) or bfloat16, the output rounded once as a
     bfloat16 model stores it; the incoming gradient then needs no cast.
+    dx_precision: "f16" (default, one float16 pass for the input gradient)
+    or "exact" (two bfloat16 passes, 16 bits of every scale).
     """
 
     def __init__(self, in_features: int, out_features: int, g: int = 128, eps: float = 1e-5,
                  device: Optional[torch.device] = None, track_zero_ratio: bool = True,
                  scale_mode: str = "absmean", threshold_mult: Optional[torch.Tensor] = None,
-                 out_dtype: torch.dtype = torch.float32):
+                 out_dtype: torch.dtype = torch.float32, dx_precision: str = "f16"):
         super().__init__()
+        if dx_precision not in ("f16", "exact"):
+            raise ValueError("dx_precision must be 'f16' or 'exact'")
+        self.dx_precision = dx_precision
         if out_dtype not in (torch.float32, torch.bfloat16):
             raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
         self.out_dtype = out_dtype
@@ -211,7 +220,8 @@ class TernaryLinear(torch.nn.Module):
         if not self._scale_ready:
             self.reset_scale()
         return TernaryLinearFn.apply(x, self.weight, self.scale, self.g, self.eps, self._zc,
-                                     self.scale_mode, self.threshold_mult, self.out_dtype)
+                                     self.scale_mode, self.threshold_mult, self.out_dtype,
+                                     self.dx_precision)
 
     def zero_ratio(self) -> float:
         """Fraction of zero codes in the last forward call (Sec. 3.1 tracks it

@@ -35,6 +35,10 @@ hipError_t launch_tgemm_bwd_dx(const uint16_t*, const uint8_t*, const float*, in
                                int64_t, int, float*, hipStream_t) {
   reached("tgemm_bwd_dx");
 }
+hipError_t launch_tgemm_bwd_dx_f16(const uint16_t*, const uint8_t*, const float*, int64_t,
+                                   int64_t, int64_t, int, float*, void*, hipStream_t) {
+  reached("tgemm_bwd_dx_f16");
+}
 hipError_t launch_tgemm_bwd_dw(const uint16_t*, const uint16_t*, int64_t, int64_t, int64_t,
                                float*, int, hipStream_t) {
   reached("tgemm_bwd_dw");

@@ -37,17 +37,17 @@ def L():
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:tm_status|int|const char\*)\s+(tm_[a-z0-9_]+)\(",
+    return sorted(set(re.findall(r"^\s*(?:tm_status|int|int64_t|const char\*)\s+(tm_[a-z0-9_]+)\(",
                                  text, re.M)))
 
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 9
+    assert L.tm_abi_version() == 10
 
 
 def test_status_strings(L):
@@ -367,6 +367,31 @@ def test_tgemm_bwd_dx_validation(L):
     assert dx(L, dY=P + 8) == EALIGN
     assert dx(L, dX=P + 2 ** 26 + 8) == EALIGN
     assert dx(L, dX=P) == EINVAL
+
+
+def dx16(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,
+         dX=P + 2 ** 26, ws=P + 2 ** 27, wsb=None):
+    if wsb is None:
+        wsb = L.tm_tgemm_bwd_dx_f16_workspace(M, N)
+    return L.tm_tgemm_bwd_dx_f16(dY, codes, scales, M, N, K, g, dX, ws, wsb, None)
+
+
+def test_tgemm_bwd_dx_f16_validation(L):
+    # workspace bytes: float16 copy of dY, row exponents, scale maxima (256-byte pieces)
+    assert L.tm_tgemm_bwd_dx_f16_workspace(16, 256) == 16 * 256 * 2 + 256 + 1024
+    assert L.tm_tgemm_bwd_dx_f16_workspace(16384, 8512) == 16384 * 8512 * 2 + 65536 + 1024
+    assert L.tm_tgemm_bwd_dx_f16_workspace(0, 256) == -1
+    assert L.tm_tgemm_bwd_dx_f16_workspace(2 ** 40, 2 ** 40) == -1
+    for kw in ("dY", "codes", "scales", "dX", "ws"):
+        assert dx16(L, **{kw: 0}) == EINVAL, kw
+    assert dx16(L, N=250) == ESHAPE
+    assert dx16(L, K=100) == ESHAPE
+    assert dx16(L, wsb=16 * 256 * 2) == ESHAPE            # one piece short
+    assert dx16(L, ws=P + 2 ** 27 + 16) == EALIGN         # workspace needs 256 bytes
+    assert dx16(L, dX=P + 2 ** 26 + 8) == EALIGN
+    assert dx16(L, ws=P + 2 ** 26) == EINVAL              # workspace over dX
+    assert dx16(L, ws=P + 2 ** 25 - 512) == EINVAL        # workspace runs into the scales
+    assert dx16(L, ws=P) == EINVAL                        # workspace over dY
 
 
 def dw(L, dY=P, X=P + 2 ** 24, M=16, N=256, K=512, dW=P + 2 ** 26, acc=0):

@@ -357,7 +357,7 @@ def test_bwd_dx_ragged(g):
     W = synth.weights(rng, N, K, True)
     dY = synth.activations(rng, M, N, std=synth.DY_STD)
     c, s, _, q, s32, _ = oracle_packed(W, g)
-    dX = host(ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g))
+    dX = host(ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g, precision="exact"))
     err = O.rel_fro_error(dX, O.gemm_bwd_dx(dY, q, s32, g))
     print(f"  rel fro err {err:.3e}", flush=True)
     assert err <= REL_DESIGN
@@ -369,7 +369,7 @@ def test_bwd_dx_in_proj_sampled_rows():
     W = synth.layer_weight(cfg, synth.SEED_W)
     dY = synth.layer_acts(cfg.M, cfg.N, synth.SEED_DY, std=synth.DY_STD)
     c, s, _, q, s32, _ = oracle_packed(W, 128)
-    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, 128)
+    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, 128, precision="exact")
     rows = np.sort(np.random.default_rng(10).choice(cfg.M, 256, replace=False))
     got = host(dX[torch.from_numpy(rows).cuda()])
     err = O.rel_fro_error(got, O.gemm_bwd_dx(dY[rows], q, s32, 128))
@@ -389,7 +389,7 @@ def test_bwd_dx_split_and_ragged_tiles(M, N, K, g):
     W = synth.weights(rng, N, K, True)
     dY = synth.activations(rng, M, N, std=synth.DY_STD)
     c, s, _, q, s32, _ = oracle_packed(W, g)
-    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g)
+    dX = ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g, precision="exact")
     rows = np.sort(np.random.default_rng(3).choice(M, min(M, 384), replace=False))
     got = host(dX[torch.from_numpy(rows).cuda()])
     err = O.rel_fro_error(got, O.gemm_bwd_dx(dY[rows], q, s32, g))
@@ -408,7 +408,7 @@ def test_bwd_dx_exact_unit_scales():
     c, s, _, qo, s32, _ = oracle_packed(W, g, 0.0)
     assert np.array_equal(qo, np.where(q == 0, 1, q)) and np.all(s32 == 0.5)   # sign of W
     dYi = synth.f32_to_bf16_bits(rng.integers(-4, 5, size=(M, N)).astype(np.float32))
-    dX = host(ops.tgemm_bwd_dx(dev_bf16(dYi), c, s, g))
+    dX = host(ops.tgemm_bwd_dx(dev_bf16(dYi), c, s, g, precision="exact"))
     np.testing.assert_array_equal(dX, O.gemm_bwd_dx(dYi, qo, s32, g))
 
 

@@ -50,6 +50,8 @@ class Step:
         self.zc = torch.empty((1,), dtype=torch.int64, device="cuda")
         self.Y = torch.empty((M, N), device="cuda")
         self.dX = torch.empty((M, K), device="cuda")
+        self.dX2 = torch.empty((M, K), device="cuda")
+        self.ws = torch.empty(ops.dx_f16_workspace_bytes(M, N), dtype=torch.uint8, device="cuda")
         self.dW = torch.empty((N, K), device="cuda")
         self.y = torch.empty((3, 2, N), device="cuda")
 
@@ -58,7 +60,8 @@ class Step:
         o.ternarize_pack(self.W, g, 1e-5, codes=self.codes, scales=self.s, scales_f16=self.s16,
                          zero_count=self.zc)
         o.tgemm_fwd(self.X, self.codes, self.s, g, Y=self.Y)
-        o.tgemm_bwd_dx(self.dY, self.codes, self.s, g, dX=self.dX)
+        o.tgemm_bwd_dx(self.dY, self.codes, self.s, g, dX=self.dX, workspace=self.ws)
+        o.tgemm_bwd_dx(self.dY, self.codes, self.s, g, dX=self.dX2, precision="exact")
         o.tgemm_bwd_dw_ste(self.dY, self.X, dW=self.dW)
         # the same packed matrix three times over (count = 3, stride 0 is not
         # allowed, so the GEMV reads a stacked copy made by a kernel of torch)
@@ -68,7 +71,7 @@ class Step:
     def outputs(self):
         torch.cuda.synchronize()
         return {k: getattr(self, k).detach().cpu().clone()
-                for k in ("codes", "s", "s16", "zc", "Y", "dX", "dW", "y")}
+                for k in ("codes", "s", "s16", "zc", "Y", "dX", "dX2", "dW", "y")}
 
 
 # bit-exact: codes, scales, counts, the GEMV, and Y (its tiles are cut into
@@ -82,7 +85,7 @@ def _compare(got, ref, label):
         a, b = got[k], ref[k]
         if k in EXACT:
             assert torch.equal(a, b), f"{label}: {k} differs"
-        else:  # dX, dW: float32 atomics over the cut contraction, order may vary
+        else:  # dX (both forms), dW: float32 atomics over the cut contraction
             rel = float((a.double() - b.double()).norm() / b.double().norm())
             assert rel <= 1e-6, f"{label}: {k} rel {rel:.2e}"
 
@@ -94,6 +97,7 @@ def test_side_stream_matches_default_stream():
     side = torch.cuda.Stream()
     st.Y.fill_(float("nan"))
     st.dX.fill_(float("nan"))
+    st.dX2.fill_(float("nan"))
     torch.cuda.synchronize()
     with torch.cuda.stream(side):
         st.run()
@@ -117,8 +121,9 @@ def test_graph_capture_and_replays():
     with torch.cuda.graph(graph):
         st.run()
     for rep in range(3):
-        for t in (st.Y, st.dX, st.dW, st.y):
+        for t in (st.Y, st.dX, st.dX2, st.dW, st.y):
             t.fill_(float("nan"))   # eager work between replays
+        st.ws.fill_(255)            # the dX workspace is scratch: garbage in it is fine
         st.zc.fill_(-1)
         torch.cuda.synchronize()
         graph.replay()

@@ -66,15 +66,15 @@ def _oracle_codes(W, g, eps=1e-5):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("g", [64, 128])
-def test_forward_backward_against_oracle(g):
+@pytest.mark.parametrize("g,dx_precision", [(64, "f16"), (128, "f16"), (128, "exact")])
+def test_forward_backward_against_oracle(g, dx_precision):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2606_18114_amd.qat import TernaryLinear
     rng = np.random.default_rng(31 + g)
     N, K = 200, 512
     W = synth.weights(rng, N, K, outliers=True)
-    layer = TernaryLinear.from_weight(torch.from_numpy(W).cuda(), g=g)
+    layer = TernaryLinear.from_weight(torch.from_numpy(W).cuda(), g=g, dx_precision=dx_precision)
     xf = rng.standard_normal((3, 40, K), dtype=np.float32)
     x = _bf16(xf).requires_grad_(True)
     r = torch.from_numpy(rng.standard_normal((3, 40, N), dtype=np.float32)).cuda()
@@ -89,7 +89,7 @@ def test_forward_backward_against_oracle(g):
     e_y = O.rel_fro_error(y.detach().cpu().numpy().reshape(-1, N), O.gemm_fwd(xb, q, s, g))
     e_dx = O.rel_fro_error(x.grad.float().cpu().numpy().reshape(-1, K), O.gemm_bwd_dx(rb, q, s, g))
     e_dw = O.rel_fro_error(layer.weight.grad.cpu().numpy(), O.gemm_bwd_dw(rb, xb))
-    print(f"[qat] g={g} y {e_y:.2e} dX (bf16) {e_dx:.2e} dW {e_dw:.2e}", flush=True)
+    print(f"[qat] g={g} {dx_precision} y {e_y:.2e} dX (bf16) {e_dx:.2e} dW {e_dw:.2e}", flush=True)
     assert e_y <= REL_DESIGN
     assert e_dx <= REL_BAR  # dX is returned in the activations' dtype (bf16)
     assert e_dw <= REL_DESIGN
