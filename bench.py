@@ -4,8 +4,9 @@ A step is one pass of the whole path on synthetic Mamba-2 1.3B-shaped data:
   * in_proj QAT step (8512 x 2048 weights, 16384 tokens, g = 128):
     ternarize_pack -> tgemm_fwd -> tgemm_bwd_dx (one float16 pass, its
     prepass included) -> tgemm_bwd_dw_ste;
-  * one decode token over all 48 layers: tgemv over the 48 packed in_proj
-    matrices and over the 48 packed out_proj matrices (batch 1).
+  * one decode token over all 48 layers: the GEMV over the 48 packed in_proj
+    matrices and the 48 packed out_proj matrices (batch 1), both stacks in
+    one launch (tm_tgemv_pair).
 All inputs are resident in HBM before the timed region.  Per-kernel times
 come from HIP events recorded on the stream the kernels run on.
 
@@ -79,8 +80,7 @@ def log(msg):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-KERNEL_SOURCES = {"tgemm_fwd": "tgemm_fwd.hip", "tgemv_in_proj": "tgemv.hip",
-                  "tgemv_out_proj": "tgemv.hip"}
+KERNEL_SOURCES = {"tgemm_fwd": "tgemm_fwd.hip", "tgemv_pair": "tgemv.hip"}
 
 
 def measured_traffic(kernel):
@@ -172,8 +172,15 @@ def main():
     torch.cuda.synchronize()
     log(f"decode arenas ready in {time.time() - t0:.1f}s")
 
-    names = ["ternarize_pack", "tgemm_fwd", "tgemm_bwd_dx", "tgemm_bwd_dw_ste",
-             "tgemv_in_proj", "tgemv_out_proj"]
+    names = ["ternarize_pack", "tgemm_fwd", "tgemm_bwd_dx", "tgemm_bwd_dw_ste", "tgemv_pair"]
+
+    def decode_token(xk, yk, arenas=None):
+        """One decode token over the 48 in_proj and 48 out_proj matrices in
+        one launch (tm_tgemv_pair); arenas: (in codes, in s16, out codes, out
+        s16) to read instead of the resident ones."""
+        a, b = dec["in"], dec["out"]
+        ci, si, co, so = arenas or (a["codes"], a["s16"], b["codes"], b["s16"])
+        ops.tgemv_pair(a[xk], ci, si, b[xk], co, so, a["cfg"].g, y0=a[yk], y1=b[yk])
 
     def step(ev):
         ev[0].record()
@@ -185,14 +192,10 @@ def main():
         ev[3].record()
         ops.tgemm_bwd_dw_ste(dY, X, dW=dW)
         ev[4].record()
-        d = dec["in"]
-        ops.tgemv(d["x"], d["codes"], d["s16"], d["cfg"].g, y=d["y"])
+        decode_token("x", "y")
         ev[5].record()
-        d = dec["out"]
-        ops.tgemv(d["x"], d["codes"], d["s16"], d["cfg"].g, y=d["y"])
-        ev[6].record()
 
-    mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(7)]
+    mk = lambda: [torch.cuda.Event(enable_timing=True) for _ in range(6)]
     for _ in range(args.warmup):
         step(mk())
     torch.cuda.synchronize()
@@ -225,6 +228,7 @@ def main():
 
     # ---------------- decode as a server runs it: tokens back to back ----------------
     def serving(batch, tokens):
+        """(in_proj ms, out_proj ms, two-launch token ms, one-launch token ms)"""
         xk, yk = ("x", "y") if batch == B else ("x4", "y4")
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(tokens)]
         for _ in range(3):
@@ -251,12 +255,24 @@ def main():
                 ops.tgemv(d[xk], d["codes"], d["s16"], d["cfg"].g, y=d[yk])
         e1.record()
         torch.cuda.synchronize()
+        two = e0.elapsed_time(e1) / tokens
+        # ... and in one launch per token
+        for _ in range(3):
+            decode_token(xk, yk)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(2_000_000)
+        e0.record()
+        for t in range(tokens):
+            decode_token(xk, yk)
+        e1.record()
+        torch.cuda.synchronize()
         return (float(np.mean([e[0].elapsed_time(e[1]) for e in ev])),
                 float(np.mean([e[1].elapsed_time(e[2]) for e in ev])),
-                e0.elapsed_time(e1) / tokens)
+                two, e0.elapsed_time(e1) / tokens)
     serve = {b: serving(b, max(args.steps, 10)) for b in sorted({B, 4})}
     cold = ({} if "cold" in args.skip
-            else cold_figures(ops, dec, W, dW, codes, scales, g, eps, max(args.steps // 4, 3)))
+            else cold_figures(ops, dec, W, dW, codes, scales, g, eps, max(args.steps // 4, 3),
+                              decode_token))
     small = None if "small" in args.skip else small_configs(ops, dev, args.steps)
     sweep = None if "sweep" in args.skip else group_sweep(ops, dev, max(args.steps // 2, 5))
 
@@ -294,8 +310,7 @@ def main():
         "tgemm_fwd": ("mfma", fl),
         "tgemm_bwd_dx": ("mfma", fl),
         "tgemm_bwd_dw_ste": ("mfma", fl),
-        "tgemv_in_proj": ("hbm", gemv_bytes(dcfg_in)),
-        "tgemv_out_proj": ("hbm", gemv_bytes(dcfg_out)),
+        "tgemv_pair": ("hbm", gemv_bytes(dcfg_in) + gemv_bytes(dcfg_out)),
     }
     kernels = {}
     for n in names:
@@ -316,30 +331,36 @@ def main():
             frac=round(ach / PEAK_BF16_TFLOPS, 4),
             what="two bfloat16 passes (16 bits of every scale); not part of the step")
     # in the step (after the training kernels) ...
-    dec_ms = per["tgemv_in_proj"] + per["tgemv_out_proj"]
+    dec_ms = per["tgemv_pair"]
     dec_bytes = gemv_bytes(dcfg_in) + gemv_bytes(dcfg_out)
     dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
-    # ... and tokens back to back
+    # ... and tokens back to back (one launch per token; the two-launch form
+    # and its per-projection events beside it)
     decode_serving = {}
-    for b, (t_in_ms, t_out_ms, t_tok_ms) in serve.items():
+    for b, (t_in_ms, t_out_ms, t_two_ms, t_tok_ms) in serve.items():
         nb = gemv_bytes(dcfg_in, b) + gemv_bytes(dcfg_out, b)
         gbps = nb / (t_tok_ms * 1e-3) / 1e9
+        gbps2 = nb / (t_two_ms * 1e-3) / 1e9
         decode_serving[f"B{b}"] = {
             "us_per_token": round(t_tok_ms * 1e3, 2),
             "GBps": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM_GBPS, 4),
             "bytes_per_token": nb,
-            "per_kernel_events": {"in_proj_us": round(t_in_ms * 1e3, 2),
-                                  "out_proj_us": round(t_out_ms * 1e3, 2)}}
+            "two_launches": {"us_per_token": round(t_two_ms * 1e3, 2), "GBps": round(gbps2, 1),
+                             "frac_hbm": round(gbps2 / PEAK_HBM_GBPS, 4),
+                             "per_kernel_events": {"in_proj_us": round(t_in_ms * 1e3, 2),
+                                                   "out_proj_us": round(t_out_ms * 1e3, 2)}}}
     for b in serve:
         ck = cold.get(f"decode_B{b}")
         if ck:
             decode_serving[f"B{b}"]["cold"] = ck
+        ck2 = cold.get(f"decode_B{b}_two_launches")
+        if ck2:
+            decode_serving[f"B{b}"]["two_launches"]["cold"] = ck2
     srv = decode_serving[f"B{B}"]
     srv_cold = srv.get("cold", srv)
 
     fwd = kernels["tgemm_fwd"]
-    t_in, t_out = measured_traffic("tgemv_in_proj"), measured_traffic("tgemv_out_proj")
-    dec_traffic = None if t_in is None or t_out is None else t_in + t_out
+    dec_traffic = measured_traffic("tgemv_pair")
     out = {
         "metric": "ternary GEMM TFLOP/s (in_proj, 16k tokens) + batch-1 tgemv GB/s, % of roofline",
         "value": fwd["achieved"],
@@ -375,9 +396,10 @@ def main():
         "roofline_tgemv": {"bound": "hbm", "achieved": srv_cold["GBps"], "peak": PEAK_HBM_GBPS,
                            "unit": "GB/s", "frac": srv_cold["frac_hbm"],
                            "traffic": dec_traffic, "algorithmic_per_token": dec_bytes,
-                           "kernel": "tgemv, 48 in_proj + 48 out_proj layers, tokens back to "
-                                     "back, " + ("weights rotated over >= 1.1 GiB of copies (cold)"
-                                                 if "cold" in srv else "one weight arena (warm)"),
+                           "kernel": "tgemv_pair, 48 in_proj + 48 out_proj layers in one launch, "
+                                     "tokens back to back, "
+                                     + ("weights rotated over >= 1.1 GiB of copies (cold)"
+                                        if "cold" in srv else "one weight arena (warm)"),
                            "warm": {"achieved": srv["GBps"], "frac": srv["frac_hbm"]}},
         "kernels": kernels,
         "qat_block": qat_block,
@@ -433,13 +455,13 @@ def main():
 ROTATE_BYTES = 1.1 * 2 ** 30   # cold figures rotate over this much distinct input
 
 
-def cold_figures(ops, dec, W, dW, codes, scales, g, eps, reps):
+def cold_figures(ops, dec, W, dW, codes, scales, g, eps, reps, decode_token):
     """HBM-bound calls with their inputs rotated over >= 1.1 GiB of distinct
     copies, so no call finds its input in the 256 MB memory-side cache or the
     L2 (the "cold" figures; the warm ones repeat one input):
       * the decode token (48 in_proj + 48 out_proj matrices), B = 1 and 4,
         cycling over copies of both arenas, tokens back to back under one
-        event pair;
+        event pair, in one launch per token (tm_tgemv_pair) and in two;
       * ternarize_pack, the threshold-multiplier and given-threshold
         ternarizers, cycling over copies of the in_proj W;
       * the group-magnitude gradient, cycling over copies of dW.
@@ -457,29 +479,34 @@ def cold_figures(ops, dec, W, dW, codes, scales, g, eps, reps):
         if dec["in"][xk].shape[1] != batch:
             continue
 
-        def token(t):
+        def token_two(t):
             for kind in ("in", "out"):
                 d = dec[kind]
                 c, sc = sets[t % nsets][kind]
                 ops.tgemv(d[xk], c, sc, d["cfg"].g, y=d[yk])
-        for t in range(2 * nsets):
-            token(t)
-        torch.cuda.synchronize()
-        ntok = max(reps, 5) * nsets
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda._sleep(2_000_000)
-        e0.record()
-        for t in range(ntok):
-            token(t)
-        e1.record()
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / ntok
+
+        def token_one(t):
+            st = sets[t % nsets]
+            decode_token(xk, yk, (st["in"][0], st["in"][1], st["out"][0], st["out"][1]))
         nb = sum(L * (c.N * c.K / 4 + 2 * c.N * c.K / c.g + 2 * batch * c.K + 4 * batch * c.N)
                  for c, L in ((dec[k]["cfg"], dec[k]["codes"].shape[0]) for k in ("in", "out")))
-        res[f"decode_B{batch}"] = {"us_per_token": round(us, 2),
-                                   "GBps": round(nb / (us * 1e-6) / 1e9, 1),
-                                   "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
-                                   "copies": nsets}
+        for key, token in ((f"decode_B{batch}", token_one),
+                           (f"decode_B{batch}_two_launches", token_two)):
+            for t in range(2 * nsets):
+                token(t)
+            torch.cuda.synchronize()
+            ntok = max(reps, 5) * nsets
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(2_000_000)
+            e0.record()
+            for t in range(ntok):
+                token(t)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / ntok
+            res[key] = {"us_per_token": round(us, 2), "GBps": round(nb / (us * 1e-6) / 1e9, 1),
+                        "frac_hbm": round(nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                        "copies": nsets}
     del sets
     # W and dW copies
     N, K = W.shape

@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 10
+#define TM_ABI_VERSION 11
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -224,6 +224,28 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
                    const uint16_t* scales_f16, int32_t count, int32_t B,
                    int64_t N, int64_t K, int32_t g, float* y, tm_stream stream);
+
+/*
+ * tm_tgemv_pair — the decode product of tm_tgemv (Sec. 8, batch-1 decoding
+ * bound by weight traffic) over two strided stacks in one launch, e.g. all
+ * in_proj layers and all out_proj layers of a decode token:
+ *   y0[c, b, n] = sum_k x0[c, b, k] * q0_c[n, k] * s0_c[n, k/g]  (c < count0)
+ *   y1[c, b, n] = sum_k x1[c, b, k] * q1_c[n, k] * s1_c[n, k/g]  (c < count1)
+ * Each stack's arguments, layout, alignment and limits are those of
+ * tm_tgemv; the stacks share B and g.  Neither output may overlap the other
+ * or any input.  The workgroups of the second stack follow those of the
+ * first in one grid, so the GPU does not drain between the stacks.  Shapes
+ * whose staging differs between the stacks run as two launches instead.
+ * Results are deterministic and equal tm_tgemv's on the same stack bit for
+ * bit, except where tm_tgemv splits K for a stack of few row blocks (fewer
+ * than two per CU): there the last bits can differ.
+ */
+tm_status tm_tgemv_pair(const uint16_t* x0, const uint8_t* codes0,
+                        const uint16_t* scales0, int32_t count0, int64_t N0,
+                        int64_t K0, float* y0, const uint16_t* x1,
+                        const uint8_t* codes1, const uint16_t* scales1,
+                        int32_t count1, int64_t N1, int64_t K1, float* y1,
+                        int32_t B, int32_t g, tm_stream stream);
 
 /*
  * tm_dgemv — decode-time product of a layer kept in FP16 (Sec. 7,

@@ -104,6 +104,32 @@ tm_status bwd_dx_checked(const uint16_t* dY, const uint8_t* codes, const float* 
   return TM_OK;
 }
 
+// argument checks of one strided stack of tm_tgemv; out / ins: the spans of
+// y and of x, codes, scales
+tm_status tgemv_checked(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
+                        int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
+                        Span* out, Span* ins) {
+  if (!x || !codes || !scales_f16 || !y) return TM_EINVAL;
+  if (count < 1 || count > 65535 || B < 1 || B > 16 || N < 1) return TM_ESHAPE;
+  if (tm_status st = shape_kg(K, g)) return st;
+  int64_t cbm, sbm, xb, cb, sb, yb, ybm;
+  if (!bytes_of(N, K / 4, 1, &cbm) || !bytes_of(N, K / g, 2, &sbm) ||
+      !bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of(count, cbm, 1, &cb) ||
+      !bytes_of(count, sbm, 1, &sb) || !bytes_of((int64_t)B, N, 4, &ybm) ||
+      !bytes_of(count, ybm, 1, &yb))
+    return TM_ESHAPE;
+  if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
+  if (cbm > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside one matrix
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
+    return TM_EALIGN;
+  *out = span(y, yb);
+  ins[0] = span(x, xb);
+  ins[1] = span(codes, cb);
+  ins[2] = span(scales_f16, sb);
+  if (overlap(*out, ins[0]) || overlap(*out, ins[1]) || overlap(*out, ins[2])) return TM_EINVAL;
+  return TM_OK;
+}
+
 // argument checks of the mixer step; workspace NULL: the library's own
 // scratch array (no overlap check needed: no caller array can overlap it)
 // gate_only: the gated float32 output of tm_mixer_gate in place of the
@@ -381,23 +407,27 @@ tm_status tm_mixer_step_noalloc(const float* zxbcdt, int32_t B, int32_t nheads, 
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
                    int32_t count, int32_t B, int64_t N, int64_t K, int32_t g, float* y,
                    tm_stream stream) {
-  if (!x || !codes || !scales_f16 || !y) return TM_EINVAL;
-  if (count < 1 || count > 65535 || B < 1 || B > 16 || N < 1) return TM_ESHAPE;
-  if (tm_status st = shape_kg(K, g)) return st;
-  int64_t cbm, sbm, xb, cb, sb, yb, ybm;
-  if (!bytes_of(N, K / 4, 1, &cbm) || !bytes_of(N, K / g, 2, &sbm) ||
-      !bytes_of((int64_t)count * B, K, 2, &xb) || !bytes_of(count, cbm, 1, &cb) ||
-      !bytes_of(count, sbm, 1, &sb) || !bytes_of((int64_t)B, N, 4, &ybm) ||
-      !bytes_of(count, ybm, 1, &yb))
-    return TM_ESHAPE;
-  if ((N + 63) / 64 > kMaxGridBlocks) return TM_ESHAPE;
-  if (cbm > (int64_t(1) << 31)) return TM_ESHAPE;  // 32-bit offsets inside one matrix
-  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales_f16, 2) || !aligned(y, 16))
-    return TM_EALIGN;
-  const Span o = span(y, yb);
-  if (overlap(o, span(x, xb)) || overlap(o, span(codes, cb)) || overlap(o, span(scales_f16, sb)))
-    return TM_EINVAL;
+  Span out, ins[3];
+  if (tm_status st = tgemv_checked(x, codes, scales_f16, count, B, N, K, g, y, &out, ins))
+    return st;
   return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
+}
+
+tm_status tm_tgemv_pair(const uint16_t* x0, const uint8_t* codes0, const uint16_t* scales0,
+                        int32_t count0, int64_t N0, int64_t K0, float* y0, const uint16_t* x1,
+                        const uint8_t* codes1, const uint16_t* scales1, int32_t count1,
+                        int64_t N1, int64_t K1, float* y1, int32_t B, int32_t g,
+                        tm_stream stream) {
+  Span o0, o1, i0[3], i1[3];
+  if (tm_status st = tgemv_checked(x0, codes0, scales0, count0, B, N0, K0, g, y0, &o0, i0))
+    return st;
+  if (tm_status st = tgemv_checked(x1, codes1, scales1, count1, B, N1, K1, g, y1, &o1, i1))
+    return st;
+  if (overlap(o0, o1)) return TM_EINVAL;
+  for (int i = 0; i < 3; ++i)
+    if (overlap(o0, i1[i]) || overlap(o1, i0[i])) return TM_EINVAL;
+  return hip_status(tmk::launch_tgemv_pair(x0, codes0, scales0, count0, N0, K0, y0, x1, codes1,
+                                           scales1, count1, N1, K1, y1, B, g, to_hip(stream)));
 }
 
 tm_status tm_tgemv_rms(const float* src, const float* norm_w, float eps, const uint8_t* codes,

@@ -63,6 +63,12 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
 hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
+// two strided stacks of matrices (e.g. a decode token's in_proj and out_proj
+// layers) in one launch; same g and B, everything else per stack
+hipError_t launch_tgemv_pair(const uint16_t* x0, const uint8_t* c0, const uint16_t* s0, int n0,
+                             int64_t N0, int64_t K0, float* y0, const uint16_t* x1,
+                             const uint8_t* c1, const uint16_t* s1, int n1, int64_t N1,
+                             int64_t K1, float* y1, int B, int g, hipStream_t stream);
 // Fused decode projection: x = bf16(src / sqrt(mean(src^2) + eps) * nw) per
 // batch row, y = (or +=, accum) x times the ternary matrix.  Shapes the
 // kernel stages in one part (tgemv_rms_fits) only.

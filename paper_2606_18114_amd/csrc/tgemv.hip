@@ -506,13 +506,56 @@ __device__ __forceinline__ void slot_compute(const uint8_t* smem, const SlotRegs
 // rows and of the weight into registers, the sums of squares are taken per
 // 16-column piece and then per row in a fixed order (deterministic).
 // accum: y += the product instead of y = (each element has one owner lane).
-template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS, bool RMS>
+//
+// PAIR (one launch over two stacks of matrices, e.g. the in_proj and the
+// out_proj layers of a decode token): the grid is one-dimensional, the first
+// pr.nb0 workgroups take the stack given by the regular arguments (pr.rb0 row
+// blocks per matrix), the rest the stack in `pr`; the stacks share g, B and
+// the launch shape, so the tail of the first overlaps the head of the second
+// instead of draining the GPU between two launches.
+struct GemvPair {
+  const uint16_t* x;
+  const uint8_t* codes;
+  const uint16_t* s16;
+  float* y;
+  int64_t N, K, KP, xms, yms, nb0, rb0, rb1;
+};
+
+template <int G, int WAVES, int RING, int SK, int NR, bool SW, bool XD, bool KS, bool RMS,
+          bool PAIR = false>
 __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
-    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales_f16, int B, int64_t N, int64_t K, int64_t KP,
-    int64_t xms, int64_t yms, float* __restrict__ y, const float* __restrict__ xr,
-    const float* __restrict__ nw, float eps, int accum) {
+    const uint16_t* __restrict__ x_a, const uint8_t* __restrict__ codes_a,
+    const uint16_t* __restrict__ scales_a, int B, int64_t N_a, int64_t K_a, int64_t KP_a,
+    int64_t xms_a, int64_t yms_a, float* __restrict__ y_a, const float* __restrict__ xr,
+    const float* __restrict__ nw, float eps, int accum, GemvPair pr = GemvPair{}) {
   static_assert(!RMS || XD, "the fused normalization stages x directly");
+  static_assert(!PAIR || (XD && !KS && !RMS), "pairs take the plain staged-x form");
+  // the stack of this workgroup (uniform), its matrix and its row block
+  const uint16_t* x = x_a;
+  const uint8_t* codes = codes_a;
+  const uint16_t* scales_f16 = scales_a;
+  float* y = y_a;
+  int64_t N = N_a, K = K_a, KP = KP_a, xms = xms_a, yms = yms_a;
+  int64_t mat = blockIdx.y, rblk = blockIdx.x;
+  if constexpr (PAIR) {
+    const int64_t bid = blockIdx.x;
+    if (bid < pr.nb0) {
+      mat = bid / pr.rb0;
+      rblk = bid % pr.rb0;
+    } else {
+      x = pr.x;
+      codes = pr.codes;
+      scales_f16 = pr.s16;
+      y = pr.y;
+      N = pr.N;
+      K = pr.K;
+      KP = pr.KP;
+      xms = pr.xms;
+      yms = pr.yms;
+      mat = (bid - pr.nb0) / pr.rb1;
+      rblk = (bid - pr.nb0) % pr.rb1;
+    }
+  }
   using Plan = SlotPlan<G, SK, SW>;
   constexpr int H = G < 128 ? 128 / G : 1;
   constexpr int CPS = SK / 128;
@@ -525,10 +568,9 @@ __global__ __launch_bounds__(64 * WAVES) void tgemv_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15;
   const int q = lane >> 4;
-  const int64_t mat = blockIdx.y;
   const int nslot = (int)((K + SK - 1) / SK);
-  const int64_t rowb = KS ? (int64_t)blockIdx.x * kGemvWaveRows
-                          : (int64_t)blockIdx.x * (kGemvWaveRows * WAVES) + wave * kGemvWaveRows;
+  const int64_t rowb = KS ? rblk * kGemvWaveRows
+                          : rblk * (kGemvWaveRows * WAVES) + wave * kGemvWaveRows;
   const int s0 = KS ? wave : 0;       // first slot of this wave
   const int sstep = KS ? WAVES : 1;   // slot stride
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
@@ -927,6 +969,91 @@ static hipError_t launch_any_g(const uint16_t* x, const uint8_t* codes, const ui
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream) {
   return launch_any_g(x, codes, s16, count, B, N, K, g, y, stream, nullptr, nullptr, 0.f, 0);
+}
+
+// Two stacks in one launch (PAIR) when both take the plain staged-x form
+// with the same scale-load form; otherwise two launches.
+template <int G>
+static hipError_t launch_pair_g(const uint16_t* x0, const uint8_t* c0, const uint16_t* s0,
+                                int n0, int64_t N0, int64_t K0, float* y0, const uint16_t* x1,
+                                const uint8_t* c1, const uint16_t* s1, int n1, int64_t N1,
+                                int64_t K1, float* y1, int B, hipStream_t stream) {
+  constexpr int H = G < 128 ? 128 / G : 1;
+  constexpr int SK = kGemvSlotK, RING = kGemvRing, WAVES = kGemvWaves;
+  const int R = kTerms * B * H;
+  auto kp_of = [&](int64_t K) { return (K + SK - 1) / SK * SK; };
+  auto staged = [&](int64_t K) {  // the XD condition of launch_gw with KP covering K
+    const int rmax = R < 64 ? R : 64;
+    int budget = kGemvXBytes;
+    if (budget < rmax * (SK + kGemvXPad)) budget = rmax * (SK + kGemvXPad);
+    const int64_t kp = (int64_t)(budget / rmax - kGemvXPad) / SK * SK;
+    return kp >= K && R <= 16 && B * ((K + 127) / 128 * 8) <= 2 * 64 * WAVES;
+  };
+  auto words = [&](int64_t K, const uint16_t* sp) {
+    return (K / G) % 2 == 0 && SK / G >= 2 && ((uintptr_t)sp & 3) == 0;
+  };
+  const bool sw0 = words(K0, s0), sw1 = words(K1, s1);
+  const int64_t rb0 = (N0 + 127) / 128, rb1 = (N1 + 127) / 128;
+  const int64_t nb0 = (int64_t)n0 * rb0, nb1 = (int64_t)n1 * rb1;
+  if (!staged(K0) || !staged(K1) || sw0 != sw1 || nb0 + nb1 > 0x7FFFFFFF) {
+    const hipError_t e = launch_g<G>(x0, c0, s0, n0, B, N0, K0, y0, stream, nullptr, nullptr,
+                                     0.f, 0);
+    if (e != hipSuccess) return e;
+    return launch_g<G>(x1, c1, s1, n1, B, N1, K1, y1, stream, nullptr, nullptr, 0.f, 0);
+  }
+  const int64_t KP0 = kp_of(K0), KP1 = kp_of(K1);
+  auto lds_of = [&](int slot_bytes, int64_t KP, int64_t K) {
+    const int64_t KR = (K + 511) / 512 * 512;
+    size_t xa = (size_t)R * (KP + kGemvXPad);
+    if ((size_t)B * KR * 2 > xa) xa = (size_t)B * KR * 2;
+    const size_t ea = ((size_t)R * (KP / 32) + 15) / 16 * 16;
+    return (size_t)WAVES * slot_bytes + xa + ea + 128;
+  };
+  GemvPair pr;
+  pr.x = x1;
+  pr.codes = c1;
+  pr.s16 = s1;
+  pr.y = y1;
+  pr.N = N1;
+  pr.K = K1;
+  pr.KP = KP1;
+  pr.xms = (int64_t)B * K1;
+  pr.yms = (int64_t)B * N1;
+  pr.nb0 = nb0;
+  pr.rb0 = rb0;
+  pr.rb1 = rb1;
+  const dim3 grid((unsigned)(nb0 + nb1)), block(64 * WAVES);
+#define TM_GEMV_PAIR(SW_)                                                                      \
+  do {                                                                                         \
+    constexpr int kSlot = RING * SlotPlan<G, SK, SW_>::kSlotBytes;                             \
+    const size_t la = lds_of(kSlot, KP0, K0), lb = lds_of(kSlot, KP1, K1);                     \
+    hipLaunchKernelGGL((tgemv_kernel<G, WAVES, RING, SK, 1, SW_, true, false, false, true>),   \
+                       grid, block, la > lb ? la : lb, stream, x0, c0, s0, B, N0, K0, KP0,     \
+                       (int64_t)B * K0, (int64_t)B * N0, y0, nullptr, nullptr, 0.f, 0, pr);    \
+  } while (0)
+  if constexpr (SK / G >= 2) {
+    if (sw0) {
+      TM_GEMV_PAIR(true);
+      return hipGetLastError();
+    }
+  }
+  TM_GEMV_PAIR(false);
+#undef TM_GEMV_PAIR
+  return hipGetLastError();
+}
+
+hipError_t launch_tgemv_pair(const uint16_t* x0, const uint8_t* c0, const uint16_t* s0, int n0,
+                             int64_t N0, int64_t K0, float* y0, const uint16_t* x1,
+                             const uint8_t* c1, const uint16_t* s1, int n1, int64_t N1,
+                             int64_t K1, float* y1, int B, int g, hipStream_t stream) {
+  switch (g) {
+    case 32:  return launch_pair_g<32>(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, stream);
+    case 64:  return launch_pair_g<64>(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, stream);
+    case 128: return launch_pair_g<128>(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, stream);
+    case 256: return launch_pair_g<256>(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, stream);
+    case 512: return launch_pair_g<512>(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 static_assert(kTerms == 4 && kGemvSlotK == 512 && kGemvWaves == 4,

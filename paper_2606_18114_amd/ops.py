@@ -38,6 +38,8 @@ SIGNATURES = {
     "tm_tgemm_bwd_dx_f16_workspace": (ctypes.c_int64, [_I64, _I64]),
     "tm_tgemm_bwd_dw_ste": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _P, _I32, _P]),
     "tm_tgemv": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _I64, _I32, _P, _P]),
+    "tm_tgemv_pair": (ctypes.c_int, [_P, _P, _P, _I32, _I64, _I64, _P, _P, _P, _P, _I32, _I64,
+                                     _I64, _P, _I32, _I32, _P]),
     "tm_ternarize_pack_thresh": (ctypes.c_int,
                                  [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P, _P]),
     "tm_group_code_dot": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _P]),
@@ -372,6 +374,39 @@ def tgemv(x: torch.Tensor, codes: torch.Tensor, scales_f16: torch.Tensor, g: int
                         _stream())
     _check("tm_tgemv", st)
     return y
+
+
+def _gemv_stack(x, codes, scales_f16, g, y, tag):
+    _need(x, f"x{tag}", _BF16, 3)
+    _need(codes, f"codes{tag}", _U8, 3)
+    _need(scales_f16, f"scales{tag}", _F16, 3)
+    count, B, K = x.shape
+    N = codes.shape[1]
+    _shape(codes, f"codes{tag}", (count, N, K // 4), x.device)
+    _shape(scales_f16, f"scales{tag}", (count, N, _groups(K, g)), x.device)
+    if y is None:
+        y = torch.empty((count, B, N), dtype=torch.float32, device=x.device)
+    _need(y, f"y{tag}", _F32, 3)
+    _shape(y, f"y{tag}", (count, B, N), x.device)
+    return count, B, N, K, y
+
+
+def tgemv_pair(x0: torch.Tensor, codes0: torch.Tensor, scales0: torch.Tensor,
+               x1: torch.Tensor, codes1: torch.Tensor, scales1: torch.Tensor, g: int = 128,
+               y0: Optional[torch.Tensor] = None, y1: Optional[torch.Tensor] = None):
+    """Two strided stacks of ``tgemv`` in one launch (``tm_tgemv_pair``), e.g. a
+    decode token's in_proj and out_proj layers; returns (y0, y1)."""
+    c0, B, N0, K0, y0 = _gemv_stack(x0, codes0, scales0, g, y0, "0")
+    c1, B1, N1, K1, y1 = _gemv_stack(x1, codes1, scales1, g, y1, "1")
+    if B1 != B:
+        raise ValueError(f"the stacks have batches {B} and {B1}; tm_tgemv_pair needs one")
+    if x1.device != x0.device:
+        raise ValueError("the two stacks live on different devices")
+    st = lib().tm_tgemv_pair(_ptr(x0), _ptr(codes0), _ptr(scales0), c0, N0, K0, _ptr(y0),
+                             _ptr(x1), _ptr(codes1), _ptr(scales1), c1, N1, K1, _ptr(y1), B, g,
+                             _stream())
+    _check("tm_tgemv_pair", st)
+    return y0, y1
 
 
 def dgemv(x: torch.Tensor, W16: torch.Tensor, y: Optional[torch.Tensor] = None) -> torch.Tensor:

@@ -49,6 +49,12 @@ hipError_t launch_tgemv(const uint16_t*, const uint8_t*, const uint16_t*, int, i
   reached("tgemv");
 }
 
+hipError_t launch_tgemv_pair(const uint16_t*, const uint8_t*, const uint16_t*, int, int64_t,
+                             int64_t, float*, const uint16_t*, const uint8_t*, const uint16_t*,
+                             int, int64_t, int64_t, float*, int, int, hipStream_t) {
+  reached("tgemv_pair");
+}
+
 hipError_t launch_dgemv(const uint16_t*, const uint16_t*, int, int, int64_t, int64_t, float*,
                         hipStream_t) {
   reached("dgemv");

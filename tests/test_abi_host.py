@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 10
+    assert L.tm_abi_version() == 11
 
 
 def test_status_strings(L):
@@ -367,6 +367,26 @@ def test_tgemm_bwd_dx_validation(L):
     assert dx(L, dY=P + 8) == EALIGN
     assert dx(L, dX=P + 2 ** 26 + 8) == EALIGN
     assert dx(L, dX=P) == EINVAL
+
+
+def gpair(L, x0=P, c0=P + 2 ** 24, s0=P + 2 ** 25, n0=2, N0=256, K0=512, y0=P + 2 ** 26,
+          x1=P + 2 ** 27, c1=P + 2 ** 28, s1=P + 2 ** 29, n1=3, N1=128, K1=1024,
+          y1=P + 2 ** 30, B=1, g=128):
+    return L.tm_tgemv_pair(x0, c0, s0, n0, N0, K0, y0, x1, c1, s1, n1, N1, K1, y1, B, g, None)
+
+
+def test_tgemv_pair_validation(L):
+    for kw in ("x0", "c0", "s0", "y0", "x1", "c1", "s1", "y1"):
+        assert gpair(L, **{kw: 0}) == EINVAL, kw
+    assert gpair(L, n0=0) == ESHAPE
+    assert gpair(L, n1=65536) == ESHAPE
+    assert gpair(L, K1=1000) == ESHAPE                   # K % 64 in the second stack
+    assert gpair(L, B=17) == ESHAPE
+    assert gpair(L, g=96) == ESHAPE
+    assert gpair(L, y1=P + 2 ** 30 + 4) == EALIGN
+    assert gpair(L, y1=P + 2 ** 26) == EINVAL            # the two outputs overlap
+    assert gpair(L, y1=P + 2 ** 24) == EINVAL            # y1 over the first stack's codes
+    assert gpair(L, y0=P + 2 ** 28) == EINVAL            # y0 over the second stack's codes
 
 
 def dx16(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,
