@@ -233,8 +233,9 @@ tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
  *   y1[c, b, n] = sum_k x1[c, b, k] * q1_c[n, k] * s1_c[n, k/g]  (c < count1)
  * Each stack's arguments, layout, alignment and limits are those of
  * tm_tgemv; the stacks share B and g.  Neither output may overlap the other
- * or any input.  The workgroups of the second stack follow those of the
- * first in one grid, so the GPU does not drain between the stacks.  Shapes
+ * or any input.  The workgroups of both stacks form one grid (those of the
+ * stack with the longer rows first), so the GPU does not drain between the
+ * stacks.  Shapes
  * whose staging differs between the stacks run as two launches instead.
  * Results are deterministic and equal tm_tgemv's on the same stack bit for
  * bit, except where tm_tgemv splits K for a stack of few row blocks (fewer
