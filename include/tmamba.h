@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 11
+#define TM_ABI_VERSION 12
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -398,6 +398,78 @@ tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                         uint16_t* ssm_state, const float* conv_w, const float* conv_b,
                         const float* dt_bias, const float* A_log, const float* D, float* gated,
                         tm_stream stream);
+
+/*
+ * A stack of ternary Mamba-2 blocks for whole-stack decoding (Sec. 8:
+ * batch-1 decoding, bound by the weight traffic; Sec. 3.2: the mixer and
+ * its states stay in FP16).  Every array is device memory, stacked along a
+ * leading layer dimension L = n_layers; d_inner = 64 nheads, d_state 128,
+ * d_conv 4, Z = 2 d_inner + 256 + nheads, conv_dim = d_inner + 256.
+ *   n_layers >= 1; d_model and d_inner multiples of g and of 64, at most 4096
+ *   and 8192 (the workgroup's x pairs); g in {64, 128, 256}; 1 <= nheads <= the
+ *   device's CU count; eps: RMSNorm epsilon (finite, >= 0)
+ *   in_codes   uint8 [L, Z, d_model/4]        in_scales  fp16 [L, Z, d_model/g]
+ *   out_codes  uint8 [L, d_model, d_inner/4]  out_scales fp16 [L, d_model, d_inner/g]
+ *   pre_w      float32 [L, d_model]   the block's pre-norm weight
+ *   conv_w     float32 [L, conv_dim, 4], conv_b float32 [L, conv_dim]
+ *   dt_bias, A_log, D  float32 [L, nheads]
+ *   norm_w     float32 [L, d_inner]   the gated RMSNorm's weight
+ *   final_w    float32 [d_model]      the final norm's weight
+ *   conv_state fp16 [L, conv_dim, 4] (8-byte aligned), conv_pos int32 [L],
+ *   ssm_state  fp16 [L, nheads, 64, 128] (16-byte aligned): the decode state,
+ *              in and out, as for tm_mixer_step with B = 1
+ * Codes, pre_w, norm_w and final_w 16-byte aligned, scales 2-byte, the other
+ * float arrays 4-byte.
+ */
+typedef struct {
+  int32_t n_layers, d_model, nheads, g;
+  float eps;
+  const uint8_t* in_codes;
+  const uint16_t* in_scales;
+  const uint8_t* out_codes;
+  const uint16_t* out_scales;
+  const float* pre_w;
+  const float* conv_w;
+  const float* conv_b;
+  const float* dt_bias;
+  const float* A_log;
+  const float* D;
+  const float* norm_w;
+  const float* final_w;
+  uint16_t* conv_state;
+  int32_t* conv_pos;
+  uint16_t* ssm_state;
+} tm_mamba2_stack;
+
+/*
+ * tm_mamba2_decode_token — one batch-1 decode token through every block of
+ * the stack in a single launch: per block, in layer order,
+ *   zx        = in_proj(bf16(rmsnorm(residual) * pre_w))        (tm_tgemv_rms)
+ *   g         = conv + FP16 SSM step + y * SiLU(z)               (tm_mixer_gate)
+ *   residual += out_proj(bf16(rmsnorm(g) * norm_w))             (tm_tgemv_rms)
+ * with residual = emb for the first block, then
+ *   x_out = bf16(rmsnorm(residual) * final_w).
+ *   stack      host pointer to the description above (read during the call)
+ *   emb        float32 [d_model] in;  x_out  bf16 [d_model] out (2-byte aligned)
+ *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads)
+ *              bytes, 256-byte aligned, owned by the caller; nothing need be
+ *              set before the call.  Its uint32 word 768 is nonzero after a
+ *              call whose grid barrier gave up waiting (not expected: the
+ *              launch is cooperative, so every workgroup is resident).
+ * One workgroup per CU in a cooperative launch; the blocks' phases are
+ * separated by grid barriers (three per block) instead of kernel launches.
+ * The ternary products take the bfloat16 x against the codes (exact
+ * products, float32 sums, float16 group scale in float32), so they agree
+ * with tm_tgemv_rms to float32 rounding; the normalizations sum in a
+ * different order, which can move an x element by one bfloat16 step.
+ * Calls sharing the state arrays or the workspace must not overlap in time.
+ */
+tm_status tm_mamba2_decode_token(const tm_mamba2_stack* stack, const float* emb,
+                                 uint16_t* x_out, void* workspace, int64_t workspace_bytes,
+                                 tm_stream stream);
+
+/* Workspace bytes of tm_mamba2_decode_token (-1 for sizes out of range). */
+int64_t tm_mamba2_decode_workspace(int32_t d_model, int32_t nheads);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

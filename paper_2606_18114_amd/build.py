@@ -36,6 +36,7 @@ SOURCES = [
     "tgemv.hip",
     "dgemv.hip",
     "mixer.hip",
+    "decode_stack.hip",
     "group_code_dot.hip",
 ]
 

@@ -1,0 +1,462 @@
+// One batch-1 decode token through a whole stack of ternary Mamba-2 blocks
+// in a single launch (paper Sec. 8: batch-1 decoding is bound by the weight
+// traffic; Sec. 3.2: the mixer stays in FP16).  Per block l, in layer order:
+//
+//   A  zx = in_proj(bf16(rmsnorm(residual) * pre_w[l]))      Z rows, K = d_model
+//   B  gated = mixer step per head (conv, FP16 SSM, y * SiLU(z))
+//   C  residual += out_proj(bf16(rmsnorm(gated) * norm_w[l]))  d_model rows, K = d_inner
+//
+// and after the last block x_out = bf16(rmsnorm(residual) * final_w).  The
+// first block's residual is the token's embedding.
+//
+// The grid is one workgroup per CU, launched cooperatively (all resident at
+// once), and the phases are separated by grid barriers: the waves' stores
+// complete, one atomic increment of a counter, a spin on the counter
+// (bounded: after 2^16 polls a flag is set and the spin ends, and every
+// later wait that sees the flag ends too, so every wave always exits soon).
+// The data that crosses workgroups (zx, the gated values and their sums,
+// the residual) is written and read with agent-scope coherent accesses.  Three barriers per block
+// replace the three kernel launches per block of the layer-by-layer decode
+// (the first is waited for by the heads' workgroups only, the second has
+// only those as arrivals).
+//
+// Ternary rows (phases A and C): one wave per output row at a time; lane l
+// takes the 16-column code words l, l + 64, ... of the row.  Each word's
+// 16 codes become eight bfloat16 pairs 2q by one shift and one AND per pair,
+// which v_dot2_f32_bf16 multiplies by the matching bfloat16 pairs of x
+// (exact products, float32 sums); the word's sum is scaled by the group's
+// float16 scale, the lanes' sums meet in a butterfly, and 0.5 * sum is the
+// output.  The normalized x of the phase is built once per workgroup in LDS
+// (every workgroup computes the same sum of squares in the same order) and
+// each lane keeps the pairs of its words in registers.  A wave loads the
+// code words and scales of its next rows (up to kDsPrefetch words per lane)
+// while it waits at the grid barrier that precedes their phase, so their
+// memory latency overlaps the wait.
+//
+// Mixer (phase B): one workgroup per head (mixer_dev.hpp), the head's float16
+// state loaded during the barrier that precedes the phase; the per-head sums
+// of g^2 feed phase C's normalization; the ring position of block l moves on
+// in phase C (after every head has read it).
+#include <type_traits>
+
+#include "launchers.hpp"
+#include "mixer_dev.hpp"
+
+namespace tmk {
+
+typedef __attribute__((ext_vector_type(2))) __bf16 ds_bf16x2;
+
+constexpr int kDsThreads = 256;
+constexpr int kDsWaves = kDsThreads / 64;
+constexpr int kDsPrefetch = 24;   // code words per lane held for the next rows
+constexpr uint32_t kDsSpinLimit = 1u << 16;   // a barrier takes microseconds
+constexpr int kDsCounters = 8;                // barrier counter words (one per XCD)
+constexpr int kDsCounterStride = 32;          // 128 bytes between them
+// the three barriers of a block have counter sets of their own; the
+// timeout flag follows them
+constexpr int kDsSetWords = kDsCounters * kDsCounterStride;
+
+struct DsArgs {
+  DecodeStackDesc s;
+  const float* emb;
+  uint16_t* x_out;
+  uint32_t* sync;   // counter sets [256 b + 32 k] (barrier b < 3, word k < 8) and the
+                    // timeout flag [768], all zero at launch
+  float* zx;        // [Z]
+  float* gated;     // [d_inner]
+  float* partial;   // [nheads]
+  float* residual;  // [d_model]
+};
+
+// Every value one workgroup hands to another between barriers is written
+// and read with agent-scope coherent accesses (ld_f32 / st_f32 <true>), so a
+// barrier only needs each wave's stores to have completed before its
+// workgroup arrives; no L2 write-back or invalidation (which cost tens of
+// microseconds per barrier when every workgroup issued them).
+// The barrier in two halves: ds_arrive (this workgroup's stores have
+// completed: one increment of the counter) and ds_wait (spin until every
+// workgroup has arrived).  Loads of the next phase's operands go between the
+// two, so their memory latency overlaps the wait.
+// The arrival counter is spread over kDsCounters words 128 bytes apart
+// (workgroup b increments word b % kDsCounters, i.e. one word per XCD), so
+// the increments of the 256 workgroups do not all queue on one address; a
+// waiter loads all the words at once and adds them.
+__device__ __forceinline__ void ds_arrive(uint32_t* ctr) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores have completed
+  __syncthreads();
+  if (threadIdx.x == 0) atomicAdd(ctr + kDsCounterStride * (blockIdx.x % kDsCounters), 1u);
+}
+__device__ __forceinline__ void ds_wait(uint32_t* ctr, uint32_t* flag, uint32_t target) {
+  if (threadIdx.x == 0) {
+    uint32_t n = 0;
+    for (;;) {
+      uint32_t c[kDsCounters];
+#pragma unroll
+      for (int k = 0; k < kDsCounters; ++k)
+        c[k] = __hip_atomic_load(ctr + kDsCounterStride * k, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      uint32_t total = 0;
+#pragma unroll
+      for (int k = 0; k < kDsCounters; ++k) total += c[k];
+      if (total >= target) break;
+      __builtin_amdgcn_s_sleep(1);
+      ++n;
+      if (n == kDsSpinLimit) {  // a workgroup never arrived: give up, report
+        atomicOr(flag, 1u);
+        break;
+      }
+      // once any workgroup has given up, every later wait ends at once
+      if ((n & 255) == 0 &&
+          __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
+        break;
+    }
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ float ds_wave_sum(float v) {
+  v += __uint_as_float(lane_xchg<1>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<2>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<4>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<8>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<16>(__float_as_uint(v)));
+  v += __uint_as_float(lane_xchg<32>(__float_as_uint(v)));
+  return v;
+}
+
+__device__ __forceinline__ uint32_t ds_bf16_rne(float v) {
+  const uint32_t b = __float_as_uint(v);
+  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+}
+
+// 16 bytes at byte offset off of a buffer, read coherently at agent scope
+// (the sc1 policy: past the per-XCD L2's stale lines)
+__device__ __forceinline__ u32x4 ds_ld16_coherent(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16);
+}
+
+// x pairs in LDS: xs[i] = bf16(src[2i] r w[2i]) | bf16(src[2i+1] r w[2i+1]) << 16,
+// r = 1 / sqrt(sumsq / K + eps), for K <= 1024 NQ.  sumsq: the sum of src^2
+// in a fixed order (the same in every workgroup), or, with part != NULL, the
+// sum of part[0 .. nparts) (lane j adds j, j + 64; nparts <= 128).  Every
+// thread issues all its loads (4 values i = tid + 256 j at 4 i, coherent
+// 16-byte loads) at once, so the phase pays one memory latency.
+template <int NQ>
+__device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
+                                          const float* __restrict__ w, int K, float eps,
+                                          const float* part, int nparts, uint32_t* xs,
+                                          float* red) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(src), (short)0, K * 4, 0x00020000);
+  float v[NQ][4];
+  float pv0 = 0.f, pv1 = 0.f;
+  if (part != nullptr) {
+    if (lane < nparts) pv0 = ld_f32<true>(part + lane);
+    if (lane + 64 < nparts) pv1 = ld_f32<true>(part + lane + 64);
+  }
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const int i = tid + kDsThreads * j;
+    u32x4 b = {0u, 0u, 0u, 0u};
+    if (4 * i < K) b = ds_ld16_coherent(rs, 16u * (uint32_t)i);
+    v[j][0] = __uint_as_float(b.x);
+    v[j][1] = __uint_as_float(b.y);
+    v[j][2] = __uint_as_float(b.z);
+    v[j][3] = __uint_as_float(b.w);
+  }
+  float sumsq;
+  if (part != nullptr) {
+    sumsq = ds_wave_sum(pv0 + pv1);
+  } else {
+    float sq = 0.f;
+#pragma unroll
+    for (int j = 0; j < NQ; ++j)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) sq = __builtin_fmaf(v[j][c], v[j][c], sq);
+    sq = ds_wave_sum(sq);
+    if (lane == 0) red[tid >> 6] = sq;
+    __syncthreads();
+    sumsq = (red[0] + red[1]) + (red[2] + red[3]);
+  }
+  const float r = 1.f / sqrtf(sumsq / (float)K + eps);
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const int i = tid + kDsThreads * j;
+    if (4 * i < K) {
+      const u32x4 wv = ld16(w + 4 * i);
+      xs[2 * i] = ds_bf16_rne(v[j][0] * r * __uint_as_float(wv.x)) |
+                  (ds_bf16_rne(v[j][1] * r * __uint_as_float(wv.y)) << 16);
+      xs[2 * i + 1] = ds_bf16_rne(v[j][2] * r * __uint_as_float(wv.z)) |
+                      (ds_bf16_rne(v[j][3] * r * __uint_as_float(wv.w)) << 16);
+    }
+  }
+  __syncthreads();
+}
+
+// The code words and scales of a wave's rows r0 + wave, + kDsWaves, ... (at
+// most kDsPrefetch / T of them), loaded ahead of their phase.
+struct DsRows {
+  uint32_t cw[kDsPrefetch];
+  uint16_t sc[kDsPrefetch];
+  float base[kDsPrefetch];  // the value each row's output is added to (or 0)
+  int first, count;  // rows first, first + kDsWaves, ... (count of them)
+};
+
+// T = code words per lane and row (K <= 1024 T); a wave holds up to
+// kDsPrefetch / T rows at a time
+// base (NULL: none): the values the rows' outputs are added to, read with
+// coherent loads along with the codes
+template <int G, int T>
+__device__ __forceinline__ void ds_rows_load(DsRows& p, const uint8_t* __restrict__ codes,
+                                             const uint16_t* __restrict__ s16, int K, int first,
+                                             int end, const float* base) {
+  constexpr int kRows = kDsPrefetch / T;
+  const int lane = threadIdx.x & 63;
+  const int nw = K / 16;
+  int count = (end - first + kDsWaves - 1) / kDsWaves;
+  count = count < 0 ? 0 : (count > kRows ? kRows : count);
+  p.first = first;
+  p.count = count;
+#pragma unroll
+  for (int i = 0; i < kRows * T; ++i) {
+    const int j = i / T, t = i % T, w = lane + 64 * t;
+    p.cw[i] = 0u;
+    p.sc[i] = 0;
+    if (j < count && w < nw) {
+      const int64_t r = first + (int64_t)j * kDsWaves;
+      p.cw[i] = reinterpret_cast<const uint32_t*>(codes + r * (K / 4))[w];
+      p.sc[i] = s16[r * (K / G) + (16 * w) / G];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kRows; ++j)
+    p.base[j] = base != nullptr && j < count ? ld_f32<true>(base + first + j * kDsWaves) : 0.f;
+}
+
+// out(r, base + y) for the rows held in p: y = sum_k x[k] q[r, k] s16[r, k / G].
+// With at most two words per lane every row slot is computed (slots past the
+// rows held have zero codes), so all the rows' dependency chains interleave;
+// with more, rows go in pairs.  Each chain is split into even and odd pairs.
+template <int G, int T>
+__device__ __forceinline__ float ds_row_sum(const DsRows& p, const uint32_t (&xr)[T][8],
+                                            int j) {
+  float aj = 0.f;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const uint32_t cw = p.cw[j * T + t];
+    float e = 0.f, o = 0.f;
+#pragma unroll
+    for (int q = 0; q < 8; q += 2) {
+      const uint32_t p0 = (cw << (14 - 2 * q)) & kPairMask;
+      const uint32_t p1 = (cw << (12 - 2 * q)) & kPairMask;
+      e = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(ds_bf16x2, p0),
+                                          __builtin_bit_cast(ds_bf16x2, xr[t][q]), e, false);
+      o = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(ds_bf16x2, p1),
+                                          __builtin_bit_cast(ds_bf16x2, xr[t][q + 1]), o, false);
+    }
+    aj = __builtin_fmaf(e + o, h2f(p.sc[j * T + t]), aj);
+  }
+  return aj;
+}
+
+template <int G, int T, typename Out>
+__device__ __forceinline__ void ds_rows_compute(const DsRows& p, const uint32_t (&xr)[T][8],
+                                                Out out) {
+  constexpr int kRows = kDsPrefetch / T;
+  constexpr int kStep = T <= 2 ? kRows : 2;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j0 = 0; j0 < kRows; j0 += kStep) {
+    if (j0 < p.count) {
+      float acc[kStep];
+#pragma unroll
+      for (int jj = 0; jj < kStep; ++jj) acc[jj] = ds_row_sum<G, T>(p, xr, j0 + jj < kRows ? j0 + jj : j0);
+#pragma unroll
+      for (int jj = 0; jj < kStep; ++jj) acc[jj] = ds_wave_sum(acc[jj]);
+      if (lane == 0) {
+#pragma unroll
+        for (int jj = 0; jj < kStep; ++jj)
+          if (j0 + jj < p.count) out(p.first + (j0 + jj) * kDsWaves, p.base[j0 + jj] + 0.5f * acc[jj]);
+      }
+    }
+  }
+}
+
+// this lane's x pairs (words lane, lane + 64, ...; zero past the row)
+template <int T>
+__device__ __forceinline__ void ds_x_regs(const uint32_t* xs, int K, uint32_t (&xr)[T][8]) {
+  const int lane = threadIdx.x & 63;
+  const int nw = K / 16;
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int w = lane + 64 * t;
+    u32x4 a = {0u, 0u, 0u, 0u}, b = {0u, 0u, 0u, 0u};
+    if (w < nw) {
+      a = *reinterpret_cast<const u32x4*>(xs + 8 * w);
+      b = *reinterpret_cast<const u32x4*>(xs + 8 * w + 4);
+    }
+    xr[t][0] = a.x; xr[t][1] = a.y; xr[t][2] = a.z; xr[t][3] = a.w;
+    xr[t][4] = b.x; xr[t][5] = b.y; xr[t][6] = b.z; xr[t][7] = b.w;
+  }
+}
+
+// all rows [.., r1) of the wave: the prefetched first ones, then the rest
+template <int G, int T, typename Out>
+__device__ __forceinline__ void ds_rows_all(DsRows& p, const uint8_t* codes, const uint16_t* s16,
+                                            int K, int r1, const uint32_t (&xr)[T][8],
+                                            const float* base, Out out) {
+  for (;;) {
+    ds_rows_compute<G, T>(p, xr, out);
+    const int next = p.first + p.count * kDsWaves;
+    if (p.count == 0 || next >= r1) break;
+    ds_rows_load<G, T>(p, codes, s16, K, next, r1, base);
+  }
+}
+
+// TA, TC: code words per lane of an in_proj row (d_model <= 1024 TA) and of
+// an out_proj row (d_inner <= 1024 TC)
+template <int G, int TA, int TC>
+__global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
+  const DecodeStackDesc& s = a.s;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int P = (int)gridDim.x, bid = (int)blockIdx.x;
+  const int D = s.d_model, H = s.nheads, DI = H * kMxP;
+  const int Z = 2 * DI + 2 * kMxN + H;
+  const int conv_dim = DI + 2 * kMxN;
+  __shared__ __attribute__((aligned(16))) uint32_t xs[(TA > TC ? TA : TC) * 64 * 8];
+  __shared__ float red[kDsWaves];
+
+  const int za = (Z + P - 1) / P, zr0 = bid * za < Z ? bid * za : Z;
+  const int zr1 = zr0 + za < Z ? zr0 + za : Z;
+  const int ca = (D + P - 1) / P, cr0 = bid * ca < D ? bid * ca : D;
+  const int cr1 = cr0 + ca < D ? cr0 + ca : D;
+  uint32_t* bar_a = a.sync;                    // in_proj rows done (all workgroups)
+  uint32_t* bar_b = a.sync + kDsSetWords;      // mixer done (the heads' workgroups)
+  uint32_t* bar_c = a.sync + 2 * kDsSetWords;  // residual done (all workgroups)
+  uint32_t* flag = a.sync + 3 * kDsSetWords;
+  DsRows rows;
+  u32x4 sv[4];
+
+  // block 0's in_proj rows
+  ds_rows_load<G, TA>(rows, s.in_codes, s.in_s16, D, zr0 + wave, zr1, nullptr);
+  for (int l = 0; l < s.n_layers; ++l) {
+    const uint8_t* inc = s.in_codes + (int64_t)l * Z * (D / 4);
+    const uint16_t* ins = s.in_s16 + (int64_t)l * Z * (D / G);
+    const uint8_t* outc = s.out_codes + (int64_t)l * D * (DI / 4);
+    const uint16_t* outs = s.out_s16 + (int64_t)l * D * (DI / G);
+    const float* src = l == 0 ? a.emb : a.residual;
+
+    // ---- A: in_proj of the normalized residual
+    ds_norm_x<TA>(src, s.pre_w + (int64_t)l * D, D, s.eps, nullptr, 0, xs, red);
+    {
+      uint32_t xr[TA][8];
+      ds_x_regs<TA>(xs, D, xr);
+      ds_rows_all<G, TA>(rows, inc, ins, D, zr1, xr, nullptr,
+                         [&](int r, float y) { st_f32<true>(a.zx + r, y); });
+    }
+    // the mixer's state, and this workgroup's out_proj rows, during the barrier
+    // (only the heads' workgroups wait for every in_proj row; the others go
+    // on to wait for the heads)
+    ds_arrive(bar_a);
+    uint16_t* ssm_h = s.ssm_state + ((int64_t)l * H + bid) * kMxP * kMxN;
+    if (bid < H) mixer_state_load(ssm_h, tid, sv);
+    ds_rows_load<G, TC>(rows, outc, outs, DI, cr0 + wave, cr1, src);
+
+    // ---- B: mixer step, one workgroup per head
+    if (bid < H) {
+      ds_wait(bar_a, flag, (uint32_t)(l + 1) * (uint32_t)P);
+      const int pos = s.conv_pos[l] & 3;
+      mixer_head_step<true>(a.zx, bid, H, s.conv_state + (int64_t)l * conv_dim * 4, ssm_h, sv,
+                      [&]() { return pos; }, s.conv_w + (int64_t)l * conv_dim * 4,
+                      s.conv_b + (int64_t)l * conv_dim, s.dt_bias + (int64_t)l * H,
+                      s.A_log + (int64_t)l * H, s.D + (int64_t)l * H, a.gated,
+                      a.partial + bid);
+      ds_arrive(bar_b);
+    }
+    ds_wait(bar_b, flag, (uint32_t)(l + 1) * (uint32_t)H);
+
+    // ---- C: out_proj of the normalized gate, added into the residual
+    // (the heads' sums of g^2 give the norm, in the same order everywhere)
+    ds_norm_x<TC>(a.gated, s.norm_w + (int64_t)l * DI, DI, s.eps, a.partial, H, xs, red);
+    {
+      uint32_t xr[TC][8];
+      ds_x_regs<TC>(xs, DI, xr);
+      ds_rows_all<G, TC>(rows, outc, outs, DI, cr1, xr, src,
+                         [&](int r, float y) { st_f32<true>(a.residual + r, y); });
+    }
+    if (bid == 0 && tid == 0) s.conv_pos[l] = (s.conv_pos[l] + 1) & 3;
+    // the next block's in_proj rows during the barrier
+    ds_arrive(bar_c);
+    if (l + 1 < s.n_layers)
+      ds_rows_load<G, TA>(rows, inc + (int64_t)Z * (D / 4), ins + (int64_t)Z * (D / G), D,
+                          zr0 + wave, zr1, nullptr);
+    ds_wait(bar_c, flag, (uint32_t)(l + 1) * (uint32_t)P);
+  }
+  // final norm of the residual (workgroup 0)
+  if (bid == 0) {
+    ds_norm_x<TA>(s.n_layers > 0 ? a.residual : a.emb, s.final_w, D, s.eps, nullptr, 0, xs,
+                      red);
+    uint32_t* xo = reinterpret_cast<uint32_t*>(a.x_out);
+    for (int i = tid; i < D / 2; i += kDsThreads) xo[i] = xs[i];
+  }
+}
+
+// the instantiation for group size g and (TA, TC) rounded up to a supported
+// pair, or NULL
+static const void* decode_stack_fn(int g, int ta, int tc) {
+  auto pick = [&](auto gt) -> const void* {
+    constexpr int G = decltype(gt)::value;
+    if (ta <= 1 && tc <= 1) return reinterpret_cast<const void*>(&decode_stack_kernel<G, 1, 1>);
+    if (ta <= 1 && tc <= 2) return reinterpret_cast<const void*>(&decode_stack_kernel<G, 1, 2>);
+    if (ta <= 2 && tc <= 4) return reinterpret_cast<const void*>(&decode_stack_kernel<G, 2, 4>);
+    if (ta <= 4 && tc <= 8) return reinterpret_cast<const void*>(&decode_stack_kernel<G, 4, 8>);
+    return nullptr;
+  };
+  switch (g) {
+    case 64:  return pick(std::integral_constant<int, 64>{});
+    case 128: return pick(std::integral_constant<int, 128>{});
+    case 256: return pick(std::integral_constant<int, 256>{});
+    default: return nullptr;
+  }
+}
+
+hipError_t launch_decode_stack(const DecodeStackDesc& s, const float* emb, uint16_t* x_out,
+                               void* workspace, hipStream_t stream) {
+  auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
+  const int64_t DI = (int64_t)s.nheads * kMxP, Z = 2 * DI + 2 * kMxN + s.nheads;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  DsArgs a;
+  a.s = s;
+  a.emb = emb;
+  a.x_out = x_out;
+  const int64_t hd = kDecodeStackSyncBytes;
+  a.sync = reinterpret_cast<uint32_t*>(ws);
+  a.zx = reinterpret_cast<float*>(ws + hd);
+  a.gated = reinterpret_cast<float*>(ws + hd + up(Z * 4));
+  a.partial = reinterpret_cast<float*>(ws + hd + up(Z * 4) + up(DI * 4));
+  a.residual =
+      reinterpret_cast<float*>(ws + hd + up(Z * 4) + up(DI * 4) + up((int64_t)s.nheads * 4));
+  static_assert(4 * (3 * kDsSetWords + 1) <= kDecodeStackSyncBytes,
+                "barrier words fit the workspace header");
+  // the barrier counter and the timeout flag start at zero (a fill kernel,
+  // so the call stays capturable)
+  hipError_t e = launch_fill_zero_f32(reinterpret_cast<float*>(ws), 3 * kDsSetWords + 1, stream);
+  if (e != hipSuccess) return e;
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  const int cus = current_cu_count();
+  const int ta = (s.d_model / 16 + 63) / 64, tc = (s.nheads * kMxP / 16 + 63) / 64;
+  const void* fn = decode_stack_fn(s.g, ta, tc);
+  if (fn == nullptr) return hipErrorInvalidValue;
+  int per_cu = 0;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kDsThreads, 0)) !=
+      hipSuccess)
+    return e;
+  if (per_cu < 1 || cus < s.nheads) return hipErrorInvalidValue;
+  void* args[] = {&a};
+  return hipLaunchCooperativeKernel(fn, dim3((unsigned)cus), dim3(kDsThreads), args, 0, stream);
+}
+
+}  // namespace tmk

@@ -117,6 +117,40 @@ hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* c
                              const float* conv_b, const float* dt_bias, const float* A_log,
                              const float* D, float* gated, hipStream_t stream);
 
+// One batch-1 decode token through a stack of ternary Mamba-2 blocks in one
+// cooperative launch (headdim 64, d_state 128, d_conv 4); arrays per block
+// are stacked along a leading layer dimension.
+struct DecodeStackDesc {
+  int n_layers, d_model, nheads, g;
+  float eps;
+  const uint8_t* in_codes;    // [L, Z, d_model / 4], Z = 2 d_inner + 256 + nheads
+  const uint16_t* in_s16;     // [L, Z, d_model / g]
+  const uint8_t* out_codes;   // [L, d_model, d_inner / 4]
+  const uint16_t* out_s16;    // [L, d_model, d_inner / g]
+  const float* pre_w;         // [L, d_model]
+  const float* conv_w;        // [L, conv_dim, 4], conv_dim = d_inner + 256
+  const float* conv_b;        // [L, conv_dim]
+  const float* dt_bias;       // [L, nheads]
+  const float* A_log;         // [L, nheads]
+  const float* D;             // [L, nheads]
+  const float* norm_w;        // [L, d_inner]
+  const float* final_w;       // [d_model]
+  uint16_t* conv_state;       // [L, conv_dim, 4] float16 ring
+  int* conv_pos;              // [L]
+  uint16_t* ssm_state;        // [L, nheads, 64, 128] float16
+};
+// [barrier words and timeout flag: kDecodeStackSyncBytes] zx [Z] gated
+// [d_inner] partial [nheads] residual [d_model], each piece 256-byte aligned
+constexpr int kDecodeStackSyncBytes = 4096;
+inline int64_t decode_stack_workspace_bytes(int d_model, int nheads) {
+  auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
+  const int64_t di = 64 * (int64_t)nheads, z = 2 * di + 256 + nheads;
+  return kDecodeStackSyncBytes + up(z * 4) + up(di * 4) + up((int64_t)nheads * 4) +
+         up((int64_t)d_model * 4);
+}
+hipError_t launch_decode_stack(const DecodeStackDesc& s, const float* emb, uint16_t* x_out,
+                               void* workspace, hipStream_t stream);
+
 // residual += y (y may be null); x = bf16(rmsnorm(residual) * w), B rows of D
 hipError_t launch_residual_rmsnorm(float* residual, const float* y, int B, int64_t D,
                                    const float* w, float eps, uint16_t* x, hipStream_t stream);

@@ -1,48 +1,23 @@
 // One Mamba-2 mixer decode step between in_proj and out_proj: the part of a
 // decoding layer the paper keeps in FP16 (Sec. 3.2; batch-1 decode, Sec. 8).
 //
-// Kernel 1, one workgroup per (head, batch row):
-//   * causal depthwise convolution step (d_conv = 4) over the head's 64 x
-//     channels and the 2 x d_state B/C channels shared by all heads, SiLU;
-//   * dt' = softplus(dt + dt_bias), decay a = exp(-dt' exp(A_log));
-//   * state[p, n] <- a state[p, n] + dt' x[p] B[n]  (float16 state, float32
-//     arithmetic, rounded once to float16 when stored);
-//   * y[p] = sum_n state[p, n] C[n] + D x[p];  g = y * SiLU(z);
-//   * g (float32) and the head's sum of g^2 go to the workspace.
+// Kernel 1, one workgroup per (head, batch row): the per-head step of
+// mixer_dev.hpp (convolution step, float16 SSM update, gated output g =
+// y * SiLU(z)); g (float32) and the head's sum of g^2 go to the workspace.
 // The head's SSM state is loaded at the start, so its memory latency
 // overlaps the convolution.
 // (The fused decode runs kernel 1 alone and normalizes g in out_proj.)
 // Kernel 2, one workgroup per batch row: the gated RMSNorm over all d_inner
 // channels, out = bf16(g / sqrt(mean(g^2) + eps) * w), the bfloat16 input
 // of out_proj (the per-head partial sums meet in a wave butterfly); and the
-// convolution ring position advances.
-//
-// Convolution state: a ring of 4 float16 slots per channel; the window of a
-// step, oldest first, is slots (pos + 1 .. pos + 3) % 4 and the new input,
-// which then overwrites slot pos (the oldest).  Every workgroup reads the
-// B/C channels' window, so no workgroup may shift it in place while others
-// still read: the ring writes only the slot nobody reads, and the position
-// moves on in kernel 2, after every workgroup of kernel 1 is done.
+// convolution ring position advances, after every workgroup of kernel 1 is
+// done.
 #include <atomic>
 
-#include "common.hpp"
 #include "launchers.hpp"
+#include "mixer_dev.hpp"
 
 namespace tmk {
-
-constexpr int kMxP = 64;    // headdim
-constexpr int kMxN = 128;   // d_state
-constexpr int kMxThreads = 256;
-
-__device__ __forceinline__ float mx_silu(float v) { return v / (1.f + expf(-v)); }
-__device__ __forceinline__ float mx_softplus(float v) { return v > 20.f ? v : log1pf(expf(v)); }
-
-__device__ __forceinline__ float h2f(uint16_t h) {
-  return (float)__builtin_bit_cast(_Float16, h);
-}
-__device__ __forceinline__ uint16_t f2h(float f) {  // round to nearest even
-  return __builtin_bit_cast(uint16_t, (_Float16)f);
-}
 
 // grid (nheads, B); layout: zxbcdt [B, Z] with Z = 2 d_inner + 2 N + nheads,
 // conv [B, conv_dim, 4] float16 ring, ssm [B, nheads, P, N] float16,
@@ -67,104 +42,26 @@ __global__ __launch_bounds__(kMxThreads) void mixer_ssm_kernel(
   const int d_inner = nheads * kMxP;
   const int conv_dim = d_inner + 2 * kMxN;
   const int64_t Z = (int64_t)2 * d_inner + 2 * kMxN + nheads;
-  const float* row = zxbcdt + (int64_t)b * Z;
-  __shared__ float u[kMxP + 2 * kMxN];  // x of the head, then B, then C (after SiLU)
   __shared__ int pos_word;
   if (GATE && tid == 0) pos_word = atomicAdd(conv_pos, 4);
-  __shared__ float wsum[kMxThreads / 64];
-  // thread t: channel p = t / 4, states n = 32 (t % 4) .. + 31; its 64 bytes
-  // of state are loaded first
-  const int p = tid >> 2, q = tid & 3;
-  uint16_t* sp = ssm + (((int64_t)b * nheads + h) * kMxP + p) * kMxN + 32 * q;
+  uint16_t* ssm_h = ssm + ((int64_t)b * nheads + h) * kMxP * kMxN;
   u32x4 sv[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) sv[k] = ld16(sp + 8 * k);
-
-  // convolution: local channel i < 64 is x channel 64 h + i, then the B/C
-  // channels d_inner + (i - 64); a thread takes at most two channels
-  constexpr int kMxCh = (kMxP + 2 * kMxN + kMxThreads - 1) / kMxThreads;
-  uint32_t ring[kMxCh][2];
-  float xin[kMxCh];
-#pragma unroll
-  for (int t = 0; t < kMxCh; ++t) {
-    const int i = tid + t * kMxThreads;
-    if (i >= kMxP + 2 * kMxN) break;
-    const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
-    const u32x2 r2 = *reinterpret_cast<const u32x2*>(conv + ((int64_t)b * conv_dim + c) * 4);
-    ring[t][0] = r2.x;
-    ring[t][1] = r2.y;
-    xin[t] = row[d_inner + c];
-  }
-  int pos;
-  if constexpr (GATE) {
-    __syncthreads();  // the position word has arrived in LDS
-    pos = pos_word & 3;
-  } else {
-    pos = conv_pos[0] & 3;
-  }
-#pragma unroll
-  for (int t = 0; t < kMxCh; ++t) {
-    const int i = tid + t * kMxThreads;
-    if (i >= kMxP + 2 * kMxN) break;
-    const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
-    const float* w = conv_w + (int64_t)c * 4;
-    auto slot = [&](int k) {  // float16 of ring slot k (0 .. 3)
-      const uint32_t wd = ring[t][k >> 1];
-      return h2f((uint16_t)((k & 1) ? wd >> 16 : wd & 0xFFFFu));
-    };
-    float acc = conv_b[c];
-#pragma unroll
-    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(slot((pos + 1 + j) & 3), w[j], acc);
-    acc = __builtin_fmaf(xin[t], w[3], acc);
-    u[i] = mx_silu(acc);
-    // the slot nobody reads; the shared B/C channels are written by head 0
-    if (i < kMxP || h == 0) conv[((int64_t)b * conv_dim + c) * 4 + pos] = f2h(xin[t]);
-  }
-  __syncthreads();
-
-  const float dtp = mx_softplus(row[2 * d_inner + 2 * kMxN + h] + dt_bias[h]);
-  const float a = expf(-dtp * expf(A_log[h]));
-  const float xp = u[p];
-  const float dx = dtp * xp;
-  float y = 0.f;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint32_t wv[4] = {sv[k].x, sv[k].y, sv[k].z, sv[k].w};
-    uint32_t o[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int n0 = 32 * q + 8 * k + 2 * t;
-      const float s0 = __builtin_fmaf(a, h2f((uint16_t)(wv[t] & 0xFFFFu)), dx * u[kMxP + n0]);
-      const float s1 = __builtin_fmaf(a, h2f((uint16_t)(wv[t] >> 16)), dx * u[kMxP + n0 + 1]);
-      y = __builtin_fmaf(s0, u[kMxP + kMxN + n0], y);
-      y = __builtin_fmaf(s1, u[kMxP + kMxN + n0 + 1], y);
-      o[t] = (uint32_t)f2h(s0) | ((uint32_t)f2h(s1) << 16);
+  mixer_state_load(ssm_h, tid, sv);
+  auto pos_of = [&]() {
+    if constexpr (GATE) {
+      __syncthreads();  // the position word has arrived in LDS
+      return pos_word & 3;
+    } else {
+      return conv_pos[0] & 3;
     }
-    st16(sp + 8 * k, u32x4{o[0], o[1], o[2], o[3]});
-  }
-  // the four threads of a channel (lanes 4p' .. 4p' + 3 of the wave)
-  y += __uint_as_float(lane_xchg<1>(__float_as_uint(y)));
-  y += __uint_as_float(lane_xchg<2>(__float_as_uint(y)));
-  y = __builtin_fmaf(Dp[h], xp, y);
-  const float g = y * mx_silu(row[h * kMxP + p]);
-  if (q == 0) gated[(int64_t)b * d_inner + h * kMxP + p] = g;
+  };
+  mixer_head_step(zxbcdt + (int64_t)b * Z, h, nheads, conv + (int64_t)b * conv_dim * 4, ssm_h,
+                  sv, pos_of, conv_w, conv_b, dt_bias, A_log, Dp, gated + (int64_t)b * d_inner,
+                  GATE ? nullptr : partial + (int64_t)b * nheads + h);
   if constexpr (GATE) {
     if (tid == 0 && (pos_word >> 2) == (int)(gridDim.x * gridDim.y) - 1)
       atomicExch(conv_pos, (pos_word + 1) & 3);  // every other workgroup has read it
-    return;
   }
-  // sum of g^2 over the head's 64 channels: each channel counted once (q = 0)
-  float sq = q == 0 ? g * g : 0.f;
-  sq += __uint_as_float(lane_xchg<1>(__float_as_uint(sq)));
-  sq += __uint_as_float(lane_xchg<2>(__float_as_uint(sq)));
-  sq += __uint_as_float(lane_xchg<4>(__float_as_uint(sq)));
-  sq += __uint_as_float(lane_xchg<8>(__float_as_uint(sq)));
-  sq += __uint_as_float(lane_xchg<16>(__float_as_uint(sq)));
-  sq += __uint_as_float(lane_xchg<32>(__float_as_uint(sq)));
-  if ((tid & 63) == 0) wsum[tid >> 6] = sq;
-  __syncthreads();
-  if (tid == 0)
-    partial[(int64_t)b * nheads + h] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
 }
 
 // grid (B); out[b, i] = bf16(g[b, i] / sqrt(sum_h partial[b, h] / d_inner + eps) * w[i])

@@ -27,6 +27,20 @@ TM_STATUS = {0: "TM_OK", 1: "TM_EINVAL", 2: "TM_ESHAPE", 3: "TM_EALIGN", 4: "TM_
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
 _I32 = ctypes.c_int32
+class Mamba2Stack(ctypes.Structure):
+    """``tm_mamba2_stack``: the device arrays of a stack of ternary Mamba-2
+    blocks for whole-stack decoding (layer-stacked, see include/tmamba.h)."""
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("nheads", ctypes.c_int32), ("g", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("in_codes", ctypes.c_void_p), ("in_scales", ctypes.c_void_p),
+                ("out_codes", ctypes.c_void_p), ("out_scales", ctypes.c_void_p),
+                ("pre_w", ctypes.c_void_p), ("conv_w", ctypes.c_void_p),
+                ("conv_b", ctypes.c_void_p), ("dt_bias", ctypes.c_void_p),
+                ("A_log", ctypes.c_void_p), ("D", ctypes.c_void_p), ("norm_w", ctypes.c_void_p),
+                ("final_w", ctypes.c_void_p), ("conv_state", ctypes.c_void_p),
+                ("conv_pos", ctypes.c_void_p), ("ssm_state", ctypes.c_void_p)]
+
+
 SIGNATURES = {
     "tm_abi_version": (ctypes.c_int, []),
     "tm_status_str": (ctypes.c_char_p, [ctypes.c_int]),
@@ -58,6 +72,8 @@ SIGNATURES = {
     "tm_dgemv_rms": (ctypes.c_int, [_P, _P, ctypes.c_float, _P, _I32, _I64, _I64, _P, _I32, _P]),
     "tm_mixer_gate": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P]),
+    "tm_mamba2_decode_token": (ctypes.c_int, [ctypes.POINTER(Mamba2Stack), _P, _P, _P, _I64, _P]),
+    "tm_mamba2_decode_workspace": (ctypes.c_int64, [_I32, _I32]),
 }
 
 
@@ -585,3 +601,58 @@ def residual_rmsnorm(residual: torch.Tensor, y: Optional[torch.Tensor], w: torch
                                    _stream())
     _check("tm_residual_rmsnorm", st)
     return x
+
+
+STACK_FIELDS = ("in_codes", "in_scales", "out_codes", "out_scales", "pre_w", "conv_w", "conv_b",
+                "dt_bias", "A_log", "D", "norm_w", "final_w", "conv_state", "conv_pos",
+                "ssm_state")
+
+
+def mamba2_decode_workspace(d_model: int, nheads: int, device) -> torch.Tensor:
+    """Scratch for mamba2_decode_token (uint8)."""
+    n = int(lib().tm_mamba2_decode_workspace(d_model, nheads))
+    if n < 0:
+        raise ValueError(f"no stack decode for d_model={d_model}, nheads={nheads}")
+    return torch.empty((n,), dtype=torch.uint8, device=device)
+
+
+def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
+                        x_out: Optional[torch.Tensor] = None,
+                        workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One batch-1 decode token through a stack of ternary Mamba-2 blocks in a
+    single launch (``tm_mamba2_decode_token``).  arrays: the stacked device
+    tensors named as ``tm_mamba2_stack``'s fields (``STACK_FIELDS``); emb
+    float32 [d_model]; returns x_out bfloat16 [d_model] (the final norm)."""
+    P, N = MIXER_HEADDIM, MIXER_DSTATE
+    L, Z, d4 = arrays["in_codes"].shape
+    D = 4 * d4
+    H = arrays["dt_bias"].shape[1]
+    di, cd = H * P, H * P + 2 * N
+    dev = emb.device
+    want = {"in_codes": ((L, Z, D // 4), _U8), "in_scales": ((L, Z, _groups(D, g)), _F16),
+            "out_codes": ((L, D, di // 4), _U8), "out_scales": ((L, D, _groups(di, g)), _F16),
+            "pre_w": ((L, D), _F32), "conv_w": ((L, cd, 4), _F32), "conv_b": ((L, cd), _F32),
+            "dt_bias": ((L, H), _F32), "A_log": ((L, H), _F32), "D": ((L, H), _F32),
+            "norm_w": ((L, di), _F32), "final_w": ((D,), _F32),
+            "conv_state": ((L, cd, 4), _F16), "conv_pos": ((L,), (torch.int32,)),
+            "ssm_state": ((L, H, P, N), _F16)}
+    if Z != 2 * di + 2 * N + H:
+        raise ValueError(f"in_codes has {Z} rows; nheads={H} needs {2 * di + 2 * N + H}")
+    for name, (shape, dtypes) in want.items():
+        t = arrays[name]
+        _need(t, name, dtypes, len(shape))
+        _shape(t, name, shape, dev)
+    _need(emb, "emb", _F32, 1)
+    _shape(emb, "emb", (D,), dev)
+    if x_out is None:
+        x_out = torch.empty((D,), dtype=torch.bfloat16, device=dev)
+    _need(x_out, "x_out", _BF16, 1)
+    _shape(x_out, "x_out", (D,), dev)
+    if workspace is None:
+        workspace = mamba2_decode_workspace(D, H, dev)
+    _need(workspace, "workspace", _U8, 1)
+    st = Mamba2Stack(L, D, H, g, eps, *(arrays[k].data_ptr() for k in STACK_FIELDS))
+    rc = lib().tm_mamba2_decode_token(ctypes.byref(st), _ptr(emb), _ptr(x_out), _ptr(workspace),
+                                      workspace.numel(), _stream())
+    _check("tm_mamba2_decode_token", rc)
+    return x_out

@@ -156,6 +156,17 @@ class DecodeStack:
 __all__ = ["keep_first_last", "quantize_projections", "DecodeStack", "PROJECTIONS"]
 
 
+def stack_fits(B: int, d_model: int, nheads: int, g: int) -> bool:
+    """Whether tm_mamba2_decode_token takes this stack (its declaration's
+    limits; nheads must also not exceed the device's CU count)."""
+    d_inner = nheads * ops.MIXER_HEADDIM
+    shapes = (B == 1 and g in (64, 128, 256) and 64 <= d_model <= 4096 and d_model % 64 == 0
+              and d_model % g == 0 and d_inner % g == 0 and 1 <= nheads <= 128)
+    return (shapes and torch.cuda.is_available()
+            and nheads <= torch.cuda.get_device_properties(
+                torch.cuda.current_device()).multi_processor_count)
+
+
 def rms_fused_fits(B: int, K: int, g: int) -> bool:
     """Whether tm_tgemv_rms takes B rows of K columns at group size g (the
     rule its declaration states: one workgroup stages all rows at once)."""
@@ -186,19 +197,29 @@ class Mamba2Decoder:
     buffers, so a token can be captured once as a HIP graph (``capture``) and
     replayed.
 
+    or, with every block ternary and batch 1, the whole stack in one launch
+    (``tm_mamba2_decode_token``: the three phases of every block separated
+    by grid barriers instead of launches).
+
     weight(kind, l) -> float32 [N, K] master weights (kind "in": [Z, d_model],
     "out": [d_model, d_inner]); mixer(l) -> dict of float32 arrays conv_w,
     conv_b, dt_bias, A_log, D, norm_w (see ops.mixer_step); pre_norm(l) ->
     float32 [d_model].  Layers in ``keep`` stay in float16 (Sec. 7).
     fused: None picks the fused form whenever every projection's shape
     allows it (batch up to 4 at g >= 128 for the Mamba-2 1.3B shapes).
+    stack: None picks the one-launch form whenever it applies (no kept
+    layers, batch 1, ``stack_fits``); it keeps the residual in its own
+    workspace (``residual`` is not updated).
+    The packed weights, mixer parameters and states of all layers live in
+    layer-stacked arrays (``arena``); each layer's entries are views of them,
+    so every form reads and advances the same states.
     """
 
     def __init__(self, weight: Callable[[str, int], torch.Tensor], mixer: Callable[[int], dict],
                  pre_norm: Callable[[int], torch.Tensor], n_layers: int, d_model: int,
                  nheads: int, keep: Iterable[int] = (), g: int = 128, eps: float = 1e-5,
                  batch: int = 1, device: Optional[torch.device] = None,
-                 fused: Optional[bool] = None):
+                 fused: Optional[bool] = None, stack: Optional[bool] = None):
         dev = device or torch.device("cuda")
         self.L, self.B, self.g, self.eps = n_layers, batch, g, eps
         self.keep = set(keep)
@@ -212,6 +233,29 @@ class Mamba2Decoder:
         if fused and not fits:
             raise ValueError(f"batch {batch} does not fit the fused decode at g = {g}")
         self.fused = fits if fused is None else bool(fused)
+        st_ok = stack_fits(batch, d_model, nheads, g) and not self.keep
+        if stack and not st_ok:
+            raise ValueError("the one-launch stack decode needs batch 1, no kept layers and "
+                             "shapes stack_fits accepts")
+        self.stack = st_ok if stack is None else bool(stack)
+        L, f32, f16 = n_layers, torch.float32, torch.float16
+        ar = {"pre_w": torch.empty((L, d_model), dtype=f32, device=dev),
+              "conv_w": torch.empty((L, conv_dim, 4), dtype=f32, device=dev),
+              "conv_b": torch.empty((L, conv_dim), dtype=f32, device=dev),
+              "dt_bias": torch.empty((L, nheads), dtype=f32, device=dev),
+              "A_log": torch.empty((L, nheads), dtype=f32, device=dev),
+              "D": torch.empty((L, nheads), dtype=f32, device=dev),
+              "norm_w": torch.empty((L, self.d_inner), dtype=f32, device=dev),
+              "conv_state": torch.zeros((L, batch, conv_dim, 4), dtype=f16, device=dev),
+              "conv_pos": torch.zeros((L,), dtype=torch.int32, device=dev),
+              "ssm_state": torch.zeros((L, batch, nheads, P, N), dtype=f16, device=dev)}
+        if not self.keep:
+            ar["in_codes"] = torch.empty((L, self.Z, d_model // 4), dtype=torch.uint8, device=dev)
+            ar["in_scales"] = torch.empty((L, self.Z, d_model // g), dtype=f16, device=dev)
+            ar["out_codes"] = torch.empty((L, d_model, self.d_inner // 4), dtype=torch.uint8,
+                                          device=dev)
+            ar["out_scales"] = torch.empty((L, d_model, self.d_inner // g), dtype=f16, device=dev)
+        self.arena = ar
         self.layers = []
         for l in range(n_layers):
             lay = {}
@@ -222,18 +266,26 @@ class Mamba2Decoder:
                 if l in self.keep:
                     lay[kind] = ("dense", w.to(torch.float16)[None].contiguous())
                 else:
-                    codes = torch.empty((1, n, k // 4), dtype=torch.uint8, device=dev)
-                    s16 = torch.empty((1, n, k // g), dtype=torch.float16, device=dev)
+                    if f"{kind}_codes" in ar:
+                        codes = ar[f"{kind}_codes"][l:l + 1]
+                        s16 = ar[f"{kind}_scales"][l:l + 1]
+                    else:
+                        codes = torch.empty((1, n, k // 4), dtype=torch.uint8, device=dev)
+                        s16 = torch.empty((1, n, k // g), dtype=torch.float16, device=dev)
                     ops.ternarize_pack(w, g, eps, codes=codes[0], scales_f16=s16[0],
                                        want_zero_count=False)
                     lay[kind] = ("ternary", codes, s16)
             prm = mixer(l)
-            lay["mixer"] = {k: (v if isinstance(v, torch.Tensor) else torch.from_numpy(v))
-                            .to(dev, torch.float32).contiguous() for k, v in prm.items()}
-            lay["pre"] = pre_norm(l).to(dev, torch.float32).contiguous()
-            lay["conv"] = torch.zeros((batch, conv_dim, 4), dtype=torch.float16, device=dev)
-            lay["pos"] = torch.zeros((1,), dtype=torch.int32, device=dev)
-            lay["ssm"] = torch.zeros((batch, nheads, P, N), dtype=torch.float16, device=dev)
+            lay["mixer"] = {}
+            for k, v in prm.items():
+                v = v if isinstance(v, torch.Tensor) else torch.from_numpy(v)
+                ar[k][l].copy_(v.to(dev, torch.float32).reshape(ar[k][l].shape))
+                lay["mixer"][k] = ar[k][l]
+            ar["pre_w"][l].copy_(pre_norm(l).to(dev, torch.float32))
+            lay["pre"] = ar["pre_w"][l]
+            lay["conv"] = ar["conv_state"][l]
+            lay["pos"] = ar["conv_pos"][l:l + 1]
+            lay["ssm"] = ar["ssm_state"][l]
             self.layers.append(lay)
         self.final_norm = torch.ones((d_model,), dtype=torch.float32, device=dev)
         # token buffers (reused by every layer: the layers run one after another)
@@ -246,6 +298,8 @@ class Mamba2Decoder:
         self.gated = torch.empty((batch, self.d_inner), dtype=torch.float32, device=dev)
         self.ws = ops.mixer_workspace(batch, nheads, dev)
         self.x_out = torch.empty((batch, d_model), dtype=torch.bfloat16, device=dev)
+        self.arena["final_w"] = self.final_norm
+        self.stack_ws = ops.mamba2_decode_workspace(d_model, nheads, dev) if self.stack else None
         self.graph = None
 
     def set_states(self, l: int, conv: torch.Tensor, ssm: torch.Tensor, pos: int = 0) -> None:
@@ -294,9 +348,20 @@ class Mamba2Decoder:
                        workspace=self.ws, out=self.m[0])
         self._proj(lay, "out", self.m, self.y)
 
+    def token_stack(self) -> torch.Tensor:
+        """One token through every block in a single launch."""
+        a = {k: self.arena[k] for k in ops.STACK_FIELDS}
+        a["conv_state"] = a["conv_state"][:, 0]   # batch 1
+        a["ssm_state"] = a["ssm_state"][:, 0]
+        ops.mamba2_decode_token(a, self.g, self.eps, self.emb[0], x_out=self.x_out[0],
+                                workspace=self.stack_ws)
+        return self.x_out
+
     def token(self) -> torch.Tensor:
         """One decode token from ``emb`` (float32 [B, d_model]) through every
         layer; returns ``x_out`` = final norm of the residual (bfloat16)."""
+        if self.stack:
+            return self.token_stack()
         for l in range(self.L):
             self.layer_step(l)
         ops.residual_rmsnorm(self.residual, None if self.fused else self.y[0], self.final_norm,
@@ -320,8 +385,11 @@ class Mamba2Decoder:
         return self.x_out
 
     def launches_per_token(self) -> int:
-        # per layer: in_proj, mixer, out_proj (fused) or pre-norm, in_proj,
-        # mixer (2), out_proj; then the residual copy and the final norm
+        # one launch (and the clear of its barrier counter); else per layer:
+        # in_proj, mixer, out_proj (fused) or pre-norm, in_proj, mixer (2),
+        # out_proj; then the residual copy and the final norm
+        if self.stack:
+            return 2
         return (3 if self.fused else 5) * self.L + 2
 
     def bytes_per_token(self) -> float:
@@ -344,4 +412,4 @@ class Mamba2Decoder:
         return total
 
 
-__all__ += ["Mamba2Decoder", "rms_fused_fits"]
+__all__ += ["Mamba2Decoder", "rms_fused_fits", "stack_fits"]

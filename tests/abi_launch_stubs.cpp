@@ -86,6 +86,10 @@ hipError_t launch_mixer_step_noalloc(const float*, int, int, uint16_t*, int*, ui
                                      const float*, const float*, float, uint16_t*, hipStream_t) {
   reached("mixer_step_noalloc");
 }
+hipError_t launch_decode_stack(const DecodeStackDesc&, const float*, uint16_t*, void*,
+                               hipStream_t) {
+  reached("decode_stack");
+}
 hipError_t launch_residual_rmsnorm(float*, const float*, int, int64_t, const float*, float,
                                    uint16_t*, hipStream_t) {
   reached("residual_rmsnorm");

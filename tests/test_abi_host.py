@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 24
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 11
+    assert L.tm_abi_version() == 12
 
 
 def test_status_strings(L):
@@ -387,6 +387,54 @@ def test_tgemv_pair_validation(L):
     assert gpair(L, y1=P + 2 ** 26) == EINVAL            # the two outputs overlap
     assert gpair(L, y1=P + 2 ** 24) == EINVAL            # y1 over the first stack's codes
     assert gpair(L, y0=P + 2 ** 28) == EINVAL            # y0 over the second stack's codes
+
+
+def stack_desc(**kw):
+    # fake device arrays 64 MiB apart (the checks never dereference them)
+    names = ops.STACK_FIELDS
+    vals = {n: P + (i + 1) * 2 ** 26 for i, n in enumerate(names)}
+    vals.update({k: v for k, v in kw.items() if k in names})
+    dims = dict(n_layers=2, d_model=256, nheads=2, g=128, eps=1e-5)
+    dims.update({k: v for k, v in kw.items() if k in dims})
+    return ops.Mamba2Stack(dims["n_layers"], dims["d_model"], dims["nheads"], dims["g"],
+                           dims["eps"], *(vals[n] for n in names))
+
+
+def mdec(L, emb=P + 2 ** 31, x_out=P + 2 ** 31 + 2 ** 20, ws=P + 2 ** 32, wsb=None, **kw):
+    st = stack_desc(**kw)
+    if wsb is None:
+        wsb = L.tm_mamba2_decode_workspace(st.d_model, st.nheads)
+    return L.tm_mamba2_decode_token(ctypes.byref(st), emb, x_out, ws, wsb, None)
+
+
+def test_mamba2_decode_token_validation(L):
+    # [barrier words 4 KiB | zx Z | gated | partial | residual], 256-byte pieces
+    z = 2 * 128 + 256 + 2
+    assert L.tm_mamba2_decode_workspace(256, 2) == 4096 + 2304 + 512 + 256 + 1024 and z == 514
+    assert L.tm_mamba2_decode_workspace(8192, 2) == -1
+    assert L.tm_mamba2_decode_workspace(256, 0) == -1
+    assert L.tm_mamba2_decode_token(None, P, P, P, 1 << 20, None) == EINVAL
+    for name in ops.STACK_FIELDS:
+        assert mdec(L, **{name: 0}) == EINVAL, name
+    assert mdec(L, emb=0) == EINVAL
+    assert mdec(L, eps=-1.0) == EINVAL
+    assert mdec(L, eps=float("nan")) == EINVAL
+    assert mdec(L, g=32) == ESHAPE                  # g in {64, 128, 256}
+    assert mdec(L, d_model=4160) == ESHAPE          # beyond 4096
+    assert mdec(L, d_model=320) == ESHAPE           # not a multiple of g = 128
+    assert mdec(L, nheads=3) == ESHAPE              # d_inner 192 not a multiple of 128
+    assert mdec(L, nheads=129) == ESHAPE
+    assert mdec(L, n_layers=0) == ESHAPE
+    assert mdec(L, wsb=1024) == ESHAPE              # workspace too small
+    assert mdec(L, ws=P + 2 ** 32 + 128) == EALIGN
+    assert mdec(L, ssm_state=P + 15 * 2 ** 26 + 8) == EALIGN
+    assert mdec(L, conv_state=P + 13 * 2 ** 26 + 4) == EALIGN
+    assert mdec(L, x_out=P + 2 ** 31 + 1) == EALIGN
+    assert mdec(L, norm_w=P + 11 * 2 ** 26 + 4) == EALIGN   # the norm weights load 16 bytes
+    # a state array over a weight array, the output over the workspace
+    assert mdec(L, ssm_state=P + 1 * 2 ** 26) == EINVAL
+    assert mdec(L, x_out=P + 2 ** 32) == EINVAL
+    assert mdec(L, conv_pos=P + 13 * 2 ** 26 + 64) == EINVAL   # inside the conv ring
 
 
 def dx16(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,

@@ -1,0 +1,121 @@
+"""GPU parity of the one-launch stack decode (tm_mamba2_decode_token): a
+batch-1 token through every ternary Mamba-2 block with grid barriers between
+the phases, against the oracle's own decode (oracle ternarization, float16
+states carried by each side), and against the layer-by-layer fused decode on
+the same states.
+
+Bars as for the layer-by-layer decoder: the two sides round the activations
+handed to a projection to bfloat16 from float32 and float64 values (and the
+stack kernel sums its normalizations in another order than the fused
+launches), so an element may land one bfloat16 step apart; outputs stay
+within two bfloat16 steps plus 1e-3 of their largest element, states within
+1e-3 (Frobenius).
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from paper_2606_18114_amd import synth  # noqa: E402
+from test_gpu_mixer import OracleDecoder, _bf16_to_f64, _d, ring_to_window  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_18114_amd import ops
+    ops.lib()
+
+
+def _decoder(seed, L, d_model, H, g=128, stack=None, outliers=True):
+    from paper_2606_18114_amd.stack import Mamba2Decoder
+    rng = np.random.default_rng(seed)
+    Z = 2 * 64 * H + 256 + H
+    Ws = {("in", l): synth.weights(rng, Z, d_model, outliers=outliers) for l in range(L)}
+    Ws.update({("out", l): synth.weights(rng, d_model, H * 64) for l in range(L)})
+    mix = [synth.mixer_params(rng, H) for _ in range(L)]
+    pre = [(1 + 0.1 * rng.standard_normal(d_model)).astype(np.float32) for _ in range(L)]
+    dec = Mamba2Decoder(lambda k, l: _d(Ws[(k, l)]), lambda l: mix[l],
+                        lambda l: torch.from_numpy(pre[l]), L, d_model, H, keep=(), g=g,
+                        batch=1, stack=stack)
+    states = []
+    for l in range(L):
+        conv, ssm = synth.mixer_states(rng, 1, H)
+        states.append((conv, ssm))
+        dec.set_states(l, _d(conv.view(np.int16)).view(torch.float16),
+                       _d(ssm.view(np.int16)).view(torch.float16))
+    return dec, Ws, mix, pre, states
+
+
+def _timeout_flag(dec):
+    torch.cuda.synchronize()
+    return int(dec.stack_ws[3072:3076].view(torch.int32).cpu()[0])
+
+
+@pytest.mark.parametrize("L,d_model,H,g", [(3, 256, 2, 128), (2, 512, 8, 64), (2, 1024, 4, 256)])
+def test_stack_decode_against_oracle(L, d_model, H, g):
+    dec, Ws, mix, pre, states = _decoder(17 + L + H, L, d_model, H, g)
+    assert dec.stack and dec.launches_per_token() == 2
+    ref_dec = OracleDecoder(Ws, mix, pre, states, (), g, dec.eps)
+    rng = np.random.default_rng(50 + H)
+    print(f"[stack decode] L={L} d_model={d_model} nheads={H} g={g}", flush=True)
+    for t in range(3):
+        emb = rng.standard_normal((1, d_model)).astype(np.float32)
+        dec.emb.copy_(_d(emb))
+        got = _bf16_to_f64(dec.token())
+        ref = ref_dec.token(emb)
+        torch.cuda.synchronize()
+        bar = 2.0 ** -7 * np.abs(ref) + 1e-3 * np.abs(ref).max()
+        err = np.abs(got - ref)
+        assert np.all(err <= bar), f"token {t}: max err / bar {float((err / bar).max()):.3f}"
+    assert _timeout_flag(dec) == 0
+    from oracle import ternary as O
+    for l, lay in enumerate(dec.layers):
+        conv_ref, ssm_ref = ref_dec.states[l]
+        pos = int(lay["pos"].cpu()[0])
+        assert pos == 3
+        win = ring_to_window(lay["conv"].cpu().numpy(), pos)
+        assert O.rel_fro_error(win.astype(np.float64), conv_ref.astype(np.float64)) <= 1e-3
+        assert O.rel_fro_error(lay["ssm"].cpu().numpy().astype(np.float64),
+                               ssm_ref.astype(np.float64)) <= 1e-3
+
+
+def test_stack_decode_full_size_against_oracle():
+    """Two blocks of the Mamba-2 1.3B shapes (d_model 2048, 64 heads,
+    in_proj 8512 x 2048, out_proj 2048 x 4096), three tokens, against the
+    oracle's decode; then the layer-by-layer fused decode from the same
+    weights and states stays within twice the bar of the one-launch decode
+    (each is within the bar of the exact result)."""
+    a, Ws, mix, pre, states = _decoder(3, 2, synth.D_MODEL, 64, stack=True)
+    b, *_ = _decoder(3, 2, synth.D_MODEL, 64, stack=False)
+    assert a.stack and not b.stack and b.fused
+    ref_dec = OracleDecoder(Ws, mix, pre, states, (), a.g, a.eps)
+    rng = np.random.default_rng(77)
+    for t in range(3):
+        emb = rng.standard_normal((1, synth.D_MODEL)).astype(np.float32)
+        a.emb.copy_(_d(emb))
+        b.emb.copy_(_d(emb))
+        xa = _bf16_to_f64(a.token())
+        xb = _bf16_to_f64(b.token())
+        ref = ref_dec.token(emb)
+        torch.cuda.synchronize()
+        bar = 2.0 ** -7 * np.abs(ref) + 1e-3 * np.abs(ref).max()
+        ra = float((np.abs(xa - ref) / bar).max())
+        rb = float((np.abs(xb - ref) / bar).max())
+        rab = float((np.abs(xa - xb) / (2 * bar)).max())
+        print(f"[stack decode] full size token {t}: err/bar stack {ra:.3f} fused {rb:.3f} "
+              f"stack-vs-fused/2bar {rab:.3f}", flush=True)
+        assert ra <= 1.0 and rab <= 1.0
+    assert _timeout_flag(a) == 0
+    from oracle import ternary as O
+    for l, lay in enumerate(a.layers):
+        conv_ref, ssm_ref = ref_dec.states[l]
+        pos = int(lay["pos"].cpu()[0])
+        win = ring_to_window(lay["conv"].cpu().numpy(), pos)
+        assert O.rel_fro_error(win.astype(np.float64), conv_ref.astype(np.float64)) <= 1e-3
+        assert O.rel_fro_error(lay["ssm"].cpu().numpy().astype(np.float64),
+                               ssm_ref.astype(np.float64)) <= 1e-3
