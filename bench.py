@@ -759,7 +759,7 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1, fused=True, stack=False)
     pre-norm -> in_proj -> mixer step (convolution, FP16 SSM state update,
     gated RMSNorm) -> out_proj, then the final norm.  Fused: 3 launches per
     layer (the norms inside the projections' staging, the residual add in
-    out_proj's store); unfused: 5; stack: the whole token in one cooperative
+    out_proj's store); unfused: 5; stack: the whole token in one
     launch with grid barriers between the phases.  Timed eagerly (one Python
     call per launch) and as one captured HIP graph per token (where the
     launches can be captured); states persist from token to token."""
@@ -801,7 +801,7 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1, fused=True, stack=False)
     try:
         dec.capture()
         us_graph = timed(dec.replay, n)
-    except RuntimeError as e:  # a cooperative launch may not be capturable
+    except RuntimeError as e:  # a launch that cannot be captured
         log(f"decode blocks (stack={dec.stack}): no graph capture ({str(e)[:120]})")
     nb = dec.bytes_per_token()
     best = us_graph if us_graph is not None else us_eager

@@ -454,10 +454,14 @@ typedef struct {
  *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads)
  *              bytes, 256-byte aligned, owned by the caller; nothing need be
  *              set before the call.  Its uint32 word 768 is nonzero after a
- *              call whose grid barrier gave up waiting (not expected: the
- *              launch is cooperative, so every workgroup is resident).
- * One workgroup per CU in a cooperative launch; the blocks' phases are
- * separated by grid barriers (three per block) instead of kernel launches.
+ *              call whose grid barrier gave up waiting; the outputs and
+ *              states of such a call are not valid.
+ * One workgroup per CU; the blocks' phases are separated by grid barriers
+ * (three per block) instead of kernel launches, so every workgroup must be
+ * resident at once.  A CU holds several of them, so on an otherwise idle GPU
+ * they all start together; other kernels running at the same time (other
+ * streams or processes) can delay some, and a barrier waits for them for
+ * tens of milliseconds before it gives up and sets the flag above.
  * The ternary products take the bfloat16 x against the codes (exact
  * products, float32 sums, float16 group scale in float32), so they agree
  * with tm_tgemv_rms to float32 rounding; the normalizations sum in a

@@ -9,11 +9,18 @@
 // and after the last block x_out = bf16(rmsnorm(residual) * final_w).  The
 // first block's residual is the token's embedding.
 //
-// The grid is one workgroup per CU, launched cooperatively (all resident at
-// once), and the phases are separated by grid barriers: the waves' stores
-// complete, one atomic increment of a counter, a spin on the counter
-// (bounded: after 2^16 polls a flag is set and the spin ends, and every
-// later wait that sees the flag ends too, so every wave always exits soon).
+// The grid is one workgroup per CU, and the phases are separated by grid
+// barriers: the waves' stores complete, one atomic increment of a counter, a
+// spin on the counter (bounded: after 2^16 polls a flag is set and the spin
+// ends, and every later wait that sees the flag ends too, so every wave
+// always exits soon).  The barriers need every workgroup resident at once.
+// A CU holds three of these workgroups (registers; the LDS use is small), so
+// on a GPU with nothing else running all of them start at once.  The launch
+// is an ordinary one: the runtime's cooperative launch gives the same
+// placement but spaced the tokens 10 to 120 us apart (it waited for the
+// previous kernel to drain before dispatching), against about 3 us here.  If
+// other work holds CUs, workgroups start late and the spin covers the wait;
+// one that outlasts the spin limit shows in the flag.
 // The data that crosses workgroups (zx, the gated values and their sums,
 // the residual) is written and read with agent-scope coherent accesses.  Three barriers per block
 // replace the three kernel launches per block of the layer-by-layer decode
@@ -444,8 +451,6 @@ hipError_t launch_decode_stack(const DecodeStackDesc& s, const float* emb, uint1
   // so the call stays capturable)
   hipError_t e = launch_fill_zero_f32(reinterpret_cast<float*>(ws), 3 * kDsSetWords + 1, stream);
   if (e != hipSuccess) return e;
-  int dev = 0;
-  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   const int cus = current_cu_count();
   const int ta = (s.d_model / 16 + 63) / 64, tc = (s.nheads * kMxP / 16 + 63) / 64;
   const void* fn = decode_stack_fn(s.g, ta, tc);
@@ -454,9 +459,10 @@ hipError_t launch_decode_stack(const DecodeStackDesc& s, const float* emb, uint1
   if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kDsThreads, 0)) !=
       hipSuccess)
     return e;
+  // every workgroup must fit at once (one per CU)
   if (per_cu < 1 || cus < s.nheads) return hipErrorInvalidValue;
   void* args[] = {&a};
-  return hipLaunchCooperativeKernel(fn, dim3((unsigned)cus), dim3(kDsThreads), args, 0, stream);
+  return hipLaunchKernel(fn, dim3((unsigned)cus), dim3(kDsThreads), args, 0, stream);
 }
 
 }  // namespace tmk

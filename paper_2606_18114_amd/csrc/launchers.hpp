@@ -118,7 +118,7 @@ hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* c
                              const float* D, float* gated, hipStream_t stream);
 
 // One batch-1 decode token through a stack of ternary Mamba-2 blocks in one
-// cooperative launch (headdim 64, d_state 128, d_conv 4); arrays per block
+// launch with grid barriers (headdim 64, d_state 128, d_conv 4); arrays per block
 // are stacked along a leading layer dimension.
 struct DecodeStackDesc {
   int n_layers, d_model, nheads, g;
