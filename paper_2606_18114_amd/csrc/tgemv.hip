@@ -77,7 +77,9 @@ constexpr int kGemvRing = 1;
 constexpr int kGemvSlotK = 512;
 constexpr int kGemvBlocks = 2;                   // 16-row MFMA blocks per wave
 constexpr int kGemvWaveRows = 16 * kGemvBlocks;  // 32
-constexpr int kGemvXBytes = 32 * 1024;           // LDS budget for the split x
+// LDS budget for the split x: 36 KiB holds a whole in_proj row (K = 2048)
+// for 16 A rows (batch 4 at g >= 128), three workgroups still fit a CU
+constexpr int kGemvXBytes = 36 * 1024;
 constexpr int kGemvXPad = 16;                    // bytes between A rows in LDS (bank spread)
 
 typedef __attribute__((ext_vector_type(8))) int i32x8;
@@ -918,6 +920,12 @@ static hipError_t launch_gw(const uint16_t* x, const uint8_t* codes, const uint1
     const int bp = B - b0 < bmax ? B - b0 : bmax;
     const int rp = kTerms * bp * H;
     if (rp <= 16) {
+      if constexpr (SK / G >= 2) {
+        if (sw) {
+          TM_GEMV_LAUNCH(1, true, bp, b0);
+          continue;
+        }
+      }
       TM_GEMV_LAUNCH(1, false, bp, b0);
     } else if constexpr (!KS) {  // the split form is only chosen for R <= 16
       if (rp <= 32)
@@ -948,6 +956,11 @@ static hipError_t launch_g(const uint16_t* x, const uint8_t* codes, const uint16
     return launch_gw<G, kGemvWaves, true>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps,
                                           accum);
   }
+  // many A rows (batch 4 at g >= 128): the split x fills much of a
+  // workgroup's LDS, so eight waves share it (twice the rows per staging)
+  // where the grid still gives every CU several workgroups
+  if (R > 8 && (int64_t)count * ((N + 255) / 256) >= 4 * (int64_t)current_cu_count())
+    return launch_gw<G, 8, false>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps, accum);
   return launch_gw<G, kGemvWaves, false>(x, codes, s16, count, B, N, K, y, stream, xr, nw, eps,
                                          accum);
 }
