@@ -39,7 +39,10 @@ __device__ __forceinline__ float half_hi(uint32_t w) {
 }
 
 // Grid: (ceil(N / (R * kDgWaves)), count); wave w of workgroup i owns rows
-// (i * kDgWaves + w) * R .. + R - 1.  LDS: B * K floats (+ B row factors).
+// (i * kDgWaves + w) * R .. + R - 1.  LDS: x as B * K floats, or for more
+// than one batch row as bfloat16 (half the LDS reads per weight piece, which
+// otherwise bound a batch of 4: 8 reads of 16 bytes per 16 bytes of weights;
+// the values widen with a shift or an AND per element), then B row factors.
 // RMS (one matrix; a decoding block's normalization fused into the staging):
 // x[b, k] = bf16(xr[b, k] / sqrt(mean_k xr[b, k]^2 + eps) * nw[k]), the row
 // sums taken by one wave per row in a fixed order.  accum: y += instead of =.
@@ -48,7 +51,11 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ W, int B, int64_t N,
     int64_t K, float* __restrict__ y, const float* __restrict__ xr,
     const float* __restrict__ nw, float eps, int accum) {
+  constexpr bool XB = BMAX > 1;  // x in LDS as bfloat16
   extern __shared__ __attribute__((aligned(16))) float xs[];
+  uint16_t* const xh = reinterpret_cast<uint16_t*>(xs);
+  float* const rfac = reinterpret_cast<float*>(
+      reinterpret_cast<uint8_t*>(xs) + ((int64_t)B * K * (XB ? 2 : 4) + 15) / 16 * 16);
   const int64_t mat = blockIdx.y;
   const uint16_t* xm = x + mat * (int64_t)B * K;
   const uint16_t* Wm = W + mat * N * K;
@@ -56,8 +63,28 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 
+  // this wave's rows (one batch row: the first pass's weight loads go out
+  // before x is staged, so their latency overlaps the staging; with more
+  // batch rows that costs more than it gains, measured)
+  const int64_t row0 = ((int64_t)blockIdx.x * kDgWaves + wave) * R;
+  u32x4 wv[R][SEG];
+  // all loads of a pass at once (rows past N and columns past K re-read an
+  // in-bounds piece and are not used)
+  auto load_pass = [&](int64_t k0) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int64_t n = row0 + r < N ? row0 + r : N - 1;
+#pragma unroll
+      for (int j = 0; j < SEG; ++j) {
+        int64_t col = k0 + (int64_t)kDgChunk * j + 8 * lane;
+        col = col < K ? col : K - 8;
+        wv[r][j] = ld16(Wm + n * K + col);
+      }
+    }
+  };
+  if constexpr (!XB) load_pass(0);
+
   if constexpr (RMS) {
-    float* rfac = xs + (int64_t)B * K;
     for (int b = wave; b < B; b += kDgWaves) {
       float sq = 0.f;
       for (int64_t k = 4 * lane; k < K; k += 256) {
@@ -81,14 +108,21 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const uint32_t bits = __float_as_uint(__uint_as_float(a[t]) * r * __uint_as_float(c[t]));
-        o[t] = ((bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16) << 16;  // bf16, nearest even
+        o[t] = (bits + 0x7FFFu + ((bits >> 16) & 1u)) >> 16;  // bf16, nearest even
       }
-      st16(xs + 4 * i, u32x4{o[0], o[1], o[2], o[3]});
+      if constexpr (XB)
+        *reinterpret_cast<u32x2*>(xh + 4 * i) = u32x2{o[0] | (o[1] << 16), o[2] | (o[3] << 16)};
+      else
+        st16(xs + 4 * i, u32x4{o[0] << 16, o[1] << 16, o[2] << 16, o[3] << 16});
     }
   }
-  // x -> float32 in LDS (8 values per thread and step; K % 8 == 0)
+  // x -> LDS (8 values per thread and step; K % 8 == 0), as float32 or as is
   for (int64_t i = threadIdx.x; !RMS && i < (int64_t)B * K / 8; i += 64 * kDgWaves) {
     const u32x4 v = ld16(xm + 8 * i);
+    if constexpr (XB) {
+      st16(xh + 8 * i, v);
+      continue;
+    }
     const uint32_t a[4] = {v.x, v.y, v.z, v.w};
     float f[8];
 #pragma unroll
@@ -103,7 +137,6 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
   }
   __syncthreads();
 
-  const int64_t row0 = ((int64_t)blockIdx.x * kDgWaves + wave) * R;
   float acc[R][BMAX];
 #pragma unroll
   for (int r = 0; r < R; ++r)
@@ -111,19 +144,7 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
     for (int b = 0; b < BMAX; ++b) acc[r][b] = 0.f;
 
   for (int64_t k0 = 0; k0 < K; k0 += (int64_t)kDgChunk * SEG) {
-    // all loads of this pass first (rows past N and columns past K re-read
-    // an in-bounds piece and are not used)
-    u32x4 wv[R][SEG];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const int64_t n = row0 + r < N ? row0 + r : N - 1;
-#pragma unroll
-      for (int j = 0; j < SEG; ++j) {
-        int64_t col = k0 + (int64_t)kDgChunk * j + 8 * lane;
-        col = col < K ? col : K - 8;
-        wv[r][j] = ld16(Wm + n * K + col);
-      }
-    }
+    if (XB || k0 > 0) load_pass(k0);
 #pragma unroll
     for (int j = 0; j < SEG; ++j) {
       const int64_t col = k0 + (int64_t)kDgChunk * j + 8 * lane;
@@ -131,12 +152,23 @@ __global__ __launch_bounds__(64 * kDgWaves) void dgemv_kernel(
 #pragma unroll
       for (int b = 0; b < BMAX; ++b) {
         if (b >= B) break;
-        const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col);
-        const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col + 4);
-        const float xv[8] = {__uint_as_float(x0.x), __uint_as_float(x0.y),
-                             __uint_as_float(x0.z), __uint_as_float(x0.w),
-                             __uint_as_float(x1.x), __uint_as_float(x1.y),
-                             __uint_as_float(x1.z), __uint_as_float(x1.w)};
+        float xv[8];
+        if constexpr (XB) {
+          const u32x4 h = *reinterpret_cast<const u32x4*>(xh + (int64_t)b * K + col);
+          const uint32_t hv[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            xv[2 * t] = __uint_as_float(hv[t] << 16);
+            xv[2 * t + 1] = __uint_as_float(hv[t] & 0xFFFF0000u);
+          }
+        } else {
+          const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col);
+          const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + (int64_t)b * K + col + 4);
+          xv[0] = __uint_as_float(x0.x); xv[1] = __uint_as_float(x0.y);
+          xv[2] = __uint_as_float(x0.z); xv[3] = __uint_as_float(x0.w);
+          xv[4] = __uint_as_float(x1.x); xv[5] = __uint_as_float(x1.y);
+          xv[6] = __uint_as_float(x1.z); xv[7] = __uint_as_float(x1.w);
+        }
 #pragma unroll
         for (int r = 0; r < R; ++r) {
           const uint32_t wa[4] = {wv[r][j].x, wv[r][j].y, wv[r][j].z, wv[r][j].w};
@@ -170,10 +202,12 @@ template <int BMAX, bool RMS>
 static hipError_t launch_dgemv_b(const uint16_t* x, const uint16_t* W, int count, int B,
                                  int64_t N, int64_t K, float* y, hipStream_t stream,
                                  const float* xr, const float* nw, float eps, int accum) {
-  const size_t lds = ((size_t)B * K + (RMS ? 16 : 0)) * sizeof(float);
-  // four rows per wave, or two when the launch has few rows per CU
+  const size_t lds = ((size_t)B * K * (BMAX > 1 ? 2 : 4) + 15) / 16 * 16 + (RMS ? 16 * 4 : 0);
+  // four rows per wave, or two when the launch has few rows per CU or (one
+  // batch row) the rows are long: K > 2048 takes a row in one pass, 8
+  // pieces per lane
   const int64_t blocks4 = (N + 4 * kDgWaves - 1) / (4 * kDgWaves) * count;
-  if (blocks4 >= 2 * (int64_t)current_cu_count()) {
+  if (blocks4 >= 2 * (int64_t)current_cu_count() && (BMAX > 1 || K <= 4 * kDgChunk)) {
     const dim3 grid((unsigned)((N + 4 * kDgWaves - 1) / (4 * kDgWaves)), (unsigned)count);
     hipLaunchKernelGGL((dgemv_kernel<BMAX, 4, 4, RMS>), grid, dim3(64 * kDgWaves), lds, stream, x,
                        W, B, N, K, y, xr, nw, eps, accum);
