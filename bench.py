@@ -823,9 +823,10 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1, fused=True, stack=False)
 def decode_mixed_stack(dev, tokens, batch=1):
     """Layer-selective quantization (Sec. 7, Table 10): the 48-layer decode
     token with the first two and last two blocks kept in FP16 (2 bytes per
-    weight, tm_dgemv) and the other 44 ternary (tm_tgemv): four launches per
-    token (ternary and FP16 arenas of each projection kind).  Warm (one set
-    of arenas) and cold (tokens cycling over copies, >= 1.1 GiB)."""
+    weight, tm_dgemv) and the other 44 ternary: three launches per token (the
+    ternary arenas of both projection kinds in one, tm_tgemv_pair, then each
+    kind's FP16 arena).  Warm (one set of arenas) and cold (tokens cycling
+    over copies, >= 1.1 GiB)."""
     import torch
     from paper_2606_18114_amd import synth
     from paper_2606_18114_amd.stack import DecodeStack, keep_first_last
@@ -845,7 +846,7 @@ def decode_mixed_stack(dev, tokens, batch=1):
     nb = st.bytes_per_token()
     copies = [None] + [st.arena_copy() for _ in range(int(np.ceil(ROTATE_BYTES / nb)) - 1)]
     res = {"kept_layers": keep, "bytes_per_token": nb, "batch": batch,
-           "launches_per_token": 4}
+           "launches_per_token": 3}
     for mode in ("warm", "cold"):
         pick = (lambda t: None) if mode == "warm" else (lambda t: copies[t % len(copies)])
         for t in range(2 * len(copies)):

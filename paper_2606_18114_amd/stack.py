@@ -68,7 +68,8 @@ class DecodeStack:
     (kind "in" or "out"); layers in ``keep`` are stored as float16, the
     others ternarized (``tm_ternarize_pack``) into codes + float16 scales.
     Each kind's ternary layers and kept layers form two contiguous arenas in
-    layer order, so a token is four launches.  Inputs and outputs of a token
+    layer order, so a token is three launches: both kinds' ternary arenas in
+    one (``tm_tgemv_pair``), then each kind's kept layers.  Inputs and outputs of a token
     live in per-kind buffers ``x[kind]`` [L, B, K] and ``y[kind]`` [L, B, N]
     in layer order; the launches read and write views of them.
     """
@@ -125,10 +126,16 @@ class DecodeStack:
         ``arenas`` (optional) replaces the weight arenas, e.g. copies used to
         keep the caches cold."""
         a = arenas or {}
+        cs = {k: (a.get(("codes", k), self.codes[k]), a.get(("s16", k), self.s16[k]))
+              for k in kinds}
+        pair = self.tern and len(kinds) == 2
+        if pair:  # both kinds' ternary layers in one launch
+            k0, k1 = kinds
+            ops.tgemv_pair(self._xt[k0], *cs[k0], self._xt[k1], *cs[k1], self.g,
+                           y0=self._yt[k0], y1=self._yt[k1])
         for kind in kinds:
-            if self.tern:
-                ops.tgemv(self._xt[kind], a.get(("codes", kind), self.codes[kind]),
-                          a.get(("s16", kind), self.s16[kind]), self.g, y=self._yt[kind])
+            if self.tern and not pair:
+                ops.tgemv(self._xt[kind], *cs[kind], self.g, y=self._yt[kind])
             if self.keep:
                 ops.dgemv(self._xd[kind], a.get(("w16", kind), self.w16[kind]),
                           y=self._yd[kind])
