@@ -651,6 +651,8 @@ def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
     if workspace is None:
         workspace = mamba2_decode_workspace(D, H, dev)
     _need(workspace, "workspace", _U8, 1)
+    if workspace.device != dev:
+        raise ValueError(f"workspace is on {workspace.device}, the operands on {dev}")
     st = Mamba2Stack(L, D, H, g, eps, *(arrays[k].data_ptr() for k in STACK_FIELDS))
     rc = lib().tm_mamba2_decode_token(ctypes.byref(st), _ptr(emb), _ptr(x_out), _ptr(workspace),
                                       workspace.numel(), _stream())
