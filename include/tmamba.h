@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 12
+#define TM_ABI_VERSION 13
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -114,6 +114,32 @@ tm_status tm_ternarize_pack(const float* W, int64_t N, int64_t K, int32_t g,
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
                        const float* scales, int64_t M, int64_t N, int64_t K,
                        int32_t g, float* Y, tm_stream stream);
+
+/*
+ * tm_tgemm_fwd_ws — tm_tgemm_fwd with a small workspace through which the two
+ * parts of each cut tile meet (Sec. 3.1, the same product): when the
+ * tiles left over are cut in two along K, the part that finishes first
+ * writes its sums into Y and the second adds its own to them, so Y needs no
+ * clearing, the parts issue half the atomics, and repeated calls give
+ * identical bits (two addends).  Tiles cut into more parts add with
+ * atomics as in tm_tgemm_fwd.
+ *   workspace        device memory owned by the caller, at least
+ *                    tm_tgemm_fwd_workspace() bytes, 4-byte aligned,
+ *                    overlapping no other argument; its contents are
+ *                    scratch (cleared by the call, nothing kept after it)
+ *   workspace_bytes  its size (TM_ESHAPE if too small)
+ *   every other argument, limit and status as for tm_tgemm_fwd.
+ * The second part of a cut tile waits (bounded) for the first, which is
+ * already running when the wait starts.  Calls that share a workspace must
+ * not run concurrently.
+ */
+tm_status tm_tgemm_fwd_ws(const uint16_t* X, const uint8_t* codes,
+                          const float* scales, int64_t M, int64_t N, int64_t K,
+                          int32_t g, float* Y, void* workspace,
+                          int64_t workspace_bytes, tm_stream stream);
+
+/* Workspace bytes of tm_tgemm_fwd_ws (independent of the shape). */
+int64_t tm_tgemm_fwd_workspace(void);
 
 /*
  * tm_tgemm_fwd_bf16 — tm_tgemm_fwd with the output in bfloat16: each float32

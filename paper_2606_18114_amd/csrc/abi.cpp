@@ -52,9 +52,10 @@ hipStream_t to_hip(tm_stream s) { return reinterpret_cast<hipStream_t>(s); }
 constexpr int64_t kMaxGridBlocks = (int64_t(1) << 31) - 1;
 
 // Y holds es-byte elements: 4 (float32) or 2 (bfloat16 bits)
+// workspace NULL: the calls without one (cut tiles add with atomics)
 tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int32_t g, void* Y, int es,
-                            tm_stream stream) {
+                            void* workspace, int64_t workspace_bytes, tm_stream stream) {
   if (!X || !codes || !scales || !Y) return TM_EINVAL;
   if (M < 1 || N < 1) return TM_ESHAPE;
   if (tm_status st = shape_kg(K, g)) return st;
@@ -69,8 +70,16 @@ tm_status tgemm_fwd_checked(const uint16_t* X, const uint8_t* codes, const float
   const Span y = span(Y, yb);
   if (overlap(y, span(X, xb)) || overlap(y, span(codes, cb)) || overlap(y, span(scales, sb)))
     return TM_EINVAL;
-  return hip_status(
-      tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, es == 2, to_hip(stream)));
+  if (workspace) {
+    if (workspace_bytes < tm_tgemm_fwd_workspace()) return TM_ESHAPE;
+    if (!aligned(workspace, 4)) return TM_EALIGN;
+    const Span w = span(workspace, tm_tgemm_fwd_workspace());
+    if (overlap(w, y) || overlap(w, span(X, xb)) || overlap(w, span(codes, cb)) ||
+        overlap(w, span(scales, sb)))
+      return TM_EINVAL;
+  }
+  return hip_status(tmk::launch_tgemm_fwd(X, codes, scales, M, N, K, g, Y, es == 2,
+                                          static_cast<uint32_t*>(workspace), to_hip(stream)));
 }
 
 // argument checks of both dX calls; workspace NULL: the two-pass call,
@@ -290,13 +299,23 @@ tm_status tm_scale_ste_grad(const float* W, const uint8_t* codes, const float* s
 
 tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales, int64_t M,
                        int64_t N, int64_t K, int32_t g, float* Y, tm_stream stream) {
-  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 4, stream);
+  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 4, nullptr, 0, stream);
+}
+
+int64_t tm_tgemm_fwd_workspace(void) { return 8 * (int64_t)tmk::kFwdMaxTicketTiles; }
+
+tm_status tm_tgemm_fwd_ws(const uint16_t* X, const uint8_t* codes, const float* scales,
+                          int64_t M, int64_t N, int64_t K, int32_t g, float* Y, void* workspace,
+                          int64_t workspace_bytes, tm_stream stream) {
+  if (!workspace) return TM_EINVAL;
+  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 4, workspace, workspace_bytes,
+                           stream);
 }
 
 tm_status tm_tgemm_fwd_bf16(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int32_t g, uint16_t* Y,
                             tm_stream stream) {
-  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 2, stream);
+  return tgemm_fwd_checked(X, codes, scales, M, N, K, g, Y, 2, nullptr, 0, stream);
 }
 
 tm_status tm_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,

@@ -39,10 +39,13 @@ hipError_t launch_group_code_dot(const uint8_t* codes, const float* dW, int64_t 
 hipError_t launch_scale_ste_grad(const float* W, const uint8_t* codes, const float* scale,
                                  const float* dWhat, int64_t N, int64_t K, int g, float eps,
                                  float* ds, float* dw, hipStream_t stream);
-// Y: float32 [M, N], or bfloat16 bits [M, N] when bf16_out
+// Y: float32 [M, N], or bfloat16 bits [M, N] when bf16_out.  tickets:
+// NULL, or 2 * kFwdMaxTicketTiles words of caller memory through which the
+// two parts of each cut tile meet (then Y is not cleared first)
+constexpr int kFwdMaxTicketTiles = 1024;
 hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int g, void* Y, bool bf16_out,
-                            hipStream_t stream);
+                            uint32_t* tickets, hipStream_t stream);
 hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const float* scales,
                                int64_t M, int64_t N, int64_t K, int g, float* dX,
                                hipStream_t stream);

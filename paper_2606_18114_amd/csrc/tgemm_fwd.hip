@@ -55,6 +55,10 @@ namespace tmk {
 
 constexpr int kFwdBM = 256, kFwdBN = 256, kFwdBK = 64;
 constexpr int kFwdXRing = 3;
+// polls of a cut tile's flag before the second part gives up waiting (the
+// first part is already storing when the second starts to wait; this bound
+// only keeps every wave's exit certain)
+constexpr uint32_t kFwdSpinLimit = 1u << 20;
 constexpr int kFwdXStage = kFwdBM * kFwdBK * 2;  // 32 KiB of X per stage
 
 // SS: X stages per code stage (4 when K % 256 == 0, else 1)
@@ -122,9 +126,10 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ codes,
     const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
     void* __restrict__ Yv, uint32_t tiles_n, uint32_t full_rounds, uint32_t extra_units,
-    uint32_t parts) {
+    uint32_t parts, uint32_t* __restrict__ tickets) {
   using C = FwdCfg<G, SS>;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[C::kLds];
+  __shared__ uint32_t tk_word;  // arrival order of this workgroup at its cut tile
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -147,6 +152,11 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
   // zeroed there beforehand), and odd parts come first: those workgroups
   // then run half a tile out of phase with the others, which spreads the
   // output stores over time instead of all workgroups storing at once.
+  // With tickets (two parts per tile, Y not cleared): the part that reaches
+  // its epilogue first (word 2t of the tickets, t the cut tile) writes its
+  // sums into Y with coherent stores and then raises word 2t + 1; the second
+  // waits for that word and adds its sums with atomics.  Two addends give the
+  // same bits in either order, and only half the atomics.
   const uint32_t F = full_rounds;
   const bool has_x = bid < extra_units;
   const uint32_t nu = F + (has_x ? 1u : 0u);
@@ -417,6 +427,29 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
     {
       const int64_t mrow = m0 + wm * 128;
       constexpr int ES = BF ? 2 : 4;  // bytes per output element
+      // two-part cut tile with tickets: which part arrives first
+      const bool tk = !BF && part && tickets != nullptr;
+      const uint32_t tkt = 2u * (bid / parts);
+      bool tk_second = false;
+      if (tk) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          const uint32_t order = atomicAdd(tickets + tkt, 1u);
+          if (order != 0u) {
+            // the first part is already in its epilogue: wait (bounded) until
+            // its sums have reached memory
+            for (uint32_t n = 0; n < kFwdSpinLimit; ++n) {
+              if (__hip_atomic_load(tickets + tkt + 1, __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT) != 0u)
+                break;
+              __builtin_amdgcn_s_sleep(2);
+            }
+          }
+          tk_word = order;
+        }
+        __syncthreads();
+        tk_second = tk_word != 0u;
+      }
       uint8_t* ytile = reinterpret_cast<uint8_t*>(Yv) + (mrow * N + n0) * ES;
       const bool full_m = mrow + 128 <= M;
 #pragma unroll
@@ -436,7 +469,14 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
             for (int i4 = 0; i4 < 4; ++i4) {
 #pragma unroll
               for (int i1 = 0; i1 < 4; ++i1) {
-                if (row < M) atomicAdd(reinterpret_cast<float*>(yp), f * acc[a][b][4 * i4 + i1]);
+                if (row < M) {
+                  const float v = f * acc[a][b][4 * i4 + i1];
+                  if (tk && !tk_second)  // first of two: write through to memory
+                    __hip_atomic_store(reinterpret_cast<float*>(yp), v, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                  else
+                    atomicAdd(reinterpret_cast<float*>(yp), v);
+                }
                 yp += pv;
                 ++row;
               }
@@ -494,6 +534,13 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
             }
         }
       }
+      if (tk && !tk_second) {
+        // every wave's coherent stores have completed: raise the tile's flag
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (threadIdx.x == 0)
+          __hip_atomic_store(tickets + tkt + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
   // loads issued for stages past the end must land before the workgroup's
@@ -503,7 +550,7 @@ __global__ __launch_bounds__(512) void tgemm_fwd_kernel(
 
 hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float* scales,
                             int64_t M, int64_t N, int64_t K, int g, void* Y, bool bf16_out,
-                            hipStream_t stream) {
+                            uint32_t* tickets, hipStream_t stream) {
   const int64_t tm = (M + kFwdBM - 1) / kFwdBM, tn = (N + kFwdBN - 1) / kFwdBN;
   const int64_t ntiles = tm * tn;
   const int cus = current_cu_count();
@@ -521,7 +568,13 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
   if (parts > trips) parts = trips;
   if (parts < 1 || bf16_out) parts = 1;  // bfloat16 results are not summed in parts
   const int64_t extra = R * parts;
-  if (parts > 1) {
+  // two parts per cut tile and tickets given: the first part writes, the
+  // second adds (Y is not cleared; the tickets are, by a fill kernel)
+  if (parts != 2 || R > kFwdMaxTicketTiles) tickets = nullptr;
+  if (tickets) {
+    hipError_t e = launch_fill_zero_f32(reinterpret_cast<float*>(tickets), 2 * R, stream);
+    if (e != hipSuccess) return e;
+  } else if (parts > 1) {
     // the cut tiles accumulate atomically: clear their rows of Y first (a
     // fill kernel, not a memset node, so the call can be captured)
     const int64_t r0 = F * P / tn * kFwdBM;
@@ -533,7 +586,7 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
                  np = (uint32_t)parts;
 #define TM_FWD_L(GG, SS_, BF_)                                                                 \
   hipLaunchKernelGGL((tgemm_fwd_kernel<GG, SS_, BF_>), grid, block, 0, stream, X, codes, scales, \
-                     M, N, K, Y, t_n, fr, xu, np)
+                     M, N, K, Y, t_n, fr, xu, np, tickets)
 #define TM_FWD(GG)                                                                             \
   case GG:                                                                                     \
     if (wide) {                                                                                \

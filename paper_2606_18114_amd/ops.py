@@ -46,6 +46,8 @@ SIGNATURES = {
     "tm_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "tm_ternarize_pack": (ctypes.c_int, [_P, _I64, _I64, _I32, ctypes.c_float, _P, _P, _P, _P, _P]),
     "tm_tgemm_fwd": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
+    "tm_tgemm_fwd_ws": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P, _I64, _P]),
+    "tm_tgemm_fwd_workspace": (ctypes.c_int64, []),
     "tm_tgemm_bwd_dx": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P]),
     "tm_tgemm_bwd_dx_f16": (ctypes.c_int,
                             [_P, _P, _P, _I64, _I64, _I64, _I32, _P, _P, _I64, _P]),
@@ -274,9 +276,13 @@ def scale_ste_grad(W: torch.Tensor, codes: torch.Tensor, scale: torch.Tensor,
 
 def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
               Y: Optional[torch.Tensor] = None,
-              out_dtype: torch.dtype = torch.float32) -> torch.Tensor:
-    """Y[M, N] = X . (q * s)^T in float32, or rounded once to bfloat16
-    (out_dtype=torch.bfloat16, ``tm_tgemm_fwd_bf16``)."""
+              out_dtype: torch.dtype = torch.float32, *,
+              workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Y[M, N] = X . (q * s)^T in float32 (``tm_tgemm_fwd_ws``: the two parts of
+    a cut tile meet through a small workspace, uint8 of at least
+    ``fwd_workspace_bytes()`` bytes, allocated here when not given), or
+    rounded once to bfloat16 (out_dtype=torch.bfloat16,
+    ``tm_tgemm_fwd_bf16``)."""
     _need(X, "X", _BF16, 2)
     _need(codes, "codes", _U8, 2)
     _need(scales, "scales", _F32, 2)
@@ -295,10 +301,23 @@ def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int
                                      _stream())
         _check("tm_tgemm_fwd_bf16", st)
     else:
-        st = lib().tm_tgemm_fwd(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
-                                _stream())
-        _check("tm_tgemm_fwd", st)
+        need = fwd_workspace_bytes()
+        if workspace is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+        _need(workspace, "workspace", _U8, 1)
+        if workspace.numel() < need:
+            raise ValueError(f"workspace has {workspace.numel()} bytes, {need} needed")
+        if workspace.device != X.device:
+            raise ValueError(f"workspace is on {workspace.device}, the operands on {X.device}")
+        st = lib().tm_tgemm_fwd_ws(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
+                                   _ptr(workspace), workspace.numel(), _stream())
+        _check("tm_tgemm_fwd_ws", st)
     return Y
+
+
+def fwd_workspace_bytes() -> int:
+    """Workspace bytes of ``tm_tgemm_fwd_ws`` (a constant)."""
+    return int(lib().tm_tgemm_fwd_workspace())
 
 
 def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,

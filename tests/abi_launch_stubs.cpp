@@ -28,7 +28,7 @@ hipError_t launch_scale_ste_grad(const float*, const uint8_t*, const float*, con
   reached("scale_ste_grad");
 }
 hipError_t launch_tgemm_fwd(const uint16_t*, const uint8_t*, const float*, int64_t, int64_t,
-                            int64_t, int, void*, bool, hipStream_t) {
+                            int64_t, int, void*, bool, uint32_t*, hipStream_t) {
   reached("tgemm_fwd");
 }
 hipError_t launch_tgemm_bwd_dx(const uint16_t*, const uint8_t*, const float*, int64_t, int64_t,

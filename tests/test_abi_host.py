@@ -43,11 +43,11 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 24
+    assert len(names) == 26
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 12
+    assert L.tm_abi_version() == 13
 
 
 def test_status_strings(L):
@@ -336,6 +336,25 @@ def test_tgemm_fwd_validation(L):
     assert fwd(L, Y=P + 2 ** 26 + 4) == EALIGN
     assert fwd(L, Y=P + 4096) == EINVAL                 # Y overlaps X
     assert fwd(L, Y=P + 2 ** 24 - 4096) == EINVAL       # Y overlaps codes
+
+
+def test_tgemm_fwd_ws_validation(L):
+    # ticket words of up to 1024 cut tiles, two per tile
+    assert L.tm_tgemm_fwd_workspace() == 8192
+
+    def f(X=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,
+          Y=P + 2 ** 26, ws=P + 2 ** 27, wsb=8192):
+        return L.tm_tgemm_fwd_ws(X, codes, scales, M, N, K, g, Y, ws, wsb, None)
+    for kw in ("X", "codes", "scales", "Y", "ws"):
+        assert f(**{kw: 0}) == EINVAL, kw
+    assert f(M=0) == ESHAPE
+    assert f(K=544) == ESHAPE
+    assert f(wsb=8188) == ESHAPE                      # one word short
+    assert f(ws=P + 2 ** 27 + 2) == EALIGN
+    assert f(Y=P + 2 ** 26 + 4) == EALIGN
+    assert f(ws=P + 2 ** 26) == EINVAL                # workspace over Y
+    assert f(ws=P + 2 ** 25 - 4096) == EINVAL         # workspace runs into the scales
+    assert f(ws=P + 64) == EINVAL                     # workspace over X
 
 
 def test_tgemm_fwd_bf16_validation(L):

@@ -313,6 +313,55 @@ def test_fwd_split_tiles_exact_and_complete():
     assert err <= REL_DESIGN
 
 
+def _fwd_no_workspace(X, c, s, g, Y):
+    """tm_tgemm_fwd itself: the cut tiles' parts add with atomics."""
+    ops = _ops()
+    M, K = X.shape
+    st = ops.lib().tm_tgemm_fwd(X.data_ptr(), c.data_ptr(), s.data_ptr(), M, c.shape[0], K, g,
+                                Y.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    return Y
+
+
+def test_fwd_two_part_tiles_workspace_and_atomics():
+    """Tiles cut in two along K meet through the workspace (the first part
+    writes, the second adds): every element is written over a NaN-filled Y,
+    repeated calls give identical bits, and the call without a workspace
+    (both parts adding atomically into a cleared Y) agrees to float32
+    rounding; with integer inputs and power-of-two scales both are exact."""
+    ops = _ops()
+    rng = np.random.default_rng(23)
+    # 128 tiles of 256 x 256 for 256 compute units: every tile cut in two
+    M, N, K, g = 4096, 2048, 4096, 128
+    print(f"[fwd] two-part tiles M={M} N={N} K={K} g={g}", flush=True)
+    W = synth.weights(rng, N, K, outliers=False)
+    X = dev_bf16(synth.activations(rng, M, K))
+    c, s, _, q, s32, _ = oracle_packed(W, g)
+    outs = []
+    for _ in range(2):
+        Y = torch.full((M, N), float("nan"), device="cuda")
+        outs.append(host(ops.tgemm_fwd(X, c, s, g, Y=Y)))
+    assert np.isfinite(outs[0]).all()
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    Ya = host(_fwd_no_workspace(X, c, s, g, torch.full((M, N), float("nan"), device="cuda")))
+    assert np.isfinite(Ya).all()
+    diff = O.rel_fro_error(Ya, outs[0])
+    print(f"  workspace vs atomics rel fro {diff:.3e}", flush=True)
+    assert diff <= 1e-6
+    # exact: small integers and power-of-two scales (272 tiles: 16 cut in two)
+    M, N, K, g = 4352, 4096, 512, 128
+    qi = rng.integers(-1, 2, (N, K)).astype(np.int8)
+    sc = (2.0 ** rng.integers(-3, 3, (N, K // g))).astype(np.float32)
+    Xi = rng.integers(-8, 9, (M, K)).astype(np.float32)
+    Xd = dev_bf16(synth.f32_to_bf16_bits(Xi))
+    cd, sd = torch.from_numpy(O.pack(qi)).cuda(), dev_f32(sc)
+    ref = O.gemm_fwd(Xi, qi, sc, g)
+    Yw = host(ops.tgemm_fwd(Xd, cd, sd, g, Y=torch.full((M, N), float("nan"), device="cuda")))
+    Yn = host(_fwd_no_workspace(Xd, cd, sd, g, torch.full((M, N), float("nan"), device="cuda")))
+    np.testing.assert_array_equal(Yw, ref)
+    np.testing.assert_array_equal(Yn, ref)
+
+
 @pytest.mark.parametrize("M,N,K,g", [(300, 520, 1024, 64), (4100, 600, 512, 128),
                                      (257, 8, 128, 32), (2048, 2048, 576, 64)])
 def test_fwd_bf16_output(M, N, K, g):
