@@ -121,8 +121,8 @@ tm_status tm_tgemm_fwd(const uint16_t* X, const uint8_t* codes,
  * tiles left over are cut in two along K, the part that finishes first
  * writes its sums into Y and the second adds its own to them, so Y needs no
  * clearing, the parts issue half the atomics, and repeated calls give
- * identical bits (two addends).  Tiles cut into more parts add with
- * atomics as in tm_tgemm_fwd.
+ * identical bits (two addends).  Tiles cut into more parts, and launches
+ * with fewer than 16 cut tiles, add with atomics as in tm_tgemm_fwd.
  *   workspace        device memory owned by the caller, at least
  *                    tm_tgemm_fwd_workspace() bytes, 4-byte aligned,
  *                    overlapping no other argument; its contents are

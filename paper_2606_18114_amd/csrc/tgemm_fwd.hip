@@ -59,6 +59,8 @@ constexpr int kFwdXRing = 3;
 // first part is already storing when the second starts to wait; this bound
 // only keeps every wave's exit certain)
 constexpr uint32_t kFwdSpinLimit = 1u << 20;
+// fewest cut tiles for which the two parts meet through the tickets
+constexpr int64_t kFwdMinTicketTiles = 16;
 constexpr int kFwdXStage = kFwdBM * kFwdBK * 2;  // 32 KiB of X per stage
 
 // SS: X stages per code stage (4 when K % 256 == 0, else 1)
@@ -569,8 +571,10 @@ hipError_t launch_tgemm_fwd(const uint16_t* X, const uint8_t* codes, const float
   if (parts < 1 || bf16_out) parts = 1;  // bfloat16 results are not summed in parts
   const int64_t extra = R * parts;
   // two parts per cut tile and tickets given: the first part writes, the
-  // second adds (Y is not cleared; the tickets are, by a fill kernel)
-  if (parts != 2 || R > kFwdMaxTicketTiles) tickets = nullptr;
+  // second adds (Y is not cleared; the tickets are, by a fill kernel).  With
+  // few cut tiles the atomics cost little and the second part's wait for the
+  // first (which then finishes at about the same time) would show: atomics.
+  if (parts != 2 || R < kFwdMinTicketTiles || R > kFwdMaxTicketTiles) tickets = nullptr;
   if (tickets) {
     hipError_t e = launch_fill_zero_f32(reinterpret_cast<float*>(tickets), 2 * R, stream);
     if (e != hipSuccess) return e;

@@ -280,7 +280,7 @@ def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int
               workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Y[M, N] = X . (q * s)^T in float32 (``tm_tgemm_fwd_ws``: the two parts of
     a cut tile meet through a small workspace, uint8 of at least
-    ``fwd_workspace_bytes()`` bytes, allocated here when not given), or
+    ``fwd_workspace_bytes()`` bytes; when not given, one kept per stream), or
     rounded once to bfloat16 (out_dtype=torch.bfloat16,
     ``tm_tgemm_fwd_bf16``)."""
     _need(X, "X", _BF16, 2)
@@ -302,22 +302,42 @@ def tgemm_fwd(X: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int
         _check("tm_tgemm_fwd_bf16", st)
     else:
         need = fwd_workspace_bytes()
+        stream = _stream()
         if workspace is None:
-            workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+            workspace = _stream_workspace(X.device, stream, need)
         _need(workspace, "workspace", _U8, 1)
         if workspace.numel() < need:
             raise ValueError(f"workspace has {workspace.numel()} bytes, {need} needed")
         if workspace.device != X.device:
             raise ValueError(f"workspace is on {workspace.device}, the operands on {X.device}")
         st = lib().tm_tgemm_fwd_ws(_ptr(X), _ptr(codes), _ptr(scales), M, N, K, g, _ptr(Y),
-                                   _ptr(workspace), workspace.numel(), _stream())
+                                   _ptr(workspace), workspace.numel(), stream)
         _check("tm_tgemm_fwd_ws", st)
     return Y
 
 
+_STREAM_WS: dict = {}
+
+
+def _stream_workspace(device: torch.device, stream: int, nbytes: int) -> torch.Tensor:
+    """A small scratch buffer kept per (device, stream): calls on one stream
+    run in order, so they may share it (calls on different streams get
+    their own)."""
+    key = (device.index, stream)
+    ws = _STREAM_WS.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = _STREAM_WS[key] = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return ws
+
+
+_FWD_WS_BYTES: list = []
+
+
 def fwd_workspace_bytes() -> int:
-    """Workspace bytes of ``tm_tgemm_fwd_ws`` (a constant)."""
-    return int(lib().tm_tgemm_fwd_workspace())
+    """Workspace bytes of ``tm_tgemm_fwd_ws`` (a constant of the library)."""
+    if not _FWD_WS_BYTES:
+        _FWD_WS_BYTES.append(int(lib().tm_tgemm_fwd_workspace()))
+    return _FWD_WS_BYTES[0]
 
 
 def tgemm_bwd_dx(dY: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, g: int = 128,
