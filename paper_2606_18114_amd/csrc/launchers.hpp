@@ -64,6 +64,10 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
                                int64_t K, float* dW, int accumulate, hipStream_t stream);
 // dst[0 .. n) = 0 (float32), by a plain fill kernel
 hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream);
+// zeroes tiles t0 .. t0 + count - 1 of a float32 [rows, cols] array dealt in
+// 256 x 256 tiles, tiles_c per row of tiles (cols % 4 == 0, 16-byte aligned)
+hipError_t launch_zero_tiles_f32(float* out, int64_t rows, int64_t cols, int64_t tiles_c,
+                                 int64_t t0, int64_t count, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
 // two strided stacks of matrices (e.g. a decode token's in_proj and out_proj

@@ -291,6 +291,26 @@ __global__ __launch_bounds__(256) void tgemm_bwd_dw_kernel(
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// zeroes tiles t0 .. t0 + count - 1 of a float32 [rows, cols] array dealt in
+// 256 x 256 tiles (tile t: row block t / tiles_c, column block t % tiles_c),
+// skipping rows and columns past the array: one workgroup of 64 threads per
+// tile row (cols % 4 == 0, 16-byte aligned base)
+__global__ void zero_tiles_f32(float* __restrict__ out, int64_t rows, int64_t cols,
+                               uint32_t tiles_c, uint32_t t0) {
+  const uint32_t t = t0 + blockIdx.x / 256u;
+  const int64_t r = (int64_t)(t / tiles_c) * 256 + blockIdx.x % 256u;
+  const int64_t c = (int64_t)(t % tiles_c) * 256 + 4 * threadIdx.x;
+  if (r < rows && c < cols) *reinterpret_cast<f32x4*>(out + r * cols + c) = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+hipError_t launch_zero_tiles_f32(float* out, int64_t rows, int64_t cols, int64_t tiles_c,
+                                 int64_t t0, int64_t count, hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_tiles_f32, dim3((unsigned)(count * 256)), dim3(64), 0, stream, out,
+                     rows, cols, (uint32_t)tiles_c, (uint32_t)t0);
+  return hipGetLastError();
+}
+
 hipError_t launch_fill_zero_f32(float* dst, int64_t n, hipStream_t stream) {
   const int64_t threads = (n + 3) / 4;
   hipLaunchKernelGGL(fill_zero_f32, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
@@ -308,8 +328,8 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t* dY, const uint16_t* X, int64_t M,
   int64_t parts = rem ? P / rem : 1;
   const int64_t nst = (M + kDwBM - 1) / kDwBM;
   if (parts > nst) parts = nst;
-  if (rem && !accumulate) {  // the cut tiles are summed with atomics
-    const hipError_t e = launch_fill_zero_f32(dW, N * K, stream);
+  if (rem && !accumulate) {  // the cut tiles (the last rem) are summed with atomics
+    const hipError_t e = launch_zero_tiles_f32(dW, N, K, tk, ntiles - rem, rem, stream);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(tgemm_bwd_dw_kernel, dim3((unsigned)P), dim3(256), 0, stream, dY, X, M, N,

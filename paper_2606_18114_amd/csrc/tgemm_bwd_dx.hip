@@ -473,7 +473,7 @@ hipError_t launch_tgemm_bwd_dx(const uint16_t* dY, const uint8_t* codes, const f
   const int64_t nst = (N + kDxBN - 1) / kDxBN;
   if (parts > nst) parts = nst;
   if (rem) {  // the cut tiles are summed with atomics
-    const hipError_t e = launch_fill_zero_f32(dX, M * K, stream);
+    const hipError_t e = launch_zero_tiles_f32(dX, M, K, tk, ntiles - rem, rem, stream);
     if (e != hipSuccess) return e;
   }
   const auto* cw = reinterpret_cast<const uint32_t*>(codes);

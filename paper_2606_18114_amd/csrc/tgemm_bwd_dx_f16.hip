@@ -547,7 +547,7 @@ hipError_t launch_tgemm_bwd_dx_f16(const uint16_t* dY, const uint8_t* codes, con
   const int64_t nst = (N + kHxBN - 1) / kHxBN;
   if (parts > nst) parts = nst;
   if (rem) {
-    const hipError_t e = launch_fill_zero_f32(dX, M * K, stream);
+    const hipError_t e = launch_zero_tiles_f32(dX, M, K, tk, ntiles - rem, rem, stream);
     if (e != hipSuccess) return e;
   }
   const auto* cw = reinterpret_cast<const uint32_t*>(codes);

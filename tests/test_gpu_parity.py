@@ -496,6 +496,36 @@ def test_bwd_dw_split_tiles(M, N, K):
     assert err <= REL_DESIGN and err2 <= REL_DESIGN
 
 
+def test_backward_cut_tiles_over_nan_outputs():
+    """Only the tiles cut along the contraction are cleared before their
+    parts add up; every other output is stored whole.  Outputs that start
+    as NaN come out complete and right: dW of the in_proj shape (272 tiles,
+    16 cut) and dX in both forms (17 x 16 tiles, 16 cut)."""
+    ops = _ops()
+    rng = np.random.default_rng(29)
+    M, N, K = 96, synth.IN_PROJ_N, synth.D_MODEL
+    print(f"[dw] cut tiles over NaN M={M} N={N} K={K}", flush=True)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    X = synth.activations(rng, M, K)
+    dW = torch.full((N, K), float("nan"), device="cuda")
+    got = host(ops.tgemm_bwd_dw_ste(dev_bf16(dY), dev_bf16(X), dW=dW))
+    assert np.isfinite(got).all()
+    assert O.rel_fro_error(got, O.gemm_bwd_dw(dY, X)) <= REL_DESIGN
+    M, N, K, g = 4352, 264, 4096, 128
+    print(f"[dx] cut tiles over NaN M={M} N={N} K={K}", flush=True)
+    W = synth.weights(rng, N, K, True)
+    dY = synth.activations(rng, M, N, std=synth.DY_STD)
+    c, s, _, q, s32, _ = oracle_packed(W, g)
+    ref = O.gemm_bwd_dx(dY, q, s32, g)
+    for precision, bar in (("exact", REL_DESIGN), ("f16", 5e-4)):
+        dX = torch.full((M, K), float("nan"), device="cuda")
+        got = host(ops.tgemm_bwd_dx(dev_bf16(dY), c, s, g, dX=dX, precision=precision))
+        assert np.isfinite(got).all(), precision
+        err = O.rel_fro_error(got, ref)
+        print(f"  {precision}: rel fro err {err:.3e}", flush=True)
+        assert err <= bar, precision
+
+
 def test_bwd_dw_one_hot_tokens():
     """One-hot token rows make dW rows copies of dY columns (exact)."""
     ops = _ops()
