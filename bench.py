@@ -288,6 +288,8 @@ def main():
                   "all_ternary_unfused": decode_mamba2_blocks(dev, args.steps, fused=False),
                   "first_last_2_fp16": decode_mamba2_blocks(
                       dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2)),
+                  "first_last_2_fp16_one_launch": decode_mamba2_blocks(
+                      dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2), stack=True),
                   "all_ternary_B4": decode_mamba2_blocks(dev, args.steps, batch=4)}
 
     # ---------------- QAT block: both projections through autograd ----------------

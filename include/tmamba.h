@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 13
+#define TM_ABI_VERSION 14
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -446,6 +446,14 @@ tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
  *              in and out, as for tm_mixer_step with B = 1
  * Codes, pre_w, norm_w and final_w 16-byte aligned, scales 2-byte, the other
  * float arrays 4-byte.
+ * Blocks kept in FP16 (Sec. 7, layer-selective quantization), optional:
+ *   n_kept     0 .. 64 (0: every block ternary; the fields below unused)
+ *   kept       HOST array int32 [n_kept]: the kept blocks' indices, strictly
+ *              ascending, each < n_layers (read during the call)
+ *   in_w16     float16 [n_kept, Z, d_model], out_w16 float16 [n_kept,
+ *              d_model, d_inner]: their projections, in the order of kept
+ *              (16-byte aligned); the code and scale arenas keep their
+ *              [n_layers, ...] shape, the kept blocks' entries unread
  */
 typedef struct {
   int32_t n_layers, d_model, nheads, g;
@@ -465,6 +473,10 @@ typedef struct {
   uint16_t* conv_state;
   int32_t* conv_pos;
   uint16_t* ssm_state;
+  int32_t n_kept;
+  const int32_t* kept;
+  const uint16_t* in_w16;
+  const uint16_t* out_w16;
 } tm_mamba2_stack;
 
 /*
@@ -475,6 +487,9 @@ typedef struct {
  *   residual += out_proj(bf16(rmsnorm(g) * norm_w))             (tm_tgemv_rms)
  * with residual = emb for the first block, then
  *   x_out = bf16(rmsnorm(residual) * final_w).
+ * A block kept in FP16 takes its two projections from in_w16 / out_w16
+ * (tm_dgemv_rms: each float16 weight times the float32 value of the
+ * bfloat16 x, float32 sums).
  *   stack      host pointer to the description above (read during the call)
  *   emb        float32 [d_model] in;  x_out  bf16 [d_model] out (2-byte aligned)
  *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads)

@@ -548,6 +548,19 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
       !aligned(s.conv_state, 8) || !aligned(s.conv_pos, 4) || !aligned(s.ssm_state, 16) ||
       !aligned(emb, 4) || !aligned(x_out, 2) || !aligned(workspace, 256))
     return TM_EALIGN;
+  // blocks kept in FP16
+  if (s.n_kept < 0 || s.n_kept > tmk::kDecodeStackMaxKept) return TM_ESHAPE;
+  int64_t iwb = 0, owb = 0;
+  if (s.n_kept > 0) {
+    if (!s.kept || !s.in_w16 || !s.out_w16) return TM_EINVAL;
+    for (int i = 0; i < s.n_kept; ++i)
+      if (s.kept[i] < 0 || s.kept[i] >= L || (i > 0 && s.kept[i] <= s.kept[i - 1]))
+        return TM_ESHAPE;
+    if (!bytes_of((int64_t)s.n_kept * Z, Dm, 2, &iwb) ||
+        !bytes_of((int64_t)s.n_kept * Dm, DI, 2, &owb))
+      return TM_ESHAPE;
+    if (!aligned(s.in_w16, 16) || !aligned(s.out_w16, 16)) return TM_EALIGN;
+  }
   const Span outs[5] = {span(s.conv_state, csb), span(s.conv_pos, L * 4), span(s.ssm_state, ssb),
                         span(x_out, Dm * 2), span(workspace, need)};
   const Span ins[13] = {span(s.in_codes, icb), span(s.in_scales, isb), span(s.out_codes, ocb),
@@ -561,6 +574,9 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
       if (overlap(outs[i], outs[j])) return TM_EINVAL;
     for (const Span& in : ins)
       if (overlap(outs[i], in)) return TM_EINVAL;
+    if (s.n_kept > 0 && (overlap(outs[i], span(s.in_w16, iwb)) ||
+                         overlap(outs[i], span(s.out_w16, owb))))
+      return TM_EINVAL;
   }
   tmk::DecodeStackDesc d;
   d.n_layers = s.n_layers;
@@ -583,6 +599,10 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
   d.conv_state = s.conv_state;
   d.conv_pos = s.conv_pos;
   d.ssm_state = s.ssm_state;
+  d.n_kept = s.n_kept;
+  for (int i = 0; i < tmk::kDecodeStackMaxKept; ++i) d.kept[i] = i < s.n_kept ? s.kept[i] : -1;
+  d.in_w16 = s.n_kept > 0 ? s.in_w16 : nullptr;
+  d.out_w16 = s.n_kept > 0 ? s.out_w16 : nullptr;
   return hip_status(tmk::launch_decode_stack(d, emb, x_out, workspace, to_hip(stream)));
 }
 

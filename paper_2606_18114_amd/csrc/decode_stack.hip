@@ -2,6 +2,7 @@
 // in a single launch (paper Sec. 8: batch-1 decoding is bound by the weight
 // traffic; Sec. 3.2: the mixer stays in FP16).  Per block l, in layer order:
 //
+// (a block kept in FP16 takes its projections from float16 weights instead)
 //   A  zx = in_proj(bf16(rmsnorm(residual) * pre_w[l]))      Z rows, K = d_model
 //   B  gated = mixer step per head (conv, FP16 SSM, y * SiLU(z))
 //   C  residual += out_proj(bf16(rmsnorm(gated) * norm_w[l]))  d_model rows, K = d_inner
@@ -14,7 +15,7 @@
 // spin on the counter (bounded: after 2^16 polls a flag is set and the spin
 // ends, and every later wait that sees the flag ends too, so every wave
 // always exits soon).  The barriers need every workgroup resident at once.
-// A CU holds three of these workgroups (registers; the LDS use is small), so
+// A CU holds two of these workgroups (registers; the LDS use is small), so
 // on a GPU with nothing else running all of them start at once.  The launch
 // is an ordinary one: the runtime's cooperative launch gives the same
 // placement but spaced the tokens 10 to 120 us apart (it waited for the
@@ -290,6 +291,70 @@ __device__ __forceinline__ void ds_rows_compute(const DsRows& p, const uint32_t 
   }
 }
 
+// Rows r0 + wave, + kDsWaves, ... (< r1) of a float16 matrix W [rows, K] (a
+// block kept in FP16): out(r, base[r] + sum_k x[k] W[r, k]), base NULL: 0.
+// A wave takes up to four rows at a time (8 / T, so 64 registers hold their
+// pieces), their 16-byte pieces (the columns of the lane's x pairs) loaded
+// together; each float16 weight times the float32 value of its bfloat16 x is
+// exact, summed in float32 in a fixed order.
+template <int T, typename Out>
+__device__ __forceinline__ void ds_dense_rows(const uint16_t* __restrict__ W, int K, int r0,
+                                              int r1, const uint32_t (&xr)[T][8],
+                                              const float* base, Out out) {
+  constexpr int kR = T >= 8 ? 1 : (T >= 4 ? 2 : 4);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nw = K / 16;
+  for (int r = r0 + wave; r < r1; r += kR * kDsWaves) {
+    u32x4 wv[kR][T][2];
+    float bv[kR];
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      const int ri = r + i * kDsWaves;
+      const int rr = ri < r1 ? ri : r;  // past the range: row r again (not used)
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const int w = lane + 64 * t;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          wv[i][t][h] = u32x4{0u, 0u, 0u, 0u};
+          if (w < nw) wv[i][t][h] = ld16(W + (int64_t)rr * K + 16 * w + 8 * h);
+        }
+      }
+      bv[i] = base != nullptr && ri < r1 ? ld_f32<true>(base + ri) : 0.f;
+    }
+    float acc[kR];
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      float e = 0.f, o = 0.f;
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t wq[4] = {wv[i][t][h].x, wv[i][t][h].y, wv[i][t][h].z, wv[i][t][h].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t xp = xr[t][4 * h + q];
+            e = __builtin_fmaf(h2f((uint16_t)(wq[q] & 0xFFFFu)), __uint_as_float(xp << 16), e);
+            o = __builtin_fmaf(h2f((uint16_t)(wq[q] >> 16)), __uint_as_float(xp & 0xFFFF0000u), o);
+          }
+        }
+      acc[i] = ds_wave_sum(e + o);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int i = 0; i < kR; ++i)
+        if (r + i * kDsWaves < r1) out(r + i * kDsWaves, bv[i] + acc[i]);
+    }
+  }
+}
+
+// index of block l among the blocks kept in FP16, or -1 (ternary)
+__device__ __forceinline__ int ds_kept(const DecodeStackDesc& s, int l) {
+  for (int i = 0; i < s.n_kept; ++i)
+    if (s.kept[i] == l) return i;
+  return -1;
+}
+
 // this lane's x pairs (words lane, lane + 64, ...; zero past the row)
 template <int T>
 __device__ __forceinline__ void ds_x_regs(const uint32_t* xs, int K, uint32_t (&xr)[T][8]) {
@@ -347,7 +412,8 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
   u32x4 sv[4];
 
   // block 0's in_proj rows
-  ds_rows_load<G, TA>(rows, s.in_codes, s.in_s16, D, zr0 + wave, zr1, nullptr);
+  int kd = ds_kept(s, 0);
+  if (kd < 0) ds_rows_load<G, TA>(rows, s.in_codes, s.in_s16, D, zr0 + wave, zr1, nullptr);
   for (int l = 0; l < s.n_layers; ++l) {
     const uint8_t* inc = s.in_codes + (int64_t)l * Z * (D / 4);
     const uint16_t* ins = s.in_s16 + (int64_t)l * Z * (D / G);
@@ -360,8 +426,11 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
     {
       uint32_t xr[TA][8];
       ds_x_regs<TA>(xs, D, xr);
-      ds_rows_all<G, TA>(rows, inc, ins, D, zr1, xr, nullptr,
-                         [&](int r, float y) { st_f32<true>(a.zx + r, y); });
+      auto put = [&](int r, float y) { st_f32<true>(a.zx + r, y); };
+      if (kd < 0)
+        ds_rows_all<G, TA>(rows, inc, ins, D, zr1, xr, nullptr, put);
+      else
+        ds_dense_rows<TA>(s.in_w16 + (int64_t)kd * Z * D, D, zr0, zr1, xr, nullptr, put);
     }
     // the mixer's state, and this workgroup's out_proj rows, during the barrier
     // (only the heads' workgroups wait for every in_proj row; the others go
@@ -369,7 +438,7 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
     ds_arrive(bar_a);
     uint16_t* ssm_h = s.ssm_state + ((int64_t)l * H + bid) * kMxP * kMxN;
     if (bid < H) mixer_state_load(ssm_h, tid, sv);
-    ds_rows_load<G, TC>(rows, outc, outs, DI, cr0 + wave, cr1, src);
+    if (kd < 0) ds_rows_load<G, TC>(rows, outc, outs, DI, cr0 + wave, cr1, src);
 
     // ---- B: mixer step, one workgroup per head
     if (bid < H) {
@@ -390,13 +459,17 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
     {
       uint32_t xr[TC][8];
       ds_x_regs<TC>(xs, DI, xr);
-      ds_rows_all<G, TC>(rows, outc, outs, DI, cr1, xr, src,
-                         [&](int r, float y) { st_f32<true>(a.residual + r, y); });
+      auto put = [&](int r, float y) { st_f32<true>(a.residual + r, y); };
+      if (kd < 0)
+        ds_rows_all<G, TC>(rows, outc, outs, DI, cr1, xr, src, put);
+      else
+        ds_dense_rows<TC>(s.out_w16 + (int64_t)kd * D * DI, DI, cr0, cr1, xr, src, put);
     }
     if (bid == 0 && tid == 0) s.conv_pos[l] = (s.conv_pos[l] + 1) & 3;
     // the next block's in_proj rows during the barrier
     ds_arrive(bar_c);
-    if (l + 1 < s.n_layers)
+    kd = l + 1 < s.n_layers ? ds_kept(s, l + 1) : -1;
+    if (l + 1 < s.n_layers && kd < 0)
       ds_rows_load<G, TA>(rows, inc + (int64_t)Z * (D / 4), ins + (int64_t)Z * (D / G), D,
                           zr0 + wave, zr1, nullptr);
     ds_wait(bar_c, flag, (uint32_t)(l + 1) * (uint32_t)P);

@@ -127,6 +127,7 @@ hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* c
 // One batch-1 decode token through a stack of ternary Mamba-2 blocks in one
 // launch with grid barriers (headdim 64, d_state 128, d_conv 4); arrays per block
 // are stacked along a leading layer dimension.
+constexpr int kDecodeStackMaxKept = 64;
 struct DecodeStackDesc {
   int n_layers, d_model, nheads, g;
   float eps;
@@ -145,6 +146,12 @@ struct DecodeStackDesc {
   uint16_t* conv_state;       // [L, conv_dim, 4] float16 ring
   int* conv_pos;              // [L]
   uint16_t* ssm_state;        // [L, nheads, 64, 128] float16
+  // blocks kept in FP16: their indices (ascending), and their projections
+  // (those blocks' entries of the code arenas are not read)
+  int n_kept;
+  int kept[kDecodeStackMaxKept];
+  const uint16_t* in_w16;     // [n_kept, Z, d_model] float16
+  const uint16_t* out_w16;    // [n_kept, d_model, d_inner] float16
 };
 // [barrier words and timeout flag: kDecodeStackSyncBytes] zx [Z] gated
 // [d_inner] partial [nheads] residual [d_model], each piece 256-byte aligned

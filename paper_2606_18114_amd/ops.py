@@ -38,7 +38,9 @@ class Mamba2Stack(ctypes.Structure):
                 ("conv_b", ctypes.c_void_p), ("dt_bias", ctypes.c_void_p),
                 ("A_log", ctypes.c_void_p), ("D", ctypes.c_void_p), ("norm_w", ctypes.c_void_p),
                 ("final_w", ctypes.c_void_p), ("conv_state", ctypes.c_void_p),
-                ("conv_pos", ctypes.c_void_p), ("ssm_state", ctypes.c_void_p)]
+                ("conv_pos", ctypes.c_void_p), ("ssm_state", ctypes.c_void_p),
+                ("n_kept", ctypes.c_int32), ("kept", ctypes.POINTER(ctypes.c_int32)),
+                ("in_w16", ctypes.c_void_p), ("out_w16", ctypes.c_void_p)]
 
 
 SIGNATURES = {
@@ -657,11 +659,16 @@ def mamba2_decode_workspace(d_model: int, nheads: int, device) -> torch.Tensor:
 
 def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
                         x_out: Optional[torch.Tensor] = None,
-                        workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """One batch-1 decode token through a stack of ternary Mamba-2 blocks in a
-    single launch (``tm_mamba2_decode_token``).  arrays: the stacked device
-    tensors named as ``tm_mamba2_stack``'s fields (``STACK_FIELDS``); emb
-    float32 [d_model]; returns x_out bfloat16 [d_model] (the final norm)."""
+                        workspace: Optional[torch.Tensor] = None, kept=(),
+                        in_w16: Optional[torch.Tensor] = None,
+                        out_w16: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One batch-1 decode token through a stack of Mamba-2 blocks in a single
+    launch (``tm_mamba2_decode_token``).  arrays: the stacked device tensors
+    named as ``tm_mamba2_stack``'s fields (``STACK_FIELDS``); emb float32
+    [d_model]; returns x_out bfloat16 [d_model] (the final norm).  kept: the
+    indices (ascending) of blocks kept in FP16, whose projections are in_w16
+    float16 [len(kept), Z, d_model] and out_w16 [len(kept), d_model,
+    d_inner]."""
     P, N = MIXER_HEADDIM, MIXER_DSTATE
     L, Z, d4 = arrays["in_codes"].shape
     D = 4 * d4
@@ -692,7 +699,17 @@ def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
     _need(workspace, "workspace", _U8, 1)
     if workspace.device != dev:
         raise ValueError(f"workspace is on {workspace.device}, the operands on {dev}")
-    st = Mamba2Stack(L, D, H, g, eps, *(arrays[k].data_ptr() for k in STACK_FIELDS))
+    kept = [int(i) for i in kept]
+    nk = len(kept)
+    kept_arr = (ctypes.c_int32 * max(nk, 1))(*kept)
+    if nk:
+        _need(in_w16, "in_w16", _F16, 3)
+        _shape(in_w16, "in_w16", (nk, Z, D), dev)
+        _need(out_w16, "out_w16", _F16, 3)
+        _shape(out_w16, "out_w16", (nk, D, di), dev)
+    st = Mamba2Stack(L, D, H, g, eps, *(arrays[k].data_ptr() for k in STACK_FIELDS),
+                     nk, kept_arr if nk else None, _ptr(in_w16) if nk else None,
+                     _ptr(out_w16) if nk else None)
     rc = lib().tm_mamba2_decode_token(ctypes.byref(st), _ptr(emb), _ptr(x_out), _ptr(workspace),
                                       workspace.numel(), _stream())
     _check("tm_mamba2_decode_token", rc)

@@ -163,6 +163,9 @@ class DecodeStack:
 __all__ = ["keep_first_last", "quantize_projections", "DecodeStack", "PROJECTIONS"]
 
 
+MAX_KEPT_STACK = 64  # kept layers the one-launch decode takes
+
+
 def stack_fits(B: int, d_model: int, nheads: int, g: int) -> bool:
     """Whether tm_mamba2_decode_token takes this stack (its declaration's
     limits; nheads must also not exceed the device's CU count)."""
@@ -214,9 +217,9 @@ class Mamba2Decoder:
     float32 [d_model].  Layers in ``keep`` stay in float16 (Sec. 7).
     fused: None picks the fused form whenever every projection's shape
     allows it (batch up to 4 at g >= 128 for the Mamba-2 1.3B shapes).
-    stack: None picks the one-launch form whenever it applies (no kept
-    layers, batch 1, ``stack_fits``); it keeps the residual in its own
-    workspace (``residual`` is not updated).
+    stack: None picks the one-launch form whenever it applies (batch 1, at
+    most ``MAX_KEPT_STACK`` kept layers, ``stack_fits``); it keeps the
+    residual in its own workspace (``residual`` is not updated).
     The packed weights, mixer parameters and states of all layers live in
     layer-stacked arrays (``arena``); each layer's entries are views of them,
     so every form reads and advances the same states.
@@ -240,10 +243,10 @@ class Mamba2Decoder:
         if fused and not fits:
             raise ValueError(f"batch {batch} does not fit the fused decode at g = {g}")
         self.fused = fits if fused is None else bool(fused)
-        st_ok = stack_fits(batch, d_model, nheads, g) and not self.keep
+        st_ok = stack_fits(batch, d_model, nheads, g) and len(self.keep) <= MAX_KEPT_STACK
         if stack and not st_ok:
-            raise ValueError("the one-launch stack decode needs batch 1, no kept layers and "
-                             "shapes stack_fits accepts")
+            raise ValueError(f"the one-launch stack decode needs batch 1, at most "
+                             f"{MAX_KEPT_STACK} kept layers and shapes stack_fits accepts")
         self.stack = st_ok if stack is None else bool(stack)
         L, f32, f16 = n_layers, torch.float32, torch.float16
         ar = {"pre_w": torch.empty((L, d_model), dtype=f32, device=dev),
@@ -256,12 +259,17 @@ class Mamba2Decoder:
               "conv_state": torch.zeros((L, batch, conv_dim, 4), dtype=f16, device=dev),
               "conv_pos": torch.zeros((L,), dtype=torch.int32, device=dev),
               "ssm_state": torch.zeros((L, batch, nheads, P, N), dtype=f16, device=dev)}
-        if not self.keep:
-            ar["in_codes"] = torch.empty((L, self.Z, d_model // 4), dtype=torch.uint8, device=dev)
-            ar["in_scales"] = torch.empty((L, self.Z, d_model // g), dtype=f16, device=dev)
-            ar["out_codes"] = torch.empty((L, d_model, self.d_inner // 4), dtype=torch.uint8,
-                                          device=dev)
-            ar["out_scales"] = torch.empty((L, d_model, self.d_inner // g), dtype=f16, device=dev)
+        # packed weights of every layer (a kept layer's entries stay zero and
+        # unread), and the float16 projections of the kept layers, in order
+        ar["in_codes"] = torch.zeros((L, self.Z, d_model // 4), dtype=torch.uint8, device=dev)
+        ar["in_scales"] = torch.zeros((L, self.Z, d_model // g), dtype=f16, device=dev)
+        ar["out_codes"] = torch.zeros((L, d_model, self.d_inner // 4), dtype=torch.uint8,
+                                      device=dev)
+        ar["out_scales"] = torch.zeros((L, d_model, self.d_inner // g), dtype=f16, device=dev)
+        self.kept = sorted(self.keep)
+        nk = len(self.kept)
+        ar["in_w16"] = torch.empty((nk, self.Z, d_model), dtype=f16, device=dev)
+        ar["out_w16"] = torch.empty((nk, d_model, self.d_inner), dtype=f16, device=dev)
         self.arena = ar
         self.layers = []
         for l in range(n_layers):
@@ -271,14 +279,13 @@ class Mamba2Decoder:
                 if tuple(w.shape) != (n, k):
                     raise ValueError(f"layer {l} {kind}_proj has shape {tuple(w.shape)}")
                 if l in self.keep:
-                    lay[kind] = ("dense", w.to(torch.float16)[None].contiguous())
+                    d = self.kept.index(l)
+                    w16 = ar[f"{kind}_w16"][d:d + 1]
+                    w16.copy_(w.to(torch.float16)[None])
+                    lay[kind] = ("dense", w16)
                 else:
-                    if f"{kind}_codes" in ar:
-                        codes = ar[f"{kind}_codes"][l:l + 1]
-                        s16 = ar[f"{kind}_scales"][l:l + 1]
-                    else:
-                        codes = torch.empty((1, n, k // 4), dtype=torch.uint8, device=dev)
-                        s16 = torch.empty((1, n, k // g), dtype=torch.float16, device=dev)
+                    codes = ar[f"{kind}_codes"][l:l + 1]
+                    s16 = ar[f"{kind}_scales"][l:l + 1]
                     ops.ternarize_pack(w, g, eps, codes=codes[0], scales_f16=s16[0],
                                        want_zero_count=False)
                     lay[kind] = ("ternary", codes, s16)
@@ -361,7 +368,8 @@ class Mamba2Decoder:
         a["conv_state"] = a["conv_state"][:, 0]   # batch 1
         a["ssm_state"] = a["ssm_state"][:, 0]
         ops.mamba2_decode_token(a, self.g, self.eps, self.emb[0], x_out=self.x_out[0],
-                                workspace=self.stack_ws)
+                                workspace=self.stack_ws, kept=self.kept,
+                                in_w16=self.arena["in_w16"], out_w16=self.arena["out_w16"])
         return self.x_out
 
     def token(self) -> torch.Tensor:

@@ -47,7 +47,7 @@ def test_exports_every_declared_symbol(L):
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 13
+    assert L.tm_abi_version() == 14
 
 
 def test_status_strings(L):
@@ -415,8 +415,16 @@ def stack_desc(**kw):
     vals.update({k: v for k, v in kw.items() if k in names})
     dims = dict(n_layers=2, d_model=256, nheads=2, g=128, eps=1e-5)
     dims.update({k: v for k, v in kw.items() if k in dims})
-    return ops.Mamba2Stack(dims["n_layers"], dims["d_model"], dims["nheads"], dims["g"],
-                           dims["eps"], *(vals[n] for n in names))
+    st = ops.Mamba2Stack(dims["n_layers"], dims["d_model"], dims["nheads"], dims["g"],
+                         dims["eps"], *(vals[n] for n in names))
+    if "kept" in kw:  # host list of kept blocks; their float16 arrays after the others
+        kept = kw["kept"]
+        st.n_kept = kw.get("n_kept", len(kept))
+        st._kept_keepalive = (ctypes.c_int32 * max(len(kept), 1))(*kept)
+        st.kept = ctypes.cast(st._kept_keepalive, ctypes.POINTER(ctypes.c_int32)) if kept else None
+        st.in_w16 = kw.get("in_w16", P + 20 * 2 ** 26)
+        st.out_w16 = kw.get("out_w16", P + 21 * 2 ** 26)
+    return st
 
 
 def mdec(L, emb=P + 2 ** 31, x_out=P + 2 ** 31 + 2 ** 20, ws=P + 2 ** 32, wsb=None, **kw):
@@ -454,6 +462,16 @@ def test_mamba2_decode_token_validation(L):
     assert mdec(L, ssm_state=P + 1 * 2 ** 26) == EINVAL
     assert mdec(L, x_out=P + 2 ** 32) == EINVAL
     assert mdec(L, conv_pos=P + 13 * 2 ** 26 + 64) == EINVAL   # inside the conv ring
+    # blocks kept in FP16: a host list, ascending, below n_layers, at most 64
+    assert mdec(L, kept=[0], n_layers=3, wsb=1024) == ESHAPE    # still checks the rest
+    assert mdec(L, kept=[2], n_layers=2) == ESHAPE               # past the last block
+    assert mdec(L, kept=[1, 0], n_layers=3) == ESHAPE            # not ascending
+    assert mdec(L, kept=[1, 1], n_layers=3) == ESHAPE            # repeated
+    assert mdec(L, kept=[0], n_kept=65, n_layers=3) == ESHAPE
+    assert mdec(L, kept=[], n_kept=1, n_layers=3) == EINVAL      # no list
+    assert mdec(L, kept=[0], n_layers=3, in_w16=0) == EINVAL
+    assert mdec(L, kept=[0], n_layers=3, out_w16=P + 21 * 2 ** 26 + 8) == EALIGN
+    assert mdec(L, kept=[0], n_layers=3, ssm_state=P + 20 * 2 ** 26) == EINVAL  # over in_w16
 
 
 def dx16(L, dY=P, codes=P + 2 ** 24, scales=P + 2 ** 25, M=16, N=256, K=512, g=128,
