@@ -290,7 +290,9 @@ def main():
                       dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2)),
                   "first_last_2_fp16_one_launch": decode_mamba2_blocks(
                       dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2), stack=True),
-                  "all_ternary_B4": decode_mamba2_blocks(dev, args.steps, batch=4)}
+                  "all_ternary_B4": decode_mamba2_blocks(dev, args.steps, batch=4),
+                  "all_ternary_B4_one_launch": decode_mamba2_blocks(dev, args.steps, batch=4,
+                                                                    stack=True)}
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)
@@ -814,9 +816,10 @@ def decode_mamba2_blocks(dev, tokens, keep=(), batch=1, fused=True, stack=False)
            "us_per_token_graph": None if us_graph is None else round(us_graph, 2),
            "GBps_best": round(nb / (best * 1e-6) / 1e9, 1),
            "frac_hbm_best": round(nb / (best * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+           "tokens_per_s_best": round(batch / (best * 1e-6), 1),
            "what": "48 Mamba-2 1.3B blocks in layer order (pre-norm, in_proj 8512x2048, "
                    "conv + FP16 SSM state + gated RMSNorm, out_proj 2048x4096) + final norm, "
-                   "one token, states carried over"}
+                   "one token per batch row, states carried over"}
     del dec
     torch.cuda.empty_cache()
     return res

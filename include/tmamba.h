@@ -61,7 +61,7 @@ typedef enum {
 
 typedef struct ihipStream_t* tm_stream; /* the same type as hipStream_t */
 
-#define TM_ABI_VERSION 14
+#define TM_ABI_VERSION 15
 
 /* ABI version of the loaded library (TM_ABI_VERSION it was built with). */
 int tm_abi_version(void);
@@ -427,13 +427,16 @@ tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
 
 /*
  * A stack of ternary Mamba-2 blocks for whole-stack decoding (Sec. 8:
- * batch-1 decoding, bound by the weight traffic; Sec. 3.2: the mixer and
- * its states stay in FP16).  Every array is device memory, stacked along a
- * leading layer dimension L = n_layers; d_inner = 64 nheads, d_state 128,
+ * small-batch decoding, bound by the weight traffic; Sec. 3.2: the mixer
+ * and its states stay in FP16).  Every array is device memory, stacked along
+ * a leading layer dimension L = n_layers; d_inner = 64 nheads, d_state 128,
  * d_conv 4, Z = 2 d_inner + 256 + nheads, conv_dim = d_inner + 256.
  *   n_layers >= 1; d_model and d_inner multiples of g and of 64, at most 4096
  *   and 8192 (the workgroup's x pairs); g in {64, 128, 256}; 1 <= nheads <= the
  *   device's CU count; eps: RMSNorm epsilon (finite, >= 0)
+ *   batch      1 .. 4 tokens decoded together (one per batch row); above 1,
+ *              d_model <= 2048, d_inner <= 4096 and nheads * batch <= the
+ *              device's CU count
  *   in_codes   uint8 [L, Z, d_model/4]        in_scales  fp16 [L, Z, d_model/g]
  *   out_codes  uint8 [L, d_model, d_inner/4]  out_scales fp16 [L, d_model, d_inner/g]
  *   pre_w      float32 [L, d_model]   the block's pre-norm weight
@@ -441,9 +444,10 @@ tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
  *   dt_bias, A_log, D  float32 [L, nheads]
  *   norm_w     float32 [L, d_inner]   the gated RMSNorm's weight
  *   final_w    float32 [d_model]      the final norm's weight
- *   conv_state fp16 [L, conv_dim, 4] (8-byte aligned), conv_pos int32 [L],
- *   ssm_state  fp16 [L, nheads, 64, 128] (16-byte aligned): the decode state,
- *              in and out, as for tm_mixer_step with B = 1
+ *   conv_state fp16 [L, batch, conv_dim, 4] (8-byte aligned), conv_pos int32
+ *              [L] (one ring position for every batch row),
+ *   ssm_state  fp16 [L, batch, nheads, 64, 128] (16-byte aligned): the decode
+ *              state, in and out, as for tm_mixer_step with B = batch
  * Codes, pre_w, norm_w and final_w 16-byte aligned, scales 2-byte, the other
  * float arrays 4-byte.
  * Blocks kept in FP16 (Sec. 7, layer-selective quantization), optional:
@@ -477,11 +481,12 @@ typedef struct {
   const int32_t* kept;
   const uint16_t* in_w16;
   const uint16_t* out_w16;
+  int32_t batch;
 } tm_mamba2_stack;
 
 /*
- * tm_mamba2_decode_token — one batch-1 decode token through every block of
- * the stack in a single launch: per block, in layer order,
+ * tm_mamba2_decode_token — one decode token per batch row through every
+ * block of the stack in a single launch: per block, in layer order,
  *   zx        = in_proj(bf16(rmsnorm(residual) * pre_w))        (tm_tgemv_rms)
  *   g         = conv + FP16 SSM step + y * SiLU(z)               (tm_mixer_gate)
  *   residual += out_proj(bf16(rmsnorm(g) * norm_w))             (tm_tgemv_rms)
@@ -491,18 +496,20 @@ typedef struct {
  * (tm_dgemv_rms: each float16 weight times the float32 value of the
  * bfloat16 x, float32 sums).
  *   stack      host pointer to the description above (read during the call)
- *   emb        float32 [d_model] in;  x_out  bf16 [d_model] out (2-byte aligned)
- *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads)
- *              bytes, 256-byte aligned, owned by the caller; nothing need be
+ *   emb        float32 [batch, d_model] in (16-byte aligned);  x_out  bf16
+ *              [batch, d_model] out (4-byte aligned: stored in pairs)
+ *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads,
+ *              batch) bytes, 256-byte aligned, owned by the caller; nothing need be
  *              set before the call.  Its uint32 word 768 is nonzero after a
  *              call whose grid barrier gave up waiting; the outputs and
  *              states of such a call are not valid.
  * One workgroup per CU; the blocks' phases are separated by grid barriers
  * (three per block) instead of kernel launches, so every workgroup must be
- * resident at once.  A CU holds several of them, so on an otherwise idle GPU
- * they all start together; other kernels running at the same time (other
- * streams or processes) can delay some, and a barrier waits for them for
- * tens of milliseconds before it gives up and sets the flag above.
+ * resident at once: on an otherwise idle GPU each CU takes one and they all
+ * start together; other kernels running at the same time (other streams or
+ * processes) can delay some, and a barrier waits for them for tens of
+ * milliseconds before it gives up and sets the flag above.  The mixer step
+ * takes one workgroup per head and batch row.
  * The ternary products take the bfloat16 x against the codes (exact
  * products, float32 sums, float16 group scale in float32), so they agree
  * with tm_tgemv_rms to float32 rounding; the normalizations sum in a
@@ -514,7 +521,7 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* stack, const float* emb,
                                  tm_stream stream);
 
 /* Workspace bytes of tm_mamba2_decode_token (-1 for sizes out of range). */
-int64_t tm_mamba2_decode_workspace(int32_t d_model, int32_t nheads);
+int64_t tm_mamba2_decode_workspace(int32_t d_model, int32_t nheads, int32_t batch);
 
 /*
  * Scale-parameterization variants (paper appendix, Decoupled Quantization

@@ -512,9 +512,11 @@ tm_status tm_mixer_gate(const float* zxbcdt, int32_t B, int32_t nheads, int32_t 
                                            to_hip(stream)));
 }
 
-int64_t tm_mamba2_decode_workspace(int32_t d_model, int32_t nheads) {
-  if (d_model < 1 || d_model > 4096 || nheads < 1 || nheads > 128) return -1;
-  return tmk::decode_stack_workspace_bytes(d_model, nheads);
+int64_t tm_mamba2_decode_workspace(int32_t d_model, int32_t nheads, int32_t batch) {
+  if (d_model < 1 || d_model > 4096 || nheads < 1 || nheads > 128 || batch < 1 ||
+      batch > tmk::kDecodeStackMaxBatch)
+    return -1;
+  return tmk::decode_stack_workspace_bytes(d_model, nheads, batch);
 }
 
 tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, uint16_t* x_out,
@@ -528,25 +530,28 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
   if (!(s.eps >= 0.0f) || !std::isfinite(s.eps)) return TM_EINVAL;
   if (s.g != 64 && s.g != 128 && s.g != 256) return TM_ESHAPE;
   if (s.n_layers < 1 || s.n_layers > 65535 || s.nheads < 1 || s.nheads > 128) return TM_ESHAPE;
-  const int64_t L = s.n_layers, Dm = s.d_model, H = s.nheads, DI = 64 * H;
+  const int64_t L = s.n_layers, Dm = s.d_model, H = s.nheads, DI = 64 * H, B = s.batch;
   if (Dm < 64 || Dm > 4096 || Dm % 64 != 0 || Dm % s.g != 0 || DI % s.g != 0) return TM_ESHAPE;
-  if (H > tmk::current_cu_count()) return TM_ESHAPE;  // one workgroup per head
+  if (B < 1 || B > tmk::kDecodeStackMaxBatch || (B > 1 && (Dm > 2048 || DI > 4096)))
+    return TM_ESHAPE;
+  // one workgroup per head and batch row
+  if (H * B > tmk::current_cu_count()) return TM_ESHAPE;
   const int64_t Z = 2 * DI + 256 + H, CD = DI + 256;
   int64_t icb, isb, ocb, osb, csb, ssb;
   if (!bytes_of(L * Z, Dm / 4, 1, &icb) || !bytes_of(L * Z, Dm / s.g, 2, &isb) ||
       !bytes_of(L * Dm, DI / 4, 1, &ocb) || !bytes_of(L * Dm, DI / s.g, 2, &osb) ||
-      !bytes_of(L * CD, 4, 2, &csb) || !bytes_of(L * H * 64, 128, 2, &ssb))
+      !bytes_of(L * B * CD, 4, 2, &csb) || !bytes_of(L * B * H * 64, 128, 2, &ssb))
     return TM_ESHAPE;
   if (Z * (Dm / 4) > (int64_t(1) << 31) || Dm * (DI / 4) > (int64_t(1) << 31))
     return TM_ESHAPE;  // 32-bit offsets inside one matrix
-  const int64_t need = tmk::decode_stack_workspace_bytes((int)Dm, (int)H);
+  const int64_t need = tmk::decode_stack_workspace_bytes((int)Dm, (int)H, (int)B);
   if (workspace_bytes < need) return TM_ESHAPE;
   if (!aligned(s.in_codes, 16) || !aligned(s.out_codes, 16) || !aligned(s.in_scales, 2) ||
       !aligned(s.out_scales, 2) || !aligned(s.pre_w, 16) || !aligned(s.conv_w, 4) ||
       !aligned(s.conv_b, 4) || !aligned(s.dt_bias, 4) || !aligned(s.A_log, 4) ||
       !aligned(s.D, 4) || !aligned(s.norm_w, 16) || !aligned(s.final_w, 16) ||
       !aligned(s.conv_state, 8) || !aligned(s.conv_pos, 4) || !aligned(s.ssm_state, 16) ||
-      !aligned(emb, 4) || !aligned(x_out, 2) || !aligned(workspace, 256))
+      !aligned(emb, 16) || !aligned(x_out, 4) || !aligned(workspace, 256))
     return TM_EALIGN;
   // blocks kept in FP16
   if (s.n_kept < 0 || s.n_kept > tmk::kDecodeStackMaxKept) return TM_ESHAPE;
@@ -562,13 +567,13 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
     if (!aligned(s.in_w16, 16) || !aligned(s.out_w16, 16)) return TM_EALIGN;
   }
   const Span outs[5] = {span(s.conv_state, csb), span(s.conv_pos, L * 4), span(s.ssm_state, ssb),
-                        span(x_out, Dm * 2), span(workspace, need)};
+                        span(x_out, B * Dm * 2), span(workspace, need)};
   const Span ins[13] = {span(s.in_codes, icb), span(s.in_scales, isb), span(s.out_codes, ocb),
                         span(s.out_scales, osb), span(s.pre_w, L * Dm * 4),
                         span(s.conv_w, L * CD * 16), span(s.conv_b, L * CD * 4),
                         span(s.dt_bias, L * H * 4), span(s.A_log, L * H * 4),
                         span(s.D, L * H * 4), span(s.norm_w, L * DI * 4),
-                        span(s.final_w, Dm * 4), span(emb, Dm * 4)};
+                        span(s.final_w, Dm * 4), span(emb, B * Dm * 4)};
   for (int i = 0; i < 5; ++i) {
     for (int j = i + 1; j < 5; ++j)
       if (overlap(outs[i], outs[j])) return TM_EINVAL;
@@ -583,6 +588,7 @@ tm_status tm_mamba2_decode_token(const tm_mamba2_stack* st, const float* emb, ui
   d.d_model = s.d_model;
   d.nheads = s.nheads;
   d.g = s.g;
+  d.batch = s.batch;
   d.eps = s.eps;
   d.in_codes = s.in_codes;
   d.in_s16 = s.in_scales;

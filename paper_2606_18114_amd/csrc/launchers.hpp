@@ -124,12 +124,13 @@ hipError_t launch_mixer_gate(const float* zxbcdt, int B, int nheads, uint16_t* c
                              const float* conv_b, const float* dt_bias, const float* A_log,
                              const float* D, float* gated, hipStream_t stream);
 
-// One batch-1 decode token through a stack of ternary Mamba-2 blocks in one
-// launch with grid barriers (headdim 64, d_state 128, d_conv 4); arrays per block
-// are stacked along a leading layer dimension.
+// One decode token per batch row (batch 1 .. 4) through a stack of ternary
+// Mamba-2 blocks in one launch with grid barriers (headdim 64, d_state 128,
+// d_conv 4); arrays per block are stacked along a leading layer dimension.
 constexpr int kDecodeStackMaxKept = 64;
+constexpr int kDecodeStackMaxBatch = 4;
 struct DecodeStackDesc {
-  int n_layers, d_model, nheads, g;
+  int n_layers, d_model, nheads, g, batch;
   float eps;
   const uint8_t* in_codes;    // [L, Z, d_model / 4], Z = 2 d_inner + 256 + nheads
   const uint16_t* in_s16;     // [L, Z, d_model / g]
@@ -143,9 +144,9 @@ struct DecodeStackDesc {
   const float* D;             // [L, nheads]
   const float* norm_w;        // [L, d_inner]
   const float* final_w;       // [d_model]
-  uint16_t* conv_state;       // [L, conv_dim, 4] float16 ring
-  int* conv_pos;              // [L]
-  uint16_t* ssm_state;        // [L, nheads, 64, 128] float16
+  uint16_t* conv_state;       // [L, batch, conv_dim, 4] float16 ring
+  int* conv_pos;              // [L] (one position for every batch row)
+  uint16_t* ssm_state;        // [L, batch, nheads, 64, 128] float16
   // blocks kept in FP16: their indices (ascending), and their projections
   // (those blocks' entries of the code arenas are not read)
   int n_kept;
@@ -153,14 +154,15 @@ struct DecodeStackDesc {
   const uint16_t* in_w16;     // [n_kept, Z, d_model] float16
   const uint16_t* out_w16;    // [n_kept, d_model, d_inner] float16
 };
-// [barrier words and timeout flag: kDecodeStackSyncBytes] zx [Z] gated
-// [d_inner] partial [nheads] residual [d_model], each piece 256-byte aligned
+// [barrier words and timeout flag: kDecodeStackSyncBytes] zx [batch, Z]
+// gated [batch, d_inner] partial [batch, nheads] residual [batch, d_model],
+// each piece 256-byte aligned
 constexpr int kDecodeStackSyncBytes = 4096;
-inline int64_t decode_stack_workspace_bytes(int d_model, int nheads) {
+inline int64_t decode_stack_workspace_bytes(int d_model, int nheads, int batch) {
   auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
-  const int64_t di = 64 * (int64_t)nheads, z = 2 * di + 256 + nheads;
-  return kDecodeStackSyncBytes + up(z * 4) + up(di * 4) + up((int64_t)nheads * 4) +
-         up((int64_t)d_model * 4);
+  const int64_t b = batch, di = 64 * (int64_t)nheads, z = 2 * di + 256 + nheads;
+  return kDecodeStackSyncBytes + up(b * z * 4) + up(b * di * 4) + up(b * nheads * 4) +
+         up(b * d_model * 4);
 }
 hipError_t launch_decode_stack(const DecodeStackDesc& s, const float* emb, uint16_t* x_out,
                                void* workspace, hipStream_t stream);

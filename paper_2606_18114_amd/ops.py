@@ -40,7 +40,8 @@ class Mamba2Stack(ctypes.Structure):
                 ("final_w", ctypes.c_void_p), ("conv_state", ctypes.c_void_p),
                 ("conv_pos", ctypes.c_void_p), ("ssm_state", ctypes.c_void_p),
                 ("n_kept", ctypes.c_int32), ("kept", ctypes.POINTER(ctypes.c_int32)),
-                ("in_w16", ctypes.c_void_p), ("out_w16", ctypes.c_void_p)]
+                ("in_w16", ctypes.c_void_p), ("out_w16", ctypes.c_void_p),
+                ("batch", ctypes.c_int32)]
 
 
 SIGNATURES = {
@@ -77,7 +78,7 @@ SIGNATURES = {
     "tm_mixer_gate": (ctypes.c_int, [_P, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P]),
     "tm_mamba2_decode_token": (ctypes.c_int, [ctypes.POINTER(Mamba2Stack), _P, _P, _P, _I64, _P]),
-    "tm_mamba2_decode_workspace": (ctypes.c_int64, [_I32, _I32]),
+    "tm_mamba2_decode_workspace": (ctypes.c_int64, [_I32, _I32, _I32]),
 }
 
 
@@ -649,11 +650,12 @@ STACK_FIELDS = ("in_codes", "in_scales", "out_codes", "out_scales", "pre_w", "co
                 "ssm_state")
 
 
-def mamba2_decode_workspace(d_model: int, nheads: int, device) -> torch.Tensor:
+def mamba2_decode_workspace(d_model: int, nheads: int, device, batch: int = 1) -> torch.Tensor:
     """Scratch for mamba2_decode_token (uint8)."""
-    n = int(lib().tm_mamba2_decode_workspace(d_model, nheads))
+    n = int(lib().tm_mamba2_decode_workspace(d_model, nheads, batch))
     if n < 0:
-        raise ValueError(f"no stack decode for d_model={d_model}, nheads={nheads}")
+        raise ValueError(f"no stack decode for d_model={d_model}, nheads={nheads}, "
+                         f"batch={batch}")
     return torch.empty((n,), dtype=torch.uint8, device=device)
 
 
@@ -662,10 +664,12 @@ def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
                         workspace: Optional[torch.Tensor] = None, kept=(),
                         in_w16: Optional[torch.Tensor] = None,
                         out_w16: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """One batch-1 decode token through a stack of Mamba-2 blocks in a single
-    launch (``tm_mamba2_decode_token``).  arrays: the stacked device tensors
-    named as ``tm_mamba2_stack``'s fields (``STACK_FIELDS``); emb float32
-    [d_model]; returns x_out bfloat16 [d_model] (the final norm).  kept: the
+    """One decode token per batch row through a stack of Mamba-2 blocks in a
+    single launch (``tm_mamba2_decode_token``).  arrays: the stacked device
+    tensors named as ``tm_mamba2_stack``'s fields (``STACK_FIELDS``).  emb
+    float32 [d_model] (batch 1; the states then [L, conv_dim, 4] and [L,
+    nheads, 64, 128]) or [B, d_model] with B = 1 .. 4 (the states [L, B,
+    ...]); returns x_out bfloat16 of emb's shape (the final norm).  kept: the
     indices (ascending) of blocks kept in FP16, whose projections are in_w16
     float16 [len(kept), Z, d_model] and out_w16 [len(kept), d_model,
     d_inner]."""
@@ -675,27 +679,32 @@ def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
     H = arrays["dt_bias"].shape[1]
     di, cd = H * P, H * P + 2 * N
     dev = emb.device
+    if emb.dim() not in (1, 2):
+        raise ValueError(f"emb must be [d_model] or [B, d_model], got {tuple(emb.shape)}")
+    B = 1 if emb.dim() == 1 else emb.shape[0]
+    lead = (L,) if emb.dim() == 1 else (L, B)
     want = {"in_codes": ((L, Z, D // 4), _U8), "in_scales": ((L, Z, _groups(D, g)), _F16),
             "out_codes": ((L, D, di // 4), _U8), "out_scales": ((L, D, _groups(di, g)), _F16),
             "pre_w": ((L, D), _F32), "conv_w": ((L, cd, 4), _F32), "conv_b": ((L, cd), _F32),
             "dt_bias": ((L, H), _F32), "A_log": ((L, H), _F32), "D": ((L, H), _F32),
             "norm_w": ((L, di), _F32), "final_w": ((D,), _F32),
-            "conv_state": ((L, cd, 4), _F16), "conv_pos": ((L,), (torch.int32,)),
-            "ssm_state": ((L, H, P, N), _F16)}
+            "conv_state": (lead + (cd, 4), _F16), "conv_pos": ((L,), (torch.int32,)),
+            "ssm_state": (lead + (H, P, N), _F16)}
     if Z != 2 * di + 2 * N + H:
         raise ValueError(f"in_codes has {Z} rows; nheads={H} needs {2 * di + 2 * N + H}")
     for name, (shape, dtypes) in want.items():
         t = arrays[name]
         _need(t, name, dtypes, len(shape))
         _shape(t, name, shape, dev)
-    _need(emb, "emb", _F32, 1)
-    _shape(emb, "emb", (D,), dev)
+    shp = tuple(emb.shape[:-1]) + (D,)
+    _need(emb, "emb", _F32, emb.dim())
+    _shape(emb, "emb", shp, dev)
     if x_out is None:
-        x_out = torch.empty((D,), dtype=torch.bfloat16, device=dev)
-    _need(x_out, "x_out", _BF16, 1)
-    _shape(x_out, "x_out", (D,), dev)
+        x_out = torch.empty(shp, dtype=torch.bfloat16, device=dev)
+    _need(x_out, "x_out", _BF16, emb.dim())
+    _shape(x_out, "x_out", shp, dev)
     if workspace is None:
-        workspace = mamba2_decode_workspace(D, H, dev)
+        workspace = mamba2_decode_workspace(D, H, dev, B)
     _need(workspace, "workspace", _U8, 1)
     if workspace.device != dev:
         raise ValueError(f"workspace is on {workspace.device}, the operands on {dev}")
@@ -709,7 +718,7 @@ def mamba2_decode_token(arrays: dict, g: int, eps: float, emb: torch.Tensor,
         _shape(out_w16, "out_w16", (nk, D, di), dev)
     st = Mamba2Stack(L, D, H, g, eps, *(arrays[k].data_ptr() for k in STACK_FIELDS),
                      nk, kept_arr if nk else None, _ptr(in_w16) if nk else None,
-                     _ptr(out_w16) if nk else None)
+                     _ptr(out_w16) if nk else None, B)
     rc = lib().tm_mamba2_decode_token(ctypes.byref(st), _ptr(emb), _ptr(x_out), _ptr(workspace),
                                       workspace.numel(), _stream())
     _check("tm_mamba2_decode_token", rc)

@@ -170,10 +170,11 @@ def stack_fits(B: int, d_model: int, nheads: int, g: int) -> bool:
     """Whether tm_mamba2_decode_token takes this stack (its declaration's
     limits; nheads must also not exceed the device's CU count)."""
     d_inner = nheads * ops.MIXER_HEADDIM
-    shapes = (B == 1 and g in (64, 128, 256) and 64 <= d_model <= 4096 and d_model % 64 == 0
-              and d_model % g == 0 and d_inner % g == 0 and 1 <= nheads <= 128)
+    shapes = (1 <= B <= 4 and g in (64, 128, 256) and 64 <= d_model <= 4096
+              and d_model % 64 == 0 and d_model % g == 0 and d_inner % g == 0
+              and 1 <= nheads <= 128 and (B == 1 or (d_model <= 2048 and d_inner <= 4096)))
     return (shapes and torch.cuda.is_available()
-            and nheads <= torch.cuda.get_device_properties(
+            and nheads * B <= torch.cuda.get_device_properties(
                 torch.cuda.current_device()).multi_processor_count)
 
 
@@ -207,9 +208,9 @@ class Mamba2Decoder:
     buffers, so a token can be captured once as a HIP graph (``capture``) and
     replayed.
 
-    or, with every block ternary and batch 1, the whole stack in one launch
-    (``tm_mamba2_decode_token``: the three phases of every block separated
-    by grid barriers instead of launches).
+    or the whole stack in one launch (``tm_mamba2_decode_token``: the three
+    phases of every block separated by grid barriers instead of launches;
+    batch 1 .. 4, kept blocks included).
 
     weight(kind, l) -> float32 [N, K] master weights (kind "in": [Z, d_model],
     "out": [d_model, d_inner]); mixer(l) -> dict of float32 arrays conv_w,
@@ -217,9 +218,9 @@ class Mamba2Decoder:
     float32 [d_model].  Layers in ``keep`` stay in float16 (Sec. 7).
     fused: None picks the fused form whenever every projection's shape
     allows it (batch up to 4 at g >= 128 for the Mamba-2 1.3B shapes).
-    stack: None picks the one-launch form whenever it applies (batch 1, at
-    most ``MAX_KEPT_STACK`` kept layers, ``stack_fits``); it keeps the
-    residual in its own workspace (``residual`` is not updated).
+    stack: None picks the one-launch form whenever it applies (at most
+    ``MAX_KEPT_STACK`` kept layers, ``stack_fits``); it keeps the residual in
+    its own workspace (``residual`` is not updated).
     The packed weights, mixer parameters and states of all layers live in
     layer-stacked arrays (``arena``); each layer's entries are views of them,
     so every form reads and advances the same states.
@@ -245,8 +246,8 @@ class Mamba2Decoder:
         self.fused = fits if fused is None else bool(fused)
         st_ok = stack_fits(batch, d_model, nheads, g) and len(self.keep) <= MAX_KEPT_STACK
         if stack and not st_ok:
-            raise ValueError(f"the one-launch stack decode needs batch 1, at most "
-                             f"{MAX_KEPT_STACK} kept layers and shapes stack_fits accepts")
+            raise ValueError(f"the one-launch stack decode needs at most {MAX_KEPT_STACK} "
+                             f"kept layers and shapes stack_fits accepts")
         self.stack = st_ok if stack is None else bool(stack)
         L, f32, f16 = n_layers, torch.float32, torch.float16
         ar = {"pre_w": torch.empty((L, d_model), dtype=f32, device=dev),
@@ -313,7 +314,8 @@ class Mamba2Decoder:
         self.ws = ops.mixer_workspace(batch, nheads, dev)
         self.x_out = torch.empty((batch, d_model), dtype=torch.bfloat16, device=dev)
         self.arena["final_w"] = self.final_norm
-        self.stack_ws = ops.mamba2_decode_workspace(d_model, nheads, dev) if self.stack else None
+        self.stack_ws = (ops.mamba2_decode_workspace(d_model, nheads, dev, batch)
+                         if self.stack else None)
         self.graph = None
 
     def set_states(self, l: int, conv: torch.Tensor, ssm: torch.Tensor, pos: int = 0) -> None:
@@ -363,11 +365,9 @@ class Mamba2Decoder:
         self._proj(lay, "out", self.m, self.y)
 
     def token_stack(self) -> torch.Tensor:
-        """One token through every block in a single launch."""
+        """One token per batch row through every block in a single launch."""
         a = {k: self.arena[k] for k in ops.STACK_FIELDS}
-        a["conv_state"] = a["conv_state"][:, 0]   # batch 1
-        a["ssm_state"] = a["ssm_state"][:, 0]
-        ops.mamba2_decode_token(a, self.g, self.eps, self.emb[0], x_out=self.x_out[0],
+        ops.mamba2_decode_token(a, self.g, self.eps, self.emb, x_out=self.x_out,
                                 workspace=self.stack_ws, kept=self.kept,
                                 in_w16=self.arena["in_w16"], out_w16=self.arena["out_w16"])
         return self.x_out

@@ -47,7 +47,7 @@ def test_exports_every_declared_symbol(L):
     for n in names:
         assert hasattr(L, n), n
         assert n in ops.SIGNATURES, n
-    assert L.tm_abi_version() == 14
+    assert L.tm_abi_version() == 15
 
 
 def test_status_strings(L):
@@ -417,6 +417,7 @@ def stack_desc(**kw):
     dims.update({k: v for k, v in kw.items() if k in dims})
     st = ops.Mamba2Stack(dims["n_layers"], dims["d_model"], dims["nheads"], dims["g"],
                          dims["eps"], *(vals[n] for n in names))
+    st.batch = kw.get("batch", 1)
     if "kept" in kw:  # host list of kept blocks; their float16 arrays after the others
         kept = kw["kept"]
         st.n_kept = kw.get("n_kept", len(kept))
@@ -430,16 +431,21 @@ def stack_desc(**kw):
 def mdec(L, emb=P + 2 ** 31, x_out=P + 2 ** 31 + 2 ** 20, ws=P + 2 ** 32, wsb=None, **kw):
     st = stack_desc(**kw)
     if wsb is None:
-        wsb = L.tm_mamba2_decode_workspace(st.d_model, st.nheads)
+        wsb = L.tm_mamba2_decode_workspace(st.d_model, st.nheads, max(st.batch, 1))
     return L.tm_mamba2_decode_token(ctypes.byref(st), emb, x_out, ws, wsb, None)
 
 
 def test_mamba2_decode_token_validation(L):
     # [barrier words 4 KiB | zx Z | gated | partial | residual], 256-byte pieces
     z = 2 * 128 + 256 + 2
-    assert L.tm_mamba2_decode_workspace(256, 2) == 4096 + 2304 + 512 + 256 + 1024 and z == 514
-    assert L.tm_mamba2_decode_workspace(8192, 2) == -1
-    assert L.tm_mamba2_decode_workspace(256, 0) == -1
+    ws = L.tm_mamba2_decode_workspace
+    assert ws(256, 2, 1) == 4096 + 2304 + 512 + 256 + 1024 and z == 514
+    # batch 3: every piece three rows
+    assert ws(256, 2, 3) == 4096 + 6400 + 1536 + 256 + 3072
+    assert ws(8192, 2, 1) == -1
+    assert ws(256, 0, 1) == -1
+    assert ws(256, 2, 0) == -1
+    assert ws(256, 2, 5) == -1
     assert L.tm_mamba2_decode_token(None, P, P, P, 1 << 20, None) == EINVAL
     for name in ops.STACK_FIELDS:
         assert mdec(L, **{name: 0}) == EINVAL, name
@@ -457,7 +463,16 @@ def test_mamba2_decode_token_validation(L):
     assert mdec(L, ssm_state=P + 15 * 2 ** 26 + 8) == EALIGN
     assert mdec(L, conv_state=P + 13 * 2 ** 26 + 4) == EALIGN
     assert mdec(L, x_out=P + 2 ** 31 + 1) == EALIGN
+    assert mdec(L, x_out=P + 2 ** 31 + 2) == EALIGN           # stored in bfloat16 pairs
     assert mdec(L, norm_w=P + 11 * 2 ** 26 + 4) == EALIGN   # the norm weights load 16 bytes
+    assert mdec(L, emb=P + 2 ** 31 + 4) == EALIGN           # so does the embedding
+    # batches: 1 .. 4 rows, up to d_model 2048 / d_inner 4096 above 1
+    assert mdec(L, batch=0, wsb=1 << 20) == ESHAPE
+    assert mdec(L, batch=5, wsb=1 << 20) == ESHAPE
+    assert mdec(L, batch=2, d_model=4096) == ESHAPE
+    assert mdec(L, batch=2, nheads=66) == ESHAPE            # d_inner 4224
+    assert mdec(L, batch=2, wsb=ws(256, 2, 1)) == ESHAPE
+    assert mdec(L, batch=2, x_out=P + 2 ** 32 - 512) == EINVAL   # second row over the workspace
     # a state array over a weight array, the output over the workspace
     assert mdec(L, ssm_state=P + 1 * 2 ** 26) == EINVAL
     assert mdec(L, x_out=P + 2 ** 32) == EINVAL

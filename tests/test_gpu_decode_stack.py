@@ -1,8 +1,8 @@
 """GPU parity of the one-launch stack decode (tm_mamba2_decode_token): a
-batch-1 token through every ternary Mamba-2 block with grid barriers between
-the phases, against the oracle's own decode (oracle ternarization, float16
-states carried by each side), and against the layer-by-layer fused decode on
-the same states.
+token per batch row (batch 1 .. 4) through every Mamba-2 block with grid
+barriers between the phases, against the oracle's own decode (oracle
+ternarization, float16 states carried by each side), and against the
+layer-by-layer fused decode on the same states.
 
 Bars as for the layer-by-layer decoder: the two sides round the activations
 handed to a projection to bfloat16 from float32 and float64 values (and the
@@ -31,7 +31,7 @@ def gpu():
     ops.lib()
 
 
-def _decoder(seed, L, d_model, H, g=128, stack=None, outliers=True, keep=()):
+def _decoder(seed, L, d_model, H, g=128, stack=None, outliers=True, keep=(), batch=1):
     from paper_2606_18114_amd.stack import Mamba2Decoder
     rng = np.random.default_rng(seed)
     Z = 2 * 64 * H + 256 + H
@@ -41,10 +41,10 @@ def _decoder(seed, L, d_model, H, g=128, stack=None, outliers=True, keep=()):
     pre = [(1 + 0.1 * rng.standard_normal(d_model)).astype(np.float32) for _ in range(L)]
     dec = Mamba2Decoder(lambda k, l: _d(Ws[(k, l)]), lambda l: mix[l],
                         lambda l: torch.from_numpy(pre[l]), L, d_model, H, keep=keep, g=g,
-                        batch=1, stack=stack)
+                        batch=batch, stack=stack)
     states = []
     for l in range(L):
-        conv, ssm = synth.mixer_states(rng, 1, H)
+        conv, ssm = synth.mixer_states(rng, batch, H)
         states.append((conv, ssm))
         dec.set_states(l, _d(conv.view(np.int16)).view(torch.float16),
                        _d(ssm.view(np.int16)).view(torch.float16))
@@ -133,30 +133,32 @@ def test_stack_decode_kept_fp16_layers(L, d_model, H, g, keep):
             assert e["a"][i] <= max(1e-3, min(2 * e["b"][i], 4e-3)), (l, i, e)
 
 
-def test_stack_decode_full_size_against_oracle():
+@pytest.mark.parametrize("B", [1, 4])
+def test_stack_decode_full_size_against_oracle(B):
     """Two blocks of the Mamba-2 1.3B shapes (d_model 2048, 64 heads,
-    in_proj 8512 x 2048, out_proj 2048 x 4096), three tokens, against the
-    oracle's decode; then the layer-by-layer fused decode from the same
-    weights and states stays within twice the bar of the one-launch decode
-    (each is within the bar of the exact result)."""
-    a, Ws, mix, pre, states = _decoder(3, 2, synth.D_MODEL, 64, stack=True)
-    b, *_ = _decoder(3, 2, synth.D_MODEL, 64, stack=False)
+    in_proj 8512 x 2048, out_proj 2048 x 4096), three tokens per batch row
+    (batch 4: 256 mixer workgroups), against the oracle's decode; then the
+    layer-by-layer fused decode from the same weights and states stays
+    within twice the bar of the one-launch decode (each is within the bar of
+    the exact result)."""
+    a, Ws, mix, pre, states = _decoder(3, 2, synth.D_MODEL, 64, stack=True, batch=B)
+    b, *_ = _decoder(3, 2, synth.D_MODEL, 64, stack=False, batch=B)
     assert a.stack and not b.stack and b.fused
     ref_dec = OracleDecoder(Ws, mix, pre, states, (), a.g, a.eps)
     rng = np.random.default_rng(77)
     for t in range(3):
-        emb = rng.standard_normal((1, synth.D_MODEL)).astype(np.float32)
+        emb = rng.standard_normal((B, synth.D_MODEL)).astype(np.float32)
         a.emb.copy_(_d(emb))
         b.emb.copy_(_d(emb))
         xa = _bf16_to_f64(a.token())
         xb = _bf16_to_f64(b.token())
         ref = ref_dec.token(emb)
         torch.cuda.synchronize()
-        bar = 2.0 ** -7 * np.abs(ref) + 1e-3 * np.abs(ref).max()
+        bar = 2.0 ** -7 * np.abs(ref) + 1e-3 * np.abs(ref).max(axis=1, keepdims=True)
         ra = float((np.abs(xa - ref) / bar).max())
         rb = float((np.abs(xb - ref) / bar).max())
         rab = float((np.abs(xa - xb) / (2 * bar)).max())
-        print(f"[stack decode] full size token {t}: err/bar stack {ra:.3f} fused {rb:.3f} "
+        print(f"[stack decode] full size B={B} token {t}: err/bar stack {ra:.3f} fused {rb:.3f} "
               f"stack-vs-fused/2bar {rab:.3f}", flush=True)
         assert ra <= 1.0 and rab <= 1.0
     assert _timeout_flag(a) == 0
@@ -168,3 +170,89 @@ def test_stack_decode_full_size_against_oracle():
         assert O.rel_fro_error(win.astype(np.float64), conv_ref.astype(np.float64)) <= 1e-3
         assert O.rel_fro_error(lay["ssm"].cpu().numpy().astype(np.float64),
                                ssm_ref.astype(np.float64)) <= 1e-3
+
+
+@pytest.mark.parametrize("L,d_model,H,g,B,keep", [(3, 256, 2, 128, 4, ()),
+                                                  (2, 512, 8, 64, 2, (1,)),
+                                                  (3, 1024, 4, 256, 3, (0,)),
+                                                  (2, 256, 64, 128, 4, (1,))])
+def test_stack_decode_batches(L, d_model, H, g, B, keep):
+    """B tokens at once (one per batch row; the mixer's workgroups one per
+    head and row, 256 of them at 64 heads and B = 4), blocks kept in FP16
+    among them, against the oracle's decode of the same batch and next to
+    the layer-by-layer fused decode: outputs of every row within the bars
+    above, states as in the kept-block test."""
+    a, Ws, mix, pre, states = _decoder(90 + L + H + B, L, d_model, H, g, stack=True, keep=keep,
+                                       batch=B)
+    b, *_ = _decoder(90 + L + H + B, L, d_model, H, g, stack=False, keep=keep, batch=B)
+    assert a.stack and a.B == B and not b.stack and a.launches_per_token() == 2
+    ref_dec = OracleDecoder(Ws, mix, pre, states, keep, g, a.eps)
+    rng = np.random.default_rng(70 + B)
+    print(f"[stack decode] batch {B} kept {keep} L={L} d_model={d_model} nheads={H} g={g}",
+          flush=True)
+    for t in range(3):
+        emb = rng.standard_normal((B, d_model)).astype(np.float32)
+        a.emb.copy_(_d(emb))
+        b.emb.copy_(_d(emb))
+        xa = _bf16_to_f64(a.token())
+        xb = _bf16_to_f64(b.token())
+        ref = ref_dec.token(emb)
+        torch.cuda.synchronize()
+        assert xa.shape == ref.shape == (B, d_model)
+        bar = 2.0 ** -7 * np.abs(ref) + 1e-3 * np.abs(ref).max(axis=1, keepdims=True)
+        ra = (np.abs(xa - ref) / bar).max(axis=1)
+        rb = (np.abs(xb - ref) / bar).max(axis=1)
+        print(f"  token {t}: err/bar per row one launch {np.round(ra, 3).tolist()}, "
+              f"layer by layer {np.round(rb, 3).tolist()}", flush=True)
+        assert np.all(ra <= 1.0) and np.all(rb <= 1.0)
+    assert _timeout_flag(a) == 0
+    from oracle import ternary as O
+    for l in range(L):
+        conv_ref, ssm_ref = ref_dec.states[l]
+        assert int(a.layers[l]["pos"].cpu()[0]) == 3
+        for r in range(B):
+            e = {}
+            for name, dec in (("a", a), ("b", b)):
+                lay = dec.layers[l]
+                win = ring_to_window(lay["conv"].cpu().numpy(), int(lay["pos"].cpu()[0]))
+                e[name] = (O.rel_fro_error(win[r].astype(np.float64),
+                                           conv_ref[r].astype(np.float64)),
+                           O.rel_fro_error(lay["ssm"].cpu().numpy()[r].astype(np.float64),
+                                           ssm_ref[r].astype(np.float64)))
+            for i in range(2):
+                assert e["a"][i] <= max(1e-3, min(2 * e["b"][i], 4e-3)), (l, r, i, e)
+
+
+def test_stack_decode_batch_rows_match_batch_one():
+    """Each row of a batch-4 one-launch decode against batch-1 one-launch
+    decodes of that row alone (same weights, states and embeddings): the two
+    forms sum in different orders (the batched rows reduce through one
+    four-way butterfly), so rows agree to the bars of the oracle test, and
+    the row's states to 1e-3."""
+    B, L, d_model, H = 4, 2, 512, 4
+    a, Ws, mix, pre, states = _decoder(123, L, d_model, H, stack=True, batch=B)
+    singles = []
+    for r in range(B):
+        d1, *_ = _decoder(123, L, d_model, H, stack=True, batch=1)
+        for l in range(L):
+            conv, ssm = states[l]
+            d1.set_states(l, _d(conv[r:r + 1].view(np.int16)).view(torch.float16),
+                          _d(ssm[r:r + 1].view(np.int16)).view(torch.float16))
+        singles.append(d1)
+    rng = np.random.default_rng(321)
+    for t in range(2):
+        emb = rng.standard_normal((B, d_model)).astype(np.float32)
+        a.emb.copy_(_d(emb))
+        xa = _bf16_to_f64(a.token())
+        for r, d1 in enumerate(singles):
+            d1.emb.copy_(_d(emb[r:r + 1]))
+            x1 = _bf16_to_f64(d1.token())[0]
+            bar = 2.0 ** -7 * np.abs(x1) + 1e-3 * np.abs(x1).max()
+            assert np.all(np.abs(xa[r] - x1) <= 2 * bar), (t, r)
+    assert _timeout_flag(a) == 0
+    from oracle import ternary as O
+    for l in range(L):
+        for r, d1 in enumerate(singles):
+            sa = a.layers[l]["ssm"].cpu().numpy()[r].astype(np.float64)
+            s1 = d1.layers[l]["ssm"].cpu().numpy()[0].astype(np.float64)
+            assert O.rel_fro_error(sa, s1) <= 1e-3, (l, r)

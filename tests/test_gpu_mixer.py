@@ -136,7 +136,8 @@ def test_residual_rmsnorm():
     assert np.array_equal(_bf16_to_f64(x2), got)
 
 
-def _small_decoder(seed, keep=(2,), B=1, L=3, fused=None):
+def _small_decoder(seed, keep=(2,), B=1, L=3, fused=None, stack=False):
+    # layer-by-layer forms (the one-launch form has tests of its own)
     from paper_2606_18114_amd.stack import Mamba2Decoder
     rng = np.random.default_rng(seed)
     d_model, H = 256, 2
@@ -147,7 +148,7 @@ def _small_decoder(seed, keep=(2,), B=1, L=3, fused=None):
     pre = [(1 + 0.1 * rng.standard_normal(d_model)).astype(np.float32) for _ in range(L)]
     dec = Mamba2Decoder(lambda k, l: _d(Ws[(k, l)]), lambda l: mix[l],
                         lambda l: torch.from_numpy(pre[l]), L, d_model, H, keep=keep,
-                        g=128, batch=B, fused=fused)
+                        g=128, batch=B, fused=fused, stack=stack)
     states = []
     for l in range(L):
         conv, ssm = synth.mixer_states(rng, B, H)
