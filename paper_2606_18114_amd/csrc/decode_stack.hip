@@ -165,6 +165,7 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(src), (short)0, K * 4, 0x00020000);
   float v[NQ][4];
+  u32x4 wv[NQ];
   float pv0 = 0.f, pv1 = 0.f;
   if (part != nullptr) {
     if (lane < nparts) pv0 = ld_f32<true>(part + lane);
@@ -174,7 +175,11 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
   for (int j = 0; j < NQ; ++j) {
     const int i = tid + kDsThreads * j;
     u32x4 b = {0u, 0u, 0u, 0u};
-    if (4 * i < K) b = ds_ld16_coherent(rs, 16u * (uint32_t)i);
+    wv[j] = b;
+    if (4 * i < K) {
+      b = ds_ld16_coherent(rs, 16u * (uint32_t)i);
+      wv[j] = ld16(w + 4 * i);  // the weights in flight with the values
+    }
     v[j][0] = __uint_as_float(b.x);
     v[j][1] = __uint_as_float(b.y);
     v[j][2] = __uint_as_float(b.z);
@@ -199,11 +204,10 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
   for (int j = 0; j < NQ; ++j) {
     const int i = tid + kDsThreads * j;
     if (4 * i < K) {
-      const u32x4 wv = ld16(w + 4 * i);
-      xs[2 * i] = ds_bf16_rne(v[j][0] * r * __uint_as_float(wv.x)) |
-                  (ds_bf16_rne(v[j][1] * r * __uint_as_float(wv.y)) << 16);
-      xs[2 * i + 1] = ds_bf16_rne(v[j][2] * r * __uint_as_float(wv.z)) |
-                      (ds_bf16_rne(v[j][3] * r * __uint_as_float(wv.w)) << 16);
+      xs[2 * i] = ds_bf16_rne(v[j][0] * r * __uint_as_float(wv[j].x)) |
+                  (ds_bf16_rne(v[j][1] * r * __uint_as_float(wv[j].y)) << 16);
+      xs[2 * i + 1] = ds_bf16_rne(v[j][2] * r * __uint_as_float(wv[j].z)) |
+                      (ds_bf16_rne(v[j][3] * r * __uint_as_float(wv[j].w)) << 16);
     }
   }
   __syncthreads();
@@ -464,6 +468,13 @@ __device__ __forceinline__ void ds_norm_xb(const float* __restrict__ src,
   const int tid = threadIdx.x, lane = tid & 63;
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<float*>(src), (short)0, nb * K * 4, 0x00020000);
+  u32x4 wv[NQ];  // the weights, in flight with the first chunk's values
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const int i = tid + kDsThreads * j;
+    wv[j] = u32x4{0u, 0u, 0u, 0u};
+    if (4 * i < K) wv[j] = ld16(w + 4 * i);
+  }
 #pragma unroll
   for (int b0 = 0; b0 < NB; b0 += kC) {
     if (b0 >= nb) break;
@@ -521,11 +532,10 @@ __device__ __forceinline__ void ds_norm_xb(const float* __restrict__ src,
       for (int j = 0; j < NQ; ++j) {
         const int i = tid + kDsThreads * j;
         if (4 * i < K) {
-          const u32x4 wv = ld16(w + 4 * i);
-          xb[2 * i] = ds_bf16_rne(v[c][j][0] * r * __uint_as_float(wv.x)) |
-                      (ds_bf16_rne(v[c][j][1] * r * __uint_as_float(wv.y)) << 16);
-          xb[2 * i + 1] = ds_bf16_rne(v[c][j][2] * r * __uint_as_float(wv.z)) |
-                          (ds_bf16_rne(v[c][j][3] * r * __uint_as_float(wv.w)) << 16);
+          xb[2 * i] = ds_bf16_rne(v[c][j][0] * r * __uint_as_float(wv[j].x)) |
+                      (ds_bf16_rne(v[c][j][1] * r * __uint_as_float(wv[j].y)) << 16);
+          xb[2 * i + 1] = ds_bf16_rne(v[c][j][2] * r * __uint_as_float(wv[j].z)) |
+                          (ds_bf16_rne(v[c][j][3] * r * __uint_as_float(wv[j].w)) << 16);
         }
       }
     }
@@ -728,8 +738,7 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
       else
         ds_dense_rows<TA>(s.in_w16 + (int64_t)kd * Z * D, D, zr0, zr1, xr, nullptr, put);
     } else {
-      ds_norm_xb<TA, NB>(src, s.pre_w + (int64_t)l * D, D, s.eps, nullptr, 0, nb, xs, kXs,
-                                red);
+      ds_norm_xb<TA, NB>(src, s.pre_w + (int64_t)l * D, D, s.eps, nullptr, 0, nb, xs, kXs, red);
       auto put = [&](int r, int b, float y) { st_f32<true>(a.zx + (int64_t)b * Z + r, y); };
       if (kd < 0)
         ds_rows_all_b<G, TA, NB>(rows, inc, ins, D, zr1, xs, kXs, nb, nullptr, 0, put);
@@ -771,8 +780,8 @@ __global__ __launch_bounds__(kDsThreads) void decode_stack_kernel(DsArgs a) {
       else
         ds_dense_rows<TC>(s.out_w16 + (int64_t)kd * D * DI, DI, cr0, cr1, xr, src, put);
     } else {
-      ds_norm_xb<TC, NB>(a.gated, s.norm_w + (int64_t)l * DI, DI, s.eps, a.partial, H, nb,
-                                xs, kXs, red);
+      ds_norm_xb<TC, NB>(a.gated, s.norm_w + (int64_t)l * DI, DI, s.eps, a.partial, H, nb, xs,
+                         kXs, red);
       auto put = [&](int r, int b, float y) { st_f32<true>(a.residual + (int64_t)b * D + r, y); };
       if (kd < 0)
         ds_rows_all_b<G, TC, NB>(rows, outc, outs, DI, cr1, xs, kXs, nb, src, D, put);
@@ -813,7 +822,8 @@ static const void* decode_stack_fn(int g, int ta, int tc, int nb) {
     // (batches: rows up to d_model 2048 and d_inner 4096, where the
     // registers hold every value without spilling)
     if constexpr (NB == 1)
-      if (ta <= 4 && tc <= 8) return reinterpret_cast<const void*>(&decode_stack_kernel<G, 4, 8, 1>);
+      if (ta <= 4 && tc <= 8)
+        return reinterpret_cast<const void*>(&decode_stack_kernel<G, 4, 8, 1>);
     return nullptr;
   };
   auto by_batch = [&](auto gt) -> const void* {

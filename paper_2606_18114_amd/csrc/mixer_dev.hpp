@@ -90,10 +90,12 @@ __device__ __forceinline__ void mixer_head_step(
   // channels d_inner + (i - 64); a thread takes at most two channels
   constexpr int kMxCh = (kMxP + 2 * kMxN + kMxThreads - 1) / kMxThreads;
   uint32_t ring[kMxCh][2];
-  float xin[kMxCh];
-  // the head's dt and this thread's z, loaded with the conv inputs
+  float xin[kMxCh], cw[kMxCh][4], cb[kMxCh];
+  // the head's dt and this thread's z, loaded with the conv inputs, and every
+  // parameter of the step, so the step pays one memory latency
   const float dt_raw = ld_f32<COH>(row + 2 * d_inner + 2 * kMxN + h);
   const float zp = ld_f32<COH>(row + h * kMxP + p);
+  const float dtb = dt_bias[h], alog = A_log[h], dskip = Dp[h];
 #pragma unroll
   for (int t = 0; t < kMxCh; ++t) {
     const int i = tid + t * kMxThreads;
@@ -103,6 +105,9 @@ __device__ __forceinline__ void mixer_head_step(
     ring[t][0] = r2.x;
     ring[t][1] = r2.y;
     xin[t] = ld_f32<COH>(row + d_inner + c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cw[t][j] = conv_w[(int64_t)c * 4 + j];
+    cb[t] = conv_bias[c];
   }
   const int pos = pos_of();
 #pragma unroll
@@ -110,23 +115,22 @@ __device__ __forceinline__ void mixer_head_step(
     const int i = tid + t * kMxThreads;
     if (i >= kMxP + 2 * kMxN) break;
     const int c = i < kMxP ? h * kMxP + i : d_inner + (i - kMxP);
-    const float* w = conv_w + (int64_t)c * 4;
     auto slot = [&](int k) {  // float16 of ring slot k (0 .. 3)
       const uint32_t wd = ring[t][k >> 1];
       return h2f((uint16_t)((k & 1) ? wd >> 16 : wd & 0xFFFFu));
     };
-    float acc = conv_bias[c];
+    float acc = cb[t];
 #pragma unroll
-    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(slot((pos + 1 + j) & 3), w[j], acc);
-    acc = __builtin_fmaf(xin[t], w[3], acc);
+    for (int j = 0; j < 3; ++j) acc = __builtin_fmaf(slot((pos + 1 + j) & 3), cw[t][j], acc);
+    acc = __builtin_fmaf(xin[t], cw[t][3], acc);
     u[i] = mx_silu(acc);
     // the slot nobody reads; the shared B/C channels are written by head 0
     if (i < kMxP || h == 0) conv_b[(int64_t)c * 4 + pos] = f2h(xin[t]);
   }
   __syncthreads();
 
-  const float dtp = mx_softplus(dt_raw + dt_bias[h]);
-  const float a = expf(-dtp * expf(A_log[h]));
+  const float dtp = mx_softplus(dt_raw + dtb);
+  const float a = expf(-dtp * expf(alog));
   const float xp = u[p];
   const float dx = dtp * xp;
   uint16_t* sp = ssm_h + p * kMxN + 32 * q;
@@ -149,7 +153,7 @@ __device__ __forceinline__ void mixer_head_step(
   // the four threads of a channel (lanes 4p' .. 4p' + 3 of the wave)
   y += __uint_as_float(lane_xchg<1>(__float_as_uint(y)));
   y += __uint_as_float(lane_xchg<2>(__float_as_uint(y)));
-  y = __builtin_fmaf(Dp[h], xp, y);
+  y = __builtin_fmaf(dskip, xp, y);
   const float g = y * mx_silu(zp);
   if (q == 0) st_f32<COH>(gated_b + h * kMxP + p, g);
   if (part == nullptr) return;
