@@ -282,6 +282,35 @@ def test_fwd_exact_cases():
     np.testing.assert_array_equal(Y, O.gemm_fwd(Xi, q, sc, g))
 
 
+@pytest.mark.parametrize("g", [64, 128])
+def test_fwd_wide_scale_ratios(g):
+    """The forward keeps its sums in units of the current group's scale and
+    rescales by c / s at each group boundary (exact for powers of two).  Group
+    scales 2^50 and 2^-50 side by side (ratios 2^100, with sum_k |X| ~ 400 far
+    inside the declared 1e38 precondition), and random powers of two in
+    2^-40 .. 2^40, against the float64 oracle element by element: each error
+    within float32 accumulation of the products, |err| <= K 2^-23 sum|terms|
+    (terms x q s), and no output non-finite."""
+    ops = _ops()
+    M, N, K = 130, 96, 512
+    rng = np.random.default_rng(11 + g)
+    q = rng.integers(-1, 2, (N, K)).astype(np.int8)
+    e = np.where((np.arange(K // g) % 2 == 0)[None, :], 50, -50) * np.ones((N, 1), np.int64)
+    e[N // 2:] = rng.integers(-40, 41, (N - N // 2, K // g))
+    sc = np.ldexp(np.ones((N, K // g)), e).astype(np.float32)
+    X = synth.activations(rng, M, K)
+    Xf = synth.bf16_bits_to_f32(X).astype(np.float64)
+    c, s = torch.from_numpy(O.pack(q)).cuda(), dev_f32(sc)
+    Y = host(ops.tgemm_fwd(dev_bf16(X), c, s, g)).astype(np.float64)
+    ref = O.gemm_fwd(X, q, sc, g)
+    mag = np.abs(Xf) @ np.abs(O.dequantize(q, sc, g).astype(np.float64)).T
+    assert np.all(np.isfinite(Y))
+    err = np.abs(Y - ref)
+    worst = float((err / np.maximum(mag, 1e-300)).max())
+    print(f"  g={g}: worst |err| / sum|terms| {worst:.2e}", flush=True)
+    assert np.all(err <= K * 2.0 ** -23 * mag)
+
+
 def test_fwd_split_tiles_exact_and_complete():
     """Tiles cut along K into parts that add with atomics: integer inputs give
     exact sums whatever order the parts land in, and every output element is
