@@ -164,6 +164,9 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
   const int tid = threadIdx.x, lane = tid & 63;
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(src), (short)0, K * 4, 0x00020000);
+  // the weights in flight with the values, up to four per thread (more
+  // would spill registers; longer rows load them after the sum)
+  constexpr bool kEarlyW = NQ <= 4;
   float v[NQ][4];
   u32x4 wv[NQ];
   float pv0 = 0.f, pv1 = 0.f;
@@ -178,7 +181,7 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
     wv[j] = b;
     if (4 * i < K) {
       b = ds_ld16_coherent(rs, 16u * (uint32_t)i);
-      wv[j] = ld16(w + 4 * i);  // the weights in flight with the values
+      if (kEarlyW) wv[j] = ld16(w + 4 * i);
     }
     v[j][0] = __uint_as_float(b.x);
     v[j][1] = __uint_as_float(b.y);
@@ -204,6 +207,7 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
   for (int j = 0; j < NQ; ++j) {
     const int i = tid + kDsThreads * j;
     if (4 * i < K) {
+      if (!kEarlyW) wv[j] = ld16(w + 4 * i);
       xs[2 * i] = ds_bf16_rne(v[j][0] * r * __uint_as_float(wv[j].x)) |
                   (ds_bf16_rne(v[j][1] * r * __uint_as_float(wv[j].y)) << 16);
       xs[2 * i + 1] = ds_bf16_rne(v[j][2] * r * __uint_as_float(wv[j].z)) |
@@ -296,7 +300,9 @@ template <int G, int T, typename Out>
 __device__ __forceinline__ void ds_rows_compute(const DsRows& p, const uint32_t (&xr)[T][8],
                                                 Out out) {
   constexpr int kRows = kDsPrefetch / T;
-  constexpr int kStep = T <= 2 ? kRows : 2;
+  // groups of up to nine rows (a wave's share of in_proj at d_model 2048),
+  // so the slots past the rows held are not computed
+  constexpr int kStep = T <= 2 ? (kRows < 9 ? kRows : 9) : 2;
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int j0 = 0; j0 < kRows; j0 += kStep) {
@@ -550,7 +556,7 @@ __device__ __forceinline__ void ds_rows_compute_b(const DsRows& p, const uint32_
                                                   int xstride, int K, int nb, Out out) {
   static_assert(NB == 4, "batch slots of the four-way butterfly");
   constexpr int kRows = kDsPrefetch / T;
-  constexpr int kStep = kRows < 6 ? kRows : 6;
+  constexpr int kStep = kRows < 9 ? kRows : 9;
   const int lane = threadIdx.x & 63;
   const int nw = K / 16, bl = lane >> 4;
   const bool writer = (lane & 15) == 0 && bl < nb;
