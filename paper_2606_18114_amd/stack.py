@@ -14,7 +14,8 @@ quality lost to ternarization).
   (``tm_tgemv`` for the ternary layers, ``tm_dgemv`` for the kept ones).
 * ``Mamba2Decoder``: decode in layer order through whole Mamba-2 blocks
   (pre-norm, in_proj, the FP16 mixer step of Sec. 3.2, out_proj), one token
-  capturable as a HIP graph (Sec. 8: batch-1 decode).
+  capturable as a HIP graph, or the whole stack in one launch (Sec. 8:
+  small-batch decode).
 
 Only argument marshalling and packing happen here; every product runs in
 the library's kernels.
