@@ -139,6 +139,25 @@ __device__ __forceinline__ float ds_wave_sum(float v) {
   return v;
 }
 
+// The four sums a[0 .. 3] of a wave in one butterfly: the lanes swap halves
+// of their values across 32 and 16 lanes, then reduce the rest, so that
+// lanes 16 b .. 16 b + 15 end with the total of a[b] over the 64 lanes.
+__device__ __forceinline__ float ds_wave_sum4(const float (&a)[4]) {
+  const int lane = threadIdx.x & 63;
+  const bool hi = (lane & 32) != 0;
+  float k0 = hi ? a[2] : a[0], k1 = hi ? a[3] : a[1];
+  k0 += __uint_as_float(lane_xchg<32>(__float_as_uint(hi ? a[0] : a[2])));
+  k1 += __uint_as_float(lane_xchg<32>(__float_as_uint(hi ? a[1] : a[3])));
+  const bool mid = (lane & 16) != 0;
+  float k = mid ? k1 : k0;
+  k += __uint_as_float(lane_xchg<16>(__float_as_uint(mid ? k0 : k1)));
+  k += __uint_as_float(lane_xchg<1>(__float_as_uint(k)));
+  k += __uint_as_float(lane_xchg<2>(__float_as_uint(k)));
+  k += __uint_as_float(lane_xchg<4>(__float_as_uint(k)));
+  k += __uint_as_float(lane_xchg<8>(__float_as_uint(k)));
+  return k;
+}
+
 __device__ __forceinline__ uint32_t ds_bf16_rne(float v) {
   const uint32_t b = __float_as_uint(v);
   return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
@@ -271,9 +290,9 @@ __device__ __forceinline__ void ds_rows_load(DsRows& p, const uint8_t* __restric
 }
 
 // out(r, base + y) for the rows held in p: y = sum_k x[k] q[r, k] s16[r, k / G].
-// With at most two words per lane every row slot is computed (slots past the
-// rows held have zero codes), so all the rows' dependency chains interleave;
-// with more, rows go in pairs.  Each chain is split into even and odd pairs.
+// With at most two words per lane the rows go in groups of up to nine, all
+// their dependency chains interleaved; with more, in pairs.  Each chain is
+// split into even and odd pairs.
 template <int G, int T>
 __device__ __forceinline__ float ds_row_sum(const DsRows& p, const uint32_t (&xr)[T][8],
                                             int j) {
@@ -303,19 +322,28 @@ __device__ __forceinline__ void ds_rows_compute(const DsRows& p, const uint32_t 
   // groups of up to nine rows (a wave's share of in_proj at d_model 2048),
   // so the slots past the rows held are not computed
   constexpr int kStep = T <= 2 ? (kRows < 9 ? kRows : 9) : 2;
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, rl = lane >> 4;
 #pragma unroll
   for (int j0 = 0; j0 < kRows; j0 += kStep) {
     if (j0 < p.count) {
       float acc[kStep];
 #pragma unroll
-      for (int jj = 0; jj < kStep; ++jj) acc[jj] = ds_row_sum<G, T>(p, xr, j0 + jj < kRows ? j0 + jj : j0);
+      for (int jj = 0; jj < kStep; ++jj)
+        acc[jj] = ds_row_sum<G, T>(p, xr, j0 + jj < kRows ? j0 + jj : j0);
+      // the rows' sums meet four at a time; lane 16 i writes row jq + i
 #pragma unroll
-      for (int jj = 0; jj < kStep; ++jj) acc[jj] = ds_wave_sum(acc[jj]);
-      if (lane == 0) {
+      for (int jq = 0; jq < kStep; jq += 4) {
+        float a4[4], b4[4];
 #pragma unroll
-        for (int jj = 0; jj < kStep; ++jj)
-          if (j0 + jj < p.count) out(p.first + (j0 + jj) * kDsWaves, p.base[j0 + jj] + 0.5f * acc[jj]);
+        for (int i = 0; i < 4; ++i) {
+          a4[i] = jq + i < kStep ? acc[jq + i] : 0.f;
+          b4[i] = jq + i < kStep && j0 + jq + i < kRows ? p.base[j0 + jq + i] : 0.f;
+        }
+        const float v = ds_wave_sum4(a4);
+        const float bv = rl == 0 ? b4[0] : (rl == 1 ? b4[1] : (rl == 2 ? b4[2] : b4[3]));
+        const int j = j0 + jq + rl;
+        if ((lane & 15) == 0 && jq + rl < kStep && j < p.count)
+          out(p.first + j * kDsWaves, bv + 0.5f * v);
       }
     }
   }
@@ -424,25 +452,6 @@ __device__ __forceinline__ void ds_rows_all(DsRows& p, const uint8_t* codes, con
 // against each row's x pairs (read from LDS per word column, once per group
 // of rows), and each (row, batch row) keeps its own float32 sum, in the same
 // order as the batch-1 form.  Slots b >= nb see zero x.
-
-// The four sums a[0 .. 3] of a wave in one butterfly: the lanes swap halves
-// of their values across 32 and 16 lanes, then reduce the rest, so that
-// lanes 16 b .. 16 b + 15 end with the total of a[b] over the 64 lanes.
-__device__ __forceinline__ float ds_wave_sum4(const float (&a)[4]) {
-  const int lane = threadIdx.x & 63;
-  const bool hi = (lane & 32) != 0;
-  float k0 = hi ? a[2] : a[0], k1 = hi ? a[3] : a[1];
-  k0 += __uint_as_float(lane_xchg<32>(__float_as_uint(hi ? a[0] : a[2])));
-  k1 += __uint_as_float(lane_xchg<32>(__float_as_uint(hi ? a[1] : a[3])));
-  const bool mid = (lane & 16) != 0;
-  float k = mid ? k1 : k0;
-  k += __uint_as_float(lane_xchg<16>(__float_as_uint(mid ? k0 : k1)));
-  k += __uint_as_float(lane_xchg<1>(__float_as_uint(k)));
-  k += __uint_as_float(lane_xchg<2>(__float_as_uint(k)));
-  k += __uint_as_float(lane_xchg<4>(__float_as_uint(k)));
-  k += __uint_as_float(lane_xchg<8>(__float_as_uint(k)));
-  return k;
-}
 
 // this lane's x pairs of word column w for every batch row (zero past the
 // row and for b >= nb)
