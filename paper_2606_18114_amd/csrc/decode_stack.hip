@@ -64,7 +64,7 @@ constexpr int kDsThreads = 256;
 constexpr int kDsWaves = kDsThreads / 64;
 constexpr int kDsPrefetch = 24;   // code words per lane held for the next rows
 constexpr uint32_t kDsSpinLimit = 1u << 16;   // a barrier takes microseconds
-constexpr int kDsCounters = 8;                // barrier counter words (one per XCD)
+constexpr int kDsCounters = 32;               // barrier counter words (four per XCD)
 constexpr int kDsCounterStride = 32;          // 128 bytes between them
 // the three barriers of a block have counter sets of their own; the
 // timeout flag follows them
@@ -75,7 +75,7 @@ struct DsArgs {
   const float* emb;
   uint16_t* x_out;
   uint32_t* sync;   // counter sets [256 b + 32 k] (barrier b < 3, word k < 8) and the
-                    // timeout flag [768], all zero at launch
+                    // timeout flag [3072], all zero at launch
   float* zx;        // [nb, Z]
   float* gated;     // [nb, d_inner]
   float* partial;   // [nb, nheads]
@@ -93,31 +93,36 @@ struct DsArgs {
 // workgroup has arrived).  Loads of the next phase's operands go between the
 // two, so their memory latency overlaps the wait.
 // The arrival counter is spread over kDsCounters words 128 bytes apart
-// (workgroup b increments word b % kDsCounters, i.e. one word per XCD), so
-// the increments of the 256 workgroups do not all queue on one address; a
-// waiter loads all the words at once and adds them.
+// (workgroup b increments word b % kDsCounters: eight workgroups of one XCD
+// per word), so the increments of the 256 workgroups do not all queue on one
+// address; the first wave of a waiter loads all the words at once, one per
+// lane, and adds them across the lanes.
 __device__ __forceinline__ void ds_arrive(uint32_t* ctr) {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's stores have completed
   __syncthreads();
   if (threadIdx.x == 0) atomicAdd(ctr + kDsCounterStride * (blockIdx.x % kDsCounters), 1u);
 }
 __device__ __forceinline__ void ds_wait(uint32_t* ctr, uint32_t* flag, uint32_t target) {
-  if (threadIdx.x == 0) {
+  static_assert(kDsCounters <= 64, "one counter word per lane");
+  if (threadIdx.x < 64) {  // the first wave, every lane active
+    const int lane = threadIdx.x;
     uint32_t n = 0;
     for (;;) {
-      uint32_t c[kDsCounters];
-#pragma unroll
-      for (int k = 0; k < kDsCounters; ++k)
-        c[k] = __hip_atomic_load(ctr + kDsCounterStride * k, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-      uint32_t total = 0;
-#pragma unroll
-      for (int k = 0; k < kDsCounters; ++k) total += c[k];
-      if (total >= target) break;
+      uint32_t c = lane < kDsCounters
+                       ? __hip_atomic_load(ctr + kDsCounterStride * lane, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT)
+                       : 0u;
+      c += lane_xchg<1>(c);
+      c += lane_xchg<2>(c);
+      c += lane_xchg<4>(c);
+      c += lane_xchg<8>(c);
+      c += lane_xchg<16>(c);
+      c += lane_xchg<32>(c);
+      if (c >= target) break;  // the total, the same in every lane
       __builtin_amdgcn_s_sleep(1);
       ++n;
       if (n == kDsSpinLimit) {  // a workgroup never arrived: give up, report
-        atomicOr(flag, 1u);
+        if (lane == 0) atomicOr(flag, 1u);
         break;
       }
       // once any workgroup has given up, every later wait ends at once
