@@ -500,7 +500,7 @@ typedef struct {
  *              [batch, d_model] out (4-byte aligned: stored in pairs)
  *   workspace  device scratch of tm_mamba2_decode_workspace(d_model, nheads,
  *              batch) bytes, 256-byte aligned, owned by the caller; nothing need be
- *              set before the call.  Its uint32 word 3072 is nonzero after a
+ *              set before the call.  Its uint32 word 6144 is nonzero after a
  *              call whose grid barrier gave up waiting; the outputs and
  *              states of such a call are not valid.
  * One workgroup per CU; the blocks' phases are separated by grid barriers

@@ -64,7 +64,7 @@ constexpr int kDsThreads = 256;
 constexpr int kDsWaves = kDsThreads / 64;
 constexpr int kDsPrefetch = 24;   // code words per lane held for the next rows
 constexpr uint32_t kDsSpinLimit = 1u << 16;   // a barrier takes microseconds
-constexpr int kDsCounters = 32;               // barrier counter words (four per XCD)
+constexpr int kDsCounters = 64;               // barrier counter words (eight per XCD)
 constexpr int kDsCounterStride = 32;          // 128 bytes between them
 // the three barriers of a block have counter sets of their own; the
 // timeout flag follows them
@@ -75,7 +75,7 @@ struct DsArgs {
   const float* emb;
   uint16_t* x_out;
   uint32_t* sync;   // counter sets [256 b + 32 k] (barrier b < 3, word k < 8) and the
-                    // timeout flag [3072], all zero at launch
+                    // timeout flag [6144], all zero at launch
   float* zx;        // [nb, Z]
   float* gated;     // [nb, d_inner]
   float* partial;   // [nb, nheads]
@@ -93,7 +93,7 @@ struct DsArgs {
 // workgroup has arrived).  Loads of the next phase's operands go between the
 // two, so their memory latency overlaps the wait.
 // The arrival counter is spread over kDsCounters words 128 bytes apart
-// (workgroup b increments word b % kDsCounters: eight workgroups of one XCD
+// (workgroup b increments word b % kDsCounters: four workgroups of one XCD
 // per word), so the increments of the 256 workgroups do not all queue on one
 // address; the first wave of a waiter loads all the words at once, one per
 // lane, and adds them across the lanes.

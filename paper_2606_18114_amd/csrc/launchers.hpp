@@ -157,7 +157,7 @@ struct DecodeStackDesc {
 // [barrier words and timeout flag: kDecodeStackSyncBytes] zx [batch, Z]
 // gated [batch, d_inner] partial [batch, nheads] residual [batch, d_model],
 // each piece 256-byte aligned
-constexpr int kDecodeStackSyncBytes = 16384;
+constexpr int kDecodeStackSyncBytes = 32768;
 inline int64_t decode_stack_workspace_bytes(int d_model, int nheads, int batch) {
   auto up = [](int64_t v) { return (v + 255) / 256 * 256; };
   const int64_t b = batch, di = 64 * (int64_t)nheads, z = 2 * di + 256 + nheads;

@@ -436,12 +436,12 @@ def mdec(L, emb=P + 2 ** 31, x_out=P + 2 ** 31 + 2 ** 20, ws=P + 2 ** 32, wsb=No
 
 
 def test_mamba2_decode_token_validation(L):
-    # [barrier words 16 KiB | zx Z | gated | partial | residual], 256-byte pieces
+    # [barrier words 32 KiB | zx Z | gated | partial | residual], 256-byte pieces
     z = 2 * 128 + 256 + 2
     ws = L.tm_mamba2_decode_workspace
-    assert ws(256, 2, 1) == 16384 + 2304 + 512 + 256 + 1024 and z == 514
+    assert ws(256, 2, 1) == 32768 + 2304 + 512 + 256 + 1024 and z == 514
     # batch 3: every piece three rows
-    assert ws(256, 2, 3) == 16384 + 6400 + 1536 + 256 + 3072
+    assert ws(256, 2, 3) == 32768 + 6400 + 1536 + 256 + 3072
     assert ws(8192, 2, 1) == -1
     assert ws(256, 0, 1) == -1
     assert ws(256, 2, 0) == -1

@@ -59,7 +59,7 @@ def _need_cus(n):
 
 def _timeout_flag(dec):
     torch.cuda.synchronize()
-    return int(dec.stack_ws[12288:12292].view(torch.int32).cpu()[0])   # word 3072
+    return int(dec.stack_ws[24576:24580].view(torch.int32).cpu()[0])   # word 6144
 
 
 @pytest.mark.parametrize("L,d_model,H,g", [(3, 256, 2, 128), (2, 512, 8, 64), (2, 1024, 4, 256)])
