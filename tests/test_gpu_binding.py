@@ -73,3 +73,33 @@ def test_products_checked(ops):
     with pytest.raises(ValueError):
         ops.tgemv(x, c3, s3, 128, y=_e((3, 2, 64)))
     torch.cuda.synchronize()
+
+
+def test_stack_decode_checked(ops):
+    """tm_mamba2_decode_token's arrays: the state arrays carry the batch
+    dimension whenever the embedding is [B, d_model], x_out matches emb, and
+    batches above 4 are refused (no case here reaches a launch)."""
+    L, D, H, g = 2, 256, 2, 128
+    di, cd = 64 * H, 64 * H + 256
+    Z = 2 * di + 256 + H
+    f16, u8 = torch.float16, torch.uint8
+
+    def arrays(lead):
+        return {"in_codes": _e((L, Z, D // 4), u8), "in_scales": _e((L, Z, D // g), f16),
+                "out_codes": _e((L, D, di // 4), u8), "out_scales": _e((L, D, di // g), f16),
+                "pre_w": _e((L, D)), "conv_w": _e((L, cd, 4)), "conv_b": _e((L, cd)),
+                "dt_bias": _e((L, H)), "A_log": _e((L, H)), "D": _e((L, H)),
+                "norm_w": _e((L, di)), "final_w": _e((D,)),
+                "conv_state": _e(lead + (cd, 4), f16),
+                "conv_pos": _e((L,), torch.int32), "ssm_state": _e(lead + (H, 64, 128), f16)}
+
+    with pytest.raises(ValueError):   # three dims
+        ops.mamba2_decode_token(arrays((L, 2)), g, 1e-5, _e((1, 2, D)))
+    with pytest.raises(ValueError):   # batch-1 states for a batch of 2
+        ops.mamba2_decode_token(arrays((L,)), g, 1e-5, _e((2, D)))
+    with pytest.raises(ValueError):   # x_out not [B, d_model]
+        ops.mamba2_decode_token(arrays((L, 2)), g, 1e-5, _e((2, D)),
+                                x_out=_e((D,), torch.bfloat16))
+    with pytest.raises((ValueError, RuntimeError)):   # batch 5
+        ops.mamba2_decode_token(arrays((L, 5)), g, 1e-5, _e((5, D)))
+    torch.cuda.synchronize()
