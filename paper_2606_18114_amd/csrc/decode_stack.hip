@@ -163,9 +163,11 @@ __device__ __forceinline__ float ds_wave_sum4(const float (&a)[4]) {
   return k;
 }
 
-__device__ __forceinline__ uint32_t ds_bf16_rne(float v) {
-  const uint32_t b = __float_as_uint(v);
-  return (b + 0x7FFFu + ((b >> 16) & 1u)) >> 16;
+// two floats as a bfloat16 pair lo | hi << 16, rounded to nearest even
+// (one v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t ds_pack_bf16(float lo, float hi) {
+  const ds_bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // 16 bytes at byte offset off of a buffer, read coherently at agent scope
@@ -232,10 +234,10 @@ __device__ __forceinline__ void ds_norm_x(const float* __restrict__ src,
     const int i = tid + kDsThreads * j;
     if (4 * i < K) {
       if (!kEarlyW) wv[j] = ld16(w + 4 * i);
-      xs[2 * i] = ds_bf16_rne(v[j][0] * r * __uint_as_float(wv[j].x)) |
-                  (ds_bf16_rne(v[j][1] * r * __uint_as_float(wv[j].y)) << 16);
-      xs[2 * i + 1] = ds_bf16_rne(v[j][2] * r * __uint_as_float(wv[j].z)) |
-                      (ds_bf16_rne(v[j][3] * r * __uint_as_float(wv[j].w)) << 16);
+      xs[2 * i] = ds_pack_bf16(v[j][0] * r * __uint_as_float(wv[j].x),
+                               v[j][1] * r * __uint_as_float(wv[j].y));
+      xs[2 * i + 1] = ds_pack_bf16(v[j][2] * r * __uint_as_float(wv[j].z),
+                                   v[j][3] * r * __uint_as_float(wv[j].w));
     }
   }
   __syncthreads();
@@ -552,10 +554,10 @@ __device__ __forceinline__ void ds_norm_xb(const float* __restrict__ src,
       for (int j = 0; j < NQ; ++j) {
         const int i = tid + kDsThreads * j;
         if (4 * i < K) {
-          xb[2 * i] = ds_bf16_rne(v[c][j][0] * r * __uint_as_float(wv[j].x)) |
-                      (ds_bf16_rne(v[c][j][1] * r * __uint_as_float(wv[j].y)) << 16);
-          xb[2 * i + 1] = ds_bf16_rne(v[c][j][2] * r * __uint_as_float(wv[j].z)) |
-                          (ds_bf16_rne(v[c][j][3] * r * __uint_as_float(wv[j].w)) << 16);
+          xb[2 * i] = ds_pack_bf16(v[c][j][0] * r * __uint_as_float(wv[j].x),
+                                   v[c][j][1] * r * __uint_as_float(wv[j].y));
+          xb[2 * i + 1] = ds_pack_bf16(v[c][j][2] * r * __uint_as_float(wv[j].z),
+                                       v[c][j][3] * r * __uint_as_float(wv[j].w));
         }
       }
     }
