@@ -264,3 +264,39 @@ def test_stack_decode_batch_rows_match_batch_one():
             sa = a.layers[l]["ssm"].cpu().numpy()[r].astype(np.float64)
             s1 = d1.layers[l]["ssm"].cpu().numpy()[0].astype(np.float64)
             assert O.rel_fro_error(sa, s1) <= 1e-3, (l, r)
+
+
+@pytest.mark.parametrize("B", [1, 4])
+def test_stack_decode_graph_replays_match_eager(B):
+    """The one-launch decode captured as a HIP graph (its barrier words are
+    cleared by a fill kernel inside the graph): three tokens eagerly, then the
+    same three from the same states as replays of one captured graph, with
+    other GPU work and host syncs in between; outputs and every block's
+    states agree bit for bit (the kernel sums in a fixed order)."""
+    _need_cus(2 * B)
+    dec, *_ = _decoder(31 + B, 3, 256, 2, stack=True, keep=(1,), batch=B)
+    assert dec.stack and dec.B == B
+    init = [(l["conv"].clone(), l["ssm"].clone(), l["pos"].clone()) for l in dec.layers]
+    emb = [torch.randn_like(dec.emb) for _ in range(3)]
+    eager = []
+    for e in emb:
+        dec.emb.copy_(e)
+        eager.append(dec.token().clone())
+    final_eager = [(l["conv"].clone(), l["ssm"].clone(), l["pos"].clone()) for l in dec.layers]
+    for lay, (c, s, p) in zip(dec.layers, init):
+        lay["conv"].copy_(c)
+        lay["ssm"].copy_(s)
+        lay["pos"].copy_(p)
+    dec.capture()
+    for lay, (c, s, p) in zip(dec.layers, init):   # capturing runs nothing
+        assert torch.equal(lay["ssm"], s) and torch.equal(lay["pos"], p)
+    for t, e in enumerate(emb):
+        dec.emb.copy_(e)
+        out = dec.replay()
+        torch.cuda.synchronize()
+        _ = torch.randn(1000, device="cuda").sum().item()   # unrelated work in between
+        assert torch.equal(out, eager[t]), f"token {t}"
+    assert _timeout_flag(dec) == 0
+    for lay, (c, s, p) in zip(dec.layers, final_eager):
+        assert torch.equal(lay["conv"], c) and torch.equal(lay["ssm"], s)
+        assert torch.equal(lay["pos"], p)
