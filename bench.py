@@ -292,7 +292,9 @@ def main():
                       dev, args.steps, keep=keep_first_last(synth.N_LAYERS, 2), stack=True),
                   "all_ternary_B4": decode_mamba2_blocks(dev, args.steps, batch=4),
                   "all_ternary_B4_one_launch": decode_mamba2_blocks(dev, args.steps, batch=4,
-                                                                    stack=True)}
+                                                                    stack=True),
+                  "all_ternary_B16_unfused": decode_mamba2_blocks(dev, args.steps, batch=16,
+                                                                  fused=False)}
 
     # ---------------- QAT block: both projections through autograd ----------------
     qat_block = None if "qat" in args.skip else qat_block_step(args, dev, X, synth)

@@ -240,6 +240,10 @@ class Mamba2Decoder:
         self.d_inner = nheads * P
         self.Z = 2 * self.d_inner + 2 * N + nheads
         conv_dim = self.d_inner + 2 * N
+        if self.keep and not (1 <= batch <= 8 and
+                              batch * max(d_model, self.d_inner) <= 16384):
+            raise ValueError(f"blocks kept in FP16 decode at batch 1 .. 8 with batch x K "
+                             f"<= 16384 (tm_dgemv); got batch {batch}")
         fits = all(rms_fused_fits(batch, k, g) if l not in self.keep else batch * k <= 16384
                    for l in range(n_layers) for k in (d_model, self.d_inner))
         if fused and not fits:

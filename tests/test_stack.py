@@ -105,3 +105,17 @@ def test_mixed_stack_decode_token(B):
     exp = sum(4 * (N * K / 4 + 2 * N * K / g) + 2 * 2 * N * K + L * (2 * B * K + 4 * B * N)
               for N, K in shapes.values())
     assert st.bytes_per_token() == exp
+
+
+def test_decoder_refuses_kept_blocks_past_batch_8():
+    """Blocks kept in FP16 decode through tm_dgemv, which takes batches up to
+    8: the decoder says so when it is built, before touching any device."""
+    torch = pytest.importorskip("torch")
+    from paper_2606_18114_amd.stack import Mamba2Decoder
+
+    def never(*a):
+        raise AssertionError("no weight is read before the check")
+
+    with pytest.raises(ValueError, match="batch 1 .. 8"):
+        Mamba2Decoder(never, never, never, 3, 256, 2, keep=(1,), batch=16,
+                      device=torch.device("cpu"))
