@@ -246,6 +246,11 @@ tm_status tm_tgemm_bwd_dw_ste(const uint16_t* dY, const uint16_t* X,
  * row blocks (fewer than two per CU, e.g. count = 1) splits K across the
  * waves of a workgroup and adds the parts in a fixed order, so its last bits
  * can differ from the same matrix inside a larger launch.
+ * Batches of 9 .. 16 rows at g >= 64 take the bfloat16 matrix cores instead:
+ * the bfloat16 x times the exact 2q of the codes (exact products, float32
+ * sums), the float16 scale applied in float32 per group, one workgroup per
+ * matrix and 16-row block with the K range split over its waves in a fixed
+ * order (deterministic); tm_tgemv_pair then launches each stack on its own.
  */
 tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes,
                    const uint16_t* scales_f16, int32_t count, int32_t B,

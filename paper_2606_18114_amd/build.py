@@ -34,6 +34,7 @@ SOURCES = [
     "tgemm_bwd_dx_f16.hip",
     "tgemm_bwd_dw.hip",
     "tgemv.hip",
+    "tgemv_b16.hip",
     "dgemv.hip",
     "mixer.hip",
     "decode_stack.hip",

@@ -113,6 +113,12 @@ tm_status bwd_dx_checked(const uint16_t* dY, const uint8_t* codes, const float* 
   return TM_OK;
 }
 
+// batches of 9 .. 16 rows at g >= 64 go to the bfloat16 matrix-core form
+// (one workgroup per matrix and 16-row block)
+bool tgemv_on_bf16_mfma(int32_t count, int32_t B, int64_t N, int32_t g) {
+  return tmk::tgemv_b16_takes(B, g) && (int64_t)count * ((N + 15) / 16) <= 0x7FFFFFFF;
+}
+
 // argument checks of one strided stack of tm_tgemv; out / ins: the spans of
 // y and of x, codes, scales
 tm_status tgemv_checked(const uint16_t* x, const uint8_t* codes, const uint16_t* scales_f16,
@@ -429,6 +435,9 @@ tm_status tm_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* scal
   Span out, ins[3];
   if (tm_status st = tgemv_checked(x, codes, scales_f16, count, B, N, K, g, y, &out, ins))
     return st;
+  if (tgemv_on_bf16_mfma(count, B, N, g))
+    return hip_status(
+        tmk::launch_tgemv_b16(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
   return hip_status(tmk::launch_tgemv(x, codes, scales_f16, count, B, N, K, g, y, to_hip(stream)));
 }
 
@@ -445,6 +454,13 @@ tm_status tm_tgemv_pair(const uint16_t* x0, const uint8_t* codes0, const uint16_
   if (overlap(o0, o1)) return TM_EINVAL;
   for (int i = 0; i < 3; ++i)
     if (overlap(o0, i1[i]) || overlap(o1, i0[i])) return TM_EINVAL;
+  if (tgemv_on_bf16_mfma(count0, B, N0, g) && tgemv_on_bf16_mfma(count1, B, N1, g)) {
+    const hipError_t e = tmk::launch_tgemv_b16(x0, codes0, scales0, count0, B, N0, K0, g, y0,
+                                               to_hip(stream));
+    if (e != hipSuccess) return hip_status(e);
+    return hip_status(tmk::launch_tgemv_b16(x1, codes1, scales1, count1, B, N1, K1, g, y1,
+                                            to_hip(stream)));
+  }
   return hip_status(tmk::launch_tgemv_pair(x0, codes0, scales0, count0, N0, K0, y0, x1, codes1,
                                            scales1, count1, N1, K1, y1, B, g, to_hip(stream)));
 }

@@ -70,6 +70,12 @@ hipError_t launch_zero_tiles_f32(float* out, int64_t rows, int64_t cols, int64_t
                                  int64_t t0, int64_t count, hipStream_t stream);
 hipError_t launch_tgemv(const uint16_t* x, const uint8_t* codes, const uint16_t* s16, int count,
                         int B, int64_t N, int64_t K, int g, float* y, hipStream_t stream);
+// batches of 9 .. 16 rows at g >= 64 on the bfloat16 matrix cores (the batch
+// rows as the MFMA's A rows); same arguments and results as launch_tgemv
+bool tgemv_b16_takes(int B, int g);
+hipError_t launch_tgemv_b16(const uint16_t* x, const uint8_t* codes, const uint16_t* s16,
+                            int count, int B, int64_t N, int64_t K, int g, float* y,
+                            hipStream_t stream);
 // two strided stacks of matrices (e.g. a decode token's in_proj and out_proj
 // layers) in one launch; same g and B, everything else per stack
 hipError_t launch_tgemv_pair(const uint16_t* x0, const uint8_t* c0, const uint16_t* s0, int n0,

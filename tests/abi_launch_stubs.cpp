@@ -44,6 +44,11 @@ hipError_t launch_tgemm_bwd_dw(const uint16_t*, const uint16_t*, int64_t, int64_
   reached("tgemm_bwd_dw");
 }
 hipError_t launch_fill_zero_f32(float*, int64_t, hipStream_t) { reached("fill_zero_f32"); }
+bool tgemv_b16_takes(int B, int g) { return B >= 9 && B <= 16 && g >= 64 && g <= 512; }
+hipError_t launch_tgemv_b16(const uint16_t*, const uint8_t*, const uint16_t*, int, int, int64_t,
+                            int64_t, int, float*, hipStream_t) {
+  reached("tgemv_b16");
+}
 hipError_t launch_tgemv(const uint16_t*, const uint8_t*, const uint16_t*, int, int, int64_t,
                         int64_t, int, float*, hipStream_t) {
   reached("tgemv");
