@@ -626,6 +626,14 @@ def test_gemv_batch16_long_k(g):
     gemv_case(2, 16, 300, 4096, g, seed=3, outliers=True)
 
 
+@pytest.mark.parametrize("g", [64, 128])
+def test_gemv_large_batch_many_blocks(g):
+    """Batches of 9 to 16 rows go to the bfloat16 matrix cores; a launch with
+    enough 16-row blocks takes four per workgroup (one read of each chunk of
+    x for 64 rows): 4 matrices of 8500 rows (ragged in 64 and 16), batch 12."""
+    gemv_case(4, 12, 8500, 2048, g, seed=7 + g, outliers=True)
+
+
 @pytest.mark.parametrize("B", [1, 4])
 def test_gemv_decode_shapes(B):
     gemv_case(2, B, synth.IN_PROJ_N, synth.D_MODEL, 128, seed=1000 + B, outliers=True)
